@@ -1,0 +1,196 @@
+/*
+ * corun.h -- C ABI of the MI355X (gfx950) CoRun decode/prefill library.
+ *
+ * CoRun (arXiv 2608.14376) makes LLM inference deterministic without
+ * batch-invariant kernels: every decode iteration is padded to one fixed batch
+ * size and replayed as one captured graph (Sec. IV, "Fixed-Shape Batched
+ * Decode"), every prompt is prefilled alone at its own length (Sec. IV,
+ * "Isolated Prefill"), and the kernels only need to be position-invariant:
+ * F_n(PX) = P F_n(X) for every permutation P at the fixed shape n (Sec. III,
+ * Definition 2).  The determinism argument (Sec. IV, "Determinism Argument")
+ * then gives, for a request at slot p of the padded step D_N,
+ *     pi_p D_N(X) = d(z)
+ * -- its logits, next token and KV append depend only on its own state z.
+ *
+ * This library provides D_N for a pre-norm grouped-query decoder (dense or
+ * mixture-of-experts), the isolated prefill, and the greedy sampler S(l)
+ * (Sec. IV, "Shape-Aligned Sampling" with no random variate).  Each live row's
+ * outputs are bitwise independent of which other requests or padding rows
+ * share the step and of the slot it occupies.
+ *
+ * Conventions (all entry points):
+ *  - Pointers marked "device" are HIP device pointers; "host" are ordinary
+ *    host memory.  The caller owns every buffer it passes.  The engine borrows
+ *    the weight, KV-cache and page-table buffers for its whole lifetime (the
+ *    captured graph bakes their addresses in) and owns only its workspace.
+ *  - Every call returns a corun_status; no call aborts or throws.  On failure
+ *    corun_last_error() returns a message for the calling thread.
+ *  - Host-side validation happens before anything is enqueued: a call that
+ *    fails validation has no side effect on device memory.
+ *  - One engine is used from one host thread at a time; calls are ordered
+ *    after prior work on the `stream` given at creation and complete before
+ *    they return (the outputs they return are host values).
+ *  - bf16 tensors are raw IEEE bfloat16 bit patterns; matrices use the
+ *    PyTorch Linear layout [out_features, in_features], row-major.
+ */
+#ifndef CORUN_H
+#define CORUN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct corun_engine corun_engine;
+
+typedef enum {
+    CORUN_OK = 0,
+    CORUN_E_INVAL = -1,     /* null pointer, out-of-range token, slot or length */
+    CORUN_E_SHAPE = -2,     /* model or batch shape the kernels do not support */
+    CORUN_E_CAPACITY = -3,  /* KV cache (or prefill workspace) too small */
+    CORUN_E_HIP = -4,       /* HIP runtime failure; message has hipGetErrorString */
+    CORUN_E_STATE = -5      /* call not valid for this engine (e.g. no prefill workspace) */
+} corun_status;
+
+enum { CORUN_KV_CONTIGUOUS = 0, CORUN_KV_PAGED = 1 };
+
+/* Model shape.  n_experts = top_k = expert_ffn = 0 selects a dense SwiGLU
+ * MLP of width `ffn`; otherwise every layer routes each token to top_k of
+ * n_experts SwiGLU experts of width expert_ffn (softmax over all experts,
+ * top_k, renormalised).  Requirements: hidden, ffn, expert_ffn multiples of
+ * 16 (a K dimension may have a tail of 8, e.g. ffn = 688); head_dim 64 or
+ * 128; n_heads a multiple of n_kv_heads with n_heads / n_kv_heads <= 16;
+ * vocab a multiple of 16. */
+typedef struct {
+    int32_t n_layers, hidden, n_heads, n_kv_heads, head_dim, ffn, vocab;
+    int32_t n_experts, top_k, expert_ffn;
+    float rms_eps, rope_theta;
+} corun_model_cfg;
+
+/* Weights: device bf16 buffers, caller-owned, borrowed for the engine's
+ * lifetime.  Per-layer fields are HOST arrays of n_layers DEVICE pointers
+ * (copied at creation).  Dense models leave the three expert fields NULL;
+ * MoE models leave w_gate_up / w_down NULL. */
+typedef struct {
+    const void *embed;                 /* [vocab, hidden] */
+    const void *final_norm;            /* [hidden] */
+    const void *lm_head;               /* [vocab, hidden] */
+    const void *const *attn_norm;      /* [L] -> [hidden] */
+    const void *const *w_qkv;          /* [L] -> [(nq + 2 nkv) d, hidden]: q rows, then k, then v, head-major */
+    const void *const *w_o;            /* [L] -> [hidden, nq d] */
+    const void *const *mlp_norm;       /* [L] -> [hidden] */
+    const void *const *w_gate_up;      /* [L] -> [2 ffn, hidden], gate rows first */
+    const void *const *w_down;         /* [L] -> [hidden, ffn] */
+    const void *const *w_router;       /* [L] -> [n_experts, hidden] */
+    const void *const *w_exp_gate_up;  /* [L] -> [n_experts, 2 expert_ffn, hidden] */
+    const void *const *w_exp_down;     /* [L] -> [n_experts, hidden, expert_ffn] */
+} corun_weights;
+
+/* KV cache: device bf16, caller-owned, borrowed.  k and v are HOST arrays of
+ * n_layers DEVICE pointers.
+ *  contiguous: each layer is [n_slots, n_kv_heads, max_seq_len, head_dim];
+ *  paged:      each layer is [num_pages, n_kv_heads, page_size, head_dim] and
+ *              page_table (DEVICE int32 [n_slots, max_pages_per_seq]) maps a
+ *              slot's token t to page page_table[slot][t / page_size] at row
+ *              t % page_size.  Capacity per slot is
+ *              max_pages_per_seq * page_size tokens.
+ * Slot b of the decode step reads and appends the cache of slot b. */
+typedef struct {
+    int32_t layout;                    /* CORUN_KV_CONTIGUOUS | CORUN_KV_PAGED */
+    int32_t n_slots;                   /* >= B_fixed */
+    int32_t max_seq_len;               /* contiguous capacity per slot (tokens) */
+    int32_t page_size, num_pages, max_pages_per_seq;   /* paged only */
+    void *const *k;
+    void *const *v;
+    const int32_t *page_table;
+} corun_kv;
+
+/* Creation options; pass NULL for defaults (all fields 0). */
+typedef struct {
+    int32_t attn_chunk;        /* split-KV chunk in tokens (multiple of 64); 0 = chosen from (model, B, capacity) */
+    int32_t max_prefill_len;   /* prefill workspace in tokens; 0 = none (corun_prefill returns CORUN_E_STATE) */
+    int32_t no_graph;          /* 1 = launch the step's kernels eagerly instead of replaying the captured graph */
+    int32_t poison_workspace;  /* 1 = fill the workspace with NaN bit patterns at creation (test aid) */
+    int32_t split_k_override;  /* >0: force this split-K factor on every projection (test aid; changes the plan) */
+} corun_options;
+
+/* Create an engine for one fixed padded batch size B_fixed (Sec. IV,
+ * "Fixed-Shape Batched Decode": the capture size).  Every plan choice --
+ * GEMM tiles, split-K factors, the attention chunk -- is a function of
+ * (cfg, B_fixed, kv capacity, options) only and never of how many rows are
+ * live.  `stream` is a hipStream_t (NULL = the null stream) that calls are
+ * ordered against.  On success *out owns a workspace and, unless no_graph,
+ * the decode step is captured as one hipGraph on the first step. */
+corun_status corun_engine_create(const corun_model_cfg *cfg, const corun_weights *w,
+                                 const corun_kv *kv, int32_t B_fixed,
+                                 const corun_options *opt, void *stream, corun_engine **out);
+
+void corun_engine_destroy(corun_engine *e);
+
+/* One padded decode step D_N over B_fixed slots (Sec. IV, "Fixed-Shape
+ * Batched Decode" and "Determinism Argument").
+ *  tokens     host int32 [B]: the token to feed each slot
+ *  valid_mask host uint8 [B]: 1 = live request, 0 = padding (its token and
+ *             seq_len are ignored; any values are allowed)
+ *  seq_lens   host int32 [B]: tokens already cached for the slot, which is
+ *             also the new token's 0-based position; a live row needs
+ *             0 <= seq_len < capacity
+ *  next_tokens host int32 [B] out: greedy next token (first index of the
+ *             maximum fp32 logit), -1 for padding rows
+ *  logits     device fp32 [B, vocab] out, or NULL: the step's logits
+ *             (padding rows hold unspecified values)
+ * Live rows append their k, v at position seq_len of their slot's cache in
+ * every layer; padding rows write nothing.  Errors: CORUN_E_INVAL (token out
+ * of range for a live row, negative seq_len), CORUN_E_CAPACITY (seq_len or
+ * a page beyond the cache). */
+corun_status corun_decode_step(corun_engine *e, const int32_t *tokens, const uint8_t *valid_mask,
+                               const int32_t *seq_lens, int32_t *next_tokens, float *logits);
+
+/* n_steps greedy decode steps with the live set fixed: step i+1 feeds each
+ * live row the token step i produced and advances its seq_len by one, all on
+ * the device (the same captured step, replayed n_steps times with no host
+ * round trip).  tokens_out: host int32 [n_steps, B] (row i = step i's
+ * next_tokens).  Requires seq_len + n_steps <= capacity for every live row. */
+corun_status corun_decode_run(corun_engine *e, int32_t n_steps, const int32_t *tokens,
+                              const uint8_t *valid_mask, const int32_t *seq_lens,
+                              int32_t *tokens_out);
+
+/* Isolated prefill of one prompt into `slot` (Sec. IV, "Isolated Prefill";
+ * the base case of the determinism argument): the prompt runs alone, with a
+ * launch plan that depends only on prompt_len, writes k, v for positions
+ * 0..prompt_len-1 of the slot in every layer, and samples the first token
+ * greedily from the last position's logits (Sec. IV, "Shape-Aligned
+ * Sampling": one sampling row).
+ *  prompt      host int32 [prompt_len], each in [0, vocab)
+ *  token_out   host int32 out
+ *  last_logits device fp32 [vocab] out, or NULL
+ * Errors: CORUN_E_STATE without a prefill workspace, CORUN_E_CAPACITY if
+ * prompt_len exceeds it or the slot's cache, CORUN_E_INVAL otherwise. */
+corun_status corun_prefill(corun_engine *e, const int32_t *prompt, int32_t prompt_len, int32_t slot,
+                           int32_t *token_out, float *last_logits);
+
+/* Host-only checks, usable without a GPU: the shape rules of
+ * corun_model_cfg / corun_kv, and the per-row checks of corun_decode_step
+ * for a batch of B rows (n_steps further tokens of capacity are required). */
+corun_status corun_check_config(const corun_model_cfg *cfg, const corun_kv *kv, int32_t B_fixed);
+corun_status corun_check_batch(const corun_model_cfg *cfg, const corun_kv *kv, const int32_t *page_table_host,
+                               int32_t B, const int32_t *tokens, const uint8_t *valid_mask,
+                               const int32_t *seq_lens, int32_t n_steps);
+
+/* The launch plan an engine would use (host-only, no GPU): fills `out` with
+ * up to `cap` int32 values -- B, padded M, then (N, K, split_k, k_chunk) for
+ * the qkv, o, gate_up (or expert), down and lm_head projections, then the
+ * attention chunk and its maximum split count.  Returns the count written or
+ * a negative corun_status. */
+int32_t corun_describe_plan(const corun_model_cfg *cfg, const corun_kv *kv, int32_t B_fixed,
+                            const corun_options *opt, int32_t *out, int32_t cap);
+
+/* Message for the calling thread's last non-OK status ("" if none). */
+const char *corun_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CORUN_H */

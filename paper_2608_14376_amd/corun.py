@@ -1,0 +1,236 @@
+"""ctypes binding of the C ABI declared in ``include/corun.h``.
+
+Argument marshalling only: every step of the decode and prefill path runs in
+the HIP kernels of ``libcorun.so``.  There is no fallback -- if the library
+is missing, :func:`load` raises.  Torch tensors are accepted where the ABI
+takes device or host pointers; torch is used for device memory and streams.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcorun.so")
+
+OK, E_INVAL, E_SHAPE, E_CAPACITY, E_HIP, E_STATE = 0, -1, -2, -3, -4, -5
+KV_CONTIGUOUS, KV_PAGED = 0, 1
+
+EXPORTS = ("corun_engine_create", "corun_engine_destroy", "corun_decode_step", "corun_decode_run",
+           "corun_prefill", "corun_check_config", "corun_check_batch", "corun_describe_plan",
+           "corun_last_error")
+
+
+class ModelCfg(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in (
+        "n_layers", "hidden", "n_heads", "n_kv_heads", "head_dim", "ffn", "vocab",
+        "n_experts", "top_k", "expert_ffn")] + [("rms_eps", C.c_float), ("rope_theta", C.c_float)]
+
+
+_PP = C.POINTER(C.c_void_p)
+
+
+class Weights(C.Structure):
+    _fields_ = [("embed", C.c_void_p), ("final_norm", C.c_void_p), ("lm_head", C.c_void_p)] + [
+        (n, _PP) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down",
+                           "w_router", "w_exp_gate_up", "w_exp_down")]
+
+
+class KV(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in (
+        "layout", "n_slots", "max_seq_len", "page_size", "num_pages", "max_pages_per_seq")] + [
+        ("k", _PP), ("v", _PP), ("page_table", C.c_void_p)]
+
+
+class Options(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in (
+        "attn_chunk", "max_prefill_len", "no_graph", "poison_workspace", "split_k_override")]
+
+
+class CorunError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"corun status {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load():
+    """Open libcorun.so (built by ``python -m paper_2608_14376_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_14376_amd.build`")
+    L = C.CDLL(LIB_PATH)
+    st = C.c_int
+    L.corun_engine_create.restype = st
+    L.corun_engine_create.argtypes = [C.POINTER(ModelCfg), C.POINTER(Weights), C.POINTER(KV), C.c_int32,
+                                      C.POINTER(Options), C.c_void_p, C.POINTER(C.c_void_p)]
+    L.corun_engine_destroy.restype = None
+    L.corun_engine_destroy.argtypes = [C.c_void_p]
+    L.corun_decode_step.restype = st
+    L.corun_decode_step.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+    L.corun_decode_run.restype = st
+    L.corun_decode_run.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+    L.corun_prefill.restype = st
+    L.corun_prefill.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]
+    L.corun_check_config.restype = st
+    L.corun_check_config.argtypes = [C.POINTER(ModelCfg), C.POINTER(KV), C.c_int32]
+    L.corun_check_batch.restype = st
+    L.corun_check_batch.argtypes = [C.POINTER(ModelCfg), C.POINTER(KV), C.c_void_p, C.c_int32, C.c_void_p,
+                                    C.c_void_p, C.c_void_p, C.c_int32]
+    L.corun_describe_plan.restype = C.c_int32
+    L.corun_describe_plan.argtypes = [C.POINTER(ModelCfg), C.POINTER(KV), C.c_int32, C.POINTER(Options),
+                                      C.c_void_p, C.c_int32]
+    L.corun_last_error.restype = C.c_char_p
+    L.corun_last_error.argtypes = []
+    _lib = L
+    return L
+
+
+def last_error() -> str:
+    return load().corun_last_error().decode()
+
+
+def _check(status: int):
+    if status != OK:
+        raise CorunError(status, last_error())
+
+
+def model_cfg(c: dict) -> ModelCfg:
+    return ModelCfg(c["n_layers"], c["hidden"], c["n_heads"], c["n_kv_heads"], c["head_dim"], c["ffn"],
+                    c["vocab"], c.get("n_experts", 0), c.get("top_k", 0), c.get("expert_ffn", 0),
+                    float(c["rms_eps"]), float(c["rope_theta"]))
+
+
+def _ptr_array(tensors, keep):
+    if not tensors:
+        return C.cast(None, _PP)
+    arr = (C.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+    keep.append(arr)
+    return C.cast(arr, _PP)
+
+
+def kv_struct(layout: int, n_slots: int, k, v, keep, max_seq_len=0, page_size=0, num_pages=0,
+              max_pages_per_seq=0, page_table=None) -> KV:
+    return KV(layout, n_slots, max_seq_len, page_size, num_pages, max_pages_per_seq,
+              _ptr_array(k, keep), _ptr_array(v, keep),
+              page_table.data_ptr() if page_table is not None else None)
+
+
+def options(attn_chunk=0, max_prefill_len=0, no_graph=False, poison_workspace=False, split_k_override=0):
+    return Options(attn_chunk, max_prefill_len, int(no_graph), int(poison_workspace), split_k_override)
+
+
+def _np(a, dt):
+    return np.ascontiguousarray(a, dtype=dt)
+
+
+def check_config(cfg: dict, kv: KV, B: int) -> int:
+    c = model_cfg(cfg)
+    return load().corun_check_config(C.byref(c), C.byref(kv), B)
+
+
+def check_batch(cfg: dict, kv: KV, tokens, valid, seq_lens, n_steps=1, page_table_host=None) -> int:
+    c = model_cfg(cfg)
+    t, vm, s = _np(tokens, np.int32), _np(valid, np.uint8), _np(seq_lens, np.int32)
+    pt = None if page_table_host is None else _np(page_table_host, np.int32)
+    return load().corun_check_batch(C.byref(c), C.byref(kv), None if pt is None else pt.ctypes.data, t.size,
+                                    t.ctypes.data, vm.ctypes.data, s.ctypes.data, n_steps)
+
+
+def describe_plan(cfg: dict, kv: KV, B: int, opt: Options | None = None) -> dict:
+    c = model_cfg(cfg)
+    out = np.zeros(64, np.int32)
+    n = load().corun_describe_plan(C.byref(c), C.byref(kv), B, C.byref(opt) if opt else None,
+                                   out.ctypes.data, 64)
+    if n < 0:
+        raise CorunError(n, last_error())
+    v = out[:n].tolist()
+    plan = {"B": v[0], "Mp": v[1]}
+    for i, name in enumerate(("qkv", "o", "gate_up", "down", "lm_head")):
+        N, K, S, Kc = v[2 + 4 * i: 6 + 4 * i]
+        plan[name] = {"N": N, "K": K, "split_k": S, "k_chunk": Kc}
+    plan["attn_chunk"], plan["attn_max_splits"] = v[22], v[23]
+    return plan
+
+
+class Engine:
+    """One fixed-B engine.  `weights` is a workload.Weights of device bf16
+    tensors; `k`, `v` lists of per-layer device bf16 cache tensors."""
+
+    def __init__(self, cfg: dict, weights, B: int, k, v, layout=KV_CONTIGUOUS, page_size=0, page_table=None,
+                 opt: Options | None = None, stream=None):
+        import torch
+        L = load()
+        self.cfg, self.B = cfg, B
+        self._keep = [weights, k, v, page_table]
+        keep = self._keep
+        w = weights
+        self._w = Weights(w.embed.data_ptr(), w.final_norm.data_ptr(), w.lm_head.data_ptr(),
+                          _ptr_array(w.attn_norm, keep), _ptr_array(w.w_qkv, keep), _ptr_array(w.w_o, keep),
+                          _ptr_array(w.mlp_norm, keep), _ptr_array(w.w_gate_up, keep), _ptr_array(w.w_down, keep),
+                          _ptr_array(w.w_router, keep), _ptr_array(w.w_exp_gate_up, keep),
+                          _ptr_array(w.w_exp_down, keep))
+        if layout == KV_PAGED:
+            num_pages, _, ps, _ = k[0].shape
+            assert ps == page_size
+            n_slots, mpp = page_table.shape
+            self._kv = kv_struct(layout, n_slots, k, v, keep, 0, page_size, num_pages, mpp, page_table)
+            self.capacity = mpp * page_size
+        else:
+            n_slots, _, S, _ = k[0].shape
+            self._kv = kv_struct(layout, n_slots, k, v, keep, max_seq_len=S)
+            self.capacity = S
+        self._cfg = model_cfg(cfg)
+        self._opt = opt if opt is not None else options()
+        if stream is None:
+            stream = torch.cuda.current_stream()
+        self._stream = stream
+        h = C.c_void_p()
+        _check(L.corun_engine_create(C.byref(self._cfg), C.byref(self._w), C.byref(self._kv), B,
+                                     C.byref(self._opt), C.c_void_p(stream.cuda_stream), C.byref(h)))
+        self._h = h
+        self._L = L
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._L.corun_engine_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def plan(self) -> dict:
+        return describe_plan(self.cfg, self._kv, self.B, self._opt)
+
+    def decode_step(self, tokens, valid, seq_lens, logits=None) -> np.ndarray:
+        t, vm, s = _np(tokens, np.int32), _np(valid, np.uint8), _np(seq_lens, np.int32)
+        assert t.size == vm.size == s.size == self.B
+        nxt = np.empty(self.B, np.int32)
+        if logits is not None:
+            assert logits.is_cuda and logits.dtype.is_floating_point and logits.numel() == self.B * self.cfg["vocab"]
+        _check(self._L.corun_decode_step(self._h, t.ctypes.data, vm.ctypes.data, s.ctypes.data, nxt.ctypes.data,
+                                         None if logits is None else logits.data_ptr()))
+        return nxt
+
+    def decode_run(self, n_steps, tokens, valid, seq_lens) -> np.ndarray:
+        t, vm, s = _np(tokens, np.int32), _np(valid, np.uint8), _np(seq_lens, np.int32)
+        out = np.empty((n_steps, self.B), np.int32)
+        _check(self._L.corun_decode_run(self._h, n_steps, t.ctypes.data, vm.ctypes.data, s.ctypes.data,
+                                        out.ctypes.data))
+        return out
+
+    def prefill(self, prompt, slot: int, last_logits=None) -> int:
+        p = _np(prompt, np.int32)
+        tok = np.empty(1, np.int32)
+        _check(self._L.corun_prefill(self._h, p.ctypes.data, p.size, slot, tok.ctypes.data,
+                                     None if last_logits is None else last_logits.data_ptr()))
+        return int(tok[0])

@@ -1,0 +1,676 @@
+// engine.cpp -- host side of the C ABI in include/corun.h: validation, the
+// per-B launch plan, workspace, and the captured decode graph.
+//
+// The plan is a pure function of (model shape, B, cache capacity, options):
+// it is computed once at creation and never looks at which rows are live.
+// That is what makes the fixed-shape step position-invariant end to end
+// (Sec. IV, "Fixed-Shape Batched Decode"; Sec. III, Definition 2).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "corun.h"
+#include "kernels.h"
+
+using namespace corun;
+
+namespace {
+
+thread_local std::string g_err;
+
+corun_status fail(corun_status s, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+#define HIP_TRY(expr)                                                                            \
+    do {                                                                                         \
+        hipError_t e_ = (expr);                                                                  \
+        if (e_ != hipSuccess) return fail(CORUN_E_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+    } while (0)
+
+#define ST_TRY(expr)                     \
+    do {                                 \
+        corun_status s_ = (expr);        \
+        if (s_ != CORUN_OK) return s_;   \
+    } while (0)
+
+int kv_capacity(const corun_kv *kv)
+{
+    return kv->layout == CORUN_KV_PAGED ? kv->max_pages_per_seq * kv->page_size : kv->max_seq_len;
+}
+
+// One projection: N outputs, K inputs, split-K into S chunks of Kc.
+struct Proj {
+    int N = 0, K = 0, S = 1, Kc = 0;
+};
+
+struct Plan {
+    int B = 0, Mp = 0, mt = 1;
+    Proj qkv, o, gu, down, lm;
+    int chunk = 0, max_splits = 0;
+};
+
+int mt_for(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
+
+// Split-K factor from the projection shape and M only.  Aim for about 2048
+// wavefronts (8 per CU) so enough weight bytes are in flight to cover HBM
+// latency; each split keeps at least 256 K elements.
+Proj choose_proj(int N, int K, int M, int split_override, int max_split_rows_factor)
+{
+    Proj p;
+    p.N = N;
+    p.K = K;
+    const int col_waves = (N + 63) / 64;
+    const int mt = mt_for(M);
+    const int m_tiles = (M + 16 * mt - 1) / (16 * mt);
+    int S = (2048 + col_waves * m_tiles - 1) / (col_waves * m_tiles);
+    S = std::min(S, std::max(1, K / 256));
+    if (max_split_rows_factor > 0) S = std::min(S, max_split_rows_factor);
+    if (split_override > 0) S = split_override;
+    S = std::max(1, std::min(S, (K + 31) / 32));
+    p.Kc = ((K + S - 1) / S + 31) / 32 * 32;
+    p.S = (K + p.Kc - 1) / p.Kc;
+    return p;
+}
+
+// Attention chunk: fixed per engine from (B, kv heads, capacity): enough
+// (row, head, split) blocks to fill the GPU when every row is at capacity.
+// The split kernel keeps q and the chunk's scores in LDS: G (d + chunk)
+// floats, kept within 64 KiB.
+int max_chunk_for_lds(int G, int d) { return std::min(1024, (16384 - G * d) / G / 64 * 64); }
+
+int choose_chunk(int B, int nkv, int G, int d, int cap, int override_chunk)
+{
+    const int cmax = max_chunk_for_lds(G, d);
+    if (override_chunk > 0) return std::min(override_chunk, cmax);
+    int chunk = 64;
+    while (chunk < cmax && (long long)B * nkv * ((cap + chunk - 1) / chunk) > 4096) chunk *= 2;
+    return std::min(chunk, cmax);
+}
+
+Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_options &opt)
+{
+    Plan p;
+    p.B = B;
+    p.mt = mt_for(B);
+    p.Mp = (B + 63) / 64 * 64;
+    const int H = c->hidden, d = c->head_dim;
+    const int nqkv = (c->n_heads + 2 * c->n_kv_heads) * d;
+    const int so = opt.split_k_override;
+    p.qkv = choose_proj(nqkv, H, B, so, 0);
+    p.o = choose_proj(H, c->n_heads * d, B, so, 0);
+    if (c->n_experts == 0) {
+        p.gu = choose_proj(2 * c->ffn, H, B, so, 0);
+        p.down = choose_proj(H, c->ffn, B, so, 0);
+    }
+    p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0);
+    const int cap = kv_capacity(kv);
+    p.chunk = choose_chunk(B, c->n_kv_heads, c->n_heads / c->n_kv_heads, d, cap, opt.attn_chunk);
+    p.max_splits = (cap + p.chunk - 1) / p.chunk;
+    return p;
+}
+
+}  // namespace
+
+struct corun_engine {
+    corun_model_cfg c{};
+    corun_kv kv{};
+    corun_options opt{};
+    int B = 0;
+    Plan plan;
+    hipStream_t user = nullptr, st = nullptr;
+    hipEvent_t ev = nullptr;
+
+    const uint16_t *embed = nullptr, *final_norm = nullptr, *lm_head = nullptr;
+    std::vector<const uint16_t *> attn_norm, w_qkv, w_o, mlp_norm, w_gu, w_down;
+    std::vector<uint16_t *> kc, vc;
+    KvView view{};
+
+    // decode workspace (one allocation)
+    char *ws = nullptr;
+    size_t ws_bytes = 0;
+    int32_t *d_tokens = nullptr, *d_seq = nullptr, *d_next = nullptr, *d_hist = nullptr, *d_counter = nullptr;
+    uint8_t *d_valid = nullptr;
+    float *x = nullptr, *p_qkv = nullptr, *p_o = nullptr, *p_gu = nullptr, *p_down = nullptr, *attn_ws = nullptr,
+          *logits = nullptr, *p_lm = nullptr;
+    uint16_t *h = nullptr, *q = nullptr, *o = nullptr, *a = nullptr;
+    float2 *rope = nullptr;
+    int hist_cap = 0;
+
+    // pinned host staging
+    int32_t *h_tok = nullptr, *h_seq = nullptr, *h_next = nullptr, *h_counter = nullptr, *h_hist = nullptr;
+    uint8_t *h_valid = nullptr;
+
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+
+    // prefill workspace
+    int pf_max = 0;
+    char *pws = nullptr;
+    size_t pws_bytes = 0;
+    int pf_rows_attn = 0, pf_chunk = 0, pf_max_splits = 0;
+    float *pf_x = nullptr, *pf_part = nullptr, *pf_attn = nullptr, *pf_logits = nullptr;
+    uint16_t *pf_h = nullptr, *pf_q = nullptr, *pf_o = nullptr, *pf_a = nullptr, *pf_hlast = nullptr;
+    int32_t *pf_pos = nullptr, *pf_tok = nullptr, *pf_next = nullptr;
+    size_t pf_part_elems = 0;
+};
+
+// ---------------------------------------------------------------------------
+// Host-side checks
+// ---------------------------------------------------------------------------
+
+extern "C" corun_status corun_check_config(const corun_model_cfg *c, const corun_kv *kv, int32_t B)
+{
+    if (!c || !kv) return fail(CORUN_E_INVAL, "null config");
+    if (c->n_layers <= 0 || c->hidden <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 || c->vocab <= 0)
+        return fail(CORUN_E_SHAPE, "non-positive model dimension");
+    if (c->hidden % 256 != 0) return fail(CORUN_E_SHAPE, "hidden must be a multiple of 256");
+    if (c->head_dim != 64 && c->head_dim != 128) return fail(CORUN_E_SHAPE, "head_dim must be 64 or 128");
+    if (c->n_heads % c->n_kv_heads != 0) return fail(CORUN_E_SHAPE, "n_heads must be a multiple of n_kv_heads");
+    const int G = c->n_heads / c->n_kv_heads;
+    if (!(G == 1 || G == 2 || G == 4 || G == 8 || (G == 16 && c->head_dim == 128)))
+        return fail(CORUN_E_SHAPE, "unsupported query-group size %d", G);
+    if (c->vocab % 16 != 0) return fail(CORUN_E_SHAPE, "vocab must be a multiple of 16");
+    if (c->n_experts != 0) return fail(CORUN_E_SHAPE, "mixture-of-experts layers are not supported by this build");
+    if (c->ffn <= 0 || c->ffn % 16 != 0) return fail(CORUN_E_SHAPE, "ffn must be a positive multiple of 16");
+    if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f)) return fail(CORUN_E_SHAPE, "bad eps or rope theta");
+    if (B <= 0 || B > 1024) return fail(CORUN_E_SHAPE, "B_fixed must be in [1, 1024]");
+    if (kv->n_slots < B) return fail(CORUN_E_CAPACITY, "KV cache has %d slots < B_fixed %d", kv->n_slots, B);
+    if (kv->layout == CORUN_KV_CONTIGUOUS) {
+        if (kv->max_seq_len <= 0) return fail(CORUN_E_CAPACITY, "max_seq_len must be positive");
+    } else if (kv->layout == CORUN_KV_PAGED) {
+        if (kv->page_size <= 0 || kv->num_pages <= 0 || kv->max_pages_per_seq <= 0)
+            return fail(CORUN_E_CAPACITY, "bad paged-cache geometry");
+    } else {
+        return fail(CORUN_E_INVAL, "unknown KV layout %d", kv->layout);
+    }
+    return CORUN_OK;
+}
+
+extern "C" corun_status corun_check_batch(const corun_model_cfg *c, const corun_kv *kv, const int32_t *pt_host,
+                                          int32_t B, const int32_t *tokens, const uint8_t *valid,
+                                          const int32_t *seq_lens, int32_t n_steps)
+{
+    if (!c || !kv || !tokens || !valid || !seq_lens) return fail(CORUN_E_INVAL, "null argument");
+    if (n_steps < 1) return fail(CORUN_E_INVAL, "n_steps must be >= 1");
+    const long long cap = kv_capacity(kv);
+    for (int b = 0; b < B; ++b) {
+        if (!valid[b]) continue;
+        if (tokens[b] < 0 || tokens[b] >= c->vocab)
+            return fail(CORUN_E_INVAL, "row %d: token %d outside [0, %d)", b, tokens[b], c->vocab);
+        if (seq_lens[b] < 0) return fail(CORUN_E_INVAL, "row %d: negative seq_len %d", b, seq_lens[b]);
+        if ((long long)seq_lens[b] + n_steps > cap)
+            return fail(CORUN_E_CAPACITY, "row %d: seq_len %d + %d steps exceeds capacity %lld", b, seq_lens[b],
+                        n_steps, cap);
+        if (kv->layout == CORUN_KV_PAGED && pt_host) {
+            const long long last = ((long long)seq_lens[b] + n_steps - 1) / kv->page_size;
+            for (long long j = 0; j <= last; ++j) {
+                const int32_t pg = pt_host[(long long)b * kv->max_pages_per_seq + j];
+                if (pg < 0 || pg >= kv->num_pages)
+                    return fail(CORUN_E_CAPACITY, "row %d: page %lld maps to %d outside [0, %d)", b, j, pg,
+                                kv->num_pages);
+            }
+        }
+    }
+    return CORUN_OK;
+}
+
+extern "C" int32_t corun_describe_plan(const corun_model_cfg *c, const corun_kv *kv, int32_t B,
+                                       const corun_options *opt, int32_t *out, int32_t cap)
+{
+    corun_status s = corun_check_config(c, kv, B);
+    if (s != CORUN_OK) return s;
+    corun_options o{};
+    if (opt) o = *opt;
+    Plan p = make_plan(c, kv, B, o);
+    std::vector<int32_t> v = {p.B, p.Mp};
+    for (const Proj *pr : {&p.qkv, &p.o, &p.gu, &p.down, &p.lm}) {
+        v.push_back(pr->N);
+        v.push_back(pr->K);
+        v.push_back(pr->S);
+        v.push_back(pr->Kc);
+    }
+    v.push_back(p.chunk);
+    v.push_back(p.max_splits);
+    const int n = std::min<int>((int)v.size(), cap);
+    for (int i = 0; i < n; ++i) out[i] = v[i];
+    return n;
+}
+
+extern "C" const char *corun_last_error(void) { return g_err.c_str(); }
+
+// ---------------------------------------------------------------------------
+// Workspace carving
+// ---------------------------------------------------------------------------
+namespace {
+
+struct Carver {
+    size_t off = 0;
+    template <class T>
+    size_t take(T **slot, size_t n)
+    {
+        off = (off + 255) / 256 * 256;
+        *slot = reinterpret_cast<T *>(off);   // relative; rebased after allocation
+        off += sizeof(T) * n;
+        return off;
+    }
+};
+
+template <class T>
+void rebase(T *&p, char *base)
+{
+    p = reinterpret_cast<T *>(base + reinterpret_cast<size_t>(p));
+}
+
+size_t proj_part_elems(const Proj &p, int M) { return (size_t)p.S * M * p.N; }
+
+corun_status enqueue_step(corun_engine *e)
+{
+    const corun_model_cfg &c = e->c;
+    const Plan &p = e->plan;
+    const int B = e->B, H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn;
+    const int nqkv = (nq + 2 * nkv) * d;
+    hipStream_t st = e->st;
+    HIP_TRY(launch_embed(e->embed, e->d_tokens, e->d_valid, B, H, e->x, st));
+    for (int l = 0; l < c.n_layers; ++l) {
+        HIP_TRY(launch_rmsnorm(e->x, l ? e->p_down : nullptr, l ? p.down.S : 0, (long long)B * H, B, H,
+                               e->attn_norm[l], c.rms_eps, e->h, st));
+        GemmShape g1{B, nqkv, H, p.qkv.S, p.qkv.Kc, p.mt};
+        HIP_TRY(launch_gemm(e->h, H, e->w_qkv[l], g1, e->p_qkv, (long long)B * nqkv, nqkv, st));
+        HIP_TRY(launch_qkv_post(e->p_qkv, p.qkv.S, (long long)B * nqkv, B, e->d_valid, e->d_seq, nullptr, -1, nq,
+                                nkv, d, e->rope, e->q, e->kc[l], e->vc[l], e->view, st));
+        HIP_TRY(launch_attn_split(e->q, B, e->d_valid, e->d_seq, nullptr, -1, nq, nkv, d, e->kc[l], e->vc[l],
+                                  e->view, p.chunk, p.max_splits, e->attn_ws, st));
+        HIP_TRY(launch_attn_merge(e->attn_ws, B, e->d_valid, e->d_seq, nq, nkv, d, p.chunk, p.max_splits, e->o,
+                                  st));
+        GemmShape g2{B, H, nq * d, p.o.S, p.o.Kc, p.mt};
+        HIP_TRY(launch_gemm(e->o, nq * d, e->w_o[l], g2, e->p_o, (long long)B * H, H, st));
+        HIP_TRY(launch_rmsnorm(e->x, e->p_o, p.o.S, (long long)B * H, B, H, e->mlp_norm[l], c.rms_eps, e->h, st));
+        GemmShape g3{B, 2 * F, H, p.gu.S, p.gu.Kc, p.mt};
+        HIP_TRY(launch_gemm(e->h, H, e->w_gu[l], g3, e->p_gu, (long long)B * 2 * F, 2 * F, st));
+        HIP_TRY(launch_swiglu(e->p_gu, p.gu.S, (long long)B * 2 * F, B, F, e->a, F, st));
+        GemmShape g4{B, H, F, p.down.S, p.down.Kc, p.mt};
+        HIP_TRY(launch_gemm(e->a, F, e->w_down[l], g4, e->p_down, (long long)B * H, H, st));
+    }
+    HIP_TRY(launch_rmsnorm(e->x, e->p_down, p.down.S, (long long)B * H, B, H, e->final_norm, c.rms_eps, e->h, st));
+    if (p.lm.S == 1) {
+        GemmShape gl{B, c.vocab, H, 1, p.lm.Kc, p.mt};
+        HIP_TRY(launch_gemm(e->h, H, e->lm_head, gl, e->logits, 0, c.vocab, st));
+    } else {   // test aid only: a split lm_head reduced by the feed-forward split kernel's sum
+        GemmShape gl{B, c.vocab, H, p.lm.S, p.lm.Kc, p.mt};
+        HIP_TRY(launch_gemm(e->h, H, e->lm_head, gl, e->p_lm, (long long)B * c.vocab, c.vocab, st));
+        HIP_TRY(launch_reduce_splits(e->p_lm, p.lm.S, (long long)B * c.vocab, (long long)B * c.vocab, e->logits, st));
+    }
+    HIP_TRY(launch_argmax(e->logits, B, c.vocab, e->d_valid, e->d_next, st));
+    HIP_TRY(launch_feedback(e->d_tokens, e->d_seq, e->d_valid, e->d_next, B, e->d_hist, e->d_counter, e->hist_cap,
+                            st));
+    return CORUN_OK;
+}
+
+corun_status run_step(corun_engine *e)
+{
+    if (e->opt.no_graph) return enqueue_step(e);
+    if (!e->exec) {
+        HIP_TRY(hipStreamBeginCapture(e->st, hipStreamCaptureModeThreadLocal));
+        corun_status s = enqueue_step(e);
+        hipGraph_t g = nullptr;
+        hipError_t ce = hipStreamEndCapture(e->st, &g);
+        if (s != CORUN_OK) {
+            if (g) (void)hipGraphDestroy(g);
+            return s;
+        }
+        if (ce != hipSuccess) return fail(CORUN_E_HIP, "graph capture: %s", hipGetErrorString(ce));
+        e->graph = g;
+        HIP_TRY(hipGraphInstantiate(&e->exec, g, nullptr, nullptr, 0));
+    }
+    HIP_TRY(hipGraphLaunch(e->exec, e->st));
+    return CORUN_OK;
+}
+
+corun_status enter(corun_engine *e)
+{
+    HIP_TRY(hipEventRecord(e->ev, e->user));
+    HIP_TRY(hipStreamWaitEvent(e->st, e->ev, 0));
+    return CORUN_OK;
+}
+
+corun_status check_pages(corun_engine *e, const int32_t *seq_lens, const uint8_t *valid, const int32_t *tokens,
+                         int n_rows, int n_steps)
+{
+    std::vector<int32_t> pt;
+    const int32_t *pth = nullptr;
+    if (e->kv.layout == CORUN_KV_PAGED) {
+        pt.resize((size_t)e->kv.n_slots * e->kv.max_pages_per_seq);
+        HIP_TRY(hipMemcpy(pt.data(), e->kv.page_table, pt.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+        pth = pt.data();
+    }
+    return corun_check_batch(&e->c, &e->kv, pth, n_rows, tokens, valid, seq_lens, n_steps);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Engine lifetime
+// ---------------------------------------------------------------------------
+
+static corun_status alloc_prefill(corun_engine *e)
+{
+    const corun_model_cfg &c = e->c;
+    const int L = e->pf_max, H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn;
+    const int nqkv = (nq + 2 * nkv) * d;
+    const int Lp64 = (L + 63) / 64 * 64;
+    const int maxN = std::max({nqkv, 2 * F, H});
+    // Split-K for prefill is capped so that S * Lp <= pf_max: the partial
+    // buffer then holds pf_max rows of the widest projection.
+    e->pf_part_elems = (size_t)L * maxN;
+    e->pf_chunk = std::min(256, max_chunk_for_lds(nq / nkv, d));
+    e->pf_max_splits = (L + e->pf_chunk - 1) / e->pf_chunk;
+    e->pf_rows_attn = std::min(L, 1024);
+    Carver cv;
+    cv.take(&e->pf_x, (size_t)L * H);
+    cv.take(&e->pf_part, e->pf_part_elems);
+    cv.take(&e->pf_attn, (size_t)e->pf_rows_attn * nkv * e->pf_max_splits * (nq / nkv) * (d + 2));
+    cv.take(&e->pf_logits, (size_t)c.vocab);
+    cv.take(&e->pf_h, (size_t)Lp64 * H);
+    cv.take(&e->pf_q, (size_t)L * nq * d);
+    cv.take(&e->pf_o, (size_t)Lp64 * nq * d);
+    cv.take(&e->pf_a, (size_t)Lp64 * F);
+    cv.take(&e->pf_hlast, (size_t)64 * H);
+    cv.take(&e->pf_pos, (size_t)L);
+    cv.take(&e->pf_tok, (size_t)L);
+    size_t total = cv.take(&e->pf_next, 16);
+    e->pws_bytes = total;
+    HIP_TRY(hipMalloc(&e->pws, total));
+    HIP_TRY(hipMemsetAsync(e->pws, 0, total, e->st));
+    rebase(e->pf_x, e->pws); rebase(e->pf_part, e->pws); rebase(e->pf_attn, e->pws);
+    rebase(e->pf_logits, e->pws); rebase(e->pf_h, e->pws); rebase(e->pf_q, e->pws);
+    rebase(e->pf_o, e->pws); rebase(e->pf_a, e->pws); rebase(e->pf_hlast, e->pws);
+    rebase(e->pf_pos, e->pws); rebase(e->pf_tok, e->pws); rebase(e->pf_next, e->pws);
+    HIP_TRY(launch_iota(e->pf_pos, L, e->st));
+    return CORUN_OK;
+}
+
+extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const corun_weights *w, const corun_kv *kv,
+                                            int32_t B, const corun_options *opt, void *stream, corun_engine **out)
+{
+    if (!out) return fail(CORUN_E_INVAL, "null out");
+    *out = nullptr;
+    ST_TRY(corun_check_config(cfg, kv, B));
+    if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->attn_norm || !w->w_qkv || !w->w_o ||
+        !w->mlp_norm || !w->w_gate_up || !w->w_down)
+        return fail(CORUN_E_INVAL, "missing weight pointer");
+    if (!kv->k || !kv->v) return fail(CORUN_E_INVAL, "missing KV pointers");
+    if (kv->layout == CORUN_KV_PAGED && !kv->page_table) return fail(CORUN_E_INVAL, "paged cache needs page_table");
+    corun_options o{};
+    if (opt) o = *opt;
+    if (o.attn_chunk < 0 || o.attn_chunk % 64 != 0 || o.attn_chunk > 1024)
+        return fail(CORUN_E_INVAL, "attn_chunk must be a multiple of 64 in [64, 1024]");
+    if (o.max_prefill_len < 0) return fail(CORUN_E_INVAL, "negative max_prefill_len");
+
+    corun_engine *e = new corun_engine();
+    e->c = *cfg;
+    e->kv = *kv;
+    e->opt = o;
+    e->B = B;
+    e->user = (hipStream_t)stream;
+    const int L = cfg->n_layers;
+    for (int l = 0; l < L; ++l) {
+        e->attn_norm.push_back((const uint16_t *)w->attn_norm[l]);
+        e->w_qkv.push_back((const uint16_t *)w->w_qkv[l]);
+        e->w_o.push_back((const uint16_t *)w->w_o[l]);
+        e->mlp_norm.push_back((const uint16_t *)w->mlp_norm[l]);
+        e->w_gu.push_back((const uint16_t *)w->w_gate_up[l]);
+        e->w_down.push_back((const uint16_t *)w->w_down[l]);
+        e->kc.push_back((uint16_t *)kv->k[l]);
+        e->vc.push_back((uint16_t *)kv->v[l]);
+    }
+    e->embed = (const uint16_t *)w->embed;
+    e->final_norm = (const uint16_t *)w->final_norm;
+    e->lm_head = (const uint16_t *)w->lm_head;
+    e->view.layout = kv->layout;
+    e->view.max_seq_len = kv->max_seq_len;
+    e->view.page_size = kv->page_size;
+    e->view.max_pages_per_seq = kv->max_pages_per_seq;
+    e->view.page_table = kv->page_table;
+    e->plan = make_plan(cfg, kv, B, o);
+    const Plan &p = e->plan;
+
+    auto bail = [&](corun_status s) {
+        corun_engine_destroy(e);
+        return s;
+    };
+    if (hipStreamCreateWithFlags(&e->st, hipStreamNonBlocking) != hipSuccess ||
+        hipEventCreateWithFlags(&e->ev, hipEventDisableTiming) != hipSuccess)
+        return bail(fail(CORUN_E_HIP, "stream/event creation failed"));
+
+    const int H = cfg->hidden, d = cfg->head_dim, nq = cfg->n_heads, nkv = cfg->n_kv_heads, F = cfg->ffn;
+    const int nqkv = (nq + 2 * nkv) * d;
+    const int cap = kv_capacity(kv);
+    const int rope_len = std::max(cap, o.max_prefill_len);
+    e->hist_cap = 4096;
+    Carver cv;
+    cv.take(&e->d_tokens, B);
+    cv.take(&e->d_seq, B);
+    cv.take(&e->d_next, B);
+    cv.take(&e->d_counter, 4);
+    cv.take(&e->d_hist, (size_t)e->hist_cap * B);
+    cv.take(&e->d_valid, B);
+    cv.take(&e->x, (size_t)B * H);
+    cv.take(&e->p_qkv, proj_part_elems(p.qkv, B));
+    cv.take(&e->p_o, proj_part_elems(p.o, B));
+    cv.take(&e->p_gu, proj_part_elems(p.gu, B));
+    cv.take(&e->p_down, proj_part_elems(p.down, B));
+    cv.take(&e->attn_ws, (size_t)B * nkv * p.max_splits * (nq / nkv) * (d + 2));
+    cv.take(&e->logits, (size_t)B * cfg->vocab);
+    cv.take(&e->p_lm, p.lm.S > 1 ? proj_part_elems(p.lm, B) : 1);
+    cv.take(&e->h, (size_t)p.Mp * H);
+    cv.take(&e->q, (size_t)B * nq * d);
+    cv.take(&e->o, (size_t)p.Mp * nq * d);
+    cv.take(&e->a, (size_t)p.Mp * F);
+    size_t total = cv.take(&e->rope, (size_t)rope_len * (d / 2));
+    e->ws_bytes = total;
+    if (hipMalloc(&e->ws, total) != hipSuccess) return bail(fail(CORUN_E_HIP, "workspace allocation of %zu bytes", total));
+    rebase(e->d_tokens, e->ws); rebase(e->d_seq, e->ws); rebase(e->d_next, e->ws); rebase(e->d_counter, e->ws);
+    rebase(e->d_hist, e->ws); rebase(e->d_valid, e->ws); rebase(e->x, e->ws); rebase(e->p_qkv, e->ws);
+    rebase(e->p_o, e->ws); rebase(e->p_gu, e->ws); rebase(e->p_down, e->ws); rebase(e->attn_ws, e->ws);
+    rebase(e->logits, e->ws); rebase(e->p_lm, e->ws); rebase(e->h, e->ws); rebase(e->q, e->ws); rebase(e->o, e->ws); rebase(e->a, e->ws);
+    rebase(e->rope, e->ws);
+    // Rows B..Mp-1 of the MFMA A operands (h, o, a) are read but never
+    // stored; start everything at zero, or at NaN when poisoning.
+    const uint32_t fillv = o.poison_workspace ? 0xFFFFFFFFu : 0u;
+    const size_t rope_off = (size_t)((char *)e->rope - e->ws);
+    if (launch_fill_u32((uint32_t *)e->ws, (long long)(rope_off / 4), fillv, e->st) != hipSuccess ||
+        launch_fill_u32((uint32_t *)e->d_counter, 1, (uint32_t)e->hist_cap, e->st) != hipSuccess ||
+        launch_rope_table(e->rope, rope_len, d, (double)cfg->rope_theta, e->st) != hipSuccess)
+        return bail(fail(CORUN_E_HIP, "workspace initialisation failed"));
+
+    if (hipHostMalloc((void **)&e->h_tok, sizeof(int32_t) * B * 4 + 64, 0) != hipSuccess ||
+        hipHostMalloc((void **)&e->h_valid, B + 64, 0) != hipSuccess ||
+        hipHostMalloc((void **)&e->h_hist, sizeof(int32_t) * (size_t)e->hist_cap * B, 0) != hipSuccess)
+        return bail(fail(CORUN_E_HIP, "pinned staging allocation failed"));
+    e->h_seq = e->h_tok + B;
+    e->h_next = e->h_tok + 2 * B;
+    e->h_counter = e->h_tok + 3 * B;
+
+    if (o.max_prefill_len > 0) {
+        e->pf_max = o.max_prefill_len;
+        corun_status s = alloc_prefill(e);
+        if (s != CORUN_OK) return bail(s);
+    }
+    if (hipStreamSynchronize(e->st) != hipSuccess) return bail(fail(CORUN_E_HIP, "initialisation failed"));
+    *out = e;
+    return CORUN_OK;
+}
+
+extern "C" void corun_engine_destroy(corun_engine *e)
+{
+    if (!e) return;
+    if (e->st) (void)hipStreamSynchronize(e->st);
+    if (e->exec) (void)hipGraphExecDestroy(e->exec);
+    if (e->graph) (void)hipGraphDestroy(e->graph);
+    if (e->ws) (void)hipFree(e->ws);
+    if (e->pws) (void)hipFree(e->pws);
+    if (e->h_tok) (void)hipHostFree(e->h_tok);
+    if (e->h_valid) (void)hipHostFree(e->h_valid);
+    if (e->h_hist) (void)hipHostFree(e->h_hist);
+    if (e->ev) (void)hipEventDestroy(e->ev);
+    if (e->st) (void)hipStreamDestroy(e->st);
+    delete e;
+}
+
+// ---------------------------------------------------------------------------
+// Decode
+// ---------------------------------------------------------------------------
+
+static corun_status upload_inputs(corun_engine *e, const int32_t *tokens, const uint8_t *valid,
+                                  const int32_t *seq_lens, int32_t counter)
+{
+    const int B = e->B;
+    std::memcpy(e->h_tok, tokens, sizeof(int32_t) * B);
+    std::memcpy(e->h_seq, seq_lens, sizeof(int32_t) * B);
+    std::memcpy(e->h_valid, valid, B);
+    *e->h_counter = counter;
+    HIP_TRY(hipMemcpyAsync(e->d_tokens, e->h_tok, sizeof(int32_t) * B, hipMemcpyHostToDevice, e->st));
+    HIP_TRY(hipMemcpyAsync(e->d_seq, e->h_seq, sizeof(int32_t) * B, hipMemcpyHostToDevice, e->st));
+    HIP_TRY(hipMemcpyAsync(e->d_valid, e->h_valid, B, hipMemcpyHostToDevice, e->st));
+    HIP_TRY(hipMemcpyAsync(e->d_counter, e->h_counter, sizeof(int32_t), hipMemcpyHostToDevice, e->st));
+    return CORUN_OK;
+}
+
+extern "C" corun_status corun_decode_step(corun_engine *e, const int32_t *tokens, const uint8_t *valid,
+                                          const int32_t *seq_lens, int32_t *next_tokens, float *logits)
+{
+    if (!e || !next_tokens) return fail(CORUN_E_INVAL, "null argument");
+    ST_TRY(check_pages(e, seq_lens, valid, tokens, e->B, 1));
+    ST_TRY(enter(e));
+    ST_TRY(upload_inputs(e, tokens, valid, seq_lens, e->hist_cap));
+    ST_TRY(run_step(e));
+    const int B = e->B;
+    HIP_TRY(hipMemcpyAsync(e->h_next, e->d_next, sizeof(int32_t) * B, hipMemcpyDeviceToHost, e->st));
+    if (logits)
+        HIP_TRY(hipMemcpyAsync(logits, e->logits, sizeof(float) * (size_t)B * e->c.vocab, hipMemcpyDeviceToDevice,
+                               e->st));
+    HIP_TRY(hipStreamSynchronize(e->st));
+    std::memcpy(next_tokens, e->h_next, sizeof(int32_t) * B);
+    return CORUN_OK;
+}
+
+extern "C" corun_status corun_decode_run(corun_engine *e, int32_t n_steps, const int32_t *tokens,
+                                         const uint8_t *valid, const int32_t *seq_lens, int32_t *tokens_out)
+{
+    if (!e || !tokens_out) return fail(CORUN_E_INVAL, "null argument");
+    if (n_steps < 1) return fail(CORUN_E_INVAL, "n_steps must be >= 1");
+    ST_TRY(check_pages(e, seq_lens, valid, tokens, e->B, n_steps));
+    ST_TRY(enter(e));
+    const int B = e->B;
+    int done = 0;
+    bool first = true;
+    while (done < n_steps) {
+        const int n = std::min(n_steps - done, e->hist_cap);
+        if (first) {
+            ST_TRY(upload_inputs(e, tokens, valid, seq_lens, 0));
+            first = false;
+        } else {
+            *e->h_counter = 0;
+            HIP_TRY(hipMemcpyAsync(e->d_counter, e->h_counter, sizeof(int32_t), hipMemcpyHostToDevice, e->st));
+        }
+        for (int i = 0; i < n; ++i) ST_TRY(run_step(e));
+        HIP_TRY(hipMemcpyAsync(e->h_hist, e->d_hist, sizeof(int32_t) * (size_t)n * B, hipMemcpyDeviceToHost, e->st));
+        HIP_TRY(hipStreamSynchronize(e->st));
+        std::memcpy(tokens_out + (size_t)done * B, e->h_hist, sizeof(int32_t) * (size_t)n * B);
+        done += n;
+    }
+    return CORUN_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Isolated prefill: every launch is sized by prompt_len alone.
+// ---------------------------------------------------------------------------
+
+extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, int32_t Lp, int32_t slot,
+                                      int32_t *token_out, float *last_logits)
+{
+    if (!e || !prompt || !token_out) return fail(CORUN_E_INVAL, "null argument");
+    if (e->pf_max <= 0) return fail(CORUN_E_STATE, "engine was created without a prefill workspace");
+    if (Lp < 1) return fail(CORUN_E_INVAL, "prompt_len must be >= 1");
+    if (Lp > e->pf_max) return fail(CORUN_E_CAPACITY, "prompt_len %d exceeds the prefill workspace %d", Lp, e->pf_max);
+    if (slot < 0 || slot >= e->kv.n_slots) return fail(CORUN_E_INVAL, "slot %d outside [0, %d)", slot, e->kv.n_slots);
+    if (Lp > kv_capacity(&e->kv)) return fail(CORUN_E_CAPACITY, "prompt_len %d exceeds the cache capacity", Lp);
+    for (int t = 0; t < Lp; ++t)
+        if (prompt[t] < 0 || prompt[t] >= e->c.vocab)
+            return fail(CORUN_E_INVAL, "prompt[%d] = %d outside [0, %d)", t, prompt[t], e->c.vocab);
+    if (e->kv.layout == CORUN_KV_PAGED) {
+        std::vector<int32_t> pt(e->kv.max_pages_per_seq);
+        HIP_TRY(hipMemcpy(pt.data(), e->kv.page_table + (size_t)slot * e->kv.max_pages_per_seq,
+                          pt.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+        for (int j = 0; j <= (Lp - 1) / e->kv.page_size; ++j)
+            if (pt[j] < 0 || pt[j] >= e->kv.num_pages)
+                return fail(CORUN_E_CAPACITY, "slot %d: page %d maps to %d outside [0, %d)", slot, j, pt[j],
+                            e->kv.num_pages);
+    }
+    ST_TRY(enter(e));
+    const corun_model_cfg &c = e->c;
+    const int H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn;
+    const int nqkv = (nq + 2 * nkv) * d;
+    hipStream_t st = e->st;
+    const int cap_rows = std::max(1, e->pf_max / Lp);
+    const Proj pq = choose_proj(nqkv, H, Lp, 0, cap_rows);
+    const Proj po = choose_proj(H, nq * d, Lp, 0, cap_rows);
+    const Proj pg = choose_proj(2 * F, H, Lp, 0, cap_rows);
+    const Proj pd = choose_proj(H, F, Lp, 0, cap_rows);
+    const Proj pl = choose_proj(c.vocab, H, 1, 1, 0);
+    const int mt = mt_for(Lp);
+
+    HIP_TRY(hipMemcpyAsync(e->pf_tok, prompt, sizeof(int32_t) * Lp, hipMemcpyHostToDevice, st));
+    HIP_TRY(launch_embed(e->embed, e->pf_tok, nullptr, Lp, H, e->pf_x, st));
+    for (int l = 0; l < c.n_layers; ++l) {
+        HIP_TRY(launch_rmsnorm(e->pf_x, l ? e->pf_part : nullptr, l ? pd.S : 0, (long long)Lp * H, Lp, H,
+                               e->attn_norm[l], c.rms_eps, e->pf_h, st));
+        GemmShape g1{Lp, nqkv, H, pq.S, pq.Kc, mt};
+        HIP_TRY(launch_gemm(e->pf_h, H, e->w_qkv[l], g1, e->pf_part, (long long)Lp * nqkv, nqkv, st));
+        HIP_TRY(launch_qkv_post(e->pf_part, pq.S, (long long)Lp * nqkv, Lp, nullptr, e->pf_pos, nullptr, slot, nq, nkv,
+                                d, e->rope, e->pf_q, e->kc[l], e->vc[l], e->view, st));
+        for (int r0 = 0; r0 < Lp; r0 += e->pf_rows_attn) {
+            const int nr = std::min(e->pf_rows_attn, Lp - r0);
+            HIP_TRY(launch_attn_split(e->pf_q + (size_t)r0 * nq * d, nr, nullptr, e->pf_pos + r0, nullptr, slot, nq,
+                                      nkv, d, e->kc[l], e->vc[l], e->view, e->pf_chunk, e->pf_max_splits,
+                                      e->pf_attn, st));
+            HIP_TRY(launch_attn_merge(e->pf_attn, nr, nullptr, e->pf_pos + r0, nq, nkv, d, e->pf_chunk,
+                                      e->pf_max_splits, e->pf_o + (size_t)r0 * nq * d, st));
+        }
+        GemmShape g2{Lp, H, nq * d, po.S, po.Kc, mt};
+        HIP_TRY(launch_gemm(e->pf_o, nq * d, e->w_o[l], g2, e->pf_part, (long long)Lp * H, H, st));
+        HIP_TRY(launch_rmsnorm(e->pf_x, e->pf_part, po.S, (long long)Lp * H, Lp, H, e->mlp_norm[l], c.rms_eps,
+                               e->pf_h, st));
+        GemmShape g3{Lp, 2 * F, H, pg.S, pg.Kc, mt};
+        HIP_TRY(launch_gemm(e->pf_h, H, e->w_gu[l], g3, e->pf_part, (long long)Lp * 2 * F, 2 * F, st));
+        HIP_TRY(launch_swiglu(e->pf_part, pg.S, (long long)Lp * 2 * F, Lp, F, e->pf_a, F, st));
+        GemmShape g4{Lp, H, F, pd.S, pd.Kc, mt};
+        HIP_TRY(launch_gemm(e->pf_a, F, e->w_down[l], g4, e->pf_part, (long long)Lp * H, H, st));
+    }
+    // last position only: fold its down partials, final norm, lm_head, argmax
+    const size_t last = (size_t)(Lp - 1) * H;
+    HIP_TRY(launch_rmsnorm(e->pf_x + last, e->pf_part + last, pd.S, (long long)Lp * H, 1, H, e->final_norm, c.rms_eps,
+                           e->pf_hlast, st));
+    GemmShape gl{1, c.vocab, H, 1, pl.Kc, 1};
+    HIP_TRY(launch_gemm(e->pf_hlast, H, e->lm_head, gl, e->pf_logits, 0, c.vocab, st));
+    HIP_TRY(launch_argmax(e->pf_logits, 1, c.vocab, nullptr, e->pf_next, st));
+    HIP_TRY(hipMemcpyAsync(e->h_next, e->pf_next, sizeof(int32_t), hipMemcpyDeviceToHost, st));
+    if (last_logits)
+        HIP_TRY(hipMemcpyAsync(last_logits, e->pf_logits, sizeof(float) * c.vocab, hipMemcpyDeviceToDevice, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    *token_out = e->h_next[0];
+    return CORUN_OK;
+}

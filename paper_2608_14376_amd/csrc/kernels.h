@@ -1,0 +1,88 @@
+// kernels.h -- launchers of the gfx950 kernels, called by the host engine.
+// Every launcher enqueues on `st` and returns the launch error code.  The
+// launch geometry of each is a function of its size arguments only; no kernel
+// reads the number of live rows.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace corun {
+
+// Per-row token selection and fp32 residual init: x[b] = float(E[tok_b]),
+// tok_b = valid[b] ? tokens[b] : 0.
+hipError_t launch_embed(const uint16_t *E, const int32_t *tokens, const uint8_t *valid, int rows,
+                        int H, float *x, hipStream_t st);
+
+// x[b] += sum_{s<S} part[s][b] (fixed order s = 0..S-1), then
+// h[b] = bf16(x[b] * rsqrt(mean(x[b]^2) + eps) * g).  One wavefront per row.
+hipError_t launch_rmsnorm(float *x, const float *part, int S, long long part_stride, int rows, int H,
+                          const uint16_t *g, float eps, uint16_t *h, hipStream_t st);
+
+// Projection partials: out[s][m][n] = sum_{k in chunk s} A[m][k] W[n][k]
+// for m < M_store (bf16 MFMA, fp32 accumulate).  A has lda columns and at
+// least roundup(M, 64) readable rows.  K % 8 == 0, N % 16 == 0.
+struct GemmShape {
+    int M, N, K;
+    int S;          // split-K count
+    int Kc;         // K elements per split (multiple of 32)
+    int mt;         // 16-row M tiles per wave: 1, 2 or 4
+};
+hipError_t launch_gemm(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
+                       long long split_stride, int ldo, hipStream_t st);
+
+// Reduce QKV partials, round to bf16, rotate q and k by their position,
+// round again, write q (bf16 [rows][nq*d]) and append k, v to the cache.
+struct KvView {
+    int layout;                 // 0 contiguous, 1 paged
+    int max_seq_len;            // contiguous
+    int page_size, max_pages_per_seq;
+    const int32_t *page_table;  // device
+};
+hipError_t launch_qkv_post(const float *part, int S, long long part_stride, int rows,
+                           const uint8_t *valid, const int32_t *pos, const int32_t *slot_of_row,
+                           int slot_const, int nq, int nkv, int d, const float2 *rope_tab,
+                           uint16_t *q, uint16_t *kc, uint16_t *vc, KvView kv, hipStream_t st);
+
+// Split-KV decode attention.  Row r (slot slot_of_row[r] or slot_const,
+// attending keys 0..pos[r]) is cut into chunks of `chunk` tokens; block
+// (split, kvh, r) writes the chunk's (max, sum, unnormalised acc) for the G
+// query heads of kv head kvh.  Merge combines the splits in index order.
+hipError_t launch_attn_split(const uint16_t *q, int rows, const uint8_t *valid, const int32_t *pos,
+                             const int32_t *slot_of_row, int slot_const, int nq, int nkv, int d,
+                             const uint16_t *kc, const uint16_t *vc, KvView kv, int chunk,
+                             int max_splits, float *ws, hipStream_t st);
+hipError_t launch_attn_merge(const float *ws, int rows, const uint8_t *valid, const int32_t *pos,
+                             int nq, int nkv, int d, int chunk, int max_splits, uint16_t *o,
+                             hipStream_t st);
+
+// a[m][j] = bf16(silu(bf16(sum_s gate)) * bf16(sum_s up)) over the partials
+// of the [2F] gate/up projection (gate columns first).
+hipError_t launch_swiglu(const float *part, int S, long long part_stride, int rows, int F,
+                         uint16_t *a, int lda, hipStream_t st);
+
+// out[i] = sum_{s<S} part[s * stride + i], s in order, for i < n.
+hipError_t launch_reduce_splits(const float *part, int S, long long stride, long long n, float *out,
+                                hipStream_t st);
+
+// next[b] = first index of the maximum of logits[b] (valid rows), -1 otherwise.
+hipError_t launch_argmax(const float *logits, int rows, int V, const uint8_t *valid, int32_t *next,
+                         hipStream_t st);
+
+// Device-side feedback between replayed steps: live rows take their next
+// token and advance their position; the step's tokens are appended to the
+// history at step index *counter, which then increments.
+hipError_t launch_feedback(int32_t *tokens, int32_t *seq_lens, const uint8_t *valid,
+                           const int32_t *next, int B, int32_t *history, int32_t *counter,
+                           int max_hist, hipStream_t st);
+
+// cos / sin table of the rotary embedding: tab[p][i] = (cos, sin)(p * theta^(-2i/d))
+// evaluated in fp64 and rounded to fp32.
+hipError_t launch_rope_table(float2 *tab, int max_pos, int d, double theta, hipStream_t st);
+
+// fill n bytes with the byte value v (graph-safe replacement for memset)
+hipError_t launch_fill_u32(uint32_t *p, long long n_words, uint32_t v, hipStream_t st);
+
+// prefill helpers: pos[t] = t for t < n
+hipError_t launch_iota(int32_t *p, int n, hipStream_t st);
+
+}  // namespace corun

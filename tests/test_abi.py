@@ -1,0 +1,112 @@
+"""The C ABI without a GPU: the library loads, exports every entry point the
+header declares, and its host-side checks reject bad input before anything
+is enqueued.  No compute call is made here."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_14376_amd import corun
+from paper_2608_14376_amd import workload as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    src = open(os.path.join(ROOT, "include", "corun.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(corun_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = corun.load()
+    syms = declared_symbols()
+    assert set(syms) == set(corun.EXPORTS), syms
+    for s in syms:
+        assert hasattr(lib, s), f"{s} not exported"
+
+
+def _kv(layout=corun.KV_CONTIGUOUS, n_slots=4, max_seq_len=256, page_size=16, num_pages=64, mpp=16):
+    keep = []
+    null2 = (C.c_void_p * 1)(None)
+    keep.append(null2)
+    kv = corun.KV(layout, n_slots, max_seq_len, page_size, num_pages, mpp, C.cast(null2, corun._PP),
+                  C.cast(null2, corun._PP), None)
+    kv._keep = keep
+    return kv
+
+
+def test_check_config_accepts_the_dense_configs():
+    for name in ("tiny", "8b", "32b"):
+        c = wl.config(name)
+        assert corun.check_config(c, _kv(n_slots=256, max_seq_len=4224), 256) == corun.OK
+        assert corun.check_config(c, _kv(corun.KV_PAGED, n_slots=32, num_pages=4096, mpp=2048), 32) == corun.OK
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 96, corun.E_SHAPE),
+    ("n_kv_heads", 3, corun.E_SHAPE),
+    ("hidden", 200, corun.E_SHAPE),
+    ("vocab", 1000, corun.E_SHAPE),
+    ("ffn", 0, corun.E_SHAPE),
+])
+def test_check_config_rejects_bad_shapes(field, value, status):
+    c = wl.config("tiny", **{field: value})
+    assert corun.check_config(c, _kv(), 4) == status
+    assert corun.last_error()
+
+
+def test_check_config_capacity():
+    c = wl.config("tiny")
+    assert corun.check_config(c, _kv(n_slots=2), 4) == corun.E_CAPACITY
+    assert corun.check_config(c, _kv(max_seq_len=0), 4) == corun.E_CAPACITY
+    assert corun.check_config(c, _kv(layout=7), 4) == corun.E_INVAL
+    assert corun.check_config(c, _kv(), 0) == corun.E_SHAPE
+
+
+def test_check_batch_rows():
+    c = wl.config("tiny")
+    kv = _kv(max_seq_len=128)
+    ok = dict(tokens=[1, 2, 3, 4], valid=[1, 1, 1, 1], seq_lens=[0, 5, 100, 127])
+    assert corun.check_batch(c, kv, **ok) == corun.OK
+    assert corun.check_batch(c, kv, [1, 2, 3, 1024], [1, 1, 1, 1], [0, 0, 0, 0]) == corun.E_INVAL
+    assert corun.check_batch(c, kv, [1, 2, 3, -1], [1, 1, 1, 1], [0, 0, 0, 0]) == corun.E_INVAL
+    assert corun.check_batch(c, kv, [1, 2, 3, 4], [1, 1, 1, 1], [0, 0, 0, -3]) == corun.E_INVAL
+    assert corun.check_batch(c, kv, [1, 2, 3, 4], [1, 1, 1, 1], [0, 0, 0, 128]) == corun.E_CAPACITY
+    # padding rows are never validated: any token and length
+    assert corun.check_batch(c, kv, [1, -99, 3, 10**9], [1, 0, 1, 0], [0, -5, 3, 2**31 - 1]) == corun.OK
+    # multi-step runs need room for every step
+    assert corun.check_batch(c, kv, **ok, n_steps=2) == corun.E_CAPACITY
+    assert corun.check_batch(c, kv, [1], [1], [100], n_steps=28) == corun.OK
+    assert corun.check_batch(c, kv, [1], [1], [100], n_steps=29) == corun.E_CAPACITY
+
+
+def test_check_batch_pages():
+    c = wl.config("tiny")
+    kv = _kv(corun.KV_PAGED, n_slots=2, page_size=16, num_pages=8, mpp=4)
+    pt = np.array([[0, 1, 2, 3], [4, 5, 6, 99]], np.int32)
+    assert corun.check_batch(c, kv, [1, 1], [1, 1], [40, 40], page_table_host=pt) == corun.OK
+    assert corun.check_batch(c, kv, [1, 1], [1, 1], [40, 48], page_table_host=pt) == corun.E_CAPACITY
+    assert corun.check_batch(c, kv, [1, 1], [1, 0], [40, 63], page_table_host=pt) == corun.OK
+    assert corun.check_batch(c, kv, [1, 1], [1, 1], [40, 64], page_table_host=pt) == corun.E_CAPACITY
+
+
+def test_plan_is_a_function_of_shape_only():
+    """The launch plan depends on (model, B, capacity) -- there is no input
+    through which the live rows could reach it -- and differs across B."""
+    c = wl.config("8b")
+    plans = {B: corun.describe_plan(c, _kv(n_slots=256, max_seq_len=4224), B) for B in (1, 8, 16, 64, 256)}
+    for B, p in plans.items():
+        assert p["B"] == B and p["Mp"] % 64 == 0 and p["Mp"] >= B
+        for name in ("qkv", "o", "gate_up", "down", "lm_head"):
+            pr = p[name]
+            assert pr["k_chunk"] % 32 == 0 and pr["split_k"] * pr["k_chunk"] >= pr["K"]
+            assert (pr["split_k"] - 1) * pr["k_chunk"] < pr["K"]
+        assert p["lm_head"]["split_k"] == 1
+        assert p["attn_chunk"] % 64 == 0 and p["attn_max_splits"] * p["attn_chunk"] >= 4224
+    assert plans[1] == corun.describe_plan(c, _kv(n_slots=256, max_seq_len=4224), 1)
+    assert plans[1]["qkv"]["split_k"] >= plans[256]["qkv"]["split_k"]
+    forced = corun.describe_plan(c, _kv(n_slots=256, max_seq_len=4224), 16, corun.options(split_k_override=3))
+    assert forced["qkv"]["split_k"] == 3 and forced["down"]["split_k"] == 3

@@ -1,0 +1,358 @@
+"""GPU tests on the tiny two-layer GQA decoder (B = 4): parity with the CPU
+oracle, and the determinism contract of the paper checked bit for bit --
+every live row is independent of its co-runners, of padding and of its slot
+(Sec. III, Definition 2; Sec. IV, "Determinism Argument")."""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_14376_amd import corun
+from paper_2608_14376_amd import workload as wl
+from tests.gpu_helpers import DEV, check_tokens, host_model, oracle_kv, row_rel_err, to_device
+
+pytestmark = pytest.mark.gpu
+
+B = 4
+S_CAP = 160          # cache capacity per slot: lengths up to 128 plus 8 steps and prefill tests
+TOL = 2e-2           # row-normalised max relative logit error against the oracle
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    cfg = wl.config("tiny")
+    Wc = wl.make_weights(cfg, seed=0)
+    return cfg, Wc, to_device(Wc), host_model(Wc)
+
+
+def new_cache(cfg, seed, slots=B, S=S_CAP):
+    K, V = wl.make_kv_contiguous(cfg, slots, S, seed)
+    return [k.to(DEV) for k in K], [v.to(DEV) for v in V]
+
+
+def make_engine(cfg, Wg, K, V, **opt):
+    return corun.Engine(cfg, Wg, B, K, V, opt=corun.options(**opt))
+
+
+# ---------------------------------------------------------------------------
+# Oracle parity
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_parity_with_oracle_8_greedy_steps(tiny, seed):
+    cfg, Wc, Wg, m = tiny
+    K, V = new_cache(cfg, seed=100 + seed)
+    okv = oracle_kv(K, V)
+    eng = make_engine(cfg, Wg, K, V)
+    b = wl.make_batch(B, cfg["vocab"], seed=seed, len_lo=16, len_hi=128)
+    tokens, valid, lens = b.tokens.copy(), b.valid.copy(), b.seq_lens.copy()
+    logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+    near = []
+    worst = 0.0
+    for step in range(8):
+        nxt = eng.decode_step(tokens, valid, lens, logits)
+        ref_l, _ = oracle.decode_batch(m, okv, tokens, valid, lens)
+        gl = logits.cpu().numpy()
+        for r in range(B):
+            if valid[r]:
+                e = row_rel_err(gl[r], ref_l[r])
+                worst = max(worst, e)
+                assert e <= TOL, (step, r, e)
+        check_tokens(nxt, ref_l, gl, valid, near)
+        # teacher forcing: both sides continue from the GPU's tokens
+        tokens = np.where(valid == 1, nxt, tokens).astype(np.int32)
+        lens = np.where(valid == 1, lens + 1, lens).astype(np.int32)
+    assert len(near) <= 1, near
+    print(f"max row-relative logit error {worst:.3e}, near-ties {near}")
+
+
+def test_kv_append_matches_oracle(tiny):
+    cfg, Wc, Wg, m = tiny
+    K, V = new_cache(cfg, seed=7)
+    okv = oracle_kv(K, V)
+    eng = make_engine(cfg, Wg, K, V)
+    b = wl.make_batch(B, cfg["vocab"], seed=8, len_lo=16, len_hi=128, n_live=3)
+    eng.decode_step(b.tokens, b.valid, b.seq_lens)
+    oracle.decode_batch(m, okv, b.tokens, b.valid, b.seq_lens)
+    for l in range(cfg["n_layers"]):
+        gk, gv = wl.bits(K[l]), wl.bits(V[l])
+        for r in range(B):
+            if not b.valid[r]:
+                continue
+            p = b.seq_lens[r]
+            for got, ref in ((gk[r, :, p], okv.k[l][r, :, p]), (gv[r, :, p], okv.v[l][r, :, p])):
+                g = (got.astype(np.uint32) << 16).view(np.float32)
+                o = (ref.astype(np.uint32) << 16).view(np.float32)
+                assert np.abs(g - o).max() <= 2e-2 * np.abs(o).max() + 1e-6
+            # nothing else in the slot moved
+            mask = np.ones(S_CAP, bool)
+            mask[p] = False
+            assert np.array_equal(gk[r][:, mask], okv.k[l][r][:, mask])
+
+
+# ---------------------------------------------------------------------------
+# Bitwise invariance (the method's contract)
+# ---------------------------------------------------------------------------
+
+class Requests:
+    """Four requests, each with its own token, length and cache contents."""
+
+    def __init__(self, cfg, seed):
+        r = np.random.default_rng(seed)
+        self.tokens = r.integers(0, cfg["vocab"], B).astype(np.int32)
+        self.lens = r.integers(16, 129, B).astype(np.int32)
+        self.K, self.V = new_cache(cfg, seed=seed + 1)   # request i's cache is slot i here
+
+    def place(self, K, V, mask, perm, cfg):
+        """Put request i (if live) into slot perm[i]; padding slots get NaN
+        caches, garbage tokens and garbage lengths."""
+        tokens = np.full(B, -12345, np.int32)
+        lens = np.full(B, 2**31 - 7, np.int32)
+        valid = np.zeros(B, np.uint8)
+        for l in range(cfg["n_layers"]):
+            K[l].view(torch.int16).fill_(-1)
+            V[l].view(torch.int16).fill_(-1)
+        for i in range(B):
+            if not mask[i]:
+                continue
+            s = perm[i]
+            tokens[s], lens[s], valid[s] = self.tokens[i], self.lens[i], 1
+            for l in range(cfg["n_layers"]):
+                K[l][s].copy_(self.K[l][i])
+                V[l][s].copy_(self.V[l][i])
+        return tokens, valid, lens
+
+
+def test_invariance_all_masks_all_permutations(tiny):
+    """16 occupancy masks x 24 slot permutations: each live request's logits,
+    next token and whole cache slot are bit-identical to its run with every
+    slot live in the identity placement."""
+    cfg, Wc, Wg, m = tiny
+    req = Requests(cfg, seed=40)
+    K, V = new_cache(cfg, seed=0)
+    eng = make_engine(cfg, Wg, K, V)
+    logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+
+    t, v, s = req.place(K, V, [1] * B, list(range(B)), cfg)
+    ref_next = eng.decode_step(t, v, s, logits)
+    ref_logits = logits.clone()
+    ref_k = [k.clone() for k in K]
+    ref_v = [x.clone() for x in V]
+    n_checked = 0
+    for mask in itertools.product([0, 1], repeat=B):
+        for perm in itertools.permutations(range(B)):
+            t, v, s = req.place(K, V, mask, perm, cfg)
+            nxt = eng.decode_step(t, v, s, logits)
+            for i in range(B):
+                slot = perm[i]
+                if not mask[i]:
+                    assert nxt[slot] == -1
+                    continue
+                assert nxt[slot] == ref_next[i]
+                assert torch.equal(logits[slot].view(torch.int32), ref_logits[i].view(torch.int32)), (mask, perm, i)
+                for l in range(cfg["n_layers"]):
+                    assert torch.equal(K[l][slot].view(torch.int16), ref_k[l][i].view(torch.int16))
+                    assert torch.equal(V[l][slot].view(torch.int16), ref_v[l][i].view(torch.int16))
+                n_checked += 1
+    assert n_checked == 24 * sum(sum(mk) for mk in itertools.product([0, 1], repeat=B))
+
+
+def test_repeated_runs_bitwise(tiny):
+    cfg, Wc, Wg, m = tiny
+    K, V = new_cache(cfg, seed=50)
+    K0, V0 = [k.clone() for k in K], [v.clone() for v in V]
+    eng = make_engine(cfg, Wg, K, V)
+    b = wl.make_batch(B, cfg["vocab"], seed=51, len_lo=16, len_hi=128)
+    logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+    eng.decode_step(b.tokens, b.valid, b.seq_lens, logits)
+    ref = logits.clone()
+    for _ in range(100):
+        for l in range(cfg["n_layers"]):
+            K[l].copy_(K0[l])
+            V[l].copy_(V0[l])
+        eng.decode_step(b.tokens, b.valid, b.seq_lens, logits)
+        live = torch.from_numpy(b.valid.astype(bool)).to(DEV)
+        assert torch.equal(logits[live].view(torch.int32), ref[live].view(torch.int32))
+
+
+def _run_once(cfg, Wg, seed, **opt):
+    K, V = new_cache(cfg, seed=seed)
+    eng = make_engine(cfg, Wg, K, V, **opt)
+    b = wl.make_batch(B, cfg["vocab"], seed=seed + 1, len_lo=16, len_hi=128)
+    logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+    nxt = eng.decode_step(b.tokens, b.valid, b.seq_lens, logits)
+    eng.close()
+    live = torch.from_numpy(b.valid.astype(bool)).to(DEV)
+    return nxt, logits[live].clone(), [k.clone() for k in K]
+
+
+def test_graph_replay_equals_eager(tiny):
+    cfg, Wc, Wg, m = tiny
+    a = _run_once(cfg, Wg, 60)
+    b = _run_once(cfg, Wg, 60, no_graph=True)
+    assert np.array_equal(a[0], b[0])
+    assert torch.equal(a[1].view(torch.int32), b[1].view(torch.int32))
+    assert all(torch.equal(x.view(torch.int16), y.view(torch.int16)) for x, y in zip(a[2], b[2]))
+
+
+def test_poisoned_workspace_changes_nothing(tiny):
+    """A workspace filled with NaN bit patterns at creation gives the same
+    live rows: no kernel reads workspace it did not write."""
+    cfg, Wc, Wg, m = tiny
+    a = _run_once(cfg, Wg, 70)
+    b = _run_once(cfg, Wg, 70, poison_workspace=True)
+    assert np.array_equal(a[0], b[0])
+    assert torch.equal(a[1].view(torch.int32), b[1].view(torch.int32))
+
+
+def test_negative_control_plan_change_is_detected(tiny):
+    """Table I: a reduction split chosen from something other than the fixed
+    shape changes bits.  A different split-K factor on the same inputs must
+    change some logits' low-order bits -- so the bitwise tests above would see
+    a plan that varied with the batch."""
+    cfg, Wc, Wg, m = tiny
+    # split 8 with 32-wide chunks would repeat the MFMA chain's own
+    # left-to-right association; a split of 3 regroups the sum
+    a = _run_once(cfg, Wg, 80, split_k_override=1)
+    b = _run_once(cfg, Wg, 80, split_k_override=3)
+    assert not torch.equal(a[1].view(torch.int32), b[1].view(torch.int32))
+    assert torch.allclose(a[1], b[1], rtol=1e-3, atol=1e-4)
+
+
+def test_decode_run_matches_single_steps(tiny):
+    cfg, Wc, Wg, m = tiny
+    b = wl.make_batch(B, cfg["vocab"], seed=91, len_lo=16, len_hi=128)
+    K, V = new_cache(cfg, seed=90)
+    eng = make_engine(cfg, Wg, K, V)
+    run = eng.decode_run(8, b.tokens, b.valid, b.seq_lens)
+    K2, V2 = new_cache(cfg, seed=90)
+    eng2 = make_engine(cfg, Wg, K2, V2)
+    tokens, lens = b.tokens.copy(), b.seq_lens.copy()
+    for i in range(8):
+        nxt = eng2.decode_step(tokens, b.valid, lens)
+        assert np.array_equal(nxt, run[i]), i
+        tokens = np.where(b.valid == 1, nxt, tokens).astype(np.int32)
+        lens = np.where(b.valid == 1, lens + 1, lens).astype(np.int32)
+    for l in range(cfg["n_layers"]):
+        assert torch.equal(K[l].view(torch.int16), K2[l].view(torch.int16))
+
+
+def test_bad_inputs_are_rejected_without_side_effects(tiny):
+    cfg, Wc, Wg, m = tiny
+    K, V = new_cache(cfg, seed=95)
+    K0 = [k.clone() for k in K]
+    eng = make_engine(cfg, Wg, K, V)
+    with pytest.raises(corun.CorunError) as ei:
+        eng.decode_step([1, 2, 3, cfg["vocab"]], [1, 1, 1, 1], [5, 5, 5, 5])
+    assert ei.value.status == corun.E_INVAL
+    with pytest.raises(corun.CorunError) as ei:
+        eng.decode_step([1, 2, 3, 4], [1, 1, 1, 1], [5, 5, 5, S_CAP])
+    assert ei.value.status == corun.E_CAPACITY
+    with pytest.raises(corun.CorunError) as ei:
+        eng.prefill([1, 2, 3], 0)
+    assert ei.value.status == corun.E_STATE
+    assert all(torch.equal(a, b) for a, b in zip(K, K0))
+
+
+# ---------------------------------------------------------------------------
+# Isolated prefill
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("Lp", [1, 37, 130])
+def test_prefill_parity_with_oracle(tiny, Lp):
+    cfg, Wc, Wg, m = tiny
+    K, V = new_cache(cfg, seed=110)
+    okv = oracle_kv(K, V)
+    eng = make_engine(cfg, Wg, K, V, max_prefill_len=S_CAP)
+    prompt = wl.make_prompt(cfg["vocab"], Lp, seed=111)
+    last = torch.empty(cfg["vocab"], dtype=torch.float32, device=DEV)
+    tok = eng.prefill(prompt, 2, last)
+    ref_l, ref_tok = oracle.prefill(m, okv, 2, prompt)
+    e = row_rel_err(last.cpu().numpy(), ref_l)
+    assert e <= TOL, e
+    near = []
+    check_tokens([tok], ref_l[None], last.cpu().numpy()[None], [1], near)
+    for l in range(cfg["n_layers"]):
+        g = (wl.bits(K[l])[2, :, :Lp].astype(np.uint32) << 16).view(np.float32)
+        o = (okv.k[l][2, :, :Lp].astype(np.uint32) << 16).view(np.float32)
+        assert np.abs(g - o).max() <= 2e-2 * np.abs(o).max()
+
+
+def test_prefill_identity_alone_vs_after_other_traffic(tiny):
+    """Base case of the determinism argument: a prompt prefilled into slot 0
+    of a fresh engine, or into slot 2 after fixed-B decode of other requests,
+    gives the same first token and the same KV bits; its first decode step
+    then matches too, whatever the co-runners."""
+    cfg, Wc, Wg, m = tiny
+    prompt = wl.make_prompt(cfg["vocab"], 50, seed=120)
+
+    K1, V1 = new_cache(cfg, seed=121)
+    e1 = make_engine(cfg, Wg, K1, V1, max_prefill_len=S_CAP)
+    t1 = e1.prefill(prompt, 0)
+    n1 = e1.decode_step([t1, 0, 0, 0], [1, 0, 0, 0], [50, 0, 0, 0])
+
+    K2, V2 = new_cache(cfg, seed=122)
+    e2 = make_engine(cfg, Wg, K2, V2, max_prefill_len=S_CAP)
+    other = wl.make_batch(B, cfg["vocab"], seed=123, len_lo=16, len_hi=100, n_live=4)
+    e2.decode_step(other.tokens, other.valid, other.seq_lens)
+    t2 = e2.prefill(prompt, 2)
+    toks = other.tokens.copy()
+    lens = other.seq_lens + 1
+    toks[2], lens[2] = t2, 50
+    n2 = e2.decode_step(toks, np.ones(B, np.uint8), lens)
+
+    assert t1 == t2 and n1[0] == n2[2]
+    for l in range(cfg["n_layers"]):
+        assert torch.equal(K1[l][0, :, :51].view(torch.int16), K2[l][2, :, :51].view(torch.int16))
+        assert torch.equal(V1[l][0, :, :51].view(torch.int16), V2[l][2, :, :51].view(torch.int16))
+
+
+def test_prefill_then_decode_tracks_longer_prefill(tiny):
+    """prefill(p ++ [t]) and prefill(p) then decode(t) compute the same
+    function (the oracle gives bit-equal results); on the GPU the two use
+    different launch shapes, so they agree within tolerance."""
+    cfg, Wc, Wg, m = tiny
+    p = wl.make_prompt(cfg["vocab"], 40, seed=130)
+    K, V = new_cache(cfg, seed=131)
+    eng = make_engine(cfg, Wg, K, V, max_prefill_len=S_CAP)
+    la = torch.empty(cfg["vocab"], dtype=torch.float32, device=DEV)
+    eng.prefill(np.append(p, 77), 1, la)
+    lb = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+    eng.prefill(p, 1)
+    eng.decode_step([0, 77, 0, 0], [0, 1, 0, 0], [0, 40, 0, 0], lb)
+    a, b = la.cpu().numpy(), lb[1].cpu().numpy()
+    assert np.abs(a - b).max() <= 1e-2 * np.abs(a).max()
+
+
+def test_paged_equals_contiguous_bitwise(tiny):
+    cfg, Wc, Wg, m = tiny
+    ps = 16
+    mpp = S_CAP // ps
+    num_pages = B * mpp + 3
+    pt = wl.make_page_table(B, mpp, num_pages, seed=140)
+    Kc, Vc = new_cache(cfg, seed=141)
+    Kp = [torch.full((num_pages, cfg["n_kv_heads"], ps, cfg["head_dim"]), float("nan"), dtype=torch.bfloat16,
+                     device=DEV) for _ in range(cfg["n_layers"])]
+    Vp = [t.clone() for t in Kp]
+    for l in range(cfg["n_layers"]):
+        for s in range(B):
+            for j in range(mpp):
+                Kp[l][pt[s, j]] = Kc[l][s, :, j * ps:(j + 1) * ps]
+                Vp[l][pt[s, j]] = Vc[l][s, :, j * ps:(j + 1) * ps]
+    ptd = torch.from_numpy(pt).to(DEV)
+    ec = make_engine(cfg, Wg, Kc, Vc)
+    ep = corun.Engine(cfg, Wg, B, Kp, Vp, layout=corun.KV_PAGED, page_size=ps, page_table=ptd)
+    assert ec.plan() == ep.plan()
+    b = wl.make_batch(B, cfg["vocab"], seed=142, len_lo=16, len_hi=140)
+    la = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+    lb = torch.empty_like(la)
+    for _ in range(3):
+        na = ec.decode_step(b.tokens, b.valid, b.seq_lens, la)
+        nb = ep.decode_step(b.tokens, b.valid, b.seq_lens, lb)
+        assert np.array_equal(na, nb)
+        live = torch.from_numpy(b.valid.astype(bool)).to(DEV)
+        assert torch.equal(la[live].view(torch.int32), lb[live].view(torch.int32))
+        b.tokens = np.where(b.valid == 1, na, b.tokens).astype(np.int32)
+        b.seq_lens = np.where(b.valid == 1, b.seq_lens + 1, b.seq_lens).astype(np.int32)
