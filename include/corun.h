@@ -113,6 +113,8 @@ typedef struct {
     int32_t no_graph;          /* 1 = launch the step's kernels eagerly instead of replaying the captured graph */
     int32_t poison_workspace;  /* 1 = fill the workspace with NaN bit patterns at creation (test aid) */
     int32_t split_k_override;  /* >0: force this split-K factor on every projection (test aid; changes the plan) */
+    int32_t gemm_bm;           /* 0 = automatic; 64/128/256 = force the LDS-tiled projection kernel with this
+                                  M tile (tuning aid; changes the plan) */
 } corun_options;
 
 /* Create an engine for one fixed padded batch size B_fixed (Sec. IV,
@@ -170,6 +172,33 @@ corun_status corun_decode_run(corun_engine *e, int32_t n_steps, const int32_t *t
 corun_status corun_prefill(corun_engine *e, const int32_t *prompt, int32_t prompt_len, int32_t slot,
                            int32_t *token_out, float *last_logits);
 
+/* Kernels that corun_time_kernel can time. */
+enum {
+    CORUN_K_QKV_GEMM = 0,     /* QKV projection (split-K partials) */
+    CORUN_K_O_GEMM = 1,       /* attention output projection */
+    CORUN_K_GATE_UP_GEMM = 2, /* gate/up projection */
+    CORUN_K_DOWN_GEMM = 3,    /* down projection */
+    CORUN_K_LM_HEAD = 4,      /* lm_head projection */
+    CORUN_K_ATTN_SPLIT = 5,   /* split-KV decode attention */
+    CORUN_K_ATTN_MERGE = 6,   /* fixed-order split merge */
+    CORUN_K_RMSNORM = 7,      /* residual fold + RMSNorm */
+    CORUN_K_QKV_POST = 8,     /* QKV epilogue: RoPE + KV append */
+    CORUN_K_SWIGLU = 9,       /* SwiGLU epilogue */
+    CORUN_K_ARGMAX = 10,      /* greedy argmax */
+    CORUN_K_COUNT = 11
+};
+
+/* Measurement aid: launch one kernel of the decode step n_iters times back
+ * to back on the engine's stream, launch i using layer (layer + i) mod
+ * n_layers (so weights and cache stream from HBM as in the step) and the
+ * engine's current workspace and inputs (as left by the last step), and
+ * return the mean duration per launch in microseconds, measured with HIP
+ * events around the launches.  Call after at least one decode step.
+ * Re-running a kernel rewrites the same workspace values it wrote in the
+ * step (the residual-folding RMSNorm adds its partials again; the next step
+ * recomputes the residual from the embedding). */
+corun_status corun_time_kernel(corun_engine *e, int32_t kernel, int32_t layer, int32_t n_iters, float *avg_us);
+
 /* Host-only checks, usable without a GPU: the shape rules of
  * corun_model_cfg / corun_kv, and the per-row checks of corun_decode_step
  * for a batch of B rows (n_steps further tokens of capacity are required). */
@@ -179,9 +208,9 @@ corun_status corun_check_batch(const corun_model_cfg *cfg, const corun_kv *kv, c
                                const int32_t *seq_lens, int32_t n_steps);
 
 /* The launch plan an engine would use (host-only, no GPU): fills `out` with
- * up to `cap` int32 values -- B, padded M, then (N, K, split_k, k_chunk) for
- * the qkv, o, gate_up (or expert), down and lm_head projections, then the
- * attention chunk and its maximum split count.  Returns the count written or
+ * up to `cap` int32 values -- B, padded M, then (N, K, split_k, k_chunk,
+ * m_tile) for the qkv, o, gate_up, down and lm_head projections (m_tile 0 =
+ * the skinny kernel), then the attention chunk and its maximum split count.  Returns the count written or
  * a negative corun_status. */
 int32_t corun_describe_plan(const corun_model_cfg *cfg, const corun_kv *kv, int32_t B_fixed,
                             const corun_options *opt, int32_t *out, int32_t cap);

@@ -20,7 +20,13 @@ KV_CONTIGUOUS, KV_PAGED = 0, 1
 
 EXPORTS = ("corun_engine_create", "corun_engine_destroy", "corun_decode_step", "corun_decode_run",
            "corun_prefill", "corun_check_config", "corun_check_batch", "corun_describe_plan",
-           "corun_last_error")
+           "corun_last_error", "corun_time_kernel")
+
+# kernel ids of corun_time_kernel
+K_QKV_GEMM, K_O_GEMM, K_GATE_UP_GEMM, K_DOWN_GEMM, K_LM_HEAD, K_ATTN_SPLIT, K_ATTN_MERGE, K_RMSNORM, \
+    K_QKV_POST, K_SWIGLU, K_ARGMAX = range(11)
+KERNEL_NAMES = ("qkv_gemm", "o_gemm", "gate_up_gemm", "down_gemm", "lm_head", "attn_split", "attn_merge",
+                "rmsnorm", "qkv_post", "swiglu", "argmax")
 
 
 class ModelCfg(C.Structure):
@@ -46,7 +52,7 @@ class KV(C.Structure):
 
 class Options(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
-        "attn_chunk", "max_prefill_len", "no_graph", "poison_workspace", "split_k_override")]
+        "attn_chunk", "max_prefill_len", "no_graph", "poison_workspace", "split_k_override", "gemm_bm")]
 
 
 class CorunError(RuntimeError):
@@ -86,6 +92,8 @@ def load():
     L.corun_describe_plan.restype = C.c_int32
     L.corun_describe_plan.argtypes = [C.POINTER(ModelCfg), C.POINTER(KV), C.c_int32, C.POINTER(Options),
                                       C.c_void_p, C.c_int32]
+    L.corun_time_kernel.restype = st
+    L.corun_time_kernel.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_float)]
     L.corun_last_error.restype = C.c_char_p
     L.corun_last_error.argtypes = []
     _lib = L
@@ -122,8 +130,9 @@ def kv_struct(layout: int, n_slots: int, k, v, keep, max_seq_len=0, page_size=0,
               page_table.data_ptr() if page_table is not None else None)
 
 
-def options(attn_chunk=0, max_prefill_len=0, no_graph=False, poison_workspace=False, split_k_override=0):
-    return Options(attn_chunk, max_prefill_len, int(no_graph), int(poison_workspace), split_k_override)
+def options(attn_chunk=0, max_prefill_len=0, no_graph=False, poison_workspace=False, split_k_override=0,
+            gemm_bm=0):
+    return Options(attn_chunk, max_prefill_len, int(no_graph), int(poison_workspace), split_k_override, gemm_bm)
 
 
 def _np(a, dt):
@@ -153,9 +162,9 @@ def describe_plan(cfg: dict, kv: KV, B: int, opt: Options | None = None) -> dict
     v = out[:n].tolist()
     plan = {"B": v[0], "Mp": v[1]}
     for i, name in enumerate(("qkv", "o", "gate_up", "down", "lm_head")):
-        N, K, S, Kc = v[2 + 4 * i: 6 + 4 * i]
-        plan[name] = {"N": N, "K": K, "split_k": S, "k_chunk": Kc}
-    plan["attn_chunk"], plan["attn_max_splits"] = v[22], v[23]
+        N, K, S, Kc, bm = v[2 + 5 * i: 7 + 5 * i]
+        plan[name] = {"N": N, "K": K, "split_k": S, "k_chunk": Kc, "m_tile": bm}
+    plan["attn_chunk"], plan["attn_max_splits"] = v[27], v[28]
     return plan
 
 
@@ -227,6 +236,12 @@ class Engine:
         _check(self._L.corun_decode_run(self._h, n_steps, t.ctypes.data, vm.ctypes.data, s.ctypes.data,
                                         out.ctypes.data))
         return out
+
+    def time_kernel(self, kernel: int, layer: int = 0, n_iters: int = 20) -> float:
+        """Mean launch duration in microseconds (HIP events, engine stream)."""
+        us = C.c_float()
+        _check(self._L.corun_time_kernel(self._h, kernel, layer, n_iters, C.byref(us)))
+        return float(us.value)
 
     def prefill(self, prompt, slot: int, last_logits=None) -> int:
         p = _np(prompt, np.int32)

@@ -51,9 +51,10 @@ int kv_capacity(const corun_kv *kv)
     return kv->layout == CORUN_KV_PAGED ? kv->max_pages_per_seq * kv->page_size : kv->max_seq_len;
 }
 
-// One projection: N outputs, K inputs, split-K into S chunks of Kc.
+// One projection: N outputs, K inputs, split-K into S chunks of Kc, run by
+// the skinny kernel (bm = 0) or the LDS-tiled kernel with M tile bm.
 struct Proj {
-    int N = 0, K = 0, S = 1, Kc = 0;
+    int N = 0, K = 0, S = 1, Kc = 0, bm = 0;
 };
 
 struct Plan {
@@ -64,32 +65,50 @@ struct Plan {
 
 int mt_for(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 
-// Split-K factor from the projection shape and M only.  Aim for about 2048
-// wavefronts (8 per CU) so enough weight bytes are in flight to cover HBM
-// latency; each split keeps at least 256 K elements.
-Proj choose_proj(int N, int K, int M, int split_override, int max_split_rows_factor)
+// Kernel, tile and split-K factor from the projection shape and M only.
+//  * M <= 64: the skinny kernel (weights streamed to registers); aim for
+//    about 2048 wavefronts (8 per CU) so enough weight bytes are in flight,
+//    each split keeping at least 256 K elements.
+//  * M > 64: the LDS-tiled kernel with a 128-row tile (measured faster than
+//    256 rows at M = 256: two workgroups fit a CU), split-K only as far as
+//    needed to give about two workgroups per CU, each split keeping at least
+//    512 K elements.
+Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_override)
 {
     Proj p;
     p.N = N;
     p.K = K;
-    const int col_waves = (N + 63) / 64;
-    const int mt = mt_for(M);
-    const int m_tiles = (M + 16 * mt - 1) / (16 * mt);
-    int S = (2048 + col_waves * m_tiles - 1) / (col_waves * m_tiles);
-    S = std::min(S, std::max(1, K / 256));
-    if (max_split_rows_factor > 0) S = std::min(S, max_split_rows_factor);
+    int S, align;
+    if (M <= 64 && bm_override <= 0) {
+        const int col_waves = (N + 63) / 64;
+        const int mt = mt_for(M);
+        const int m_tiles = (M + 16 * mt - 1) / (16 * mt);
+        S = (2048 + col_waves * m_tiles - 1) / (col_waves * m_tiles);
+        S = std::min(S, std::max(1, K / 256));
+        align = 32;
+    } else {
+        p.bm = bm_override > 0 ? bm_override : 128;
+        const int tiles = ((M + p.bm - 1) / p.bm) * ((N + 127) / 128);
+        const int target = p.bm == 256 ? 256 : 512;
+        S = (target + tiles - 1) / tiles;
+        S = std::min(S, std::max(1, K / 512));
+        align = 64;
+    }
+    if (max_split > 0) S = std::min(S, max_split);
     if (split_override > 0) S = split_override;
-    S = std::max(1, std::min(S, (K + 31) / 32));
-    p.Kc = ((K + S - 1) / S + 31) / 32 * 32;
+    S = std::max(1, std::min(S, (K + align - 1) / align));
+    p.Kc = ((K + S - 1) / S + align - 1) / align * align;
     p.S = (K + p.Kc - 1) / p.Kc;
     return p;
 }
 
+GemmShape shape_of(const Proj &p, int M) { return GemmShape{M, p.N, p.K, p.S, p.Kc, mt_for(M), p.bm}; }
+
 // Attention chunk: fixed per engine from (B, kv heads, capacity): enough
 // (row, head, split) blocks to fill the GPU when every row is at capacity.
-// The split kernel keeps q and the chunk's scores in LDS: G (d + chunk)
-// floats, kept within 64 KiB.
-int max_chunk_for_lds(int G, int d) { return std::min(1024, (16384 - G * d) / G / 64 * 64); }
+// The split kernel keeps the chunk's scores and the four wavefront partials
+// in LDS: G chunk + 8 G + 4 G d floats, kept within 64 KiB.
+int max_chunk_for_lds(int G, int d) { return std::min(1024, (16384 - 8 * G - 4 * G * d) / G / 64 * 64); }
 
 int choose_chunk(int B, int nkv, int G, int d, int cap, int override_chunk)
 {
@@ -108,14 +127,17 @@ Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_
     p.Mp = (B + 63) / 64 * 64;
     const int H = c->hidden, d = c->head_dim;
     const int nqkv = (c->n_heads + 2 * c->n_kv_heads) * d;
-    const int so = opt.split_k_override;
-    p.qkv = choose_proj(nqkv, H, B, so, 0);
-    p.o = choose_proj(H, c->n_heads * d, B, so, 0);
+    const int so = opt.split_k_override, bo = opt.gemm_bm;
+    p.qkv = choose_proj(nqkv, H, B, so, 0, bo);
+    p.o = choose_proj(H, c->n_heads * d, B, so, 0, bo);
     if (c->n_experts == 0) {
-        p.gu = choose_proj(2 * c->ffn, H, B, so, 0);
-        p.down = choose_proj(H, c->ffn, B, so, 0);
+        p.gu = choose_proj(2 * c->ffn, H, B, so, 0, bo);
+        p.down = choose_proj(H, c->ffn, B, so, 0, bo);
     }
-    p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0);
+    // lm_head: never split (its epilogue selects the argmax partials) except
+    // under the split override test aid; the 64-row tile has no argmax epilogue
+    p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0, bo == 64 ? 0 : bo);
+    if (p.lm.bm == 64) p.lm = choose_proj(c->vocab, H, 64, so > 0 ? so : 1, 0, 0);
     const int cap = kv_capacity(kv);
     p.chunk = choose_chunk(B, c->n_kv_heads, c->n_heads / c->n_kv_heads, d, cap, opt.attn_chunk);
     p.max_splits = (cap + p.chunk - 1) / p.chunk;
@@ -145,6 +167,7 @@ struct corun_engine {
     uint8_t *d_valid = nullptr;
     float *x = nullptr, *p_qkv = nullptr, *p_o = nullptr, *p_gu = nullptr, *p_down = nullptr, *attn_ws = nullptr,
           *logits = nullptr, *p_lm = nullptr;
+    ArgBest *amax = nullptr;
     uint16_t *h = nullptr, *q = nullptr, *o = nullptr, *a = nullptr;
     float2 *rope = nullptr;
     int hist_cap = 0;
@@ -164,6 +187,7 @@ struct corun_engine {
     float *pf_x = nullptr, *pf_part = nullptr, *pf_attn = nullptr, *pf_logits = nullptr;
     uint16_t *pf_h = nullptr, *pf_q = nullptr, *pf_o = nullptr, *pf_a = nullptr, *pf_hlast = nullptr;
     int32_t *pf_pos = nullptr, *pf_tok = nullptr, *pf_next = nullptr;
+    ArgBest *pf_amax = nullptr;
     size_t pf_part_elems = 0;
 };
 
@@ -241,6 +265,7 @@ extern "C" int32_t corun_describe_plan(const corun_model_cfg *c, const corun_kv 
         v.push_back(pr->K);
         v.push_back(pr->S);
         v.push_back(pr->Kc);
+        v.push_back(pr->bm);
     }
     v.push_back(p.chunk);
     v.push_back(p.max_splits);
@@ -276,44 +301,87 @@ void rebase(T *&p, char *base)
 
 size_t proj_part_elems(const Proj &p, int M) { return (size_t)p.S * M * p.N; }
 
-corun_status enqueue_step(corun_engine *e)
+// One kernel of layer l of the decode step; the step is these in order.
+corun_status launch_one(corun_engine *e, int which, int l)
 {
     const corun_model_cfg &c = e->c;
     const Plan &p = e->plan;
     const int B = e->B, H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn;
     const int nqkv = (nq + 2 * nkv) * d;
     hipStream_t st = e->st;
+    switch (which) {
+    case CORUN_K_QKV_GEMM: {
+        HIP_TRY(launch_proj(e->h, H, e->w_qkv[l], shape_of(p.qkv, B), e->p_qkv, (long long)B * nqkv, nqkv, st));
+        break;
+    }
+    case CORUN_K_QKV_POST:
+        HIP_TRY(launch_qkv_post(e->p_qkv, p.qkv.S, (long long)B * nqkv, B, e->d_valid, e->d_seq, nullptr, -1, nq,
+                                nkv, d, e->rope, e->q, e->kc[l], e->vc[l], e->view, st));
+        break;
+    case CORUN_K_ATTN_SPLIT:
+        HIP_TRY(launch_attn_split(e->q, B, e->d_valid, e->d_seq, nullptr, -1, nq, nkv, d, e->kc[l], e->vc[l],
+                                  e->view, p.chunk, p.max_splits, e->attn_ws, st));
+        break;
+    case CORUN_K_ATTN_MERGE:
+        HIP_TRY(launch_attn_merge(e->attn_ws, B, e->d_valid, e->d_seq, nq, nkv, d, p.chunk, p.max_splits, e->o, st));
+        break;
+    case CORUN_K_O_GEMM: {
+        HIP_TRY(launch_proj(e->o, nq * d, e->w_o[l], shape_of(p.o, B), e->p_o, (long long)B * H, H, st));
+        break;
+    }
+    case CORUN_K_RMSNORM:   // the post-attention norm (folds the O partials)
+        HIP_TRY(launch_rmsnorm(e->x, e->p_o, p.o.S, (long long)B * H, B, H, e->mlp_norm[l], c.rms_eps, e->h, st));
+        break;
+    case CORUN_K_GATE_UP_GEMM: {
+        HIP_TRY(launch_proj(e->h, H, e->w_gu[l], shape_of(p.gu, B), e->p_gu, (long long)B * 2 * F, 2 * F, st));
+        break;
+    }
+    case CORUN_K_SWIGLU:
+        HIP_TRY(launch_swiglu(e->p_gu, p.gu.S, (long long)B * 2 * F, B, F, e->a, F, st));
+        break;
+    case CORUN_K_DOWN_GEMM: {
+        HIP_TRY(launch_proj(e->a, F, e->w_down[l], shape_of(p.down, B), e->p_down, (long long)B * H, H, st));
+        break;
+    }
+    case CORUN_K_LM_HEAD:
+        if (p.lm.S == 1) {
+            HIP_TRY(launch_proj(e->h, H, e->lm_head, shape_of(p.lm, B), e->logits, 0, c.vocab, st, e->amax));
+        } else {   // test aid only: a split lm_head, reduced in split order
+            HIP_TRY(launch_proj(e->h, H, e->lm_head, shape_of(p.lm, B), e->p_lm, (long long)B * c.vocab, c.vocab,
+                                st));
+            HIP_TRY(launch_reduce_splits(e->p_lm, p.lm.S, (long long)B * c.vocab, (long long)B * c.vocab, e->logits,
+                                         st));
+        }
+        break;
+    case CORUN_K_ARGMAX:
+        if (p.lm.S == 1)
+            HIP_TRY(launch_argmax_partials(e->amax, B, gemm_col_blocks(c.vocab), e->d_valid, e->d_next, st));
+        else
+            HIP_TRY(launch_argmax(e->logits, B, c.vocab, e->d_valid, e->d_next, st));
+        break;
+    default:
+        return fail(CORUN_E_INVAL, "unknown kernel id %d", which);
+    }
+    return CORUN_OK;
+}
+
+corun_status enqueue_step(corun_engine *e)
+{
+    const corun_model_cfg &c = e->c;
+    const Plan &p = e->plan;
+    const int B = e->B, H = c.hidden;
+    hipStream_t st = e->st;
     HIP_TRY(launch_embed(e->embed, e->d_tokens, e->d_valid, B, H, e->x, st));
     for (int l = 0; l < c.n_layers; ++l) {
         HIP_TRY(launch_rmsnorm(e->x, l ? e->p_down : nullptr, l ? p.down.S : 0, (long long)B * H, B, H,
                                e->attn_norm[l], c.rms_eps, e->h, st));
-        GemmShape g1{B, nqkv, H, p.qkv.S, p.qkv.Kc, p.mt};
-        HIP_TRY(launch_gemm(e->h, H, e->w_qkv[l], g1, e->p_qkv, (long long)B * nqkv, nqkv, st));
-        HIP_TRY(launch_qkv_post(e->p_qkv, p.qkv.S, (long long)B * nqkv, B, e->d_valid, e->d_seq, nullptr, -1, nq,
-                                nkv, d, e->rope, e->q, e->kc[l], e->vc[l], e->view, st));
-        HIP_TRY(launch_attn_split(e->q, B, e->d_valid, e->d_seq, nullptr, -1, nq, nkv, d, e->kc[l], e->vc[l],
-                                  e->view, p.chunk, p.max_splits, e->attn_ws, st));
-        HIP_TRY(launch_attn_merge(e->attn_ws, B, e->d_valid, e->d_seq, nq, nkv, d, p.chunk, p.max_splits, e->o,
-                                  st));
-        GemmShape g2{B, H, nq * d, p.o.S, p.o.Kc, p.mt};
-        HIP_TRY(launch_gemm(e->o, nq * d, e->w_o[l], g2, e->p_o, (long long)B * H, H, st));
-        HIP_TRY(launch_rmsnorm(e->x, e->p_o, p.o.S, (long long)B * H, B, H, e->mlp_norm[l], c.rms_eps, e->h, st));
-        GemmShape g3{B, 2 * F, H, p.gu.S, p.gu.Kc, p.mt};
-        HIP_TRY(launch_gemm(e->h, H, e->w_gu[l], g3, e->p_gu, (long long)B * 2 * F, 2 * F, st));
-        HIP_TRY(launch_swiglu(e->p_gu, p.gu.S, (long long)B * 2 * F, B, F, e->a, F, st));
-        GemmShape g4{B, H, F, p.down.S, p.down.Kc, p.mt};
-        HIP_TRY(launch_gemm(e->a, F, e->w_down[l], g4, e->p_down, (long long)B * H, H, st));
+        for (int k : {CORUN_K_QKV_GEMM, CORUN_K_QKV_POST, CORUN_K_ATTN_SPLIT, CORUN_K_ATTN_MERGE, CORUN_K_O_GEMM,
+                      CORUN_K_RMSNORM, CORUN_K_GATE_UP_GEMM, CORUN_K_SWIGLU, CORUN_K_DOWN_GEMM})
+            ST_TRY(launch_one(e, k, l));
     }
     HIP_TRY(launch_rmsnorm(e->x, e->p_down, p.down.S, (long long)B * H, B, H, e->final_norm, c.rms_eps, e->h, st));
-    if (p.lm.S == 1) {
-        GemmShape gl{B, c.vocab, H, 1, p.lm.Kc, p.mt};
-        HIP_TRY(launch_gemm(e->h, H, e->lm_head, gl, e->logits, 0, c.vocab, st));
-    } else {   // test aid only: a split lm_head reduced by the feed-forward split kernel's sum
-        GemmShape gl{B, c.vocab, H, p.lm.S, p.lm.Kc, p.mt};
-        HIP_TRY(launch_gemm(e->h, H, e->lm_head, gl, e->p_lm, (long long)B * c.vocab, c.vocab, st));
-        HIP_TRY(launch_reduce_splits(e->p_lm, p.lm.S, (long long)B * c.vocab, (long long)B * c.vocab, e->logits, st));
-    }
-    HIP_TRY(launch_argmax(e->logits, B, c.vocab, e->d_valid, e->d_next, st));
+    ST_TRY(launch_one(e, CORUN_K_LM_HEAD, 0));
+    ST_TRY(launch_one(e, CORUN_K_ARGMAX, 0));
     HIP_TRY(launch_feedback(e->d_tokens, e->d_seq, e->d_valid, e->d_next, B, e->d_hist, e->d_counter, e->hist_cap,
                             st));
     return CORUN_OK;
@@ -390,6 +458,7 @@ static corun_status alloc_prefill(corun_engine *e)
     cv.take(&e->pf_hlast, (size_t)64 * H);
     cv.take(&e->pf_pos, (size_t)L);
     cv.take(&e->pf_tok, (size_t)L);
+    cv.take(&e->pf_amax, (size_t)gemm_col_blocks(c.vocab));
     size_t total = cv.take(&e->pf_next, 16);
     e->pws_bytes = total;
     HIP_TRY(hipMalloc(&e->pws, total));
@@ -397,7 +466,7 @@ static corun_status alloc_prefill(corun_engine *e)
     rebase(e->pf_x, e->pws); rebase(e->pf_part, e->pws); rebase(e->pf_attn, e->pws);
     rebase(e->pf_logits, e->pws); rebase(e->pf_h, e->pws); rebase(e->pf_q, e->pws);
     rebase(e->pf_o, e->pws); rebase(e->pf_a, e->pws); rebase(e->pf_hlast, e->pws);
-    rebase(e->pf_pos, e->pws); rebase(e->pf_tok, e->pws); rebase(e->pf_next, e->pws);
+    rebase(e->pf_pos, e->pws); rebase(e->pf_tok, e->pws); rebase(e->pf_amax, e->pws); rebase(e->pf_next, e->pws);
     HIP_TRY(launch_iota(e->pf_pos, L, e->st));
     return CORUN_OK;
 }
@@ -418,6 +487,8 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     if (o.attn_chunk < 0 || o.attn_chunk % 64 != 0 || o.attn_chunk > 1024)
         return fail(CORUN_E_INVAL, "attn_chunk must be a multiple of 64 in [64, 1024]");
     if (o.max_prefill_len < 0) return fail(CORUN_E_INVAL, "negative max_prefill_len");
+    if (!(o.gemm_bm == 0 || o.gemm_bm == 64 || o.gemm_bm == 128 || o.gemm_bm == 256))
+        return fail(CORUN_E_INVAL, "gemm_bm must be 0, 64, 128 or 256");
 
     corun_engine *e = new corun_engine();
     e->c = *cfg;
@@ -475,6 +546,7 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     cv.take(&e->attn_ws, (size_t)B * nkv * p.max_splits * (nq / nkv) * (d + 2));
     cv.take(&e->logits, (size_t)B * cfg->vocab);
     cv.take(&e->p_lm, p.lm.S > 1 ? proj_part_elems(p.lm, B) : 1);
+    cv.take(&e->amax, (size_t)B * gemm_col_blocks(cfg->vocab));
     cv.take(&e->h, (size_t)p.Mp * H);
     cv.take(&e->q, (size_t)B * nq * d);
     cv.take(&e->o, (size_t)p.Mp * nq * d);
@@ -485,7 +557,7 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     rebase(e->d_tokens, e->ws); rebase(e->d_seq, e->ws); rebase(e->d_next, e->ws); rebase(e->d_counter, e->ws);
     rebase(e->d_hist, e->ws); rebase(e->d_valid, e->ws); rebase(e->x, e->ws); rebase(e->p_qkv, e->ws);
     rebase(e->p_o, e->ws); rebase(e->p_gu, e->ws); rebase(e->p_down, e->ws); rebase(e->attn_ws, e->ws);
-    rebase(e->logits, e->ws); rebase(e->p_lm, e->ws); rebase(e->h, e->ws); rebase(e->q, e->ws); rebase(e->o, e->ws); rebase(e->a, e->ws);
+    rebase(e->logits, e->ws); rebase(e->p_lm, e->ws); rebase(e->amax, e->ws); rebase(e->h, e->ws); rebase(e->q, e->ws); rebase(e->o, e->ws); rebase(e->a, e->ws);
     rebase(e->rope, e->ws);
     // Rows B..Mp-1 of the MFMA A operands (h, o, a) are read but never
     // stored; start everything at zero, or at NaN when poisoning.
@@ -626,20 +698,18 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
     const int nqkv = (nq + 2 * nkv) * d;
     hipStream_t st = e->st;
     const int cap_rows = std::max(1, e->pf_max / Lp);
-    const Proj pq = choose_proj(nqkv, H, Lp, 0, cap_rows);
-    const Proj po = choose_proj(H, nq * d, Lp, 0, cap_rows);
-    const Proj pg = choose_proj(2 * F, H, Lp, 0, cap_rows);
-    const Proj pd = choose_proj(H, F, Lp, 0, cap_rows);
-    const Proj pl = choose_proj(c.vocab, H, 1, 1, 0);
-    const int mt = mt_for(Lp);
+    const Proj pq = choose_proj(nqkv, H, Lp, 0, cap_rows, 0);
+    const Proj po = choose_proj(H, nq * d, Lp, 0, cap_rows, 0);
+    const Proj pg = choose_proj(2 * F, H, Lp, 0, cap_rows, 0);
+    const Proj pd = choose_proj(H, F, Lp, 0, cap_rows, 0);
+    const Proj pl = choose_proj(c.vocab, H, 1, 1, 0, 0);
 
     HIP_TRY(hipMemcpyAsync(e->pf_tok, prompt, sizeof(int32_t) * Lp, hipMemcpyHostToDevice, st));
     HIP_TRY(launch_embed(e->embed, e->pf_tok, nullptr, Lp, H, e->pf_x, st));
     for (int l = 0; l < c.n_layers; ++l) {
         HIP_TRY(launch_rmsnorm(e->pf_x, l ? e->pf_part : nullptr, l ? pd.S : 0, (long long)Lp * H, Lp, H,
                                e->attn_norm[l], c.rms_eps, e->pf_h, st));
-        GemmShape g1{Lp, nqkv, H, pq.S, pq.Kc, mt};
-        HIP_TRY(launch_gemm(e->pf_h, H, e->w_qkv[l], g1, e->pf_part, (long long)Lp * nqkv, nqkv, st));
+        HIP_TRY(launch_proj(e->pf_h, H, e->w_qkv[l], shape_of(pq, Lp), e->pf_part, (long long)Lp * nqkv, nqkv, st));
         HIP_TRY(launch_qkv_post(e->pf_part, pq.S, (long long)Lp * nqkv, Lp, nullptr, e->pf_pos, nullptr, slot, nq, nkv,
                                 d, e->rope, e->pf_q, e->kc[l], e->vc[l], e->view, st));
         for (int r0 = 0; r0 < Lp; r0 += e->pf_rows_attn) {
@@ -650,27 +720,52 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
             HIP_TRY(launch_attn_merge(e->pf_attn, nr, nullptr, e->pf_pos + r0, nq, nkv, d, e->pf_chunk,
                                       e->pf_max_splits, e->pf_o + (size_t)r0 * nq * d, st));
         }
-        GemmShape g2{Lp, H, nq * d, po.S, po.Kc, mt};
-        HIP_TRY(launch_gemm(e->pf_o, nq * d, e->w_o[l], g2, e->pf_part, (long long)Lp * H, H, st));
+        HIP_TRY(launch_proj(e->pf_o, nq * d, e->w_o[l], shape_of(po, Lp), e->pf_part, (long long)Lp * H, H, st));
         HIP_TRY(launch_rmsnorm(e->pf_x, e->pf_part, po.S, (long long)Lp * H, Lp, H, e->mlp_norm[l], c.rms_eps,
                                e->pf_h, st));
-        GemmShape g3{Lp, 2 * F, H, pg.S, pg.Kc, mt};
-        HIP_TRY(launch_gemm(e->pf_h, H, e->w_gu[l], g3, e->pf_part, (long long)Lp * 2 * F, 2 * F, st));
+        HIP_TRY(launch_proj(e->pf_h, H, e->w_gu[l], shape_of(pg, Lp), e->pf_part, (long long)Lp * 2 * F, 2 * F, st));
         HIP_TRY(launch_swiglu(e->pf_part, pg.S, (long long)Lp * 2 * F, Lp, F, e->pf_a, F, st));
-        GemmShape g4{Lp, H, F, pd.S, pd.Kc, mt};
-        HIP_TRY(launch_gemm(e->pf_a, F, e->w_down[l], g4, e->pf_part, (long long)Lp * H, H, st));
+        HIP_TRY(launch_proj(e->pf_a, F, e->w_down[l], shape_of(pd, Lp), e->pf_part, (long long)Lp * H, H, st));
     }
     // last position only: fold its down partials, final norm, lm_head, argmax
     const size_t last = (size_t)(Lp - 1) * H;
     HIP_TRY(launch_rmsnorm(e->pf_x + last, e->pf_part + last, pd.S, (long long)Lp * H, 1, H, e->final_norm, c.rms_eps,
                            e->pf_hlast, st));
-    GemmShape gl{1, c.vocab, H, 1, pl.Kc, 1};
-    HIP_TRY(launch_gemm(e->pf_hlast, H, e->lm_head, gl, e->pf_logits, 0, c.vocab, st));
-    HIP_TRY(launch_argmax(e->pf_logits, 1, c.vocab, nullptr, e->pf_next, st));
+    HIP_TRY(launch_proj(e->pf_hlast, H, e->lm_head, shape_of(pl, 1), e->pf_logits, 0, c.vocab, st, e->pf_amax));
+    HIP_TRY(launch_argmax_partials(e->pf_amax, 1, gemm_col_blocks(c.vocab), nullptr, e->pf_next, st));
     HIP_TRY(hipMemcpyAsync(e->h_next, e->pf_next, sizeof(int32_t), hipMemcpyDeviceToHost, st));
     if (last_logits)
         HIP_TRY(hipMemcpyAsync(last_logits, e->pf_logits, sizeof(float) * c.vocab, hipMemcpyDeviceToDevice, st));
     HIP_TRY(hipStreamSynchronize(st));
     *token_out = e->h_next[0];
     return CORUN_OK;
+}
+
+extern "C" corun_status corun_time_kernel(corun_engine *e, int32_t kernel, int32_t layer, int32_t n_iters,
+                                          float *avg_us)
+{
+    if (!e || !avg_us) return fail(CORUN_E_INVAL, "null argument");
+    if (kernel < 0 || kernel >= CORUN_K_COUNT) return fail(CORUN_E_INVAL, "unknown kernel id %d", kernel);
+    if (layer < 0 || layer >= e->c.n_layers) return fail(CORUN_E_INVAL, "layer %d out of range", layer);
+    if (n_iters < 1) return fail(CORUN_E_INVAL, "n_iters must be >= 1");
+    ST_TRY(enter(e));
+    hipEvent_t t0, t1;
+    HIP_TRY(hipEventCreate(&t0));
+    HIP_TRY(hipEventCreate(&t1));
+    corun_status s = launch_one(e, kernel, layer);   // warm-up
+    if (s == CORUN_OK && hipEventRecord(t0, e->st) != hipSuccess) s = fail(CORUN_E_HIP, "event record failed");
+    // cycle through the layers so every launch streams its own weights and
+    // cache from HBM, as in the step (one layer's weights fit the 256 MB
+    // last-level cache, all of them do not)
+    for (int i = 0; s == CORUN_OK && i < n_iters; ++i) s = launch_one(e, kernel, (layer + i) % e->c.n_layers);
+    float ms = 0.f;
+    if (s == CORUN_OK) {
+        if (hipEventRecord(t1, e->st) != hipSuccess || hipEventSynchronize(t1) != hipSuccess ||
+            hipEventElapsedTime(&ms, t0, t1) != hipSuccess)
+            s = fail(CORUN_E_HIP, "event timing failed");
+    }
+    (void)hipEventDestroy(t0);
+    (void)hipEventDestroy(t1);
+    if (s == CORUN_OK) *avg_us = 1000.f * ms / n_iters;
+    return s;
 }

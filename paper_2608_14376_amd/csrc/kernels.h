@@ -21,14 +21,34 @@ hipError_t launch_rmsnorm(float *x, const float *part, int S, long long part_str
 // Projection partials: out[s][m][n] = sum_{k in chunk s} A[m][k] W[n][k]
 // for m < M_store (bf16 MFMA, fp32 accumulate).  A has lda columns and at
 // least roundup(M, 64) readable rows.  K % 8 == 0, N % 16 == 0.
+// Best (value, column) of one row over one wavefront's column block.
+struct ArgBest {
+    float v;
+    int i;
+};
+
 struct GemmShape {
     int M, N, K;
     int S;          // split-K count
     int Kc;         // K elements per split (multiple of 32)
-    int mt;         // 16-row M tiles per wave: 1, 2 or 4
+    int mt;         // skinny kernel: 16-row M tiles per wave: 1, 2 or 4
+    int bm;         // 0 = skinny kernel; 64, 128, 256 = LDS-tiled kernel with this M tile
 };
+// Dispatch on g.bm.
+hipError_t launch_proj(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
+                       long long split_stride, int ldo, hipStream_t st, ArgBest *amax = nullptr);
+// With amax != nullptr (S == 1 only) the epilogue also writes, per row m and
+// column block cb of 64 columns, amax[m * ceil(N / 64) + cb].
 hipError_t launch_gemm(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
-                       long long split_stride, int ldo, hipStream_t st);
+                       long long split_stride, int ldo, hipStream_t st, ArgBest *amax = nullptr);
+// LDS-tiled variant for large M: tiles of bm (64, 128 or 256) x 128, split-K
+// over grid.y, same output contract as launch_gemm (no argmax epilogue).
+hipError_t launch_gemm_tiled(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, int bm, float *out,
+                             long long split_stride, int ldo, hipStream_t st, ArgBest *amax = nullptr);
+inline int gemm_col_blocks(int N) { return (N + 63) / 64; }
+// next[r] = best index over the np column-block partials of row r (-1 for padding rows).
+hipError_t launch_argmax_partials(const ArgBest *part, int rows, int np, const uint8_t *valid, int32_t *next,
+                                  hipStream_t st);
 
 // Reduce QKV partials, round to bf16, rotate q and k by their position,
 // round again, write q (bf16 [rows][nq*d]) and append k, v to the cache.

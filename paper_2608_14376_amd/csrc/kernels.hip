@@ -68,6 +68,16 @@ __device__ __forceinline__ int row_slot(const int32_t *slot_of_row, int slot_con
     return slot_of_row ? slot_of_row[r] : (slot_const >= 0 ? slot_const : r);
 }
 
+// (value, index) under "larger value, then smaller index" is a total order:
+// any tree of these comparisons selects the first index of the maximum.
+__device__ __forceinline__ void better(float &v, int &i, float v2, int i2)
+{
+    if (v2 > v || (v2 == v && i2 < i)) {
+        v = v2;
+        i = i2;
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Embedding gather
 // ---------------------------------------------------------------------------
@@ -91,51 +101,94 @@ hipError_t launch_embed(const uint16_t *E, const int32_t *tokens, const uint8_t 
 
 // ---------------------------------------------------------------------------
 // RMSNorm with the residual add of the previous projection's split partials
-// folded in.  One wavefront per row; lane l owns the float4 groups
-// 4l + 256j.  The sum of squares runs sequentially per lane, then through the
-// fixed butterfly.
+// folded in.  One workgroup of min(H/4, 1024) threads per row; thread j owns
+// the float4 groups 4 (j + nth i), kept in registers (H <= 8192).  Each
+// element adds its partials in split order; the sum of squares runs
+// sequentially per thread, then through a fixed tree: the 64-lane butterfly,
+// then the wavefront sums in wavefront order.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_rmsnorm(float *__restrict__ x, const float *__restrict__ part,
-                                                 int S, long long part_stride, int rows, int H,
-                                                 const uint16_t *__restrict__ g, float eps,
-                                                 uint16_t *__restrict__ h)
+// Fixed-order sum over a block of nw wavefronts: the 64-lane butterfly,
+// then the wavefront sums added in wavefront order.
+__device__ __forceinline__ float block_sum(float v, float *red, int nw)
 {
-    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    if (row >= rows) return;
+    v = wave_sum(v);
+    const int w = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) red[w] = v;
+    __syncthreads();
+    float t = red[0];
+    for (int i = 1; i < nw; ++i) t += red[i];
+    return t;
+}
+
+template <int NG>
+__global__ __launch_bounds__(1024) void k_rmsnorm(float *__restrict__ x, const float *__restrict__ part,
+                                                  int S, long long part_stride, int rows, int H,
+                                                  const uint16_t *__restrict__ g, float eps,
+                                                  uint16_t *__restrict__ h)
+{
+    __shared__ float red[16];
+    const int row = blockIdx.x;
+    const int nth = blockDim.x;
     float *xr = x + (size_t)row * H;
+    const float *pr = part + (size_t)row * H;
+    float4 v[NG];
     float ss = 0.f;
-    for (int i = 4 * lane; i < H; i += 256) {
-        float4 v = *(const float4 *)(xr + i);
-        for (int s = 0; s < S; ++s) {
-            float4 p = *(const float4 *)(part + s * part_stride + (size_t)row * H + i);
-            v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+#pragma unroll
+    for (int j = 0; j < NG; ++j) {
+        const int i = 4 * (threadIdx.x + nth * j);
+        if (i < H) {
+            v[j] = *(const float4 *)(xr + i);
+            // partials are added in split order; their loads are issued in
+            // batches of 8 ahead of the adds
+            int s = 0;
+            for (; s + 8 <= S; s += 8) {
+                float4 p[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) p[u] = *(const float4 *)(pr + (s + u) * part_stride + i);
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    v[j].x += p[u].x; v[j].y += p[u].y; v[j].z += p[u].z; v[j].w += p[u].w;
+                }
+            }
+            for (; s < S; ++s) {
+                const float4 p = *(const float4 *)(pr + s * part_stride + i);
+                v[j].x += p.x; v[j].y += p.y; v[j].z += p.z; v[j].w += p.w;
+            }
+            if (S > 0) *(float4 *)(xr + i) = v[j];
+            ss += v[j].x * v[j].x;
+            ss += v[j].y * v[j].y;
+            ss += v[j].z * v[j].z;
+            ss += v[j].w * v[j].w;
         }
-        if (S > 0) *(float4 *)(xr + i) = v;
-        ss += v.x * v.x;
-        ss += v.y * v.y;
-        ss += v.z * v.z;
-        ss += v.w * v.w;
     }
-    ss = wave_sum(ss);
+    ss = block_sum(ss, red, nth >> 6);
     const float rstd = 1.0f / sqrtf(ss / (float)H + eps);
     uint16_t *hr = h + (size_t)row * H;
-    for (int i = 4 * lane; i < H; i += 256) {
-        float4 v = *(const float4 *)(xr + i);
-        ushort4 o;
-        o.x = f2bf(v.x * rstd * bf2f(g[i + 0]));
-        o.y = f2bf(v.y * rstd * bf2f(g[i + 1]));
-        o.z = f2bf(v.z * rstd * bf2f(g[i + 2]));
-        o.w = f2bf(v.w * rstd * bf2f(g[i + 3]));
-        *(ushort4 *)(hr + i) = o;
+#pragma unroll
+    for (int j = 0; j < NG; ++j) {
+        const int i = 4 * (threadIdx.x + nth * j);
+        if (i < H) {
+            const ushort4 gg = *(const ushort4 *)(g + i);
+            ushort4 o;
+            o.x = f2bf(v[j].x * rstd * bf2f(gg.x));
+            o.y = f2bf(v[j].y * rstd * bf2f(gg.y));
+            o.z = f2bf(v[j].z * rstd * bf2f(gg.z));
+            o.w = f2bf(v[j].w * rstd * bf2f(gg.w));
+            *(ushort4 *)(hr + i) = o;
+        }
     }
 }
 
 hipError_t launch_rmsnorm(float *x, const float *part, int S, long long part_stride, int rows, int H,
                           const uint16_t *g, float eps, uint16_t *h, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_rmsnorm, dim3((rows + 3) / 4), dim3(256), 0, st, x, part, S, part_stride, rows, H,
-                       g, eps, h);
+    if (H % 256 || H > 8192) return hipErrorInvalidValue;
+    const int groups = H / 4;
+    const int nth = groups >= 1024 ? 1024 : groups;        // multiple of 64
+    if (groups <= nth)
+        hipLaunchKernelGGL((k_rmsnorm<1>), dim3(rows), dim3(nth), 0, st, x, part, S, part_stride, rows, H, g, eps, h);
+    else
+        hipLaunchKernelGGL((k_rmsnorm<2>), dim3(rows), dim3(nth), 0, st, x, part, S, part_stride, rows, H, g, eps, h);
     return hipGetLastError();
 }
 
@@ -152,9 +205,48 @@ hipError_t launch_rmsnorm(float *x, const float *part, int S, long long part_str
 // Output lane l holds rows 4 (l / 16) + i, column l % 16 of each tile.
 // ---------------------------------------------------------------------------
 template <int MT, int NT, int KU>
+struct GemmFrags {
+    bf16x8 w[NT][KU];
+    bf16x8 a[MT][KU];
+};
+
+template <int MT, int NT, int KU>
+__device__ __forceinline__ void gemm_load(GemmFrags<MT, NT, KU> &f, const uint16_t *const (&wp)[NT],
+                                          const uint16_t *const (&ap)[MT], const bool (&arow)[MT], int k)
+{
+    const uint4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int u = 0; u < KU; ++u) f.w[nt][u] = __builtin_bit_cast(bf16x8, *(const uint4 *)(wp[nt] + k + 32 * u));
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int u = 0; u < KU; ++u)
+        {
+            uint4 v = z;
+            if (arow[mt]) v = *(const uint4 *)(ap[mt] + k + 32 * u);
+            f.a[mt][u] = __builtin_bit_cast(bf16x8, v);
+        }
+}
+
+template <int MT, int NT, int KU>
+__device__ __forceinline__ void gemm_mma(const GemmFrags<MT, NT, KU> &f, f32x4 (&acc)[MT][NT])
+{
+#pragma unroll
+    for (int u = 0; u < KU; ++u)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[mt][u], f.w[nt][u], acc[mt][nt], 0, 0, 0);
+}
+
+template <int MT, int NT, int KU>
 __global__ __launch_bounds__(256) void k_gemm(const uint16_t *__restrict__ A, int lda,
                                               const uint16_t *__restrict__ W, int M, int N, int K, int Kc,
-                                              float *__restrict__ out, long long split_stride, int ldo)
+                                              float *__restrict__ out, long long split_stride, int ldo,
+                                              ArgBest *__restrict__ amax)
 {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int r = lane & 15, kg = lane >> 4;
@@ -173,8 +265,12 @@ __global__ __launch_bounds__(256) void k_gemm(const uint16_t *__restrict__ A, in
     for (int nt = 0; nt < NT; ++nt)
         wp[nt] = W + (size_t)(n0 + 16 * min(nt, nvalid - 1) + r) * K + kg * 8;
     const uint16_t *ap[MT];
+    bool arow[MT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) ap[mt] = A + (size_t)(m0 + 16 * mt + r) * lda + kg * 8;
+    for (int mt = 0; mt < MT; ++mt) {
+        ap[mt] = A + (size_t)(m0 + 16 * mt + r) * lda + kg * 8;
+        arow[mt] = (m0 + 16 * mt + r) < M;   // rows past M contribute zeros and are never stored
+    }
 
     f32x4 acc[MT][NT];
 #pragma unroll
@@ -182,38 +278,39 @@ __global__ __launch_bounds__(256) void k_gemm(const uint16_t *__restrict__ A, in
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = (f32x4){0.f, 0.f, 0.f, 0.f};
 
+    // Main loop, software-pipelined two deep: the next batch of KU K-steps is
+    // in flight while the current one feeds the MFMAs.
+    constexpr int STEP = 32 * KU;
+    const int nfull = (kend - kbeg) / STEP;
     int k = kbeg;
-    for (; k + 32 * KU <= kend; k += 32 * KU) {
-        bf16x8 wf[NT][KU], af[MT][KU];
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-            for (int u = 0; u < KU; ++u)
-                wf[nt][u] = __builtin_bit_cast(bf16x8, *(const uint4 *)(wp[nt] + k + 32 * u));
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int u = 0; u < KU; ++u)
-                af[mt][u] = __builtin_bit_cast(bf16x8, *(const uint4 *)(ap[mt] + k + 32 * u));
-#pragma unroll
-        for (int u = 0; u < KU; ++u)
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt)
-                    acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[mt][u], wf[nt][u], acc[mt][nt],
-                                                                          0, 0, 0);
+    GemmFrags<MT, NT, KU> f0, f1;
+    if (nfull > 0) gemm_load(f0, wp, ap, arow, k);
+    for (int it = 0; it < nfull; it += 2) {
+        if (it + 1 < nfull) gemm_load(f1, wp, ap, arow, k + STEP);
+        gemm_mma(f0, acc);
+        if (it + 2 < nfull) gemm_load(f0, wp, ap, arow, k + 2 * STEP);
+        if (it + 1 < nfull) gemm_mma(f1, acc);
+        k += 2 * STEP;
     }
+    k = kbeg + nfull * STEP;
     for (; k < kend; k += 32) {   // K tail, one 32-step at a time; K % 8 == 0
         const bool in = (k + kg * 8) < kend;
         const uint4 z = {0u, 0u, 0u, 0u};
         bf16x8 wf[NT], af[MT];
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
-            wf[nt] = __builtin_bit_cast(bf16x8, in ? *(const uint4 *)(wp[nt] + k) : z);
+        {
+            uint4 v = z;
+            if (in) v = *(const uint4 *)(wp[nt] + k);
+            wf[nt] = __builtin_bit_cast(bf16x8, v);
+        }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
-            af[mt] = __builtin_bit_cast(bf16x8, in ? *(const uint4 *)(ap[mt] + k) : z);
+        {
+            uint4 v = z;
+            if (in && arow[mt]) v = *(const uint4 *)(ap[mt] + k);
+            af[mt] = __builtin_bit_cast(bf16x8, v);
+        }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -233,10 +330,208 @@ __global__ __launch_bounds__(256) void k_gemm(const uint16_t *__restrict__ A, in
                 if (row < M) o[(size_t)row * ldo + n0 + 16 * nt + r] = acc[mt][nt][i];
             }
         }
+    if (amax != nullptr) {
+        // per row: best (value, column) over this wavefront's columns -- an
+        // exact selection under the "larger value, then smaller index" order
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float bv = -INFINITY;
+                int bi = 0x7fffffff;
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt)
+                    if (nt < nvalid) better(bv, bi, acc[mt][nt][i], n0 + 16 * nt + r);
+#pragma unroll
+                for (int off = 1; off < 16; off <<= 1) {
+                    const float v2 = __shfl_xor(bv, off, 64);
+                    const int i2 = __shfl_xor(bi, off, 64);
+                    better(bv, bi, v2, i2);
+                }
+                const int row = m0 + 16 * mt + kg * 4 + i;
+                if (r == 0 && row < M) amax[(size_t)row * ncb + cb] = ArgBest{bv, bi};
+            }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Large-M projection (decode at B >= 64, prefill): LDS-tiled bf16 MFMA.
+//
+// Workgroup tile BM x BN, K in steps of 64, four wavefronts in a
+// WAVES_M x WAVES_N grid, each owning (BM/WAVES_M) x (BN/WAVES_N) of the tile
+// as 16x16 MFMA tiles.  Each K step stages A[BM][64] and W[BN][64] in LDS
+// (two stages: the next step's global loads are in flight while the current
+// stage feeds the MFMAs).  LDS rows are padded to 72 elements (144 bytes) so
+// the 16 rows read by one 16-lane group fall on disjoint banks.  Each weight
+// element is read from HBM once per M tile; at BM >= M (decode), exactly
+// once.  Every output element's K reduction runs in the same order: K steps
+// in order, each the MFMA's fixed 32-term dot product chained in order.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int WAVES_M>
+__global__ __launch_bounds__(256) void k_gemm_tiled(const uint16_t *__restrict__ A, int lda,
+                                                    const uint16_t *__restrict__ W, int M, int N, int K, int Kc,
+                                                    float *__restrict__ out, long long split_stride, int ldo,
+                                                    ArgBest *__restrict__ amax)
+{
+    constexpr int BK = 64, LDR = 72;
+    constexpr int WAVES_N = 4 / WAVES_M;
+    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+    constexpr int FM = WM / 16, FN = WN / 16;
+    constexpr int A_LD = BM / 32, W_LD = BN / 32;     // 16-byte loads per thread per stage
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDR];
+    __shared__ __attribute__((aligned(16))) uint16_t Ws[2][BN * LDR];
+
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int num_m = (M + BM - 1) / BM;
+    const int mt = blockIdx.x % num_m, ntile = blockIdx.x / num_m;
+    const int m0 = mt * BM, n0 = ntile * BN;
+    const int s = blockIdx.y;
+    const int kbeg = s * Kc, kend = min(K, kbeg + Kc);
+    const int wm0 = (wave / WAVES_N) * WM, wn0 = (wave % WAVES_N) * WN;
+    const int r16 = lane & 15, kg = lane >> 4;
+
+    // global -> register staging: thread t covers rows t/8 + 32 i, 16 bytes at column (t % 8) * 8
+    const int lrow = tid >> 3, lcol = (tid & 7) * 8;
+    // staging held in vector values (not arrays), so it stays in VGPRs
+    typedef unsigned int stageA_t __attribute__((ext_vector_type(4 * A_LD)));
+    typedef unsigned int stageW_t __attribute__((ext_vector_type(4 * W_LD)));
+    stageA_t ra;
+    stageW_t rw;
+#define CORUN_TILED_GLOAD(k0_)                                                                  \
+    do {                                                                                        \
+        const uint4 z_ = {0u, 0u, 0u, 0u};                                                      \
+        const bool kin_ = ((k0_) + lcol) < kend;                                                \
+        _Pragma("unroll") for (int i_ = 0; i_ < A_LD; ++i_) {                                   \
+            const int row_ = m0 + lrow + 32 * i_;                                               \
+            uint4 v_ = z_;                                                                      \
+            if (kin_ && row_ < M) v_ = *(const uint4 *)(A + (size_t)row_ * lda + (k0_) + lcol); \
+            ra[4 * i_ + 0] = v_.x; ra[4 * i_ + 1] = v_.y; ra[4 * i_ + 2] = v_.z; ra[4 * i_ + 3] = v_.w; \
+        }                                                                                       \
+        _Pragma("unroll") for (int i_ = 0; i_ < W_LD; ++i_) {                                   \
+            const int row_ = n0 + lrow + 32 * i_;                                               \
+            uint4 v_ = z_;                                                                      \
+            if (kin_ && row_ < N) v_ = *(const uint4 *)(W + (size_t)row_ * K + (k0_) + lcol);  \
+            rw[4 * i_ + 0] = v_.x; rw[4 * i_ + 1] = v_.y; rw[4 * i_ + 2] = v_.z; rw[4 * i_ + 3] = v_.w; \
+        }                                                                                       \
+    } while (0)
+#define CORUN_TILED_SSTORE(st_)                                                                 \
+    do {                                                                                        \
+        _Pragma("unroll") for (int i_ = 0; i_ < A_LD; ++i_)                                     \
+            *(uint4 *)(&As[st_][(lrow + 32 * i_) * LDR + lcol]) =                               \
+                (uint4){ra[4 * i_], ra[4 * i_ + 1], ra[4 * i_ + 2], ra[4 * i_ + 3]};            \
+        _Pragma("unroll") for (int i_ = 0; i_ < W_LD; ++i_)                                     \
+            *(uint4 *)(&Ws[st_][(lrow + 32 * i_) * LDR + lcol]) =                               \
+                (uint4){rw[4 * i_], rw[4 * i_ + 1], rw[4 * i_ + 2], rw[4 * i_ + 3]};            \
+    } while (0)
+
+    f32x4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+
+    int cur = 0;
+    if (kbeg < kend) {
+        CORUN_TILED_GLOAD(kbeg);
+        CORUN_TILED_SSTORE(0);
+    }
+    __syncthreads();
+    for (int k0 = kbeg; k0 < kend; k0 += BK) {
+        const bool has_next = k0 + BK < kend;
+        if (has_next) CORUN_TILED_GLOAD(k0 + BK);
+#pragma unroll
+        for (int kk = 0; kk < BK / 32; ++kk) {
+            bf16x8 af[FM], wf[FN];
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+                af[i] = *(const bf16x8 *)(&As[cur][(wm0 + 16 * i + r16) * LDR + kk * 32 + kg * 8]);
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                wf[j] = *(const bf16x8 *)(&Ws[cur][(wn0 + 16 * j + r16) * LDR + kk * 32 + kg * 8]);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], wf[j], acc[i][j], 0, 0, 0);
+        }
+        if (has_next) {
+            if (cur) CORUN_TILED_SSTORE(0);
+            else CORUN_TILED_SSTORE(1);
+        }
+        __syncthreads();
+        cur ^= 1;
+    }
+#undef CORUN_TILED_GLOAD
+#undef CORUN_TILED_SSTORE
+
+    float *o = out + (size_t)s * split_stride;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int col = n0 + wn0 + 16 * j + r16;
+            if (col >= N) continue;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int row = m0 + wm0 + 16 * i + kg * 4 + q;
+                if (row < M) o[(size_t)row * ldo + col] = acc[i][j][q];
+            }
+        }
+    if constexpr (WN == 64) {
+        if (amax != nullptr) {   // per row: best over this wavefront's 64 columns (one 64-column block)
+            const int ncb = (N + 63) / 64;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    float bv = -INFINITY;
+                    int bi = 0x7fffffff;
+#pragma unroll
+                    for (int j = 0; j < FN; ++j) {
+                        const int col = n0 + wn0 + 16 * j + r16;
+                        if (col < N) better(bv, bi, acc[i][j][q], col);
+                    }
+#pragma unroll
+                    for (int off = 1; off < 16; off <<= 1) {
+                        const float v2 = __shfl_xor(bv, off, 64);
+                        const int i2 = __shfl_xor(bi, off, 64);
+                        better(bv, bi, v2, i2);
+                    }
+                    const int row = m0 + wm0 + 16 * i + kg * 4 + q;
+                    if (r16 == 0 && row < M && n0 + wn0 < N) amax[(size_t)row * ncb + (n0 + wn0) / 64] = ArgBest{bv, bi};
+                }
+        }
+    }
+}
+
+hipError_t launch_gemm_tiled(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, int bm, float *out,
+                             long long split_stride, int ldo, hipStream_t st, ArgBest *amax)
+{
+    if (amax != nullptr && bm == 64) return hipErrorInvalidValue;   // argmax epilogue needs 64-column wavefront tiles
+    const int num_n = (g.N + 127) / 128;
+    const int num_m = (g.M + bm - 1) / bm;
+    dim3 grid(num_m * num_n, g.S);
+    switch (bm) {
+    case 64:
+        hipLaunchKernelGGL((k_gemm_tiled<64, 128, 1>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+                           split_stride, ldo, amax);
+        break;
+    case 128:
+        hipLaunchKernelGGL((k_gemm_tiled<128, 128, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+                           split_stride, ldo, amax);
+        break;
+    case 256:
+        hipLaunchKernelGGL((k_gemm_tiled<256, 128, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+                           split_stride, ldo, amax);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_gemm(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
-                       long long split_stride, int ldo, hipStream_t st)
+                       long long split_stride, int ldo, hipStream_t st, ArgBest *amax)
 {
     constexpr int NT = 4;
     const int ncb = (g.N + 16 * NT - 1) / (16 * NT);
@@ -245,15 +540,15 @@ hipError_t launch_gemm(const uint16_t *A, int lda, const uint16_t *W, const Gemm
     switch (g.mt) {
     case 1:
         hipLaunchKernelGGL((k_gemm<1, NT, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
-                           split_stride, ldo);
+                           split_stride, ldo, amax);
         break;
     case 2:
         hipLaunchKernelGGL((k_gemm<2, NT, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
-                           split_stride, ldo);
+                           split_stride, ldo, amax);
         break;
     case 4:
         hipLaunchKernelGGL((k_gemm<4, NT, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
-                           split_stride, ldo);
+                           split_stride, ldo, amax);
         break;
     default:
         return hipErrorInvalidValue;
@@ -322,68 +617,99 @@ hipError_t launch_qkv_post(const float *part, int S, long long part_stride, int 
 // Split-KV decode attention.  The split count of a row is
 // ceil((pos + 1) / chunk): a function of the row's own length only, so the
 // split is request-local and the merge order (split index) is fixed.
-// Block (split, kvh, row), one wavefront.  Scores: lane j takes tokens
-// t0 + j + 64 i, each a sequential dot over d.  Softmax statistics: exact
-// max, then a per-lane sequential sum and the fixed butterfly.  P V: lane j
-// owns d/64 output columns and walks the chunk's tokens in order.
+//
+// Block (split, kvh, row): four wavefronts, wavefront w owning the quarter
+// [t0 + w chunk/4, ...) of the chunk.
+//  * Scores S^T = K q^T on MFMA (16 tokens x 16 head slots per tile, the G
+//    real heads in slots 0..G-1): lane l loads 16 bytes of key row
+//    (l % 16) straight from the cache and ends holding tokens 4 (l / 16) + i
+//    of head l % 16.
+//  * Softmax statistics per head over the wavefront's tokens: exact max,
+//    then per-lane sequential sums and the fixed butterfly.
+//  * P V on the vector ALU: lane l owns d/64 output columns and walks the
+//    tokens in order (one coalesced value row per token).
+//  * The four wavefront partials are combined in wavefront order.
 // ---------------------------------------------------------------------------
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
 template <int D, int G>
-__global__ __launch_bounds__(64) void k_attn_split(const uint16_t *__restrict__ q, const uint8_t *__restrict__ valid,
-                                                   const int32_t *__restrict__ pos,
-                                                   const int32_t *__restrict__ slot_of_row, int slot_const,
-                                                   int nq, int nkv, const uint16_t *__restrict__ kc,
-                                                   const uint16_t *__restrict__ vc, KvView kv, int chunk,
-                                                   int max_splits, float *__restrict__ ws)
+__global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__ q, const uint8_t *__restrict__ valid,
+                                                    const int32_t *__restrict__ pos,
+                                                    const int32_t *__restrict__ slot_of_row, int slot_const,
+                                                    int nq, int nkv, const uint16_t *__restrict__ kc,
+                                                    const uint16_t *__restrict__ vc, KvView kv, int chunk,
+                                                    int max_splits, float *__restrict__ ws)
 {
     constexpr int EPL = D / 64;
     const int split = blockIdx.x, kvh = blockIdx.y, r = blockIdx.z;
-    const int lane = threadIdx.x;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     if (valid != nullptr && !valid[r]) return;
     const int n = pos[r] + 1;
     const int t0 = split * chunk;
     if (t0 >= n) return;
     const int t1 = min(n, t0 + chunk);
+    const int sub = chunk >> 2;
+    const int wt0 = t0 + wave * sub;
+    const int wt1 = min(t1, wt0 + sub);
     const int slot = row_slot(slot_of_row, slot_const, r);
 
     extern __shared__ float smem[];
-    float *qs = smem;            // [G][D]
-    float *sc = smem + G * D;    // [G][chunk]
-    const uint16_t *qr = q + (size_t)r * nq * D + (size_t)kvh * G * D;
-    for (int i = lane; i < G * D; i += 64) qs[i] = bf2f(qr[i]);
-    __syncthreads();
+    float *sc = smem + wave * G * sub;             // [G][sub] scores, then weights
+    float *cm = smem + 4 * G * sub;                // [4][G] wave maxima
+    float *cl = cm + 4 * G;                        // [4][G] wave sums
+    float *ca = cl + 4 * G;                        // [4][G][D] wave accumulators
 
+    // q^T fragments (B operand): lane l supplies head l % 16, dims 32 kk + 8 (l / 16) .. +7
+    const int hl = lane & 15, kg = lane >> 4;
+    bf16x8 qf[D / 32];
+    {
+        const uint16_t *qr = q + (size_t)r * nq * D + ((size_t)kvh * G + hl) * D + kg * 8;
+        const uint4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int kk = 0; kk < D / 32; ++kk)
+        {
+            uint4 v = z;
+            if (hl < G) v = *(const uint4 *)(qr + 32 * kk);
+            qf[kk] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
     const float scale = 1.0f / sqrtf((float)D);
-    for (int t = t0 + lane; t < t1; t += 64) {
-        const uint16_t *kr = kc + kv_offset(kv, nkv, D, slot, kvh, t);
-        float a[G];
+    for (int tb = wt0; tb < wt1; tb += 16) {
+        const int t = tb + hl;
+        const bool tin = t < wt1;
+        const uint16_t *kr = kc + kv_offset(kv, nkv, D, slot, kvh, tin ? t : wt0) + kg * 8;
+        bf16x8 kf[D / 32];
+        const uint4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int g = 0; g < G; ++g) a[g] = 0.f;
+        for (int kk = 0; kk < D / 32; ++kk) {
+            uint4 v = z;
+            if (tin) v = *(const uint4 *)(kr + 32 * kk);
+            kf[kk] = __builtin_bit_cast(bf16x8, v);
+        }
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int e = 0; e < D; e += 8) {
-            uint4 raw = *(const uint4 *)(kr + e);
-            const uint16_t *kv8 = (const uint16_t *)&raw;
+        for (int kk = 0; kk < D / 32; ++kk) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kk], qf[kk], acc, 0, 0, 0);
+        if (hl < G) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const float kf = bf2f(kv8[j]);
-#pragma unroll
-                for (int g = 0; g < G; ++g) a[g] += qs[g * D + e + j] * kf;
+            for (int i = 0; i < 4; ++i) {
+                const int tt = tb + 4 * kg + i;
+                if (tt < wt1) sc[hl * sub + (tt - wt0)] = acc[i] * scale;
             }
         }
-#pragma unroll
-        for (int g = 0; g < G; ++g) sc[g * chunk + (t - t0)] = a[g] * scale;
     }
     __syncthreads();
 
+    const int nt = max(0, wt1 - wt0);
     float mg[G], lg[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
         float m = -INFINITY;
-        for (int t = t0 + lane; t < t1; t += 64) m = fmaxf(m, sc[g * chunk + (t - t0)]);
+        for (int j = lane; j < nt; j += 64) m = fmaxf(m, sc[g * sub + j]);
         m = wave_max(m);
         float l = 0.f;
-        for (int t = t0 + lane; t < t1; t += 64) {
-            const float w = __expf(sc[g * chunk + (t - t0)] - m);
-            sc[g * chunk + (t - t0)] = w;
+        for (int j = lane; j < nt; j += 64) {
+            const float w = __expf(sc[g * sub + j] - m);
+            sc[g * sub + j] = w;
             l += w;
         }
         mg[g] = m;
@@ -396,7 +722,30 @@ __global__ __launch_bounds__(64) void k_attn_split(const uint16_t *__restrict__ 
     for (int g = 0; g < G; ++g)
 #pragma unroll
         for (int j = 0; j < EPL; ++j) acc[g][j] = 0.f;
-    for (int t = t0; t < t1; ++t) {
+    int t = wt0;
+    for (; t + 4 <= wt1; t += 4) {
+        float vf[4][EPL];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const uint16_t *vr = vc + kv_offset(kv, nkv, D, slot, kvh, t + u) + lane * EPL;
+            if constexpr (EPL == 2) {
+                const uint32_t w2 = *(const uint32_t *)vr;
+                vf[u][0] = __uint_as_float(w2 << 16);
+                vf[u][1] = __uint_as_float(w2 & 0xffff0000u);
+            } else {
+                vf[u][0] = bf2f(vr[0]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const float w = sc[g * sub + (t + u - wt0)];
+#pragma unroll
+                for (int j = 0; j < EPL; ++j) acc[g][j] += w * vf[u][j];
+            }
+    }
+    for (; t < wt1; ++t) {
         const uint16_t *vr = vc + kv_offset(kv, nkv, D, slot, kvh, t) + lane * EPL;
         float vf[EPL];
         if constexpr (EPL == 2) {
@@ -408,57 +757,100 @@ __global__ __launch_bounds__(64) void k_attn_split(const uint16_t *__restrict__ 
         }
 #pragma unroll
         for (int g = 0; g < G; ++g) {
-            const float w = sc[g * chunk + (t - t0)];
+            const float w = sc[g * sub + (t - wt0)];
 #pragma unroll
             for (int j = 0; j < EPL; ++j) acc[g][j] += w * vf[j];
         }
     }
-    float *o = ws + (((size_t)r * nkv + kvh) * max_splits + split) * (G * (D + 2));
+
+    // combine the four wavefronts in wavefront order
     if (lane == 0) {
 #pragma unroll
         for (int g = 0; g < G; ++g) {
-            o[g] = mg[g];
-            o[G + g] = lg[g];
+            cm[wave * G + g] = mg[g];
+            cl[wave * G + g] = lg[g];
         }
     }
 #pragma unroll
     for (int g = 0; g < G; ++g)
 #pragma unroll
-        for (int j = 0; j < EPL; ++j) o[2 * G + g * D + lane * EPL + j] = acc[g][j];
+        for (int j = 0; j < EPL; ++j) ca[(wave * G + g) * D + lane * EPL + j] = acc[g][j];
+    __syncthreads();
+    float *o = ws + (((size_t)r * nkv + kvh) * max_splits + split) * (G * (D + 2));
+    for (int idx = threadIdx.x; idx < G * D; idx += 256) {
+        const int g = idx / D;
+        float M = cm[g];
+#pragma unroll
+        for (int w = 1; w < 4; ++w) M = fmaxf(M, cm[w * G + g]);
+        float L = 0.f, A = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const float f = __expf(cm[w * G + g] - M);   // empty wavefronts: exp(-inf) = 0
+            L += cl[w * G + g] * f;
+            A += ca[w * G * D + idx] * f;
+        }
+        o[2 * G + idx] = A;
+        if (idx % D == 0) {
+            o[g] = M;
+            o[G + g] = L;
+        }
+    }
 }
 
+// Merge of a row's splits in split order.  Block (kvh, row), 256 threads.
+// Per head: exact maximum over the splits, weights f_s = exp(m_s - M) in
+// LDS, L = sum_s l_s f_s walked in split order by one thread, and each output
+// element's sum over s walked in split order (loads issued 8 ahead).
 template <int D, int G>
-__global__ __launch_bounds__(64) void k_attn_merge(const float *__restrict__ ws, const uint8_t *__restrict__ valid,
-                                                   const int32_t *__restrict__ pos, int nq, int nkv, int chunk,
-                                                   int max_splits, uint16_t *__restrict__ o)
+__global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ ws, const uint8_t *__restrict__ valid,
+                                                    const int32_t *__restrict__ pos, int nq, int nkv, int chunk,
+                                                    int max_splits, uint16_t *__restrict__ o)
 {
-    constexpr int EPL = D / 64;
-    const int kvh = blockIdx.x, r = blockIdx.y, lane = threadIdx.x;
+    const int kvh = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
     uint16_t *orow = o + (size_t)r * nq * D + (size_t)kvh * G * D;
     if (valid != nullptr && !valid[r]) {
-        for (int i = lane; i < G * D; i += 64) orow[i] = 0;
+        for (int i = tid; i < G * D; i += 256) orow[i] = 0;
         return;
     }
+    extern __shared__ float fs[];          // [G][max_splits] weights, then [G] sums
+    float *Ls = fs + G * max_splits;
+    __shared__ float red[4];
     const int n = pos[r] + 1;
     const int ns = (n + chunk - 1) / chunk;
-    const float *base = ws + ((size_t)r * nkv + kvh) * max_splits * (G * (D + 2));
     const int stride = G * (D + 2);
-#pragma unroll
+    const float *base = ws + ((size_t)r * nkv + kvh) * max_splits * stride;
     for (int g = 0; g < G; ++g) {
-        float M = -INFINITY;
-        for (int s = 0; s < ns; ++s) M = fmaxf(M, base[s * stride + g]);
+        float m = -INFINITY;
+        for (int sp = tid; sp < ns; sp += 256) m = fmaxf(m, base[sp * stride + g]);
+        m = wave_max(m);
+        __syncthreads();
+        if ((tid & 63) == 0) red[tid >> 6] = m;
+        __syncthreads();
+        const float M = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+        for (int sp = tid; sp < ns; sp += 256) fs[g * max_splits + sp] = __expf(base[sp * stride + g] - M);
+    }
+    __syncthreads();
+    if (tid < G) {
         float L = 0.f;
-        float acc[EPL];
+        for (int sp = 0; sp < ns; ++sp) L += base[sp * stride + G + tid] * fs[tid * max_splits + sp];
+        Ls[tid] = L;
+    }
+    __syncthreads();
+    for (int idx = tid; idx < G * D; idx += 256) {
+        const int g = idx / D;
+        const float *a = base + 2 * G + idx;
+        const float *f = fs + g * max_splits;
+        float acc = 0.f;
+        int sp = 0;
+        for (; sp + 8 <= ns; sp += 8) {
+            float v[8];
 #pragma unroll
-        for (int j = 0; j < EPL; ++j) acc[j] = 0.f;
-        for (int s = 0; s < ns; ++s) {
-            const float f = __expf(base[s * stride + g] - M);
-            L += base[s * stride + G + g] * f;
+            for (int u = 0; u < 8; ++u) v[u] = a[(size_t)(sp + u) * stride];
 #pragma unroll
-            for (int j = 0; j < EPL; ++j) acc[j] += base[s * stride + 2 * G + g * D + lane * EPL + j] * f;
+            for (int u = 0; u < 8; ++u) acc += v[u] * f[sp + u];
         }
-#pragma unroll
-        for (int j = 0; j < EPL; ++j) orow[g * D + lane * EPL + j] = f2bf(acc[j] / L);
+        for (; sp < ns; ++sp) acc += a[(size_t)sp * stride] * f[sp];
+        orow[idx] = f2bf(acc / Ls[g]);
     }
 }
 
@@ -467,8 +859,8 @@ static void launch_attn_dg(const uint16_t *q, int rows, const uint8_t *valid, co
                            const int32_t *slot_of_row, int slot_const, int nq, int nkv, const uint16_t *kc,
                            const uint16_t *vc, KvView kv, int chunk, int max_splits, float *ws, hipStream_t st)
 {
-    const size_t shm = sizeof(float) * (G * D + G * chunk);
-    hipLaunchKernelGGL((k_attn_split<D, G>), dim3(max_splits, nkv, rows), dim3(64), shm, st, q, valid, pos,
+    const size_t shm = sizeof(float) * (G * chunk + 8 * G + 4 * G * D);
+    hipLaunchKernelGGL((k_attn_split<D, G>), dim3(max_splits, nkv, rows), dim3(256), shm, st, q, valid, pos,
                        slot_of_row, slot_const, nq, nkv, kc, vc, kv, chunk, max_splits, ws);
 }
 
@@ -476,7 +868,8 @@ template <int D, int G>
 static void launch_merge_dg(const float *ws, int rows, const uint8_t *valid, const int32_t *pos, int nq,
                             int nkv, int chunk, int max_splits, uint16_t *o, hipStream_t st)
 {
-    hipLaunchKernelGGL((k_attn_merge<D, G>), dim3(nkv, rows), dim3(64), 0, st, ws, valid, pos, nq, nkv, chunk,
+    const size_t shm = sizeof(float) * (G * max_splits + G);
+    hipLaunchKernelGGL((k_attn_merge<D, G>), dim3(nkv, rows), dim3(256), shm, st, ws, valid, pos, nq, nkv, chunk,
                        max_splits, o);
 }
 
@@ -572,14 +965,6 @@ hipError_t launch_reduce_splits(const float *part, int S, long long stride, long
 // "larger value, then smaller index" is a total order, so any combining tree
 // gives the same, exact answer.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void better(float &v, int &i, float v2, int i2)
-{
-    if (v2 > v || (v2 == v && i2 < i)) {
-        v = v2;
-        i = i2;
-    }
-}
-
 __global__ __launch_bounds__(256) void k_argmax(const float *__restrict__ logits, int V,
                                                 const uint8_t *__restrict__ valid, int32_t *__restrict__ next)
 {
@@ -609,6 +994,44 @@ __global__ __launch_bounds__(256) void k_argmax(const float *__restrict__ logits
         for (int w = 1; w < 4; ++w) better(bv, bi, sv[w], si[w]);
         next[r] = (bi == 0x7fffffff) ? 0 : bi;
     }
+}
+
+__global__ __launch_bounds__(256) void k_argmax_partials(const ArgBest *__restrict__ part, int np,
+                                                         const uint8_t *__restrict__ valid, int32_t *__restrict__ next)
+{
+    const int r = blockIdx.x;
+    if (valid != nullptr && !valid[r]) {
+        if (threadIdx.x == 0) next[r] = -1;
+        return;
+    }
+    const ArgBest *p = part + (size_t)r * np;
+    float bv = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int i = threadIdx.x; i < np; i += 256) better(bv, bi, p[i].v, p[i].i);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        const float v2 = __shfl_xor(bv, off, 64);
+        const int i2 = __shfl_xor(bi, off, 64);
+        better(bv, bi, v2, i2);
+    }
+    __shared__ float sv[4];
+    __shared__ int si[4];
+    if ((threadIdx.x & 63) == 0) {
+        sv[threadIdx.x >> 6] = bv;
+        si[threadIdx.x >> 6] = bi;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int w = 1; w < 4; ++w) better(bv, bi, sv[w], si[w]);
+        next[r] = (bi == 0x7fffffff) ? 0 : bi;
+    }
+}
+
+hipError_t launch_argmax_partials(const ArgBest *part, int rows, int np, const uint8_t *valid, int32_t *next,
+                                  hipStream_t st)
+{
+    hipLaunchKernelGGL(k_argmax_partials, dim3(rows), dim3(256), 0, st, part, np, valid, next);
+    return hipGetLastError();
 }
 
 hipError_t launch_argmax(const float *logits, int rows, int V, const uint8_t *valid, int32_t *next, hipStream_t st)
@@ -686,6 +1109,13 @@ hipError_t launch_iota(int32_t *p, int n, hipStream_t st)
 {
     hipLaunchKernelGGL(k_iota, dim3((n + 255) / 256), dim3(256), 0, st, p, n);
     return hipGetLastError();
+}
+
+hipError_t launch_proj(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
+                       long long split_stride, int ldo, hipStream_t st, ArgBest *amax)
+{
+    if (g.bm > 0) return launch_gemm_tiled(A, lda, W, g, g.bm, out, split_stride, ldo, st, amax);
+    return launch_gemm(A, lda, W, g, out, split_stride, ldo, st, amax);
 }
 
 }  // namespace corun
