@@ -185,8 +185,11 @@ enum {
     CORUN_K_QKV_POST = 8,     /* QKV epilogue: RoPE + KV append */
     CORUN_K_SWIGLU = 9,       /* SwiGLU epilogue */
     CORUN_K_ARGMAX = 10,      /* greedy argmax */
-    CORUN_K_COUNT = 11
+    CORUN_K_MOE_ROUTER = 11,  /* MoE: router projection, top-k routing and dispatch (3 kernels) */
+    CORUN_K_COUNT = 12
 };
+/* For mixture-of-experts models CORUN_K_GATE_UP_GEMM / CORUN_K_SWIGLU /
+ * CORUN_K_DOWN_GEMM time the grouped expert kernels. */
 
 /* Measurement aid: launch one kernel of the decode step n_iters times back
  * to back on the engine's stream, launch i using layer (layer + i) mod

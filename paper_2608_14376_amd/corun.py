@@ -24,9 +24,9 @@ EXPORTS = ("corun_engine_create", "corun_engine_destroy", "corun_decode_step", "
 
 # kernel ids of corun_time_kernel
 K_QKV_GEMM, K_O_GEMM, K_GATE_UP_GEMM, K_DOWN_GEMM, K_LM_HEAD, K_ATTN_SPLIT, K_ATTN_MERGE, K_RMSNORM, \
-    K_QKV_POST, K_SWIGLU, K_ARGMAX = range(11)
+    K_QKV_POST, K_SWIGLU, K_ARGMAX, K_MOE_ROUTER = range(12)
 KERNEL_NAMES = ("qkv_gemm", "o_gemm", "gate_up_gemm", "down_gemm", "lm_head", "attn_split", "attn_merge",
-                "rmsnorm", "qkv_post", "swiglu", "argmax")
+                "rmsnorm", "qkv_post", "swiglu", "argmax", "moe_router")
 
 
 class ModelCfg(C.Structure):

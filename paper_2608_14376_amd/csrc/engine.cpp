@@ -59,7 +59,8 @@ struct Proj {
 
 struct Plan {
     int B = 0, Mp = 0, mt = 1;
-    Proj qkv, o, gu, down, lm;
+    Proj qkv, o, gu, down, lm, router;
+    int moe_slots = 0;   // tile slots of the expert projections: E + ceil(B top_k / 16)
     int chunk = 0, max_splits = 0;
 };
 
@@ -78,6 +79,7 @@ Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_
     Proj p;
     p.N = N;
     p.K = K;
+    if (N <= 0 || K <= 0 || M <= 0) return p;   // no such projection
     int S, align;
     if (M <= 64 && bm_override <= 0) {
         const int col_waves = (N + 63) / 64;
@@ -133,6 +135,11 @@ Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_
     if (c->n_experts == 0) {
         p.gu = choose_proj(2 * c->ffn, H, B, so, 0, bo);
         p.down = choose_proj(H, c->ffn, B, so, 0, bo);
+    } else {
+        p.router = choose_proj(c->n_experts, H, B, so, 0, bo);
+        p.gu = Proj{2 * c->expert_ffn, H, 1, H, 0};
+        p.down = Proj{H, c->expert_ffn, 1, c->expert_ffn, 0};
+        p.moe_slots = c->n_experts + (B * c->top_k + 15) / 16;
     }
     // lm_head: never split (its epilogue selects the argmax partials) except
     // under the split override test aid; the 64-row tile has no argmax epilogue
@@ -156,7 +163,16 @@ struct corun_engine {
     hipEvent_t ev = nullptr;
 
     const uint16_t *embed = nullptr, *final_norm = nullptr, *lm_head = nullptr;
-    std::vector<const uint16_t *> attn_norm, w_qkv, w_o, mlp_norm, w_gu, w_down;
+    std::vector<const uint16_t *> attn_norm, w_qkv, w_o, mlp_norm, w_gu, w_down, w_router, w_egu, w_edown;
+    bool moe = false;
+    // mixture-of-experts workspace (decode)
+    float *p_router = nullptr, *moe_w = nullptr, *moe_gu = nullptr, *moe_y = nullptr;
+    int32_t *moe_sel = nullptr, *moe_list = nullptr, *moe_tiles = nullptr;
+    uint16_t *moe_act = nullptr;
+    // and prefill
+    float *pf_moe_w = nullptr, *pf_moe_gu = nullptr, *pf_moe_y = nullptr;
+    int32_t *pf_moe_sel = nullptr, *pf_moe_list = nullptr, *pf_moe_tiles = nullptr;
+    uint16_t *pf_moe_act = nullptr;
     std::vector<uint16_t *> kc, vc;
     KvView view{};
 
@@ -207,8 +223,15 @@ extern "C" corun_status corun_check_config(const corun_model_cfg *c, const corun
     if (!(G == 1 || G == 2 || G == 4 || G == 8 || (G == 16 && c->head_dim == 128)))
         return fail(CORUN_E_SHAPE, "unsupported query-group size %d", G);
     if (c->vocab % 16 != 0) return fail(CORUN_E_SHAPE, "vocab must be a multiple of 16");
-    if (c->n_experts != 0) return fail(CORUN_E_SHAPE, "mixture-of-experts layers are not supported by this build");
-    if (c->ffn <= 0 || c->ffn % 16 != 0) return fail(CORUN_E_SHAPE, "ffn must be a positive multiple of 16");
+    if (c->n_experts != 0) {
+        if (c->n_experts < 1 || c->n_experts > 256) return fail(CORUN_E_SHAPE, "n_experts must be in [1, 256]");
+        if (c->top_k < 1 || c->top_k > 16 || c->top_k > c->n_experts)
+            return fail(CORUN_E_SHAPE, "top_k must be in [1, min(16, n_experts)]");
+        if (c->expert_ffn <= 0 || c->expert_ffn % 16 != 0)
+            return fail(CORUN_E_SHAPE, "expert_ffn must be a positive multiple of 16");
+    } else if (c->ffn <= 0 || c->ffn % 16 != 0) {
+        return fail(CORUN_E_SHAPE, "ffn must be a positive multiple of 16");
+    }
     if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f)) return fail(CORUN_E_SHAPE, "bad eps or rope theta");
     if (B <= 0 || B > 1024) return fail(CORUN_E_SHAPE, "B_fixed must be in [1, 1024]");
     if (kv->n_slots < B) return fail(CORUN_E_CAPACITY, "KV cache has %d slots < B_fixed %d", kv->n_slots, B);
@@ -301,6 +324,64 @@ void rebase(T *&p, char *base)
 
 size_t proj_part_elems(const Proj &p, int M) { return (size_t)p.S * M * p.N; }
 
+// Buffers of one mixture-of-experts layer run over `rows` rows.
+struct MoeBufs {
+    const uint8_t *valid;
+    float *router_part, *w, *gu, *y;
+    int32_t *sel, *list, *tiles;
+    uint16_t *act;
+    int slots;
+};
+
+corun_status moe_router(corun_engine *e, const MoeBufs &m, const uint16_t *h, int rows, const Proj &pr, int l)
+{
+    const corun_model_cfg &c = e->c;
+    HIP_TRY(launch_proj(h, c.hidden, e->w_router[l], shape_of(pr, rows), m.router_part, (long long)rows * c.n_experts,
+                        c.n_experts, e->st));
+    HIP_TRY(launch_moe_route(m.router_part, pr.S, (long long)rows * c.n_experts, rows, c.n_experts, c.top_k, m.valid,
+                             m.sel, m.w, e->st));
+    HIP_TRY(launch_moe_dispatch(m.sel, rows * c.top_k, c.n_experts, m.slots, m.list, m.tiles, e->st));
+    return CORUN_OK;
+}
+
+corun_status moe_expert_gate_up(corun_engine *e, const MoeBufs &m, const uint16_t *h, int l)
+{
+    const corun_model_cfg &c = e->c;
+    const int Fe = c.expert_ffn, H = c.hidden;
+    HIP_TRY(launch_moe_gemm(h, H, c.top_k, e->w_egu[l], (long long)2 * Fe * H, 2 * Fe, H, m.list, m.tiles, m.slots,
+                            m.gu, 2 * Fe, e->st));
+    return CORUN_OK;
+}
+
+corun_status moe_expert_down(corun_engine *e, const MoeBufs &m, int l)
+{
+    const corun_model_cfg &c = e->c;
+    const int Fe = c.expert_ffn, H = c.hidden;
+    HIP_TRY(launch_moe_gemm(m.act, Fe, 1, e->w_edown[l], (long long)H * Fe, H, Fe, m.list, m.tiles, m.slots, m.y, H,
+                            e->st));
+    return CORUN_OK;
+}
+
+MoeBufs decode_moe(corun_engine *e)
+{
+    return MoeBufs{e->d_valid, e->p_router, e->moe_w, e->moe_gu, e->moe_y, e->moe_sel, e->moe_list, e->moe_tiles,
+                   e->moe_act, e->plan.moe_slots};
+}
+
+// The residual fold that opens layer l (l = n_layers: the final norm): the
+// previous layer's down-projection partials, or its expert combine.
+MoeFold fold_of(corun_engine *e, const MoeBufs &m, int l)
+{
+    MoeFold f;
+    if (e->moe && l > 0) {
+        f.y = m.y;
+        f.w = m.w;
+        f.valid = m.valid;
+        f.top_k = e->c.top_k;
+    }
+    return f;
+}
+
 // One kernel of layer l of the decode step; the step is these in order.
 corun_status launch_one(corun_engine *e, int which, int l)
 {
@@ -332,17 +413,32 @@ corun_status launch_one(corun_engine *e, int which, int l)
     case CORUN_K_RMSNORM:   // the post-attention norm (folds the O partials)
         HIP_TRY(launch_rmsnorm(e->x, e->p_o, p.o.S, (long long)B * H, B, H, e->mlp_norm[l], c.rms_eps, e->h, st));
         break;
-    case CORUN_K_GATE_UP_GEMM: {
-        HIP_TRY(launch_proj(e->h, H, e->w_gu[l], shape_of(p.gu, B), e->p_gu, (long long)B * 2 * F, 2 * F, st));
+    case CORUN_K_MOE_ROUTER:
+        if (!e->moe) return fail(CORUN_E_STATE, "dense model has no router");
+        ST_TRY(moe_router(e, decode_moe(e), e->h, B, p.router, l));
         break;
-    }
+    case CORUN_K_GATE_UP_GEMM:
+        if (e->moe) {
+            ST_TRY(moe_expert_gate_up(e, decode_moe(e), e->h, l));
+        } else {
+            HIP_TRY(launch_proj(e->h, H, e->w_gu[l], shape_of(p.gu, B), e->p_gu, (long long)B * 2 * F, 2 * F, st));
+        }
+        break;
     case CORUN_K_SWIGLU:
-        HIP_TRY(launch_swiglu(e->p_gu, p.gu.S, (long long)B * 2 * F, B, F, e->a, F, st));
+        if (e->moe) {
+            const int Fe = c.expert_ffn;
+            HIP_TRY(launch_swiglu(e->moe_gu, 1, 0, B * c.top_k, Fe, e->moe_act, Fe, st));
+        } else {
+            HIP_TRY(launch_swiglu(e->p_gu, p.gu.S, (long long)B * 2 * F, B, F, e->a, F, st));
+        }
         break;
-    case CORUN_K_DOWN_GEMM: {
-        HIP_TRY(launch_proj(e->a, F, e->w_down[l], shape_of(p.down, B), e->p_down, (long long)B * H, H, st));
+    case CORUN_K_DOWN_GEMM:
+        if (e->moe) {
+            ST_TRY(moe_expert_down(e, decode_moe(e), l));
+        } else {
+            HIP_TRY(launch_proj(e->a, F, e->w_down[l], shape_of(p.down, B), e->p_down, (long long)B * H, H, st));
+        }
         break;
-    }
     case CORUN_K_LM_HEAD:
         if (p.lm.S == 1) {
             HIP_TRY(launch_proj(e->h, H, e->lm_head, shape_of(p.lm, B), e->logits, 0, c.vocab, st, e->amax));
@@ -372,14 +468,19 @@ corun_status enqueue_step(corun_engine *e)
     const int B = e->B, H = c.hidden;
     hipStream_t st = e->st;
     HIP_TRY(launch_embed(e->embed, e->d_tokens, e->d_valid, B, H, e->x, st));
+    const MoeBufs mb = decode_moe(e);
+    const int dense_S = e->moe ? 0 : p.down.S;
     for (int l = 0; l < c.n_layers; ++l) {
-        HIP_TRY(launch_rmsnorm(e->x, l ? e->p_down : nullptr, l ? p.down.S : 0, (long long)B * H, B, H,
-                               e->attn_norm[l], c.rms_eps, e->h, st));
+        HIP_TRY(launch_rmsnorm(e->x, l ? e->p_down : nullptr, l ? dense_S : 0, (long long)B * H, B, H,
+                               e->attn_norm[l], c.rms_eps, e->h, st, fold_of(e, mb, l)));
         for (int k : {CORUN_K_QKV_GEMM, CORUN_K_QKV_POST, CORUN_K_ATTN_SPLIT, CORUN_K_ATTN_MERGE, CORUN_K_O_GEMM,
-                      CORUN_K_RMSNORM, CORUN_K_GATE_UP_GEMM, CORUN_K_SWIGLU, CORUN_K_DOWN_GEMM})
+                      CORUN_K_RMSNORM})
             ST_TRY(launch_one(e, k, l));
+        if (e->moe) ST_TRY(launch_one(e, CORUN_K_MOE_ROUTER, l));
+        for (int k : {CORUN_K_GATE_UP_GEMM, CORUN_K_SWIGLU, CORUN_K_DOWN_GEMM}) ST_TRY(launch_one(e, k, l));
     }
-    HIP_TRY(launch_rmsnorm(e->x, e->p_down, p.down.S, (long long)B * H, B, H, e->final_norm, c.rms_eps, e->h, st));
+    HIP_TRY(launch_rmsnorm(e->x, e->p_down, dense_S, (long long)B * H, B, H, e->final_norm, c.rms_eps, e->h, st,
+                           fold_of(e, mb, c.n_layers)));
     ST_TRY(launch_one(e, CORUN_K_LM_HEAD, 0));
     ST_TRY(launch_one(e, CORUN_K_ARGMAX, 0));
     HIP_TRY(launch_feedback(e->d_tokens, e->d_seq, e->d_valid, e->d_next, B, e->d_hist, e->d_counter, e->hist_cap,
@@ -439,7 +540,7 @@ static corun_status alloc_prefill(corun_engine *e)
     const int L = e->pf_max, H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn;
     const int nqkv = (nq + 2 * nkv) * d;
     const int Lp64 = (L + 63) / 64 * 64;
-    const int maxN = std::max({nqkv, 2 * F, H});
+    const int maxN = std::max({nqkv, 2 * F, H, c.n_experts});
     // Split-K for prefill is capped so that S * Lp <= pf_max: the partial
     // buffer then holds pf_max rows of the widest projection.
     e->pf_part_elems = (size_t)L * maxN;
@@ -456,6 +557,16 @@ static corun_status alloc_prefill(corun_engine *e)
     cv.take(&e->pf_o, (size_t)Lp64 * nq * d);
     cv.take(&e->pf_a, (size_t)Lp64 * F);
     cv.take(&e->pf_hlast, (size_t)64 * H);
+    if (e->moe) {
+        const size_t na = (size_t)L * c.top_k, Fe = c.expert_ffn;
+        cv.take(&e->pf_moe_w, na);
+        cv.take(&e->pf_moe_gu, na * 2 * Fe);
+        cv.take(&e->pf_moe_y, na * H);
+        cv.take(&e->pf_moe_sel, na);
+        cv.take(&e->pf_moe_list, na);
+        cv.take(&e->pf_moe_tiles, (size_t)3 * (c.n_experts + (na + 15) / 16));
+        cv.take(&e->pf_moe_act, na * Fe);
+    }
     cv.take(&e->pf_pos, (size_t)L);
     cv.take(&e->pf_tok, (size_t)L);
     cv.take(&e->pf_amax, (size_t)gemm_col_blocks(c.vocab));
@@ -466,6 +577,11 @@ static corun_status alloc_prefill(corun_engine *e)
     rebase(e->pf_x, e->pws); rebase(e->pf_part, e->pws); rebase(e->pf_attn, e->pws);
     rebase(e->pf_logits, e->pws); rebase(e->pf_h, e->pws); rebase(e->pf_q, e->pws);
     rebase(e->pf_o, e->pws); rebase(e->pf_a, e->pws); rebase(e->pf_hlast, e->pws);
+    if (e->moe) {
+        rebase(e->pf_moe_w, e->pws); rebase(e->pf_moe_gu, e->pws); rebase(e->pf_moe_y, e->pws);
+        rebase(e->pf_moe_sel, e->pws); rebase(e->pf_moe_list, e->pws); rebase(e->pf_moe_tiles, e->pws);
+        rebase(e->pf_moe_act, e->pws);
+    }
     rebase(e->pf_pos, e->pws); rebase(e->pf_tok, e->pws); rebase(e->pf_amax, e->pws); rebase(e->pf_next, e->pws);
     HIP_TRY(launch_iota(e->pf_pos, L, e->st));
     return CORUN_OK;
@@ -477,9 +593,11 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     if (!out) return fail(CORUN_E_INVAL, "null out");
     *out = nullptr;
     ST_TRY(corun_check_config(cfg, kv, B));
-    if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->attn_norm || !w->w_qkv || !w->w_o ||
-        !w->mlp_norm || !w->w_gate_up || !w->w_down)
+    const bool moe = cfg->n_experts > 0;
+    if (!w || !w->embed || !w->final_norm || !w->lm_head || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm)
         return fail(CORUN_E_INVAL, "missing weight pointer");
+    if (moe ? (!w->w_router || !w->w_exp_gate_up || !w->w_exp_down) : (!w->w_gate_up || !w->w_down))
+        return fail(CORUN_E_INVAL, moe ? "missing expert weight pointer" : "missing feed-forward weight pointer");
     if (!kv->k || !kv->v) return fail(CORUN_E_INVAL, "missing KV pointers");
     if (kv->layout == CORUN_KV_PAGED && !kv->page_table) return fail(CORUN_E_INVAL, "paged cache needs page_table");
     corun_options o{};
@@ -495,6 +613,7 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     e->kv = *kv;
     e->opt = o;
     e->B = B;
+    e->moe = moe;
     e->user = (hipStream_t)stream;
     const int L = cfg->n_layers;
     for (int l = 0; l < L; ++l) {
@@ -502,8 +621,14 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
         e->w_qkv.push_back((const uint16_t *)w->w_qkv[l]);
         e->w_o.push_back((const uint16_t *)w->w_o[l]);
         e->mlp_norm.push_back((const uint16_t *)w->mlp_norm[l]);
-        e->w_gu.push_back((const uint16_t *)w->w_gate_up[l]);
-        e->w_down.push_back((const uint16_t *)w->w_down[l]);
+        if (moe) {
+            e->w_router.push_back((const uint16_t *)w->w_router[l]);
+            e->w_egu.push_back((const uint16_t *)w->w_exp_gate_up[l]);
+            e->w_edown.push_back((const uint16_t *)w->w_exp_down[l]);
+        } else {
+            e->w_gu.push_back((const uint16_t *)w->w_gate_up[l]);
+            e->w_down.push_back((const uint16_t *)w->w_down[l]);
+        }
         e->kc.push_back((uint16_t *)kv->k[l]);
         e->vc.push_back((uint16_t *)kv->v[l]);
     }
@@ -547,6 +672,17 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     cv.take(&e->logits, (size_t)B * cfg->vocab);
     cv.take(&e->p_lm, p.lm.S > 1 ? proj_part_elems(p.lm, B) : 1);
     cv.take(&e->amax, (size_t)B * gemm_col_blocks(cfg->vocab));
+    if (moe) {
+        const size_t na = (size_t)B * cfg->top_k, Fe = cfg->expert_ffn;
+        cv.take(&e->p_router, proj_part_elems(p.router, B));
+        cv.take(&e->moe_w, na);
+        cv.take(&e->moe_gu, na * 2 * Fe);
+        cv.take(&e->moe_y, na * H);
+        cv.take(&e->moe_sel, na);
+        cv.take(&e->moe_list, na);
+        cv.take(&e->moe_tiles, (size_t)3 * p.moe_slots);
+        cv.take(&e->moe_act, na * Fe);
+    }
     cv.take(&e->h, (size_t)p.Mp * H);
     cv.take(&e->q, (size_t)B * nq * d);
     cv.take(&e->o, (size_t)p.Mp * nq * d);
@@ -559,6 +695,10 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     rebase(e->p_o, e->ws); rebase(e->p_gu, e->ws); rebase(e->p_down, e->ws); rebase(e->attn_ws, e->ws);
     rebase(e->logits, e->ws); rebase(e->p_lm, e->ws); rebase(e->amax, e->ws); rebase(e->h, e->ws); rebase(e->q, e->ws); rebase(e->o, e->ws); rebase(e->a, e->ws);
     rebase(e->rope, e->ws);
+    if (moe) {
+        rebase(e->p_router, e->ws); rebase(e->moe_w, e->ws); rebase(e->moe_gu, e->ws); rebase(e->moe_y, e->ws);
+        rebase(e->moe_sel, e->ws); rebase(e->moe_list, e->ws); rebase(e->moe_tiles, e->ws); rebase(e->moe_act, e->ws);
+    }
     // Rows B..Mp-1 of the MFMA A operands (h, o, a) are read but never
     // stored; start everything at zero, or at NaN when poisoning.
     const uint32_t fillv = o.poison_workspace ? 0xFFFFFFFFu : 0u;
@@ -700,15 +840,19 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
     const int cap_rows = std::max(1, e->pf_max / Lp);
     const Proj pq = choose_proj(nqkv, H, Lp, 0, cap_rows, 0);
     const Proj po = choose_proj(H, nq * d, Lp, 0, cap_rows, 0);
-    const Proj pg = choose_proj(2 * F, H, Lp, 0, cap_rows, 0);
-    const Proj pd = choose_proj(H, F, Lp, 0, cap_rows, 0);
+    const Proj pg = e->moe ? Proj{} : choose_proj(2 * F, H, Lp, 0, cap_rows, 0);
+    const Proj pd = e->moe ? Proj{} : choose_proj(H, F, Lp, 0, cap_rows, 0);
     const Proj pl = choose_proj(c.vocab, H, 1, 1, 0, 0);
+    const Proj pr = e->moe ? choose_proj(c.n_experts, H, Lp, 0, cap_rows, 0) : Proj{};
+    const int dense_S = e->moe ? 0 : pd.S;
+    const MoeBufs pmb{nullptr, e->pf_part, e->pf_moe_w, e->pf_moe_gu, e->pf_moe_y, e->pf_moe_sel, e->pf_moe_list,
+                      e->pf_moe_tiles, e->pf_moe_act, e->moe ? c.n_experts + (Lp * c.top_k + 15) / 16 : 0};
 
     HIP_TRY(hipMemcpyAsync(e->pf_tok, prompt, sizeof(int32_t) * Lp, hipMemcpyHostToDevice, st));
     HIP_TRY(launch_embed(e->embed, e->pf_tok, nullptr, Lp, H, e->pf_x, st));
     for (int l = 0; l < c.n_layers; ++l) {
-        HIP_TRY(launch_rmsnorm(e->pf_x, l ? e->pf_part : nullptr, l ? pd.S : 0, (long long)Lp * H, Lp, H,
-                               e->attn_norm[l], c.rms_eps, e->pf_h, st));
+        HIP_TRY(launch_rmsnorm(e->pf_x, l ? e->pf_part : nullptr, l ? dense_S : 0, (long long)Lp * H, Lp, H,
+                               e->attn_norm[l], c.rms_eps, e->pf_h, st, fold_of(e, pmb, l)));
         HIP_TRY(launch_proj(e->pf_h, H, e->w_qkv[l], shape_of(pq, Lp), e->pf_part, (long long)Lp * nqkv, nqkv, st));
         HIP_TRY(launch_qkv_post(e->pf_part, pq.S, (long long)Lp * nqkv, Lp, nullptr, e->pf_pos, nullptr, slot, nq, nkv,
                                 d, e->rope, e->pf_q, e->kc[l], e->vc[l], e->view, st));
@@ -723,14 +867,28 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
         HIP_TRY(launch_proj(e->pf_o, nq * d, e->w_o[l], shape_of(po, Lp), e->pf_part, (long long)Lp * H, H, st));
         HIP_TRY(launch_rmsnorm(e->pf_x, e->pf_part, po.S, (long long)Lp * H, Lp, H, e->mlp_norm[l], c.rms_eps,
                                e->pf_h, st));
-        HIP_TRY(launch_proj(e->pf_h, H, e->w_gu[l], shape_of(pg, Lp), e->pf_part, (long long)Lp * 2 * F, 2 * F, st));
-        HIP_TRY(launch_swiglu(e->pf_part, pg.S, (long long)Lp * 2 * F, Lp, F, e->pf_a, F, st));
-        HIP_TRY(launch_proj(e->pf_a, F, e->w_down[l], shape_of(pd, Lp), e->pf_part, (long long)Lp * H, H, st));
+        if (e->moe) {
+            const int Fe = c.expert_ffn;
+            ST_TRY(moe_router(e, pmb, e->pf_h, Lp, pr, l));
+            ST_TRY(moe_expert_gate_up(e, pmb, e->pf_h, l));
+            HIP_TRY(launch_swiglu(e->pf_moe_gu, 1, 0, Lp * c.top_k, Fe, e->pf_moe_act, Fe, st));
+            ST_TRY(moe_expert_down(e, pmb, l));
+        } else {
+            HIP_TRY(launch_proj(e->pf_h, H, e->w_gu[l], shape_of(pg, Lp), e->pf_part, (long long)Lp * 2 * F, 2 * F,
+                                st));
+            HIP_TRY(launch_swiglu(e->pf_part, pg.S, (long long)Lp * 2 * F, Lp, F, e->pf_a, F, st));
+            HIP_TRY(launch_proj(e->pf_a, F, e->w_down[l], shape_of(pd, Lp), e->pf_part, (long long)Lp * H, H, st));
+        }
     }
     // last position only: fold its down partials, final norm, lm_head, argmax
     const size_t last = (size_t)(Lp - 1) * H;
-    HIP_TRY(launch_rmsnorm(e->pf_x + last, e->pf_part + last, pd.S, (long long)Lp * H, 1, H, e->final_norm, c.rms_eps,
-                           e->pf_hlast, st));
+    MoeFold lf = fold_of(e, pmb, c.n_layers);
+    if (lf.y) {   // the last position's assignments are rows (Lp-1) top_k ..
+        lf.y += (size_t)(Lp - 1) * c.top_k * H;
+        lf.w += (size_t)(Lp - 1) * c.top_k;
+    }
+    HIP_TRY(launch_rmsnorm(e->pf_x + last, e->pf_part + last, dense_S, (long long)Lp * H, 1, H, e->final_norm,
+                           c.rms_eps, e->pf_hlast, st, lf));
     HIP_TRY(launch_proj(e->pf_hlast, H, e->lm_head, shape_of(pl, 1), e->pf_logits, 0, c.vocab, st, e->pf_amax));
     HIP_TRY(launch_argmax_partials(e->pf_amax, 1, gemm_col_blocks(c.vocab), nullptr, e->pf_next, st));
     HIP_TRY(hipMemcpyAsync(e->h_next, e->pf_next, sizeof(int32_t), hipMemcpyDeviceToHost, st));

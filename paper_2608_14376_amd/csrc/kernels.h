@@ -13,10 +13,35 @@ namespace corun {
 hipError_t launch_embed(const uint16_t *E, const int32_t *tokens, const uint8_t *valid, int rows,
                         int H, float *x, hipStream_t st);
 
-// x[b] += sum_{s<S} part[s][b] (fixed order s = 0..S-1), then
-// h[b] = bf16(x[b] * rsqrt(mean(x[b]^2) + eps) * g).  One wavefront per row.
+// Mixture-of-experts combine folded into the next RMSNorm:
+// x[b] += sum_{r < top_k} w[b][r] y[b top_k + r] (rank order) for valid rows.
+struct MoeFold {
+    const float *y = nullptr;       // [rows * top_k][H] expert outputs, fp32
+    const float *w = nullptr;       // [rows][top_k] routing weights
+    const uint8_t *valid = nullptr;
+    int top_k = 0;
+};
+
+// x[b] += sum_{s<S} part[s][b] (fixed order s = 0..S-1) [+ the MoE combine],
+// then h[b] = bf16(x[b] * rsqrt(mean(x[b]^2) + eps) * g).
 hipError_t launch_rmsnorm(float *x, const float *part, int S, long long part_stride, int rows, int H,
-                          const uint16_t *g, float eps, uint16_t *h, hipStream_t st);
+                          const uint16_t *g, float eps, uint16_t *h, hipStream_t st, MoeFold mf = MoeFold{});
+
+// Mixture-of-experts routing: per valid row, top_k experts of the router
+// logits (sum of S split partials [S][rows][E]), ties to the lower id, with
+// renormalised softmax weights; padding rows get sel = -1.
+hipError_t launch_moe_route(const float *part, int S, long long part_stride, int rows, int E, int top_k,
+                            const uint8_t *valid, int32_t *sel, float *wsel, hipStream_t st);
+// Deterministic dispatch of the n_assign = rows * top_k assignments into the
+// fixed pool of n_slots 16-row tiles: list (expert-major, increasing
+// assignment) and tiles[slot] = {expert, first list index, count}.
+hipError_t launch_moe_dispatch(const int32_t *sel, int n_assign, int E, int n_slots, int32_t *list, int32_t *tiles,
+                               hipStream_t st);
+// out[a][n] = sum_k A[a / row_div][k] W_e[n][k] for every listed assignment a
+// of expert e (W_e = W + e * w_expert_stride), one launch over all tile slots.
+hipError_t launch_moe_gemm(const uint16_t *A, int lda, int row_div, const uint16_t *W, long long w_expert_stride, int N,
+                           int K, const int32_t *list, const int32_t *tiles, int n_slots, float *out, int ldo,
+                           hipStream_t st);
 
 // Projection partials: out[s][m][n] = sum_{k in chunk s} A[m][k] W[n][k]
 // for m < M_store (bf16 MFMA, fp32 accumulate).  A has lda columns and at

@@ -124,7 +124,7 @@ template <int NG>
 __global__ __launch_bounds__(1024) void k_rmsnorm(float *__restrict__ x, const float *__restrict__ part,
                                                   int S, long long part_stride, int rows, int H,
                                                   const uint16_t *__restrict__ g, float eps,
-                                                  uint16_t *__restrict__ h)
+                                                  uint16_t *__restrict__ h, MoeFold mf)
 {
     __shared__ float red[16];
     const int row = blockIdx.x;
@@ -154,7 +154,17 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float *__restrict__ x, const f
                 const float4 p = *(const float4 *)(pr + s * part_stride + i);
                 v[j].x += p.x; v[j].y += p.y; v[j].z += p.z; v[j].w += p.w;
             }
-            if (S > 0) *(float4 *)(xr + i) = v[j];
+            if (mf.y != nullptr && (mf.valid == nullptr || mf.valid[row])) {
+                // mixture-of-experts combine: sum_r w_r y_r in rank order, then added
+                float4 c = {0.f, 0.f, 0.f, 0.f};
+                for (int rk = 0; rk < mf.top_k; ++rk) {
+                    const float w = mf.w[(size_t)row * mf.top_k + rk];
+                    const float4 y = *(const float4 *)(mf.y + ((size_t)row * mf.top_k + rk) * H + i);
+                    c.x += w * y.x; c.y += w * y.y; c.z += w * y.z; c.w += w * y.w;
+                }
+                v[j].x += c.x; v[j].y += c.y; v[j].z += c.z; v[j].w += c.w;
+            }
+            if (S > 0 || mf.y != nullptr) *(float4 *)(xr + i) = v[j];
             ss += v[j].x * v[j].x;
             ss += v[j].y * v[j].y;
             ss += v[j].z * v[j].z;
@@ -180,15 +190,17 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float *__restrict__ x, const f
 }
 
 hipError_t launch_rmsnorm(float *x, const float *part, int S, long long part_stride, int rows, int H,
-                          const uint16_t *g, float eps, uint16_t *h, hipStream_t st)
+                          const uint16_t *g, float eps, uint16_t *h, hipStream_t st, MoeFold mf)
 {
     if (H % 256 || H > 8192) return hipErrorInvalidValue;
     const int groups = H / 4;
     const int nth = groups >= 1024 ? 1024 : groups;        // multiple of 64
     if (groups <= nth)
-        hipLaunchKernelGGL((k_rmsnorm<1>), dim3(rows), dim3(nth), 0, st, x, part, S, part_stride, rows, H, g, eps, h);
+        hipLaunchKernelGGL((k_rmsnorm<1>), dim3(rows), dim3(nth), 0, st, x, part, S, part_stride, rows, H, g, eps, h,
+                           mf);
     else
-        hipLaunchKernelGGL((k_rmsnorm<2>), dim3(rows), dim3(nth), 0, st, x, part, S, part_stride, rows, H, g, eps, h);
+        hipLaunchKernelGGL((k_rmsnorm<2>), dim3(rows), dim3(nth), 0, st, x, part, S, part_stride, rows, H, g, eps, h,
+                           mf);
     return hipGetLastError();
 }
 
@@ -1108,6 +1120,243 @@ __global__ void k_iota(int32_t *p, int n)
 hipError_t launch_iota(int32_t *p, int n, hipStream_t st)
 {
     hipLaunchKernelGGL(k_iota, dim3((n + 255) / 256), dim3(256), 0, st, p, n);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Mixture-of-experts layer.
+//
+// Routing (one wavefront per row): the router logits (split partials added in
+// split order), the top_k largest with ties to the lower expert id (exact
+// selections), and weights exp(l_r - l_0) / sum_r' exp(l_r' - l_0) summed in
+// rank order -- the renormalised top_k of a softmax over all experts.
+//
+// Dispatch (one workgroup): assignment a = b top_k + r goes to expert
+// sel[a]; each expert's assignments are listed in increasing a, and the
+// lists are cut into 16-row tiles placed, expert by expert, into a fixed
+// pool of E + ceil(rows top_k / 16) tile slots -- enough for any routing, so
+// no assignment is ever dropped and the launch never depends on the routing.
+// A row's expert result does not depend on the tile or the tile row it lands
+// in: each output element's K reduction runs in one fixed order.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_moe_route(const float *__restrict__ part, int S, long long part_stride,
+                                                  int E, int top_k, const uint8_t *__restrict__ valid,
+                                                  int32_t *__restrict__ sel, float *__restrict__ wsel)
+{
+    const int b = blockIdx.x, lane = threadIdx.x;
+    if (valid != nullptr && !valid[b]) {
+        if (lane < top_k) {
+            sel[(size_t)b * top_k + lane] = -1;
+            wsel[(size_t)b * top_k + lane] = 0.f;
+        }
+        return;
+    }
+    constexpr int EPL = 4;   // E <= 256
+    float l[EPL];
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) {
+        const int e = lane + 64 * j;
+        float v = -INFINITY;
+        if (e < E) {
+            v = 0.f;
+            for (int s = 0; s < S; ++s) v += part[s * part_stride + (size_t)b * E + e];
+        }
+        l[j] = v;
+    }
+    float top_l[16];
+    int top_e[16];
+    for (int r = 0; r < top_k; ++r) {
+        float bv = -INFINITY;
+        int bi = 0x7fffffff;
+#pragma unroll
+        for (int j = 0; j < EPL; ++j)
+            if (lane + 64 * j < E) better(bv, bi, l[j], lane + 64 * j);
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            const float v2 = __shfl_xor(bv, off, 64);
+            const int i2 = __shfl_xor(bi, off, 64);
+            better(bv, bi, v2, i2);
+        }
+        top_l[r] = bv;
+        top_e[r] = bi;
+#pragma unroll
+        for (int j = 0; j < EPL; ++j)
+            if (lane + 64 * j == bi) l[j] = -INFINITY;    // never chosen again (NaN-free logits assumed)
+    }
+    if (lane == 0) {
+        float z = 0.f;
+        float ev[16];
+        for (int r = 0; r < top_k; ++r) {
+            ev[r] = __expf(top_l[r] - top_l[0]);
+            z += ev[r];
+        }
+        for (int r = 0; r < top_k; ++r) {
+            sel[(size_t)b * top_k + r] = top_e[r];
+            wsel[(size_t)b * top_k + r] = ev[r] / z;
+        }
+    }
+}
+
+hipError_t launch_moe_route(const float *part, int S, long long part_stride, int rows, int E, int top_k,
+                            const uint8_t *valid, int32_t *sel, float *wsel, hipStream_t st)
+{
+    if (E > 256 || top_k > 16 || top_k > E) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_moe_route, dim3(rows), dim3(64), 0, st, part, S, part_stride, E, top_k, valid, sel, wsel);
+    return hipGetLastError();
+}
+
+// tiles[slot] = {expert, first list index, count}; count 0 = unused slot.
+__global__ __launch_bounds__(1024) void k_moe_dispatch(const int32_t *__restrict__ sel, int n_assign, int E,
+                                                       int n_slots, int32_t *__restrict__ list,
+                                                       int32_t *__restrict__ tiles)
+{
+    __shared__ int cnt[256], base[256], csel[1024];
+    const int tid = threadIdx.x;
+    for (int e = tid; e < E; e += 1024) cnt[e] = 0;
+    __syncthreads();
+    // per-expert totals (integer counts: order-independent)
+    for (int a = tid; a < n_assign; a += 1024) {
+        const int e = sel[a];
+        if (e >= 0) atomicAdd(&cnt[e], 1);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int off = 0, slot = 0;
+        for (int e = 0; e < E; ++e) {
+            base[e] = off;
+            for (int j = 0; j * 16 < cnt[e]; ++j, ++slot) {
+                tiles[3 * slot + 0] = e;
+                tiles[3 * slot + 1] = off + 16 * j;
+                tiles[3 * slot + 2] = min(16, cnt[e] - 16 * j);
+            }
+            off += cnt[e];
+        }
+        for (; slot < n_slots; ++slot) {
+            tiles[3 * slot + 0] = 0;
+            tiles[3 * slot + 1] = 0;
+            tiles[3 * slot + 2] = 0;
+        }
+    }
+    __syncthreads();
+    // placement in increasing assignment order, one 1024-assignment chunk at a time
+    for (int c0 = 0; c0 < n_assign; c0 += 1024) {
+        const int a = c0 + tid;
+        const int e = a < n_assign ? sel[a] : -1;
+        csel[tid] = e;
+        __syncthreads();
+        if (e >= 0) {
+            int rank = 0;
+            for (int j = 0; j < tid; ++j) rank += (csel[j] == e);
+            list[base[e] + rank] = a;
+        }
+        __syncthreads();
+        if (tid < E) {   // advance each expert's base past this chunk's assignments
+            int c = 0;
+            const int n = min(1024, n_assign - c0);
+            for (int j = 0; j < n; ++j) c += (csel[j] == tid);
+            base[tid] += c;
+        }
+        __syncthreads();
+    }
+}
+
+hipError_t launch_moe_dispatch(const int32_t *sel, int n_assign, int E, int n_slots, int32_t *list, int32_t *tiles,
+                               hipStream_t st)
+{
+    if (E > 256) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_moe_dispatch, dim3(1), dim3(1024), 0, st, sel, n_assign, E, n_slots, list, tiles);
+    return hipGetLastError();
+}
+
+// Expert projection on one 16-row tile of assignments: row r of the tile is
+// assignment list[start + r]; its A row is A[assignment / row_div]; the
+// output row is the assignment.  Same MFMA lane layout and pipelining as
+// k_gemm with one 16-row M tile; no split-K.
+template <int NT, int KU>
+__global__ __launch_bounds__(256) void k_moe_gemm(const uint16_t *__restrict__ A, int lda, int row_div,
+                                                  const uint16_t *__restrict__ Wbase, long long w_expert_stride,
+                                                  int N, int K, const int32_t *__restrict__ list,
+                                                  const int32_t *__restrict__ tiles, float *__restrict__ out, int ldo)
+{
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int r = lane & 15, kg = lane >> 4;
+    const int slot = blockIdx.y;
+    const int cnt = tiles[3 * slot + 2];
+    if (cnt == 0) return;
+    const int expert = tiles[3 * slot + 0], start = tiles[3 * slot + 1];
+    const int ncb = (N + 16 * NT - 1) / (16 * NT);
+    const int cb = blockIdx.x * 4 + wave;
+    if (cb >= ncb) return;
+    const int n0 = cb * 16 * NT;
+    const int nvalid = min(NT, (N - n0) / 16);
+    const uint16_t *W = Wbase + (size_t)expert * w_expert_stride;
+    const bool arow = r < cnt;
+    const int my_a = arow ? list[start + r] : 0;
+    const uint16_t *ap = A + (size_t)(my_a / row_div) * lda + kg * 8;
+    const uint16_t *wp[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) wp[nt] = W + (size_t)(n0 + 16 * min(nt, nvalid - 1) + r) * K + kg * 8;
+    f32x4 acc[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[nt] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    const uint4 z = {0u, 0u, 0u, 0u};
+    int k = 0;
+    for (; k + 32 * KU <= K; k += 32 * KU) {
+        bf16x8 wf[NT][KU], af[KU];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int u = 0; u < KU; ++u) wf[nt][u] = __builtin_bit_cast(bf16x8, *(const uint4 *)(wp[nt] + k + 32 * u));
+#pragma unroll
+        for (int u = 0; u < KU; ++u) {
+            uint4 v = z;
+            if (arow) v = *(const uint4 *)(ap + k + 32 * u);
+            af[u] = __builtin_bit_cast(bf16x8, v);
+        }
+#pragma unroll
+        for (int u = 0; u < KU; ++u)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u], wf[nt][u], acc[nt], 0, 0, 0);
+    }
+    for (; k < K; k += 32) {
+        const bool in = (k + kg * 8) < K;
+        bf16x8 wf[NT], af;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+            uint4 v = z;
+            if (in) v = *(const uint4 *)(wp[nt] + k);
+            wf[nt] = __builtin_bit_cast(bf16x8, v);
+        }
+        {
+            uint4 v = z;
+            if (in && arow) v = *(const uint4 *)(ap + k);
+            af = __builtin_bit_cast(bf16x8, v);
+        }
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf[nt], acc[nt], 0, 0, 0);
+    }
+    // output rows: tile row 4 kg + i holds assignment list[start + 4 kg + i]
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int tr = kg * 4 + i;
+        if (tr < cnt) {
+            const int a = list[start + tr];
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                if (nt < nvalid) out[(size_t)a * ldo + n0 + 16 * nt + r] = acc[nt][i];
+        }
+    }
+}
+
+hipError_t launch_moe_gemm(const uint16_t *A, int lda, int row_div, const uint16_t *W, long long w_expert_stride, int N,
+                           int K, const int32_t *list, const int32_t *tiles, int n_slots, float *out, int ldo,
+                           hipStream_t st)
+{
+    constexpr int NT = 4;
+    const int ncb = (N + 16 * NT - 1) / (16 * NT);
+    hipLaunchKernelGGL((k_moe_gemm<NT, 4>), dim3((ncb + 3) / 4, n_slots), dim3(256), 0, st, A, lda, row_div, W,
+                       w_expert_stride, N, K, list, tiles, out, ldo);
     return hipGetLastError();
 }
 

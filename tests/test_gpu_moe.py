@@ -1,0 +1,134 @@
+"""GPU tests of the mixture-of-experts layer (router, top-k routing,
+drop-free dispatch into fixed tile slots, grouped expert projections,
+rank-order combine) on a small MoE decoder: oracle parity and the
+position-invariance contract."""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_14376_amd import corun
+from paper_2608_14376_amd import workload as wl
+from tests.gpu_helpers import DEV, check_tokens, host_model, oracle_kv, row_rel_err, to_device
+
+pytestmark = pytest.mark.gpu
+
+S_CAP = 160
+TOL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def moe():
+    cfg = wl.config("tiny_moe")
+    Wc = wl.make_weights(cfg, seed=11)
+    return cfg, Wc, to_device(Wc), host_model(Wc)
+
+
+def cache(cfg, B, seed):
+    K, V = wl.make_kv_contiguous(cfg, B, S_CAP, seed)
+    return [k.to(DEV) for k in K], [v.to(DEV) for v in V]
+
+
+@pytest.mark.parametrize("B,seed", [(4, 1), (8, 2), (40, 3)])
+def test_moe_parity_with_oracle(moe, B, seed):
+    cfg, Wc, Wg, m = moe
+    K, V = cache(cfg, B, 200 + seed)
+    okv = oracle_kv(K, V)
+    eng = corun.Engine(cfg, Wg, B, K, V)
+    b = wl.make_batch(B, cfg["vocab"], seed=seed, len_lo=16, len_hi=128)
+    tokens, valid, lens = b.tokens.copy(), b.valid.copy(), b.seq_lens.copy()
+    logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+    near = []
+    for step in range(4):
+        nxt = eng.decode_step(tokens, valid, lens, logits)
+        ref, _ = oracle.decode_batch(m, okv, tokens, valid, lens)
+        gl = logits.cpu().numpy()
+        for r in range(B):
+            if valid[r]:
+                assert row_rel_err(gl[r], ref[r]) <= TOL, (step, r)
+        check_tokens(nxt, ref, gl, valid, near)
+        tokens = np.where(valid == 1, nxt, tokens).astype(np.int32)
+        lens = np.where(valid == 1, lens + 1, lens).astype(np.int32)
+    assert len(near) <= 1, near
+
+
+def test_moe_all_rows_to_the_same_experts(moe):
+    """A zero router ties every expert: every row picks experts 0..top_k-1
+    with weight 1/top_k, so 40 rows put 40 assignments on each of those
+    experts (three 16-row tiles each).  Nothing may be dropped."""
+    cfg, Wc, Wg, m = moe
+    B = 40
+    Wz = to_device(Wc)
+    Wz.w_router = [torch.zeros_like(t) for t in Wz.w_router]
+    Wzc = wl.Weights(**{**Wc.__dict__, "w_router": [torch.zeros_like(t) for t in Wc.w_router]})
+    mz = host_model(Wzc)
+    K, V = cache(cfg, B, 300)
+    okv = oracle_kv(K, V)
+    eng = corun.Engine(cfg, Wz, B, K, V)
+    b = wl.make_batch(B, cfg["vocab"], seed=301, len_lo=16, len_hi=128, n_live=B)
+    logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+    eng.decode_step(b.tokens, b.valid, b.seq_lens, logits)
+    ref, _ = oracle.decode_batch(mz, okv, b.tokens, b.valid, b.seq_lens)
+    gl = logits.cpu().numpy()
+    for r in range(B):
+        assert row_rel_err(gl[r], ref[r]) <= TOL, r
+
+
+def test_moe_invariance_masks_and_permutations(moe):
+    """Each live request's logits and cache bits are identical across all 16
+    occupancy masks and six slot permutations of a B = 4 batch, although the
+    expert tiles it shares change with every mix."""
+    cfg, Wc, Wg, m = moe
+    B = 4
+    r = np.random.default_rng(60)
+    toks = r.integers(0, cfg["vocab"], B).astype(np.int32)
+    lens = r.integers(16, 129, B).astype(np.int32)
+    K0, V0 = cache(cfg, B, 61)
+    K, V = cache(cfg, B, 0)
+    eng = corun.Engine(cfg, Wg, B, K, V)
+    logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+
+    def place(mask, perm):
+        t = np.full(B, 7, np.int32)
+        s = np.full(B, 3, np.int32)
+        v = np.zeros(B, np.uint8)
+        for l in range(cfg["n_layers"]):
+            K[l].view(torch.int16).fill_(-1)
+            V[l].view(torch.int16).fill_(-1)
+        for i in range(B):
+            if mask[i]:
+                t[perm[i]], s[perm[i]], v[perm[i]] = toks[i], lens[i], 1
+                for l in range(cfg["n_layers"]):
+                    K[l][perm[i]].copy_(K0[l][i])
+                    V[l][perm[i]].copy_(V0[l][i])
+        return t, v, s
+
+    eng.decode_step(*place([1] * B, list(range(B))), logits)
+    ref = logits.clone()
+    ref_k = [k.clone() for k in K]
+    perms = list(itertools.permutations(range(B)))[::4]
+    for mask in itertools.product([0, 1], repeat=B):
+        for perm in perms:
+            eng.decode_step(*place(mask, perm), logits)
+            for i in range(B):
+                if mask[i]:
+                    assert torch.equal(logits[perm[i]].view(torch.int32), ref[i].view(torch.int32)), (mask, perm, i)
+                    for l in range(cfg["n_layers"]):
+                        assert torch.equal(K[l][perm[i]].view(torch.int16), ref_k[l][i].view(torch.int16))
+
+
+@pytest.mark.parametrize("Lp", [9, 100])
+def test_moe_prefill_parity(moe, Lp):
+    cfg, Wc, Wg, m = moe
+    K, V = cache(cfg, 4, 400)
+    okv = oracle_kv(K, V)
+    eng = corun.Engine(cfg, Wg, 4, K, V, opt=corun.options(max_prefill_len=S_CAP))
+    prompt = wl.make_prompt(cfg["vocab"], Lp, seed=401)
+    last = torch.empty(cfg["vocab"], dtype=torch.float32, device=DEV)
+    tok = eng.prefill(prompt, 1, last)
+    ref, ref_tok = oracle.prefill(m, okv, 1, prompt)
+    assert row_rel_err(last.cpu().numpy(), ref) <= TOL
+    near = []
+    check_tokens([tok], ref[None], last.cpu().numpy()[None], [1], near)
