@@ -199,8 +199,7 @@ struct corun_engine {
     int pf_max = 0;
     char *pws = nullptr;
     size_t pws_bytes = 0;
-    int pf_rows_attn = 0, pf_chunk = 0, pf_max_splits = 0;
-    float *pf_x = nullptr, *pf_part = nullptr, *pf_attn = nullptr, *pf_logits = nullptr;
+    float *pf_x = nullptr, *pf_part = nullptr, *pf_logits = nullptr;
     uint16_t *pf_h = nullptr, *pf_q = nullptr, *pf_o = nullptr, *pf_a = nullptr, *pf_hlast = nullptr;
     int32_t *pf_pos = nullptr, *pf_tok = nullptr, *pf_next = nullptr;
     ArgBest *pf_amax = nullptr;
@@ -544,13 +543,9 @@ static corun_status alloc_prefill(corun_engine *e)
     // Split-K for prefill is capped so that S * Lp <= pf_max: the partial
     // buffer then holds pf_max rows of the widest projection.
     e->pf_part_elems = (size_t)L * maxN;
-    e->pf_chunk = std::min(256, max_chunk_for_lds(nq / nkv, d));
-    e->pf_max_splits = (L + e->pf_chunk - 1) / e->pf_chunk;
-    e->pf_rows_attn = std::min(L, 1024);
     Carver cv;
     cv.take(&e->pf_x, (size_t)L * H);
     cv.take(&e->pf_part, e->pf_part_elems);
-    cv.take(&e->pf_attn, (size_t)e->pf_rows_attn * nkv * e->pf_max_splits * (nq / nkv) * (d + 2));
     cv.take(&e->pf_logits, (size_t)c.vocab);
     cv.take(&e->pf_h, (size_t)Lp64 * H);
     cv.take(&e->pf_q, (size_t)L * nq * d);
@@ -574,7 +569,7 @@ static corun_status alloc_prefill(corun_engine *e)
     e->pws_bytes = total;
     HIP_TRY(hipMalloc(&e->pws, total));
     HIP_TRY(hipMemsetAsync(e->pws, 0, total, e->st));
-    rebase(e->pf_x, e->pws); rebase(e->pf_part, e->pws); rebase(e->pf_attn, e->pws);
+    rebase(e->pf_x, e->pws); rebase(e->pf_part, e->pws); 
     rebase(e->pf_logits, e->pws); rebase(e->pf_h, e->pws); rebase(e->pf_q, e->pws);
     rebase(e->pf_o, e->pws); rebase(e->pf_a, e->pws); rebase(e->pf_hlast, e->pws);
     if (e->moe) {
@@ -856,14 +851,7 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
         HIP_TRY(launch_proj(e->pf_h, H, e->w_qkv[l], shape_of(pq, Lp), e->pf_part, (long long)Lp * nqkv, nqkv, st));
         HIP_TRY(launch_qkv_post(e->pf_part, pq.S, (long long)Lp * nqkv, Lp, nullptr, e->pf_pos, nullptr, slot, nq, nkv,
                                 d, e->rope, e->pf_q, e->kc[l], e->vc[l], e->view, st));
-        for (int r0 = 0; r0 < Lp; r0 += e->pf_rows_attn) {
-            const int nr = std::min(e->pf_rows_attn, Lp - r0);
-            HIP_TRY(launch_attn_split(e->pf_q + (size_t)r0 * nq * d, nr, nullptr, e->pf_pos + r0, nullptr, slot, nq,
-                                      nkv, d, e->kc[l], e->vc[l], e->view, e->pf_chunk, e->pf_max_splits,
-                                      e->pf_attn, st));
-            HIP_TRY(launch_attn_merge(e->pf_attn, nr, nullptr, e->pf_pos + r0, nq, nkv, d, e->pf_chunk,
-                                      e->pf_max_splits, e->pf_o + (size_t)r0 * nq * d, st));
-        }
+        HIP_TRY(launch_prefill_attn(e->pf_q, Lp, nq, nkv, d, slot, e->kc[l], e->vc[l], e->view, e->pf_o, st));
         HIP_TRY(launch_proj(e->pf_o, nq * d, e->w_o[l], shape_of(po, Lp), e->pf_part, (long long)Lp * H, H, st));
         HIP_TRY(launch_rmsnorm(e->pf_x, e->pf_part, po.S, (long long)Lp * H, Lp, H, e->mlp_norm[l], c.rms_eps,
                                e->pf_h, st));

@@ -100,6 +100,11 @@ hipError_t launch_attn_merge(const float *ws, int rows, const uint8_t *valid, co
                              int nq, int nkv, int d, int chunk, int max_splits, uint16_t *o,
                              hipStream_t st);
 
+// Causal attention of the isolated prefill: q (bf16 [Lp][nq d]) against keys
+// 0..t of `slot` for query position t, o (bf16 [Lp][nq d]).  Sized by Lp only.
+hipError_t launch_prefill_attn(const uint16_t *q, int Lp, int nq, int nkv, int d, int slot, const uint16_t *kc,
+                               const uint16_t *vc, KvView kv, uint16_t *o, hipStream_t st);
+
 // a[m][j] = bf16(silu(bf16(sum_s gate)) * bf16(sum_s up)) over the partials
 // of the [2F] gate/up projection (gate columns first).
 hipError_t launch_swiglu(const float *part, int S, long long part_stride, int rows, int F,

@@ -1360,6 +1360,199 @@ hipError_t launch_moe_gemm(const uint16_t *A, int lda, int row_div, const uint16
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Causal attention of the isolated prefill (flash-style, no split): the
+// prompt runs alone, so any fixed order is allowed; this one computes, for
+// every query, the keys in tiles of 64 in increasing order with the online
+// softmax.
+//
+// Work units of one KV head: (query block of 32 positions for d = 128, 64 for
+// d = 64, one query head of the group).  A workgroup takes four consecutive units (in [block][head] order,
+// latest blocks first) as its four wavefronts, and the four share the key
+// and value tiles staged in LDS: K as [key][dim] rows, V transposed to
+// [dim][key].
+//  * S^T = K q^T on 16x16x32 MFMA: lane l ends holding keys 4 (l / 16) + i of
+//    query l % 16 -- exactly the B operand layout of the 16x16x16 MFMA, so
+//  * O^T += V^T P^T runs on 16x16x16 MFMA with P rounded to bf16, V^T read as
+//    8-byte rows of the transposed tile.
+// Each lane's O^T values belong to one query, so the softmax rescale is a
+// per-lane scalar; the row sum is a per-lane partial reduced across the four
+// 16-lane groups at the end.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void k_prefill_attn(const uint16_t *__restrict__ q, int Lp, int nq, int nkv,
+                                                      int slot, const uint16_t *__restrict__ kc,
+                                                      const uint16_t *__restrict__ vc, KvView kv,
+                                                      uint16_t *__restrict__ o)
+{
+    constexpr int BK = 64, QB = D == 128 ? 32 : 64, QT = QB / 16, KK = D / 32, ET = D / 16;
+    constexpr int KLD = D + 8, VLD = BK + 8;
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[BK * KLD];
+    __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VLD];
+
+    const int G = nq / nkv;
+    const int kvh = blockIdx.y;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int r16 = lane & 15, kg = lane >> 4;
+    const int nqb = (Lp + QB - 1) / QB;
+    const int units = nqb * G;
+    const int u = units - 1 - (blockIdx.x * 4 + wave);          // latest blocks first
+    const bool active = u >= 0;
+    const int qb = active ? u / G : 0, g = active ? u % G : 0;
+    const int hq = kvh * G + g;
+    const int q0 = qb * QB;
+    // the workgroup's key range ends at its latest query (its first unit)
+    const int u_first = units - 1 - blockIdx.x * 4;
+    const int wg_last_q = min(Lp, (u_first / G + 1) * QB) - 1;
+    const int my_last_q = active ? min(Lp, q0 + QB) - 1 : -1;
+
+    // q^T fragments: lane l supplies query q0 + 16 qt + l % 16, dims 32 kk + 8 (l / 16) ..
+    bf16x8 qf[QT][KK];
+    const uint4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+        const int qq = q0 + 16 * qt + r16;
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+            uint4 v = z;
+            if (active && qq < Lp) v = *(const uint4 *)(q + (size_t)qq * nq * D + (size_t)hq * D + 32 * kk + 8 * kg);
+            qf[qt][kk] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+    f32x4 acc[QT][ET];
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+        for (int et = 0; et < ET; ++et) acc[qt][et] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    float mrow[QT], lpart[QT];
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+        mrow[qt] = -INFINITY;
+        lpart[qt] = 0.f;
+    }
+    const float scale = 1.0f / sqrtf((float)D);
+
+    for (int k0 = 0; k0 <= wg_last_q; k0 += BK) {
+        // stage K rows and transposed V of keys k0 .. k0+63
+        __syncthreads();
+        for (int it = threadIdx.x; it < BK * (D / 8); it += 256) {
+            const int key = it / (D / 8), ch = it % (D / 8);
+            uint4 v = z;
+            if (k0 + key < Lp) v = *(const uint4 *)(kc + kv_offset(kv, nkv, D, slot, kvh, k0 + key) + ch * 8);
+            *(uint4 *)(&Ks[key * KLD + ch * 8]) = v;
+        }
+        for (int it = threadIdx.x; it < BK * (D / 8); it += 256) {
+            const int key = it % BK, ch = it / BK;
+            uint4 v = z;
+            if (k0 + key < Lp) v = *(const uint4 *)(vc + kv_offset(kv, nkv, D, slot, kvh, k0 + key) + ch * 8);
+            const uint16_t *e8 = (const uint16_t *)&v;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) Vt[(ch * 8 + j) * VLD + key] = e8[j];
+        }
+        __syncthreads();
+        if (k0 > my_last_q) continue;                 // wave-uniform: all keys of this tile are in our future
+
+        // scores
+        f32x4 st[QT][4];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) st[qt][t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+                const bf16x8 kf = *(const bf16x8 *)(&Ks[(16 * t + r16) * KLD + 32 * kk + 8 * kg]);
+#pragma unroll
+                for (int qt = 0; qt < QT; ++qt)
+                    st[qt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qt][kk], st[qt][t], 0, 0, 0);
+            }
+        // online softmax per query (column l % 16)
+        s16x4 pb[QT][4];
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+            const int qq = q0 + 16 * qt + r16;
+            float mt = -INFINITY;
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int key = k0 + 16 * t + 4 * kg + i;
+                    const float sv = key <= qq ? st[qt][t][i] * scale : -INFINITY;
+                    st[qt][t][i] = sv;
+                    mt = fmaxf(mt, sv);
+                }
+            mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+            mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+            const float mnew = fmaxf(mrow[qt], mt);
+            // a query with no visible key yet in this tile keeps mnew = -inf: its p are 0
+            const float alpha = mnew == -INFINITY ? 1.f : __expf(mrow[qt] - mnew);
+            float ls = 0.f;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                uint16_t pv[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float pe = mnew == -INFINITY ? 0.f : __expf(st[qt][t][i] - mnew);
+                    ls += pe;
+                    pv[i] = f2bf(pe);
+                }
+                pb[qt][t] = (s16x4){(short)pv[0], (short)pv[1], (short)pv[2], (short)pv[3]};
+            }
+            lpart[qt] = lpart[qt] * alpha + ls;
+            mrow[qt] = mnew;
+#pragma unroll
+            for (int et = 0; et < ET; ++et) {
+                acc[qt][et][0] *= alpha;
+                acc[qt][et][1] *= alpha;
+                acc[qt][et][2] *= alpha;
+                acc[qt][et][3] *= alpha;
+            }
+        }
+        // O^T += V^T P^T
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int et = 0; et < ET; ++et) {
+                const s16x4 vf = *(const s16x4 *)(&Vt[(16 * et + r16) * VLD + 16 * t + 4 * kg]);
+#pragma unroll
+                for (int qt = 0; qt < QT; ++qt)
+                    acc[qt][et] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf, pb[qt][t], acc[qt][et], 0, 0, 0);
+            }
+    }
+    if (!active) return;
+    // lane l holds O^T[dim 16 et + 4 kg + i][query l % 16]
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+        float L = lpart[qt];
+        L += __shfl_xor(L, 16, 64);
+        L += __shfl_xor(L, 32, 64);
+        const int qq = q0 + 16 * qt + r16;
+        if (qq >= Lp) continue;
+        uint16_t *orow = o + (size_t)qq * nq * D + (size_t)hq * D;
+#pragma unroll
+        for (int et = 0; et < ET; ++et)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) orow[16 * et + 4 * kg + i] = f2bf(acc[qt][et][i] / L);
+    }
+}
+
+hipError_t launch_prefill_attn(const uint16_t *q, int Lp, int nq, int nkv, int d, int slot, const uint16_t *kc,
+                               const uint16_t *vc, KvView kv, uint16_t *o, hipStream_t st)
+{
+    const int G = nq / nkv;
+    const int qb = d == 128 ? 32 : 64;
+    const int units = ((Lp + qb - 1) / qb) * G;
+    dim3 grid((units + 3) / 4, nkv);
+    if (d == 128)
+        hipLaunchKernelGGL((k_prefill_attn<128>), grid, dim3(256), 0, st, q, Lp, nq, nkv, slot, kc, vc, kv, o);
+    else if (d == 64)
+        hipLaunchKernelGGL((k_prefill_attn<64>), grid, dim3(256), 0, st, q, Lp, nq, nkv, slot, kc, vc, kv, o);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
 hipError_t launch_proj(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
                        long long split_stride, int ldo, hipStream_t st, ArgBest *amax)
 {

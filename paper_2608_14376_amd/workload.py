@@ -40,6 +40,10 @@ CONFIGS = {
     # mixture-of-experts decoder (Qwen3-30B-A3B family shape)
     "moe": dict(n_layers=48, hidden=2048, n_heads=32, n_kv_heads=4, head_dim=128, ffn=0,
                 vocab=151936, n_experts=128, top_k=8, expert_ffn=768, rms_eps=1e-6, rope_theta=1e6),
+    # two-layer decoder with the 8B family's head geometry (d = 128, 4 query
+    # heads per KV head), for oracle parity of the d = 128 kernels
+    "small128": dict(n_layers=2, hidden=512, n_heads=8, n_kv_heads=2, head_dim=128, ffn=1024,
+                     vocab=2048, n_experts=0, top_k=0, expert_ffn=0, rms_eps=1e-6, rope_theta=1e6),
     # small mixture-of-experts decoder for oracle parity
     "tiny_moe": dict(n_layers=2, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64, ffn=0,
                      vocab=1024, n_experts=16, top_k=4, expert_ffn=96, rms_eps=1e-6,
