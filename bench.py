@@ -42,49 +42,90 @@ def log(*a):
 
 def kernel_bytes_flops(cfg, B, lens_live):
     """Algorithmic HBM bytes and flops of one launch of each kernel class
-    (layer-0 launch; per-layer kernels repeat n_layers times per step)."""
+    (layer-0 launch; per-layer kernels repeat n_layers times per step).  A
+    projection moves its weights once, its bf16 input rows and its output
+    rows (bf16 where the next step rounds, fp32 where it is added to the
+    residual); padding rows are counted (padding is the method's cost).
+    Mixture-of-experts projections count every expert's weights: at B = 128
+    with top-8 of 128 experts nearly all experts are touched."""
     from paper_2608_14376_amd import corun
     H, d, nq, nkv, F, V = (cfg[k] for k in ("hidden", "head_dim", "n_heads", "n_kv_heads", "ffn", "vocab"))
+    E, k, Fe = cfg["n_experts"], cfg["top_k"], cfg["expert_ffn"]
     nqkv = (nq + 2 * nkv) * d
 
-    def gemm(N, K, out_bytes):
-        return 2 * N * K + 2 * B * K + out_bytes * B * N, 2 * B * N * K
+    def gemm(N, K, out_bytes, rows=B, mats=1):
+        return 2 * N * K * mats + 2 * rows * K + out_bytes * rows * N, 2 * rows * N * K
 
     kv_read = sum(int(L) + 1 for L in lens_live) * nkv * d * 2 * 2
     n_live = len(lens_live)
     bf = {
         corun.K_QKV_GEMM: gemm(nqkv, H, 2),
         corun.K_O_GEMM: gemm(H, nq * d, 4),
-        corun.K_GATE_UP_GEMM: gemm(2 * F, H, 2),
-        corun.K_DOWN_GEMM: gemm(H, F, 4),
         corun.K_LM_HEAD: gemm(V, H, 4),
         corun.K_ATTN_SPLIT: (kv_read + 2 * n_live * nq * d, 4 * n_live * nq * d * (sum(lens_live) / max(n_live, 1) + 1)),
         corun.K_ATTN_MERGE: (2 * B * nq * d, 0),
         corun.K_RMSNORM: (B * H * 4 * 2 + B * H * 2, 0),
         corun.K_QKV_POST: (B * nqkv * 2 + n_live * 2 * nkv * d * 2, 0),
-        corun.K_SWIGLU: (B * 2 * F * 2 + B * F * 2, 0),
         corun.K_ARGMAX: (B * V * 4, 0),
     }
-    per_step = {k: (cfg["n_layers"] if k not in (corun.K_LM_HEAD, corun.K_ARGMAX) else 1) for k in bf}
+    if E:
+        bf[corun.K_MOE_ROUTER] = gemm(E, H, 4)
+        bf[corun.K_GATE_UP_GEMM] = gemm(2 * Fe, H, 4, rows=n_live * k, mats=E)
+        bf[corun.K_SWIGLU] = (n_live * k * (2 * Fe * 4 + Fe * 2), 0)
+        bf[corun.K_DOWN_GEMM] = gemm(H, Fe, 4, rows=n_live * k, mats=E)
+    else:
+        bf[corun.K_GATE_UP_GEMM] = gemm(2 * F, H, 2)
+        bf[corun.K_SWIGLU] = (B * 2 * F * 2 + B * F * 2, 0)
+        bf[corun.K_DOWN_GEMM] = gemm(H, F, 4)
+    per_step = {kk: (cfg["n_layers"] if kk not in (corun.K_LM_HEAD, corun.K_ARGMAX) else 1) for kk in bf}
     per_step[corun.K_RMSNORM] = 2 * cfg["n_layers"] + 1
     return bf, per_step
 
 
-def run_B(cfg, W, B, args, seeds, measure_kernels):
+def make_paged(cfg, B, lens, extra, seed):
+    """Paged cache sized to the draw: each slot gets ceil((len + extra) / 16)
+    pages from a seeded permutation of the page pool; unused table entries
+    point at page 0."""
+    import torch
+
+    from paper_2608_14376_amd import workload as wl
+    ps = 16
+    need = [(int(L) + extra + ps - 1) // ps for L in lens]
+    mpp = max(need)
+    num_pages = sum(need)
+    perm = np.random.default_rng(seed).permutation(num_pages).astype(np.int32)
+    pt = np.zeros((B, mpp), np.int32)
+    o = 0
+    for b in range(B):
+        pt[b, :need[b]] = perm[o:o + need[b]]
+        o += need[b]
+    K, V = wl.make_kv_paged(cfg, num_pages, ps, seed=2000 + B, device="cuda")
+    return K, V, torch.from_numpy(pt).to("cuda"), ps
+
+
+def run_B(cfg, W, B, args, seeds, measure_kernels, paged=False, len_lo=LEN_LO, len_hi=LEN_HI,
+          log_uniform=False, live_frac=(0.25, 1.0)):
     import torch
 
     from paper_2608_14376_amd import corun
     from paper_2608_14376_amd import workload as wl
 
-    cap = LEN_HI + args.warmup + args.steps + 1
+    extra = args.warmup + args.steps + 1
     t0 = time.time()
-    K, V = wl.make_kv_contiguous(cfg, B, cap, seed=1000 + B, device="cuda")
+    batches = [wl.make_batch(B, cfg["vocab"], seed=sd, len_lo=len_lo, len_hi=len_hi, log_uniform=log_uniform,
+                             live_frac=live_frac) for sd in seeds]
+    if paged:
+        assert len(seeds) == 1, "the paged cache is sized to one draw"
+        K, V, pt, ps = make_paged(cfg, B, np.where(batches[0].valid == 1, batches[0].seq_lens, 0), extra, 3000 + B)
+        eng = corun.Engine(cfg, W, B, K, V, layout=corun.KV_PAGED, page_size=ps, page_table=pt)
+    else:
+        K, V = wl.make_kv_contiguous(cfg, B, len_hi + extra, seed=1000 + B, device="cuda")
+        eng = corun.Engine(cfg, W, B, K, V)
     torch.cuda.synchronize()
-    log(f"[bench] B={B}: KV cache {2 * len(K) * K[0].numel() * 2 / 1e9:.1f} GB filled in {time.time() - t0:.1f}s")
-    eng = corun.Engine(cfg, W, B, K, V)
+    log(f"[bench] {cfg['n_layers']}L H={cfg['hidden']} B={B} {'paged' if paged else 'contiguous'}: KV cache "
+        f"{2 * len(K) * K[0].numel() * 2 / 1e9:.1f} GB ready in {time.time() - t0:.1f}s")
     runs = []
-    for seed in seeds:
-        b = wl.make_batch(B, cfg["vocab"], seed=seed, len_lo=LEN_LO, len_hi=LEN_HI)
+    for sd, b in zip(seeds, batches):
         n_live = int(b.valid.sum())
         eng.decode_run(args.warmup, b.tokens, b.valid, b.seq_lens)
         torch.cuda.synchronize()
@@ -92,19 +133,22 @@ def run_B(cfg, W, B, args, seeds, measure_kernels):
         eng.decode_run(args.steps, b.tokens, b.valid, b.seq_lens)
         torch.cuda.synchronize()
         dt = time.perf_counter() - t
-        runs.append(dict(seed=seed, n_live=n_live, step_ms=1e3 * dt / args.steps,
+        runs.append(dict(seed=sd, n_live=n_live, step_ms=1e3 * dt / args.steps,
                          live_tok_s=n_live * args.steps / dt, slot_tok_s=B * args.steps / dt,
-                         lens=b.seq_lens[b.valid == 1].tolist()))
-        log(f"[bench] B={B} seed={seed} live={n_live} step={runs[-1]['step_ms']:.3f} ms "
+                         lens=b.seq_lens[b.valid == 1].tolist(), batch=b))
+        log(f"[bench] B={B} seed={sd} live={n_live} step={runs[-1]['step_ms']:.3f} ms "
             f"live tok/s={runs[-1]['live_tok_s']:.0f}")
     runs.sort(key=lambda r: r["live_tok_s"])
     med = runs[len(runs) // 2]
+    kv_tok = wl.kv_bytes_per_token(cfg)
     res = dict(B=B, n_live=med["n_live"], step_ms=round(med["step_ms"], 4), live_tok_s=round(med["live_tok_s"], 1),
-               slot_tok_s=round(med["slot_tok_s"], 1), seeds=[r["seed"] for r in runs])
-    kern = None
+               slot_tok_s=round(med["slot_tok_s"], 1), seeds=[r["seed"] for r in runs],
+               mean_context=round(float(np.mean(med["lens"])), 1),
+               step_bytes_algorithmic=int(wl.streamed_weight_params(cfg) * 2 + kv_tok * (sum(med["lens"]) + 2 * len(med["lens"]))))
+    res["step_hbm_frac"] = round(res["step_bytes_algorithmic"] / (med["step_ms"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
     if measure_kernels:
         # re-run the median seed's batch so the workspace holds its state
-        b = wl.make_batch(B, cfg["vocab"], seed=med["seed"], len_lo=LEN_LO, len_hi=LEN_HI)
+        b = med["batch"]
         eng.decode_run(1, b.tokens, b.valid, b.seq_lens)
         bf, per_step = kernel_bytes_flops(cfg, B, med["lens"])
         kern = {}
@@ -126,6 +170,43 @@ def run_B(cfg, W, B, args, seeds, measure_kernels):
         res["kernels"] = kern
     res["_eng"], res["_K"], res["_V"], res["_med"] = eng, K, V, med
     return res
+
+
+def _drop(res):
+    for k in ("_eng", "_K", "_V", "_med"):
+        res.pop(k, None)
+    return res
+
+
+def bench_prefill(cfg, W, lens, args):
+    """Isolated prefill of one prompt per length (the paper's base case),
+    timed end to end through corun_prefill (host prompt in, first token out).
+    Algorithmic flops: 2 Lp (weights) + the causal attention's lower
+    triangle 2 nq d Lp (Lp + 1) per layer."""
+    import torch
+
+    from paper_2608_14376_amd import corun
+    from paper_2608_14376_amd import workload as wl
+    Lmax = max(lens)
+    K, V = wl.make_kv_contiguous(cfg, 1, Lmax, seed=4000, device="cuda")
+    eng = corun.Engine(cfg, W, 1, K, V, opt=corun.options(max_prefill_len=Lmax))
+    H, d, nq, L = cfg["hidden"], cfg["head_dim"], cfg["n_heads"], cfg["n_layers"]
+    w_params = wl.streamed_weight_params(cfg) - cfg["vocab"] * H
+    out = []
+    eng.prefill(wl.make_prompt(cfg["vocab"], 256, seed=1), 0)          # warm-up
+    for Lp in lens:
+        prompt = wl.make_prompt(cfg["vocab"], Lp, seed=Lp)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        eng.prefill(prompt, 0)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t
+        flops = 2 * Lp * w_params + 2 * H * cfg["vocab"] + L * 2 * nq * d * Lp * (Lp + 1)
+        out.append(dict(Lp=Lp, ms=round(1e3 * dt, 3), tok_s=round(Lp / dt, 1),
+                        tflops=round(flops / dt / 1e12, 1), mfma_frac=round(flops / dt / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)))
+        log(f"[bench] prefill Lp={Lp}: {1e3 * dt:.1f} ms, {Lp / dt:.0f} tok/s, {flops / dt / 1e12:.0f} TFLOP/s")
+    eng.close()
+    return out
 
 
 def bitexact_check(cfg, res, n_pairs=2):
@@ -198,6 +279,32 @@ def cpu_baseline(cfg, W, res, budget_s=12.0):
                 host_cpu=_cpu_name())
 
 
+def kernel_source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "kernels.h"):
+        h.update(open(os.path.join(ROOT, "paper_2608_14376_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, B, seed):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary of this workload (FETCH_SIZE and WRITE_SIZE, each scaled by what
+    the counter reads for a plain copy of known size), or None when no
+    summary exists or the kernels have changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_8b_B{B}_seed{seed}.txt")
+    if not os.path.exists(path):
+        return None, None
+    kv = {}
+    for ln in open(path):
+        if ":" in ln and not ln.startswith("#"):
+            k, v = ln.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256_16") != kernel_source_sha():
+        return None, os.path.relpath(path, ROOT) + " (stale: kernels changed since the counters were taken)"
+    return int(float(kv["traffic_bytes_per_launch"])), os.path.relpath(path, ROOT)
+
+
 def _cpu_name():
     try:
         for ln in open("/proc/cpuinfo"):
@@ -216,8 +323,13 @@ def main():
     ap.add_argument("--B", type=int, default=256, help="headline fixed batch size")
     ap.add_argument("--sweep", default="1,8,16,64", help="further fixed batch sizes (comma list, '' for none)")
     ap.add_argument("--seeds", type=int, default=3, help="batch seeds at the headline B (median reported)")
+    ap.add_argument("--first-seed", type=int, default=1, help="first batch seed at the headline B")
     ap.add_argument("--kernel-iters", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the 32B paged, MoE and prefill workloads")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run one plain 1 GiB device copy (reference for HBM traffic counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -239,33 +351,62 @@ def main():
     log(f"[bench] weights {wl.streamed_weight_params(cfg) * 2 / 1e9:.2f} GB streamed per step, "
         f"made in {time.time() - t0:.1f}s")
 
-    head = run_B(cfg, W, args.B, args, seeds=list(range(1, args.seeds + 1)), measure_kernels=True)
+    head = run_B(cfg, W, args.B, args, seeds=list(range(args.first_seed, args.first_seed + args.seeds)),
+                 measure_kernels=True)
     bitexact = bitexact_check(cfg, head)
     log(f"[bench] bit-exact across batch mixes: {bitexact}")
     cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, W, head)
     if cpu:
         log(f"[bench] cpu oracle: {cpu['value']} tok/s on {cpu['cores']} threads")
-    for k in ("_eng", "_K", "_V"):
-        head.pop(k)
-    head.pop("_med")
+    _drop(head)
     torch.cuda.empty_cache()
 
     sweep = []
     for Bs in [int(x) for x in args.sweep.split(",") if x.strip()]:
         if Bs == args.B:
             continue
-        r = run_B(cfg, W, Bs, args, seeds=[1], measure_kernels=True)
-        for k in ("_eng", "_K", "_V", "_med"):
-            r.pop(k)
+        r = _drop(run_B(cfg, W, Bs, args, seeds=[1], measure_kernels=True))
         r.pop("kernels", None)
         sweep.append(r)
         torch.cuda.empty_cache()
 
+    extra = {}
+    if not args.no_extra:
+        # prefill on the same 8B weights
+        extra["prefill_8b"] = bench_prefill(cfg, W, [512, 2048, 8192, 32768], args)
+        del W
+        torch.cuda.empty_cache()
+        # 32B-shaped dense decode at long context on the paged cache
+        c32 = wl.config("32b")
+        W32 = wl.make_weights(c32, seed=0, device="cuda")
+        r32 = run_B(c32, W32, 32, args, seeds=[1], measure_kernels=True, paged=True, len_lo=1024, len_hi=32768,
+                    log_uniform=True, live_frac=(1.0, 1.0))
+        r32["kernels"] = {k: v for k, v in r32["kernels"].items() if k in ("attn_split", "attn_merge", "gate_up_gemm")}
+        extra["decode_32b_paged"] = _drop(r32)
+        del W32
+        torch.cuda.empty_cache()
+        # MoE decode
+        cm = wl.config("moe")
+        Wm = wl.make_weights(cm, seed=0, device="cuda")
+        rm = run_B(cm, Wm, 128, args, seeds=[1], measure_kernels=True)
+        rm["kernels"] = {k: v for k, v in rm["kernels"].items()
+                         if k in ("gate_up_gemm", "down_gemm", "moe_router", "attn_split")}
+        extra["decode_moe"] = _drop(rm)
+        del Wm
+        torch.cuda.empty_cache()
+    if args.calibrate_copy:
+        src = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] calibration copy: 1 GiB read + 1 GiB written")
+
     kern = head["kernels"]
     dom_name, dom = max(kern.items(), key=lambda kv: kv[1]["us"] * kv[1]["per_step"])
+    traffic, traffic_src = measured_traffic(dom_name, args.B, head["seeds"][len(head["seeds"]) // 2])
     roof = dict(kernel=dom_name, bound="hbm", achieved=dom["gbs"], peak=HBM_PEAK_GBS, unit="GB/s",
-                frac=round(dom["gbs"] / HBM_PEAK_GBS, 4), traffic=None,
-                bytes_per_launch=dom["bytes"], us_per_launch=dom["us"])
+                frac=round(dom["gbs"] / HBM_PEAK_GBS, 4), traffic=traffic,
+                bytes_per_launch=dom["bytes"], us_per_launch=dom["us"], traffic_source=traffic_src)
     out = {
         "metric": METRIC,
         "value": head["live_tok_s"],
@@ -287,6 +428,7 @@ def main():
         "bitexact_across_batch_mixes": bitexact,
         "headline": head,
         "sweep": sweep,
+        "extra": extra,
     }
     print(json.dumps(out), flush=True)
 

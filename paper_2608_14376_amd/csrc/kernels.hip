@@ -81,21 +81,24 @@ __device__ __forceinline__ void better(float &v, int &i, float v2, int i2)
 // ---------------------------------------------------------------------------
 // Embedding gather
 // ---------------------------------------------------------------------------
+// Grid: rows x ceil(H / 256) blocks, flattened into x (rows may exceed the
+// 65535 limit of the other grid dimensions in a long prefill).
 __global__ void k_embed(const uint16_t *__restrict__ E, const int32_t *__restrict__ tokens,
                         const uint8_t *__restrict__ valid, int H, float *__restrict__ x)
 {
-    const int b = blockIdx.y;
+    const int nb = (H + 255) / 256;
+    const int b = blockIdx.x / nb;
+    const int i = (blockIdx.x % nb) * 256 + threadIdx.x;
+    if (i >= H) return;
     const int tok = (valid == nullptr || valid[b]) ? tokens[b] : 0;
-    const uint16_t *src = E + (size_t)tok * H;
-    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < H; i += gridDim.x * blockDim.x)
-        x[(size_t)b * H + i] = bf2f(src[i]);
+    x[(size_t)b * H + i] = bf2f(E[(size_t)tok * H + i]);
 }
 
 hipError_t launch_embed(const uint16_t *E, const int32_t *tokens, const uint8_t *valid, int rows, int H,
                         float *x, hipStream_t st)
 {
-    dim3 grid((H + 255) / 256, rows);
-    hipLaunchKernelGGL(k_embed, grid, dim3(256), 0, st, E, tokens, valid, H, x);
+    const long long blocks = (long long)rows * ((H + 255) / 256);
+    hipLaunchKernelGGL(k_embed, dim3((unsigned)blocks), dim3(256), 0, st, E, tokens, valid, H, x);
     return hipGetLastError();
 }
 
@@ -579,7 +582,8 @@ __global__ void k_qkv_post(const float *__restrict__ part, int S, long long part
                            const float2 *__restrict__ rope_tab, uint16_t *__restrict__ q,
                            uint16_t *__restrict__ kc, uint16_t *__restrict__ vc, KvView kv)
 {
-    const int hd = blockIdx.x, r = blockIdx.y, i = threadIdx.x;
+    const int nh = nq + 2 * nkv;
+    const int hd = blockIdx.x % nh, r = blockIdx.x / nh, i = threadIdx.x;
     const int half = d >> 1;
     if (i >= half) return;
     if (valid != nullptr && !valid[r]) return;
@@ -620,7 +624,8 @@ hipError_t launch_qkv_post(const float *part, int S, long long part_stride, int 
                            int d, const float2 *rope_tab, uint16_t *q, uint16_t *kc, uint16_t *vc, KvView kv,
                            hipStream_t st)
 {
-    hipLaunchKernelGGL(k_qkv_post, dim3(nq + 2 * nkv, rows), dim3(64), 0, st, part, S, part_stride, valid, pos,
+    const long long blocks = (long long)rows * (nq + 2 * nkv);
+    hipLaunchKernelGGL(k_qkv_post, dim3((unsigned)blocks), dim3(64), 0, st, part, S, part_stride, valid, pos,
                        slot_of_row, slot_const, nq, nkv, d, rope_tab, q, kc, vc, kv);
     return hipGetLastError();
 }
@@ -933,8 +938,9 @@ hipError_t launch_attn_merge(const float *ws, int rows, const uint8_t *valid, co
 __global__ void k_swiglu(const float *__restrict__ part, int S, long long part_stride, int F,
                          uint16_t *__restrict__ a, int lda)
 {
-    const int r = blockIdx.y;
-    const int j = blockIdx.x * blockDim.x + threadIdx.x;
+    const int nb = (F + 255) / 256;
+    const int r = blockIdx.x / nb;
+    const int j = (blockIdx.x % nb) * 256 + threadIdx.x;
     if (j >= F) return;
     const float *p = part + (size_t)r * 2 * F;
     float gs = 0.f, us = 0.f;
@@ -951,7 +957,8 @@ __global__ void k_swiglu(const float *__restrict__ part, int S, long long part_s
 hipError_t launch_swiglu(const float *part, int S, long long part_stride, int rows, int F, uint16_t *a, int lda,
                          hipStream_t st)
 {
-    hipLaunchKernelGGL(k_swiglu, dim3((F + 255) / 256, rows), dim3(256), 0, st, part, S, part_stride, F, a, lda);
+    const long long blocks = (long long)rows * ((F + 255) / 256);
+    hipLaunchKernelGGL(k_swiglu, dim3((unsigned)blocks), dim3(256), 0, st, part, S, part_stride, F, a, lda);
     return hipGetLastError();
 }
 
