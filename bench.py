@@ -119,7 +119,7 @@ def run_B(cfg, W, B, args, seeds, measure_kernels, paged=False, len_lo=LEN_LO, l
         K, V, pt, ps = make_paged(cfg, B, np.where(batches[0].valid == 1, batches[0].seq_lens, 0), extra, 3000 + B)
         eng = corun.Engine(cfg, W, B, K, V, layout=corun.KV_PAGED, page_size=ps, page_table=pt)
     else:
-        K, V = wl.make_kv_contiguous(cfg, B, len_hi + extra, seed=1000 + B, device="cuda")
+        K, V = wl.make_kv_contiguous(cfg, B, (len_hi + extra + 15) // 16 * 16, seed=1000 + B, device="cuda")
         eng = corun.Engine(cfg, W, B, K, V)
     torch.cuda.synchronize()
     log(f"[bench] {cfg['n_layers']}L H={cfg['hidden']} B={B} {'paged' if paged else 'contiguous'}: KV cache "
@@ -188,7 +188,7 @@ def bench_prefill(cfg, W, lens, args):
     from paper_2608_14376_amd import corun
     from paper_2608_14376_amd import workload as wl
     Lmax = max(lens)
-    K, V = wl.make_kv_contiguous(cfg, 1, Lmax, seed=4000, device="cuda")
+    K, V = wl.make_kv_contiguous(cfg, 1, (Lmax + 15) // 16 * 16, seed=4000, device="cuda")
     eng = corun.Engine(cfg, W, 1, K, V, opt=corun.options(max_prefill_len=Lmax))
     H, d, nq, L = cfg["hidden"], cfg["head_dim"], cfg["n_heads"], cfg["n_layers"]
     w_params = wl.streamed_weight_params(cfg) - cfg["vocab"] * H

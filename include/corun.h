@@ -88,13 +88,18 @@ typedef struct {
 } corun_weights;
 
 /* KV cache: device bf16, caller-owned, borrowed.  k and v are HOST arrays of
- * n_layers DEVICE pointers.
- *  contiguous: each layer is [n_slots, n_kv_heads, max_seq_len, head_dim];
- *  paged:      each layer is [num_pages, n_kv_heads, page_size, head_dim] and
+ * n_layers DEVICE pointers.  Keys are stored by token, values transposed
+ * (by dimension, tokens contiguous) so that attention can feed both to the
+ * matrix cores straight from HBM:
+ *  contiguous: K layer [n_slots, n_kv_heads, max_seq_len, head_dim],
+ *              V layer [n_slots, n_kv_heads, head_dim, max_seq_len];
+ *              max_seq_len a multiple of 16;
+ *  paged:      K layer [num_pages, n_kv_heads, page_size, head_dim],
+ *              V layer [num_pages, n_kv_heads, head_dim, page_size];
  *              page_table (DEVICE int32 [n_slots, max_pages_per_seq]) maps a
- *              slot's token t to page page_table[slot][t / page_size] at row
- *              t % page_size.  Capacity per slot is
- *              max_pages_per_seq * page_size tokens.
+ *              slot's token t to page page_table[slot][t / page_size] at
+ *              position t % page_size; page_size a multiple of 16; capacity
+ *              per slot is max_pages_per_seq * page_size tokens.
  * Slot b of the decode step reads and appends the cache of slot b. */
 typedef struct {
     int32_t layout;                    /* CORUN_KV_CONTIGUOUS | CORUN_KV_PAGED */

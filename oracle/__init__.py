@@ -86,6 +86,9 @@ def lib():
         L.orc_decode_row.restype = C.c_int
         L.orc_decode_row.argtypes = [C.POINTER(_Cfg), C.POINTER(_Weights), C.POINTER(_KV),
                                      C.c_int, C.c_int, C.c_int, C.c_void_p]
+        L.orc_decode_row_margin.restype = C.c_int
+        L.orc_decode_row_margin.argtypes = [C.POINTER(_Cfg), C.POINTER(_Weights), C.POINTER(_KV),
+                                            C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p]
         L.orc_decode_batch.restype = C.c_int
         L.orc_decode_batch.argtypes = [C.POINTER(_Cfg), C.POINTER(_Weights), C.POINTER(_KV), C.c_int,
                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
@@ -210,8 +213,10 @@ class Model:
 
 @dataclass
 class KVCache:
-    """Host KV cache: per-layer uint16 arrays, contiguous [slots, nkv, S, d]
-    or paged [pages, nkv, page_size, d] with an int32 page table."""
+    """Host KV cache: per-layer uint16 arrays.  Keys by token, values
+    transposed: contiguous K [slots, nkv, S, d], V [slots, nkv, d, S]; paged
+    K [pages, nkv, page_size, d], V [pages, nkv, d, page_size] with an int32
+    page table [slots, max_pages_per_seq]."""
     k: list
     v: list
     layout: int = KV_CONTIGUOUS
@@ -268,6 +273,19 @@ def decode_row(m: Model, kv: KVCache, slot: int, token: int, pos: int) -> np.nda
     if rc:
         raise ValueError("oracle rejected the row")
     return logits
+
+
+def decode_row_margin(m: Model, kv: KVCache, slot: int, token: int, pos: int):
+    """decode_row plus the smallest top-k routing margin over the MoE layers
+    (the gap between the k-th and (k+1)-th router logits; inf if dense)."""
+    b = _Bound(m, kv)
+    logits = np.empty(m.cfg["vocab"], np.float64)
+    mg = np.empty(1, np.float64)
+    rc = lib().orc_decode_row_margin(C.byref(b.cfg), C.byref(b.w), C.byref(b.kv), slot, token, pos,
+                                     _ptr(logits), _ptr(mg))
+    if rc:
+        raise ValueError("oracle rejected the row")
+    return logits, float(mg[0])
 
 
 def decode_batch(m: Model, kv: KVCache, tokens, valid, seq_lens):

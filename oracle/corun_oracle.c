@@ -200,25 +200,40 @@ typedef struct {
 
 enum { ORC_KV_CONTIGUOUS = 0, ORC_KV_PAGED = 1 };
 
+/* KV cache layout (the library's contract).  Keys are stored by token,
+ * values transposed (by dimension):
+ *   contiguous: K [slot, kvh, t, d]        V [slot, kvh, d, t]
+ *   paged:      K [page, kvh, t % ps, d]   V [page, kvh, d, t % ps]
+ * with page = page_table[slot, t / ps]. */
 typedef struct {
     int32_t layout;
-    int32_t n_slots, max_seq_len;        /* contiguous: [slot, kvh, t, d] */
-    int32_t page_size, num_pages, max_pages_per_seq;   /* paged: [page, kvh, t % ps, d] */
+    int32_t n_slots, max_seq_len;
+    int32_t page_size, num_pages, max_pages_per_seq;
     uint16_t *const *k;                  /* [L] -> cache */
     uint16_t *const *v;
     const int32_t *page_table;           /* [n_slots, max_pages_per_seq], paged only */
 } orc_kv;
 
-/* Address of the d-vector of (layer, slot, kv head, token position). */
-static uint16_t *kv_row(const orc_cfg *c, const orc_kv *kv, uint16_t *const *base,
-                        int layer, int slot, int kvh, int t)
+/* Address of the key d-vector of (layer, slot, kv head, token position). */
+static uint16_t *k_row(const orc_cfg *c, const orc_kv *kv, int layer, int slot, int kvh, int t)
 {
     int64_t d = c->head_dim;
     if (kv->layout == ORC_KV_PAGED) {
         int32_t page = kv->page_table[(int64_t)slot * kv->max_pages_per_seq + t / kv->page_size];
-        return base[layer] + (((int64_t)page * c->n_kv_heads + kvh) * kv->page_size + t % kv->page_size) * d;
+        return kv->k[layer] + (((int64_t)page * c->n_kv_heads + kvh) * kv->page_size + t % kv->page_size) * d;
     }
-    return base[layer] + (((int64_t)slot * c->n_kv_heads + kvh) * kv->max_seq_len + t) * d;
+    return kv->k[layer] + (((int64_t)slot * c->n_kv_heads + kvh) * kv->max_seq_len + t) * d;
+}
+
+/* Address of value element e of (layer, slot, kv head, token position). */
+static uint16_t *v_elem(const orc_cfg *c, const orc_kv *kv, int layer, int slot, int kvh, int t, int e)
+{
+    int64_t d = c->head_dim;
+    if (kv->layout == ORC_KV_PAGED) {
+        int32_t page = kv->page_table[(int64_t)slot * kv->max_pages_per_seq + t / kv->page_size];
+        return kv->v[layer] + (((int64_t)page * c->n_kv_heads + kvh) * d + e) * kv->page_size + t % kv->page_size;
+    }
+    return kv->v[layer] + (((int64_t)slot * c->n_kv_heads + kvh) * d + e) * kv->max_seq_len + t;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -253,8 +268,8 @@ static void attn_block(const orc_cfg *c, const orc_weights *w, const orc_kv *kv,
     }
     /* append this token's k and v at position pos */
     for (int g = 0; g < nkv; ++g) {
-        memcpy(kv_row(c, kv, kv->k, layer, slot, g, pos), qkv + (nq + g) * d, sizeof(uint16_t) * d);
-        memcpy(kv_row(c, kv, kv->v, layer, slot, g, pos), qkv + (nq + nkv + g) * d, sizeof(uint16_t) * d);
+        memcpy(k_row(c, kv, layer, slot, g, pos), qkv + (nq + g) * d, sizeof(uint16_t) * d);
+        for (int e = 0; e < d; ++e) *v_elem(c, kv, layer, slot, g, pos, e) = qkv[(nq + nkv + g) * d + e];
     }
     /* each query head attends over keys 0..pos of its kv group */
     int n = pos + 1;
@@ -263,14 +278,16 @@ static void attn_block(const orc_cfg *c, const orc_weights *w, const orc_kv *kv,
         int g = hq / group;
         const uint16_t **K = malloc(sizeof(*K) * n);
         const uint16_t **V = malloc(sizeof(*V) * n);
+        uint16_t *vrows = malloc(sizeof(uint16_t) * (size_t)n * d);   /* value rows gathered by token */
         double *out = malloc(sizeof(double) * d);
         for (int t = 0; t < n; ++t) {
-            K[t] = kv_row(c, kv, kv->k, layer, slot, g, t);
-            V[t] = kv_row(c, kv, kv->v, layer, slot, g, t);
+            K[t] = k_row(c, kv, layer, slot, g, t);
+            for (int e = 0; e < d; ++e) vrows[(size_t)t * d + e] = *v_elem(c, kv, layer, slot, g, t, e);
+            V[t] = vrows + (size_t)t * d;
         }
         orc_attention(qkv + hq * d, K, V, n, d, out);
         for (int e = 0; e < d; ++e) o[hq * d + e] = tobf(out[e]);
-        free(K); free(V); free(out);
+        free(K); free(V); free(vrows); free(out);
     }
     orc_linear(o, nq * d, w->w_o[layer], H, acc);
     for (int i = 0; i < H; ++i) x[i] = (float)((double)x[i] + acc[i]);
@@ -321,9 +338,28 @@ void orc_route(const double *logits, int E, int top_k, int32_t *sel, double *wse
     free(p); free(used);
 }
 
+/* Gap between the top_k-th and the (top_k+1)-th largest router logits: how
+ * far the routing decision is from a tie (diagnostic; +inf when E == top_k). */
+static double route_margin(const double *logits, int E, int top_k)
+{
+    double kth = INFINITY, next = -INFINITY;
+    char *used = calloc((size_t)E, 1);
+    for (int r = 0; r <= top_k && r < E; ++r) {
+        int best = -1;
+        for (int e = 0; e < E; ++e)
+            if (!used[e] && (best < 0 || logits[e] > logits[best])) best = e;
+        used[best] = 1;
+        if (r == top_k - 1) kth = logits[best];
+        if (r == top_k) next = logits[best];
+    }
+    free(used);
+    return kth - next;
+}
+
 /* Feed-forward sub-layer for one row: RMSNorm, then either the dense SwiGLU
- * MLP or the routed mixture of SwiGLU experts, added to the residual x. */
-static void mlp_block(const orc_cfg *c, const orc_weights *w, int layer, float *x)
+ * MLP or the routed mixture of SwiGLU experts, added to the residual x.
+ * margin (optional) receives the minimum routing margin seen. */
+static void mlp_block(const orc_cfg *c, const orc_weights *w, int layer, float *x, double *margin)
 {
     int H = c->hidden;
     uint16_t *h = malloc(sizeof(uint16_t) * H);
@@ -339,6 +375,10 @@ static void mlp_block(const orc_cfg *c, const orc_weights *w, int layer, float *
         double *ws = malloc(sizeof(double) * K);
         double *acc = calloc((size_t)H, sizeof(double));
         orc_linear(h, H, w->w_router[layer], E, rl);
+        if (margin) {
+            double mg = route_margin(rl, E, K);
+            if (mg < *margin) *margin = mg;
+        }
         orc_route(rl, E, K, sel, ws);
         for (int r = 0; r < K; ++r) {     /* combine in rank order */
             int e = sel[r];
@@ -365,20 +405,29 @@ static void lm_head(const orc_cfg *c, const orc_weights *w, const float *x, doub
 /* one token of one request at position pos (= tokens already cached),      */
 /* appending its k, v at pos in every layer and returning fp64 logits.      */
 /* ------------------------------------------------------------------------ */
-int orc_decode_row(const orc_cfg *c, const orc_weights *w, const orc_kv *kv,
-                   int slot, int token, int pos, double *logits)
+/* As orc_decode_row; route_margin (optional) receives the smallest top-k
+ * routing margin over the MoE layers (+inf for a dense model). */
+int orc_decode_row_margin(const orc_cfg *c, const orc_weights *w, const orc_kv *kv,
+                          int slot, int token, int pos, double *logits, double *route_margin_out)
 {
     if (token < 0 || token >= c->vocab || pos < 0) return -1;
     int H = c->hidden;
     float *x = malloc(sizeof(float) * H);
+    if (route_margin_out) *route_margin_out = INFINITY;
     for (int i = 0; i < H; ++i) x[i] = (float)bf(w->embed[(int64_t)token * H + i]);
     for (int l = 0; l < c->n_layers; ++l) {
         attn_block(c, w, kv, l, slot, pos, x);
-        mlp_block(c, w, l, x);
+        mlp_block(c, w, l, x, route_margin_out);
     }
     lm_head(c, w, x, logits);
     free(x);
     return 0;
+}
+
+int orc_decode_row(const orc_cfg *c, const orc_weights *w, const orc_kv *kv,
+                   int slot, int token, int pos, double *logits)
+{
+    return orc_decode_row_margin(c, w, kv, slot, token, pos, logits, NULL);
 }
 
 /* The padded decode step at batch size B, computed row by row: each live row
@@ -430,7 +479,7 @@ int orc_prefill(const orc_cfg *c, const orc_weights *w, const orc_kv *kv, int sl
         /* positions in order: position t reads keys 0..t of this layer,
          * which positions 0..t have already written */
         for (int t = 0; t < Lp; ++t) attn_block(c, w, kv, l, slot, t, X + (int64_t)t * H);
-        for (int t = 0; t < Lp; ++t) mlp_block(c, w, l, X + (int64_t)t * H);
+        for (int t = 0; t < Lp; ++t) mlp_block(c, w, l, X + (int64_t)t * H, NULL);
     }
     lm_head(c, w, X + (int64_t)(Lp - 1) * H, logits);
     float *lf = malloc(sizeof(float) * c->vocab);

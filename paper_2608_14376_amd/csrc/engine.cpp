@@ -108,17 +108,12 @@ GemmShape shape_of(const Proj &p, int M) { return GemmShape{M, p.N, p.K, p.S, p.
 
 // Attention chunk: fixed per engine from (B, kv heads, capacity): enough
 // (row, head, split) blocks to fill the GPU when every row is at capacity.
-// The split kernel keeps the chunk's scores and the four wavefront partials
-// in LDS: G chunk + 8 G + 4 G d floats, kept within 64 KiB.
-int max_chunk_for_lds(int G, int d) { return std::min(1024, (16384 - 8 * G - 4 * G * d) / G / 64 * 64); }
-
-int choose_chunk(int B, int nkv, int G, int d, int cap, int override_chunk)
+int choose_chunk(int B, int nkv, int cap, int override_chunk)
 {
-    const int cmax = max_chunk_for_lds(G, d);
-    if (override_chunk > 0) return std::min(override_chunk, cmax);
+    if (override_chunk > 0) return override_chunk;
     int chunk = 64;
-    while (chunk < cmax && (long long)B * nkv * ((cap + chunk - 1) / chunk) > 4096) chunk *= 2;
-    return std::min(chunk, cmax);
+    while (chunk < 1024 && (long long)B * nkv * ((cap + chunk - 1) / chunk) > 4096) chunk *= 2;
+    return chunk;
 }
 
 Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_options &opt)
@@ -146,7 +141,7 @@ Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_
     p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0, bo == 64 ? 0 : bo);
     if (p.lm.bm == 64) p.lm = choose_proj(c->vocab, H, 64, so > 0 ? so : 1, 0, 0);
     const int cap = kv_capacity(kv);
-    p.chunk = choose_chunk(B, c->n_kv_heads, c->n_heads / c->n_kv_heads, d, cap, opt.attn_chunk);
+    p.chunk = choose_chunk(B, c->n_kv_heads, cap, opt.attn_chunk);
     p.max_splits = (cap + p.chunk - 1) / p.chunk;
     return p;
 }
@@ -235,10 +230,11 @@ extern "C" corun_status corun_check_config(const corun_model_cfg *c, const corun
     if (B <= 0 || B > 1024) return fail(CORUN_E_SHAPE, "B_fixed must be in [1, 1024]");
     if (kv->n_slots < B) return fail(CORUN_E_CAPACITY, "KV cache has %d slots < B_fixed %d", kv->n_slots, B);
     if (kv->layout == CORUN_KV_CONTIGUOUS) {
-        if (kv->max_seq_len <= 0) return fail(CORUN_E_CAPACITY, "max_seq_len must be positive");
+        if (kv->max_seq_len <= 0 || kv->max_seq_len % 16 != 0)
+            return fail(CORUN_E_CAPACITY, "max_seq_len must be a positive multiple of 16");
     } else if (kv->layout == CORUN_KV_PAGED) {
-        if (kv->page_size <= 0 || kv->num_pages <= 0 || kv->max_pages_per_seq <= 0)
-            return fail(CORUN_E_CAPACITY, "bad paged-cache geometry");
+        if (kv->page_size <= 0 || kv->page_size % 16 != 0 || kv->num_pages <= 0 || kv->max_pages_per_seq <= 0)
+            return fail(CORUN_E_CAPACITY, "bad paged-cache geometry (page_size must be a multiple of 16)");
     } else {
         return fail(CORUN_E_INVAL, "unknown KV layout %d", kv->layout);
     }

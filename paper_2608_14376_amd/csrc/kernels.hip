@@ -63,6 +63,18 @@ __device__ __forceinline__ size_t kv_offset(const KvView &kv, int nkv, int d, in
     return (((size_t)slot * nkv + kvh) * kv.max_seq_len + t) * d;
 }
 
+// Values are stored transposed: element e of token t at
+//   contiguous ((slot nkv + kvh) d + e) max_seq_len + t
+//   paged      ((page nkv + kvh) d + e) page_size + t % page_size
+__device__ __forceinline__ size_t v_offset(const KvView &kv, int nkv, int d, int slot, int kvh, int t, int e)
+{
+    if (kv.layout == 1) {
+        int page = kv.page_table[(size_t)slot * kv.max_pages_per_seq + t / kv.page_size];
+        return (((size_t)page * nkv + kvh) * d + e) * kv.page_size + (t % kv.page_size);
+    }
+    return (((size_t)slot * nkv + kvh) * d + e) * kv.max_seq_len + t;
+}
+
 __device__ __forceinline__ int row_slot(const int32_t *slot_of_row, int slot_const, int r)
 {
     return slot_of_row ? slot_of_row[r] : (slot_const >= 0 ? slot_const : r);
@@ -611,11 +623,15 @@ __global__ void k_qkv_post(const float *__restrict__ part, int S, long long part
         q[(size_t)r * nq * d + c1] = b1;
     } else {
         const int slot = row_slot(slot_of_row, slot_const, r);
-        const bool is_k = hd < nq + nkv;
-        const int kvh = is_k ? hd - nq : hd - nq - nkv;
-        uint16_t *dst = (is_k ? kc : vc) + kv_offset(kv, nkv, d, slot, kvh, p);
-        dst[i] = b0;
-        dst[i + half] = b1;
+        if (hd < nq + nkv) {
+            uint16_t *dst = kc + kv_offset(kv, nkv, d, slot, hd - nq, p);
+            dst[i] = b0;
+            dst[i + half] = b1;
+        } else {
+            const int kvh = hd - nq - nkv;
+            vc[v_offset(kv, nkv, d, slot, kvh, p, i)] = b0;
+            vc[v_offset(kv, nkv, d, slot, kvh, p, i + half)] = b1;
+        }
     }
 }
 
@@ -636,18 +652,76 @@ hipError_t launch_qkv_post(const float *part, int S, long long part_stride, int 
 // split is request-local and the merge order (split index) is fixed.
 //
 // Block (split, kvh, row): four wavefronts, wavefront w owning the quarter
-// [t0 + w chunk/4, ...) of the chunk.
-//  * Scores S^T = K q^T on MFMA (16 tokens x 16 head slots per tile, the G
-//    real heads in slots 0..G-1): lane l loads 16 bytes of key row
-//    (l % 16) straight from the cache and ends holding tokens 4 (l / 16) + i
-//    of head l % 16.
-//  * Softmax statistics per head over the wavefront's tokens: exact max,
-//    then per-lane sequential sums and the fixed butterfly.
-//  * P V on the vector ALU: lane l owns d/64 output columns and walks the
-//    tokens in order (one coalesced value row per token).
-//  * The four wavefront partials are combined in wavefront order.
+// [t0 + w chunk/4, ...) of the chunk, walked in blocks of 32 tokens:
+//  * scores S^T = K q^T on 16x16x32 MFMA, two 16-token tiles, the G query
+//    heads of the group in column slots 0..G-1: lane l loads 16 bytes of one
+//    key row per tile and ends holding head l % 16's scores of the eight
+//    consecutive tokens 8 (l / 16) .. +7 (see attn_tok);
+//  * online softmax per head: lane l keeps head l % 16's running maximum and
+//    a partial sum over its own tokens;
+//  * O += P V on 16x16x32 MFMA: the lane's eight weights (two tiles x four
+//    tokens) are its A fragment as they stand -- split into two bf16 halves
+//    hi + lo (two MFMAs) so P keeps about 16 significant bits -- and the
+//    matching B fragment is one 16-byte load of the transposed value cache
+//    (those eight tokens of one dimension);
+//  * masked tokens (past the row's length) contribute exact zeros: their
+//    value fragments are zero-filled, never multiplied.
+// The four wavefront partials are combined in wavefront order.
 // ---------------------------------------------------------------------------
 typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// Token order inside a 32-token block.  Score tile T's MFMA row m carries
+// token 8 (m / 4) + 4 T + m % 4, so that lane group kg ends up holding the
+// scores of tokens 8 kg .. 8 kg + 7 (tile 0 rows 4 kg + i, tile 1 rows
+// 4 kg + i): its P fragment is eight consecutive tokens and its value
+// fragment one 16-byte load of the transposed cache.
+__device__ __forceinline__ int attn_tok(int T, int m) { return 8 * (m >> 2) + 4 * T + (m & 3); }
+
+template <int D>
+struct AttnFrags {
+    bf16x8 k[2][D / 32];   // key rows of the two score tiles
+    uint4 v[D / 16];       // per 16-dim tile: tokens 8 kg .. 8 kg + 7 of dimension 16 et + l % 16
+};
+
+template <int D>
+__device__ __forceinline__ void attn_load(AttnFrags<D> &f, const uint16_t *__restrict__ kc, const uint16_t *__restrict__ vc,
+                                          const KvView &kv, int nkv, int slot, int kvh, int tb, int wt1, int hl, int kg)
+{
+    const uint4 z4 = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int T = 0; T < 2; ++T) {
+        const int t = tb + attn_tok(T, hl);
+        const bool tin = t < wt1;
+        const uint16_t *kr = kc + kv_offset(kv, nkv, D, slot, kvh, tin ? t : tb) + 8 * kg;
+#pragma unroll
+        for (int kk = 0; kk < D / 32; ++kk) {
+            uint4 v = z4;
+            if (tin) v = *(const uint4 *)(kr + 32 * kk);
+            f.k[T][kk] = __builtin_bit_cast(bf16x8, v);
+        }
+    }
+    const int t0 = tb + 8 * kg;                        // eight consecutive tokens, one page
+    const int nv = min(8, wt1 - t0);                   // how many of them are real
+    // one address (and page lookup) per lane; the 16-dim tiles are d apart
+    const uint16_t *vr = vc + v_offset(kv, nkv, D, slot, kvh, nv > 0 ? t0 : tb, hl);
+    const size_t estride = (size_t)16 * (kv.layout == 1 ? kv.page_size : kv.max_seq_len);
+#pragma unroll
+    for (int et = 0; et < D / 16; ++et) {
+        uint4 v = z4;
+        if (nv > 0) {
+            v = *(const uint4 *)(vr + et * estride);
+            if (nv < 8) {   // zero the tokens past the row's length (low half = earlier token)
+                uint32_t *w = (uint32_t *)&v;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (2 * j >= nv) w[j] = 0u;
+                    else if (2 * j + 1 >= nv) w[j] &= 0x0000ffffu;
+                }
+            }
+        }
+        f.v[et] = v;
+    }
+}
 
 template <int D, int G>
 __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__ q, const uint8_t *__restrict__ valid,
@@ -657,7 +731,7 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
                                                     const uint16_t *__restrict__ vc, KvView kv, int chunk,
                                                     int max_splits, float *__restrict__ ws)
 {
-    constexpr int EPL = D / 64;
+    constexpr int ET = D / 16;
     const int split = blockIdx.x, kvh = blockIdx.y, r = blockIdx.z;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     if (valid != nullptr && !valid[r]) return;
@@ -669,142 +743,129 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
     const int wt0 = t0 + wave * sub;
     const int wt1 = min(t1, wt0 + sub);
     const int slot = row_slot(slot_of_row, slot_const, r);
-
-    extern __shared__ float smem[];
-    float *sc = smem + wave * G * sub;             // [G][sub] scores, then weights
-    float *cm = smem + 4 * G * sub;                // [4][G] wave maxima
-    float *cl = cm + 4 * G;                        // [4][G] wave sums
-    float *ca = cl + 4 * G;                        // [4][G][D] wave accumulators
-
-    // q^T fragments (B operand): lane l supplies head l % 16, dims 32 kk + 8 (l / 16) .. +7
     const int hl = lane & 15, kg = lane >> 4;
+
+    __shared__ float cm[4][16], cl[4][16];
+    __shared__ float ca[4][G * D];
+
+    // q^T fragments (B operand of the scores): lane l supplies head l % 16,
+    // dims 32 kk + 8 (l / 16) .. +7
     bf16x8 qf[D / 32];
     {
         const uint16_t *qr = q + (size_t)r * nq * D + ((size_t)kvh * G + hl) * D + kg * 8;
         const uint4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int kk = 0; kk < D / 32; ++kk)
-        {
+        for (int kk = 0; kk < D / 32; ++kk) {
             uint4 v = z;
             if (hl < G) v = *(const uint4 *)(qr + 32 * kk);
             qf[kk] = __builtin_bit_cast(bf16x8, v);
         }
     }
     const float scale = 1.0f / sqrtf((float)D);
-    for (int tb = wt0; tb < wt1; tb += 16) {
-        const int t = tb + hl;
-        const bool tin = t < wt1;
-        const uint16_t *kr = kc + kv_offset(kv, nkv, D, slot, kvh, tin ? t : wt0) + kg * 8;
-        bf16x8 kf[D / 32];
-        const uint4 z = {0u, 0u, 0u, 0u};
+    f32x4 oacc[ET];
 #pragma unroll
-        for (int kk = 0; kk < D / 32; ++kk) {
-            uint4 v = z;
-            if (tin) v = *(const uint4 *)(kr + 32 * kk);
-            kf[kk] = __builtin_bit_cast(bf16x8, v);
+    for (int et = 0; et < ET; ++et) oacc[et] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    float mrun = -INFINITY, lrun = 0.f;
+
+    const int nblk = wt1 > wt0 ? (wt1 - wt0 + 31) / 32 : 0;
+    for (int ib = 0; ib < nblk; ++ib) {
+        const int tb = wt0 + 32 * ib;
+        AttnFrags<D> fa;
+        attn_load<D>(fa, kc, vc, kv, nkv, slot, kvh, tb, wt1, hl, kg);
+        f32x4 st[2];
+#pragma unroll
+        for (int T = 0; T < 2; ++T) {
+            st[T] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kk = 0; kk < D / 32; ++kk)
+                st[T] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa.k[T][kk], qf[kk], st[T], 0, 0, 0);
         }
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        // lane (hl, kg) now holds head hl's scores of tokens tb + 8 kg + 4 T + i
+        float mt = -INFINITY;
 #pragma unroll
-        for (int kk = 0; kk < D / 32; ++kk) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kk], qf[kk], acc, 0, 0, 0);
-        if (hl < G) {
+        for (int T = 0; T < 2; ++T)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int tt = tb + 4 * kg + i;
-                if (tt < wt1) sc[hl * sub + (tt - wt0)] = acc[i] * scale;
+                const float sv = (tb + 8 * kg + 4 * T + i < wt1) ? st[T][i] * scale : -INFINITY;
+                st[T][i] = sv;
+                mt = fmaxf(mt, sv);
             }
-        }
-    }
-    __syncthreads();
-
-    const int nt = max(0, wt1 - wt0);
-    float mg[G], lg[G];
+        mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+        const float mnew = fmaxf(mrun, mt);              // finite: every block has a real token
+        const float alpha = __expf(mrun - mnew);         // 0 on the first block
+        // each weight enters the matrix core as two bf16 halves, p = hi + lo,
+        // which carry about 16 significant bits; the sum uses the fp32 weight
+        uint16_t pw[8], pl[8];
+        float ls = 0.f;
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-        float m = -INFINITY;
-        for (int j = lane; j < nt; j += 64) m = fmaxf(m, sc[g * sub + j]);
-        m = wave_max(m);
-        float l = 0.f;
-        for (int j = lane; j < nt; j += 64) {
-            const float w = __expf(sc[g * sub + j] - m);
-            sc[g * sub + j] = w;
-            l += w;
-        }
-        mg[g] = m;
-        lg[g] = wave_sum(l);
-    }
-    __syncthreads();
-
-    float acc[G][EPL];
+        for (int T = 0; T < 2; ++T)
 #pragma unroll
-    for (int g = 0; g < G; ++g)
-#pragma unroll
-        for (int j = 0; j < EPL; ++j) acc[g][j] = 0.f;
-    int t = wt0;
-    for (; t + 4 <= wt1; t += 4) {
-        float vf[4][EPL];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const uint16_t *vr = vc + kv_offset(kv, nkv, D, slot, kvh, t + u) + lane * EPL;
-            if constexpr (EPL == 2) {
-                const uint32_t w2 = *(const uint32_t *)vr;
-                vf[u][0] = __uint_as_float(w2 << 16);
-                vf[u][1] = __uint_as_float(w2 & 0xffff0000u);
-            } else {
-                vf[u][0] = bf2f(vr[0]);
+            for (int i = 0; i < 4; ++i) {
+                const float pe = __expf(st[T][i] - mnew);
+                ls += pe;
+                pw[4 * T + i] = f2bf(pe);
+                pl[4 * T + i] = f2bf(pe - bf2f(pw[4 * T + i]));
             }
+        lrun = lrun * alpha + ls;
+        mrun = mnew;
+        // rescale the accumulators: lane l holds heads 4 (l / 16) + i
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float ai = __shfl(alpha, 4 * kg + i, 64);
+#pragma unroll
+            for (int et = 0; et < ET; ++et) oacc[et][i] *= ai;
+        }
+        bf16x8 pf, pfl;
+        {
+            uint4 pv, pq;
+            pv.x = (uint32_t)pw[0] | ((uint32_t)pw[1] << 16);
+            pv.y = (uint32_t)pw[2] | ((uint32_t)pw[3] << 16);
+            pv.z = (uint32_t)pw[4] | ((uint32_t)pw[5] << 16);
+            pv.w = (uint32_t)pw[6] | ((uint32_t)pw[7] << 16);
+            pq.x = (uint32_t)pl[0] | ((uint32_t)pl[1] << 16);
+            pq.y = (uint32_t)pl[2] | ((uint32_t)pl[3] << 16);
+            pq.z = (uint32_t)pl[4] | ((uint32_t)pl[5] << 16);
+            pq.w = (uint32_t)pl[6] | ((uint32_t)pl[7] << 16);
+            pf = __builtin_bit_cast(bf16x8, pv);
+            pfl = __builtin_bit_cast(bf16x8, pq);
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int g = 0; g < G; ++g) {
-                const float w = sc[g * sub + (t + u - wt0)];
-#pragma unroll
-                for (int j = 0; j < EPL; ++j) acc[g][j] += w * vf[u][j];
-            }
+        for (int et = 0; et < ET; ++et) {
+            const bf16x8 vf = __builtin_bit_cast(bf16x8, fa.v[et]);
+            oacc[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf, vf, oacc[et], 0, 0, 0);
+            oacc[et] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pfl, vf, oacc[et], 0, 0, 0);
+        }
     }
-    for (; t < wt1; ++t) {
-        const uint16_t *vr = vc + kv_offset(kv, nkv, D, slot, kvh, t) + lane * EPL;
-        float vf[EPL];
-        if constexpr (EPL == 2) {
-            const uint32_t w2 = *(const uint32_t *)vr;
-            vf[0] = __uint_as_float(w2 << 16);
-            vf[1] = __uint_as_float(w2 & 0xffff0000u);
-        } else {
-            vf[0] = bf2f(vr[0]);
-        }
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-            const float w = sc[g * sub + (t - wt0)];
-#pragma unroll
-            for (int j = 0; j < EPL; ++j) acc[g][j] += w * vf[j];
-        }
-    }
+    // per-head sum over the four 16-lane groups (fixed order)
+    lrun += __shfl_xor(lrun, 16, 64);
+    lrun += __shfl_xor(lrun, 32, 64);
 
     // combine the four wavefronts in wavefront order
-    if (lane == 0) {
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-            cm[wave * G + g] = mg[g];
-            cl[wave * G + g] = lg[g];
-        }
+    if (lane < 16) {
+        cm[wave][lane] = mrun;
+        cl[wave][lane] = lrun;
     }
 #pragma unroll
-    for (int g = 0; g < G; ++g)
+    for (int et = 0; et < ET; ++et)
 #pragma unroll
-        for (int j = 0; j < EPL; ++j) ca[(wave * G + g) * D + lane * EPL + j] = acc[g][j];
+        for (int i = 0; i < 4; ++i) {
+            const int g = 4 * kg + i;
+            if (g < G) ca[wave][g * D + 16 * et + hl] = oacc[et][i];
+        }
     __syncthreads();
     float *o = ws + (((size_t)r * nkv + kvh) * max_splits + split) * (G * (D + 2));
     for (int idx = threadIdx.x; idx < G * D; idx += 256) {
         const int g = idx / D;
-        float M = cm[g];
+        float M = cm[0][g];
 #pragma unroll
-        for (int w = 1; w < 4; ++w) M = fmaxf(M, cm[w * G + g]);
+        for (int w = 1; w < 4; ++w) M = fmaxf(M, cm[w][g]);
         float L = 0.f, A = 0.f;
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-            const float f = __expf(cm[w * G + g] - M);   // empty wavefronts: exp(-inf) = 0
-            L += cl[w * G + g] * f;
-            A += ca[w * G * D + idx] * f;
+            const float f = __expf(cm[w][g] - M);   // empty wavefronts: exp(-inf) = 0
+            L += cl[w][g] * f;
+            A += ca[w][idx] * f;
         }
         o[2 * G + idx] = A;
         if (idx % D == 0) {
@@ -876,8 +937,7 @@ static void launch_attn_dg(const uint16_t *q, int rows, const uint8_t *valid, co
                            const int32_t *slot_of_row, int slot_const, int nq, int nkv, const uint16_t *kc,
                            const uint16_t *vc, KvView kv, int chunk, int max_splits, float *ws, hipStream_t st)
 {
-    const size_t shm = sizeof(float) * (G * chunk + 8 * G + 4 * G * D);
-    hipLaunchKernelGGL((k_attn_split<D, G>), dim3(max_splits, nkv, rows), dim3(256), shm, st, q, valid, pos,
+    hipLaunchKernelGGL((k_attn_split<D, G>), dim3(max_splits, nkv, rows), dim3(256), 0, st, q, valid, pos,
                        slot_of_row, slot_const, nq, nkv, kc, vc, kv, chunk, max_splits, ws);
 }
 
@@ -1376,8 +1436,8 @@ hipError_t launch_moe_gemm(const uint16_t *A, int lda, int row_div, const uint16
 // Work units of one KV head: (query block of 32 positions for d = 128, 64 for
 // d = 64, one query head of the group).  A workgroup takes four consecutive units (in [block][head] order,
 // latest blocks first) as its four wavefronts, and the four share the key
-// and value tiles staged in LDS: K as [key][dim] rows, V transposed to
-// [dim][key].
+// and value tiles staged in LDS: K as [key][dim] rows, V as [dim][key] rows
+// (the cache already stores values transposed).
 //  * S^T = K q^T on 16x16x32 MFMA: lane l ends holding keys 4 (l / 16) + i of
 //    query l % 16 -- exactly the B operand layout of the 16x16x16 MFMA, so
 //  * O^T += V^T P^T runs on 16x16x16 MFMA with P rounded to bf16, V^T read as
@@ -1448,13 +1508,22 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const uint16_t *__restrict
             if (k0 + key < Lp) v = *(const uint4 *)(kc + kv_offset(kv, nkv, D, slot, kvh, k0 + key) + ch * 8);
             *(uint4 *)(&Ks[key * KLD + ch * 8]) = v;
         }
-        for (int it = threadIdx.x; it < BK * (D / 8); it += 256) {
-            const int key = it % BK, ch = it / BK;
+        for (int it = threadIdx.x; it < D * (BK / 8); it += 256) {
+            // eight consecutive keys of one dimension of the transposed value cache
+            const int e = it / (BK / 8), kc8 = (it % (BK / 8)) * 8;
+            const int key0 = k0 + kc8;
             uint4 v = z;
-            if (k0 + key < Lp) v = *(const uint4 *)(vc + kv_offset(kv, nkv, D, slot, kvh, k0 + key) + ch * 8);
-            const uint16_t *e8 = (const uint16_t *)&v;
+            if (key0 < Lp) {
+                v = *(const uint4 *)(vc + v_offset(kv, nkv, D, slot, kvh, key0, e));
+                const int nv = Lp - key0;           // zero the keys past the prompt
+                uint32_t *w = (uint32_t *)&v;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) Vt[(ch * 8 + j) * VLD + key] = e8[j];
+                for (int j = 0; j < 4; ++j) {
+                    if (2 * j >= nv) w[j] = 0u;
+                    else if (2 * j + 1 >= nv) w[j] &= 0x0000ffffu;
+                }
+            }
+            *(uint4 *)(&Vt[e * VLD + kc8]) = v;
         }
         __syncthreads();
         if (k0 > my_last_q) continue;                 // wave-uniform: all keys of this tile are in our future
@@ -1500,9 +1569,9 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const uint16_t *__restrict
                 uint16_t pv[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const float pe = mnew == -INFINITY ? 0.f : __expf(st[qt][t][i] - mnew);
-                    ls += pe;
-                    pv[i] = f2bf(pe);
+                    // rounded to bf16 for the matrix core; summed as rounded
+                    pv[i] = f2bf(mnew == -INFINITY ? 0.f : __expf(st[qt][t][i] - mnew));
+                    ls += bf2f(pv[i]);
                 }
                 pb[qt][t] = (s16x4){(short)pv[0], (short)pv[1], (short)pv[2], (short)pv[3]};
             }
