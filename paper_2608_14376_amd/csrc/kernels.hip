@@ -651,8 +651,8 @@ hipError_t launch_qkv_post(const float *part, int S, long long part_stride, int 
 // ceil((pos + 1) / chunk): a function of the row's own length only, so the
 // split is request-local and the merge order (split index) is fixed.
 //
-// Block (split, kvh, row): four wavefronts, wavefront w owning the quarter
-// [t0 + w chunk/4, ...) of the chunk, walked in blocks of 32 tokens:
+// Block (split, kvh, row): four wavefronts taking the chunk's 32-token blocks
+// in turn (wavefront w: blocks w, w + 4, ...), each block processed as:
 //  * scores S^T = K q^T on 16x16x32 MFMA, two 16-token tiles, the G query
 //    heads of the group in column slots 0..G-1: lane l loads 16 bytes of one
 //    key row per tile and ends holding head l % 16's scores of the eight
@@ -739,9 +739,6 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
     const int t0 = split * chunk;
     if (t0 >= n) return;
     const int t1 = min(n, t0 + chunk);
-    const int sub = chunk >> 2;
-    const int wt0 = t0 + wave * sub;
-    const int wt1 = min(t1, wt0 + sub);
     const int slot = row_slot(slot_of_row, slot_const, r);
     const int hl = lane & 15, kg = lane >> 4;
 
@@ -767,9 +764,13 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
     for (int et = 0; et < ET; ++et) oacc[et] = (f32x4){0.f, 0.f, 0.f, 0.f};
     float mrun = -INFINITY, lrun = 0.f;
 
-    const int nblk = wt1 > wt0 ? (wt1 - wt0 + 31) / 32 : 0;
+    // wavefront w takes the 32-token blocks w, w + 4, w + 8, ... of the chunk:
+    // wavefronts 2i and 2i + 1 read the two 64-byte halves of the same
+    // 128-byte lines of the transposed value cache at about the same time
+    const int wt1 = t1;
+    const int nblk = t1 > t0 + 32 * wave ? (t1 - t0 - 32 * wave + 127) / 128 : 0;
     for (int ib = 0; ib < nblk; ++ib) {
-        const int tb = wt0 + 32 * ib;
+        const int tb = t0 + 32 * wave + 128 * ib;
         AttnFrags<D> fa;
         attn_load<D>(fa, kc, vc, kv, nkv, slot, kvh, tb, wt1, hl, kg);
         f32x4 st[2];
