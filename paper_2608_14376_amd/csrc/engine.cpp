@@ -52,9 +52,10 @@ int kv_capacity(const corun_kv *kv)
 }
 
 // One projection: N outputs, K inputs, split-K into S chunks of Kc, run by
-// the skinny kernel (bm = 0) or the LDS-tiled kernel with M tile bm.
+// the skinny kernel (bm = 0), the LDS-tiled kernel with M tile bm (bn = 0)
+// or the pipelined kernel with bm x bn tiles (bn > 0).
 struct Proj {
-    int N = 0, K = 0, S = 1, Kc = 0, bm = 0;
+    int N = 0, K = 0, S = 1, Kc = 0, bm = 0, bn = 0;
 };
 
 struct Plan {
@@ -70,18 +71,29 @@ int mt_for(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 //  * M <= 64: the skinny kernel (weights streamed to registers); aim for
 //    about 2048 wavefronts (8 per CU) so enough weight bytes are in flight,
 //    each split keeping at least 256 K elements.
-//  * M > 64: the LDS-tiled kernel with a 128-row tile (measured faster than
-//    256 rows at M = 256: two workgroups fit a CU), split-K only as far as
-//    needed to give about two workgroups per CU, each split keeping at least
-//    512 K elements.
-Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_override)
+//  * M > 64, K % 64 == 0: the pipelined kernel (one workgroup per CU) with
+//    M tile 128 (M <= 128) or 256, N tile 128, or 256 x 256 once those tiles
+//    alone fill the GPU (large prefill; never for the argmax epilogue);
+//    split-K up to one round of at most 256 workgroups, each split keeping
+//    at least 512 K elements.
+//  * otherwise (or bm_override > 0): the LDS-tiled kernel with a 128-row
+//    tile (or bm_override), split-K to about two workgroups per CU.
+Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_override, bool argmax = false)
 {
     Proj p;
     p.N = N;
     p.K = K;
     if (N <= 0 || K <= 0 || M <= 0) return p;   // no such projection
     int S, align;
-    if (M <= 64 && bm_override <= 0) {
+    if (M > 64 && bm_override <= 0 && K % 64 == 0) {
+        p.bm = M <= 128 ? 128 : 256;
+        p.bn = 128;
+        if (M > 256 && !argmax && (long long)((M + 255) / 256) * ((N + 255) / 256) >= 256) p.bn = 256;
+        const long long tiles = (long long)((M + p.bm - 1) / p.bm) * ((N + p.bn - 1) / p.bn);
+        S = tiles >= 256 ? 1 : (int)(256 / tiles);
+        S = std::min(S, std::max(1, K / 512));
+        align = 64;
+    } else if (M <= 64 && bm_override <= 0) {
         const int col_waves = (N + 63) / 64;
         const int mt = mt_for(M);
         const int m_tiles = (M + 16 * mt - 1) / (16 * mt);
@@ -104,7 +116,7 @@ Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_
     return p;
 }
 
-GemmShape shape_of(const Proj &p, int M) { return GemmShape{M, p.N, p.K, p.S, p.Kc, mt_for(M), p.bm}; }
+GemmShape shape_of(const Proj &p, int M) { return GemmShape{M, p.N, p.K, p.S, p.Kc, mt_for(M), p.bm, p.bn}; }
 
 // Attention chunk: fixed per engine from (B, kv heads, capacity): enough
 // (row, head, split) blocks to fill the GPU when every row is at capacity.
@@ -138,8 +150,8 @@ Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_
     }
     // lm_head: never split (its epilogue selects the argmax partials) except
     // under the split override test aid; the 64-row tile has no argmax epilogue
-    p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0, bo == 64 ? 0 : bo);
-    if (p.lm.bm == 64) p.lm = choose_proj(c->vocab, H, 64, so > 0 ? so : 1, 0, 0);
+    p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0, bo == 64 ? 0 : bo, true);
+    if (p.lm.bm == 64) p.lm = choose_proj(c->vocab, H, 64, so > 0 ? so : 1, 0, 0, true);
     const int cap = kv_capacity(kv);
     p.chunk = choose_chunk(B, c->n_kv_heads, cap, opt.attn_chunk);
     p.max_splits = (cap + p.chunk - 1) / p.chunk;

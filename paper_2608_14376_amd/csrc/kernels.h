@@ -58,6 +58,7 @@ struct GemmShape {
     int Kc;         // K elements per split (multiple of 32)
     int mt;         // skinny kernel: 16-row M tiles per wave: 1, 2 or 4
     int bm;         // 0 = skinny kernel; 64, 128, 256 = LDS-tiled kernel with this M tile
+    int bn;         // > 0: pipelined kernel with bm x bn tiles (128 x 128, 256 x 128, 256 x 256)
 };
 // Dispatch on g.bm.
 hipError_t launch_proj(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
@@ -70,6 +71,10 @@ hipError_t launch_gemm(const uint16_t *A, int lda, const uint16_t *W, const Gemm
 // over grid.y, same output contract as launch_gemm (no argmax epilogue).
 hipError_t launch_gemm_tiled(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, int bm, float *out,
                              long long split_stride, int ldo, hipStream_t st, ArgBest *amax = nullptr);
+// Pipelined large-M variant (direct global -> LDS loads, 32x32 MFMA tiles):
+// K and Kc multiples of 64 (32 for bn == 256); argmax epilogue with bn == 128 only.
+hipError_t launch_gemm_dma(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
+                           long long split_stride, int ldo, hipStream_t st, ArgBest *amax = nullptr);
 inline int gemm_col_blocks(int N) { return (N + 63) / 64; }
 // next[r] = best index over the np column-block partials of row r (-1 for padding rows).
 hipError_t launch_argmax_partials(const ArgBest *part, int rows, int np, const uint8_t *valid, int32_t *next,

@@ -531,6 +531,262 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const uint16_t *__restrict__
     }
 }
 
+// ---------------------------------------------------------------------------
+// Large-M projection, pipelined: both operands stream global -> LDS with the
+// direct 16-byte LDS loads of gfx950 (no register staging) through a ring of
+// NST stages of BK (32 or 64) K elements, NST - 1 stages in flight while one
+// feeds the matrix cores.  The loads of a stage are the only vector-memory
+// operations of the loop, so "stage i has landed" is a fixed vmcnt: the
+// number of loads issued after it.
+//
+// Stage layout: A rows [BM][BK] then W rows [BN][BK], each row as BK / 8
+// 16-byte chunks, chunk c of row r stored at c ^ f(r) (f(r) = (r / 4) % 4 for
+// 64-byte rows, (r / 2) % 8 for 128-byte rows), which puts the 16 rows read
+// by one 16-lane group of a fragment read on 16 distinct bank groups.  One
+// load instruction of a wavefront fills 1 KB of the stage: 16 rows x 64
+// bytes or 8 rows x 128 bytes.  Whole 128-byte lines per row and instruction
+// matter: the 64-byte form roughly halves what one CU can pull while its
+// activation and weight loads share the path.
+//
+// Four wavefronts in a WGM x (4 / WGM) grid; wavefront tile (BM / WGM) x
+// (BN / (4 / WGM)) as 32x32 tiles of v_mfma_f32_32x32x16_bf16.  Every output
+// element's K reduction runs in one order (K steps in order, each the
+// instruction's fixed 16-term product) whatever its row, so rows stay
+// position-invariant.  Rows >= M and columns >= N load clamped (real) rows
+// and are never stored; K and the split chunk are multiples of BK, so no
+// stage is partial.
+//
+// Tile order: with several M tiles, workgroups are handed to the eight XCDs
+// in turn, so each XCD gets a contiguous run of tiles, walked in groups of
+// eight M tiles per N tile: the workgroups sharing a weight tile or an
+// activation tile run together on one L2.
+// ---------------------------------------------------------------------------
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ constexpr int vmcnt_imm(int n)
+{
+    return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8);   // vmcnt(n), expcnt and lgkmcnt not waited
+}
+
+// wait until at most `stages` stages of OPS loads each are outstanding
+// (s_waitcnt takes an immediate: dispatch the uniform stage count)
+template <int OPS, int S_>
+__device__ __forceinline__ void wait_stages(int stages)
+{
+    if constexpr (S_ >= 0) {
+        if (stages == S_) __builtin_amdgcn_s_waitcnt(vmcnt_imm(S_ * OPS));
+        else wait_stages<OPS, S_ - 1>(stages);
+    }
+}
+
+__device__ __forceinline__ void lds_barrier()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+template <int C>
+__device__ __forceinline__ int dma_swz(int r, int c)
+{
+    static_assert(C == 4 || C == 8, "64- or 128-byte rows");
+    if constexpr (C == 4) return r * 4 + (c ^ ((r >> 2) & 3));
+    else return r * 8 + (c ^ ((r >> 1) & 7));
+}
+
+template <int BM, int BN, int BK, int NST, int WGM>
+__global__ __launch_bounds__(256) void k_gemm_dma(const uint16_t *__restrict__ A, int lda,
+                                                  const uint16_t *__restrict__ W, int M, int N, int K, int Kc,
+                                                  float *__restrict__ out, long long split_stride, int ldo,
+                                                  ArgBest *__restrict__ amax)
+{
+    constexpr int C = BK / 8;                         // 16-byte chunks per row
+    constexpr int WGN = 4 / WGM;
+    constexpr int WM = BM / WGM, WN = BN / WGN;
+    constexpr int FM = WM / 32, FN = WN / 32;
+    constexpr int A_OPS = BM * C / 256, W_OPS = BN * C / 256;
+    constexpr int OPS = A_OPS + W_OPS, P = NST - 1;
+    constexpr int STAGE = (BM + BN) * C;             // 16-byte units
+    static_assert(P * OPS <= 63, "vmcnt range");
+    __shared__ __attribute__((aligned(16))) uint4 ring[NST * STAGE];
+
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int num_m = (M + BM - 1) / BM, num_n = (N + BN - 1) / BN;
+    int t = blockIdx.x, mt, nt;
+    if (num_m == 1) {
+        mt = 0;
+        nt = t;
+    } else {
+        const int T = num_m * num_n;
+        if (T >= 8 && gridDim.y == 1) {
+            const int x = t & 7, j = t >> 3, per = T >> 3, rem = T & 7;
+            t = x * per + min(x, rem) + j;
+        }
+        constexpr int GM = 8;
+        const int group = t / (GM * num_n), first = group * GM, gs = min(num_m - first, GM);
+        const int in = t - group * GM * num_n;
+        mt = first + in % gs;
+        nt = in / gs;
+    }
+    const int m0 = mt * BM, n0 = nt * BN;
+    const int s = blockIdx.y;
+    const int kbeg = s * Kc, kend = min(K, kbeg + Kc);
+    const int nk = kend > kbeg ? (kend - kbeg) / BK : 0;
+
+    // per load op j: source row and logical chunk of this thread's 16 bytes
+    const uint16_t *asrc[A_OPS];
+    const uint16_t *wsrc[W_OPS];
+#pragma unroll
+    for (int j = 0; j < A_OPS; ++j) {
+        const int g = j * 256 + tid, r = g / C, c = dma_swz<C>(r, g % C) - r * C;   // the swizzle is an involution
+        asrc[j] = A + (size_t)min(m0 + r, M - 1) * lda + kbeg + 8 * c;
+    }
+#pragma unroll
+    for (int j = 0; j < W_OPS; ++j) {
+        const int g = j * 256 + tid, r = g / C, c = dma_swz<C>(r, g % C) - r * C;
+        wsrc[j] = W + (size_t)min(n0 + r, N - 1) * K + kbeg + 8 * c;
+    }
+    typedef __attribute__((address_space(3))) void lds_void;
+    auto issue = [&](int slot, int kofs) {
+        uint4 *base = ring + slot * STAGE + wave * 64;
+#pragma unroll
+        for (int j = 0; j < A_OPS; ++j)
+            __builtin_amdgcn_global_load_lds((const void *)(asrc[j] + kofs), (lds_void *)(base + j * 256), 16, 0, 0);
+#pragma unroll
+        for (int j = 0; j < W_OPS; ++j)
+            __builtin_amdgcn_global_load_lds((const void *)(wsrc[j] + kofs), (lds_void *)(base + BM * C + j * 256), 16,
+                                             0, 0);
+    };
+
+    f32x16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
+
+    const int wm0 = (wave / WGN) * WM, wn0 = (wave % WGN) * WN;
+    const int r32 = lane & 31, h = lane >> 5;
+    // a stage's fragments: per 16-wide K step, FM activation and FN weight tiles
+    struct Frags {
+        bf16x8 a[BK / 16][FM], w[BK / 16][FN];
+    };
+    auto read = [&](Frags &f, int slot) {
+        const uint4 *As = ring + slot * STAGE;
+        const uint4 *Ws = As + BM * C;
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks) {
+#pragma unroll
+            for (int i = 0; i < FM; ++i) f.a[ks][i] = __builtin_bit_cast(bf16x8, As[dma_swz<C>(wm0 + 32 * i + r32, 2 * ks + h)]);
+#pragma unroll
+            for (int j = 0; j < FN; ++j) f.w[ks][j] = __builtin_bit_cast(bf16x8, Ws[dma_swz<C>(wn0 + 32 * j + r32, 2 * ks + h)]);
+        }
+    };
+    auto mma = [&](const Frags &f) {
+#pragma unroll
+        for (int ks = 0; ks < BK / 16; ++ks)
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[ks][i], f.w[ks][j], acc[i][j], 0, 0, 0);
+    };
+    // Stage i: make stage i + 1 visible, refill the slot freed by stage i - 1
+    // with stage i + P, read stage i + 1's fragments into `nxt`, then run
+    // stage i's products from `cur` while those reads are in flight.  The
+    // freed slot was read two steps ago, before the products of step i - 1
+    // that precede this step's barrier.
+    auto step = [&](int i, const Frags &cur, Frags &nxt) {
+        if (i + 1 < nk) {
+            wait_stages<OPS, P - 1>(min(P - 2, nk - 2 - i));
+            lds_barrier();
+            if (i + P < nk) issue((i + P) % NST, (i + P) * BK);
+            read(nxt, (i + 1) % NST);
+        }
+        mma(cur);
+    };
+#pragma unroll
+    for (int i = 0; i < P; ++i)
+        if (i < nk) issue(i, i * BK);
+    Frags f0, f1;
+    if (nk > 0) {
+        wait_stages<OPS, P - 1>(min(P - 1, nk - 1));
+        lds_barrier();
+        read(f0, 0);
+    }
+    int i = 0;
+    for (; i + 1 < nk; i += 2) {
+        step(i, f0, f1);
+        step(i + 1, f1, f0);
+    }
+    if (i < nk) step(i, f0, f1);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // nothing may land in LDS after the workgroup ends
+
+    // lane holds, per 32x32 tile, column r32 and rows 8 (q / 4) + 4 h + q % 4
+    float *o = out + (size_t)s * split_stride;
+#pragma unroll
+    for (int a = 0; a < FM; ++a)
+#pragma unroll
+        for (int b = 0; b < FN; ++b) {
+            const int col = n0 + wn0 + 32 * b + r32;
+            if (col >= N) continue;
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const int row = m0 + wm0 + 32 * a + 8 * (q >> 2) + 4 * h + (q & 3);
+                if (row < M) o[(size_t)row * ldo + col] = acc[a][b][q];
+            }
+        }
+    if constexpr (WN == 64) {
+        if (amax != nullptr) {   // per row: best over this wavefront's 64 columns (one 64-column block)
+            const int ncb = (N + 63) / 64;
+#pragma unroll
+            for (int a = 0; a < FM; ++a)
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    float bv = -INFINITY;
+                    int bi = 0x7fffffff;
+#pragma unroll
+                    for (int b = 0; b < FN; ++b) {
+                        const int col = n0 + wn0 + 32 * b + r32;
+                        if (col < N) better(bv, bi, acc[a][b][q], col);
+                    }
+#pragma unroll
+                    for (int off = 1; off < 32; off <<= 1) {
+                        const float v2 = __shfl_xor(bv, off, 64);
+                        const int i2 = __shfl_xor(bi, off, 64);
+                        better(bv, bi, v2, i2);
+                    }
+                    const int row = m0 + wm0 + 32 * a + 8 * (q >> 2) + 4 * h + (q & 3);
+                    if (r32 == 0 && row < M && n0 + wn0 < N) amax[(size_t)row * ncb + (n0 + wn0) / 64] = ArgBest{bv, bi};
+                }
+        }
+    }
+}
+
+hipError_t launch_gemm_dma(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
+                           long long split_stride, int ldo, hipStream_t st, ArgBest *amax)
+{
+    const int bk = g.bn == 256 ? 32 : 64;
+    if (g.K % bk != 0 || g.Kc % bk != 0 || g.M <= 0) return hipErrorInvalidValue;
+    if (amax != nullptr && g.bn != 128) return hipErrorInvalidValue;   // argmax epilogue needs 64-column wavefront tiles
+    const int num_n = (g.N + g.bn - 1) / g.bn;
+    const int num_m = (g.M + g.bm - 1) / g.bm;
+    dim3 grid(num_m * num_n, g.S);
+    if (g.bm == 128 && g.bn == 128)
+        hipLaunchKernelGGL((k_gemm_dma<128, 128, 64, 4, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+                           split_stride, ldo, amax);
+    else if (g.bm == 256 && g.bn == 128)
+        hipLaunchKernelGGL((k_gemm_dma<256, 128, 64, 3, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+                           split_stride, ldo, amax);
+    else if (g.bm == 256 && g.bn == 256)
+        hipLaunchKernelGGL((k_gemm_dma<256, 256, 32, 4, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+                           split_stride, ldo, amax);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
 hipError_t launch_gemm_tiled(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, int bm, float *out,
                              long long split_stride, int ldo, hipStream_t st, ArgBest *amax)
 {
@@ -1633,6 +1889,7 @@ hipError_t launch_prefill_attn(const uint16_t *q, int Lp, int nq, int nkv, int d
 hipError_t launch_proj(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
                        long long split_stride, int ldo, hipStream_t st, ArgBest *amax)
 {
+    if (g.bn > 0) return launch_gemm_dma(A, lda, W, g, out, split_stride, ldo, st, amax);
     if (g.bm > 0) return launch_gemm_tiled(A, lda, W, g, g.bm, out, split_stride, ldo, st, amax);
     return launch_gemm(A, lda, W, g, out, split_stride, ldo, st, amax);
 }
