@@ -31,12 +31,16 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 // fp32 -> bf16, round to nearest even; NaN stays NaN (quieted).
-__device__ __forceinline__ uint16_t f2bf(float f)
+// fp32 -> bf16, round to nearest even, NaN quieted: gfx950's v_cvt_pk_bf16_f32
+// (bit-identical, over all 2^32 inputs, to adding 0x7fff + lsb and truncating,
+// with (u >> 16) | 0x40 for NaN)
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+// two values in one instruction: a in the low half, b in the high half
+__device__ __forceinline__ uint32_t f2bf2(float a, float b)
 {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
 
 // Fixed butterfly over the 64 lanes, then lane 0's value to every lane.
@@ -1686,201 +1690,253 @@ hipError_t launch_moe_gemm(const uint16_t *A, int lda, int row_div, const uint16
 
 // ---------------------------------------------------------------------------
 // Causal attention of the isolated prefill (flash-style, no split): the
-// prompt runs alone, so any fixed order is allowed; this one computes, for
-// every query, the keys in tiles of 64 in increasing order with the online
-// softmax.
+// prompt runs alone, so any fixed order is allowed; this one takes, for every
+// query, the keys in tiles of 64 in increasing order with the online softmax.
 //
-// Work units of one KV head: (query block of 32 positions for d = 128, 64 for
-// d = 64, one query head of the group).  A workgroup takes four consecutive units (in [block][head] order,
-// latest blocks first) as its four wavefronts, and the four share the key
-// and value tiles staged in LDS: K as [key][dim] rows, V as [dim][key] rows
-// (the cache already stores values transposed).
-//  * S^T = K q^T on 16x16x32 MFMA: lane l ends holding keys 4 (l / 16) + i of
-//    query l % 16 -- exactly the B operand layout of the 16x16x16 MFMA, so
-//  * O^T += V^T P^T runs on 16x16x16 MFMA with P rounded to bf16, V^T read as
-//    8-byte rows of the transposed tile.
-// Each lane's O^T values belong to one query, so the softmax rescale is a
-// per-lane scalar; the row sum is a per-lane partial reduced across the four
-// 16-lane groups at the end.
+// Work units of one KV head: (block of 32 queries, one query head of the
+// group).  A workgroup of eight wavefronts (two per SIMD, so one wavefront's
+// softmax runs while the other's matrix products do) takes eight consecutive
+// units in [block][head] order, latest blocks first, one per wavefront; the
+// eight share key tiles ([key][d] rows) and transposed value tiles ([d][key]
+// rows, as the cache stores them), streamed global -> LDS by direct 16-byte
+// loads through a ring of three stages (one tile in use, two in flight),
+// waited on with a fixed vmcnt.
+//  * S^T = K Q^T on v_mfma_f32_32x32x16_bf16, two 32-key x 32-query tiles;
+//    MFMA row m carries key pk(m) (bits 2 and 3 of m swapped), so lane l
+//    ends holding, for query l % 32, the eight consecutive keys
+//    16 s + 8 (l / 32) .. +7 of each 16-key step s -- exactly the P^T
+//    operand of
+//  * O^T += V^T P^T on the same instruction: its V^T operand is one 16-byte
+//    read of a transposed value row.
+// Each lane's O^T values belong to one query, so the softmax max and sum
+// need one exchange between the two lane halves and the rescale is a
+// per-lane scalar, skipped when no lane's maximum moved.  P enters the matrix
+// core rounded to bf16; the row sum adds the rounded values (bf16 dot).  Keys
+// past the prompt load clamped (real) rows: their scores are masked to -inf
+// by selection, and their values are zeroed in LDS in the last, partial
+// tile, so nothing stale in the cache reaches the sums.  The output goes
+// back through LDS for row-contiguous stores.
 // ---------------------------------------------------------------------------
+__device__ __forceinline__ int pf_key_of_row(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
+
+template <int KC>
+__device__ __forceinline__ int pf_swz(int r, int c)
+{
+    // KC 16-byte chunks per row: 16 (256-byte rows) or 8 (128-byte rows)
+    if constexpr (KC == 16) return r * 16 + (c ^ (r & 15));
+    else return r * 8 + (c ^ ((r >> 1) & 7));
+}
+
 template <int D>
-__global__ __launch_bounds__(256) void k_prefill_attn(const uint16_t *__restrict__ q, int Lp, int nq, int nkv,
+__global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict__ q, int Lp, int nq, int nkv,
                                                       int slot, const uint16_t *__restrict__ kc,
                                                       const uint16_t *__restrict__ vc, KvView kv,
                                                       uint16_t *__restrict__ o)
 {
-    constexpr int BK = 64, QB = D == 128 ? 32 : 64, QT = QB / 16, KK = D / 32, ET = D / 16;
-    constexpr int KLD = D + 8, VLD = BK + 8;
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[BK * KLD];
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VLD];
+    constexpr int NW = 8, NT = 64 * NW;              // wavefronts, threads
+    constexpr int QB = 32, BKT = 64;                  // queries per wavefront, keys per tile
+    constexpr int DT = D / 32, KS = D / 16;           // 32-dim output tiles, 16-dim score steps
+    constexpr int KCH = D / 8;                        // 16-byte chunks per key row
+    constexpr int K_OPS = BKT * KCH / NT, V_OPS = D * 8 / NT, OPS = K_OPS + V_OPS;
+    constexpr int NST = 3, P = NST - 1;
+    constexpr int KSTAGE = BKT * KCH, STAGE = KSTAGE + D * 8;   // 16-byte units
+    constexpr int OPITCH = D + 8;                     // output staging row (elements)
+    static_assert(K_OPS >= 1 && V_OPS >= 1, "tile loads cover the workgroup");
+    static_assert(NW * QB * OPITCH * 2 <= NST * STAGE * 16, "output staging fits the ring");
+    __shared__ __attribute__((aligned(16))) uint4 ring[NST * STAGE];
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
     const int G = nq / nkv;
-    const int kvh = blockIdx.y;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int r16 = lane & 15, kg = lane >> 4;
+    // grid (kv head, unit group): workgroups are dispatched x fastest, so the
+    // groups with the latest (longest) query blocks of every kv head go first
+    const int kvh = blockIdx.x, grp = blockIdx.y;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int r32 = lane & 31, h = lane >> 5;
     const int nqb = (Lp + QB - 1) / QB;
     const int units = nqb * G;
-    const int u = units - 1 - (blockIdx.x * 4 + wave);          // latest blocks first
+    const int u = units - 1 - (grp * NW + wave);                // latest blocks first
     const bool active = u >= 0;
     const int qb = active ? u / G : 0, g = active ? u % G : 0;
     const int hq = kvh * G + g;
     const int q0 = qb * QB;
-    // the workgroup's key range ends at its latest query (its first unit)
-    const int u_first = units - 1 - blockIdx.x * 4;
+    const int u_first = units - 1 - grp * NW;
     const int wg_last_q = min(Lp, (u_first / G + 1) * QB) - 1;
     const int my_last_q = active ? min(Lp, q0 + QB) - 1 : -1;
+    const int ntiles = wg_last_q / BKT + 1;
 
-    // q^T fragments: lane l supplies query q0 + 16 qt + l % 16, dims 32 kk + 8 (l / 16) ..
-    bf16x8 qf[QT][KK];
-    const uint4 z = {0u, 0u, 0u, 0u};
+    // tile loads: op j of thread t is 16-byte unit 512 j + t of the K part
+    // (row / KCH) or of the V^T part (row / 8)
+    typedef __attribute__((address_space(3))) void lds_void;
+    auto issue = [&](int slot_, int k0) {
+        uint4 *base = ring + slot_ * STAGE + wave * 64;
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-        const int qq = q0 + 16 * qt + r16;
+        for (int j = 0; j < K_OPS; ++j) {
+            const int gi = j * NT + tid, r = gi / KCH, c = pf_swz<KCH>(r, gi % KCH) - r * KCH;
+            const int key = min(k0 + r, Lp - 1);
+            __builtin_amdgcn_global_load_lds((const void *)(kc + kv_offset(kv, nkv, D, slot, kvh, key) + 8 * c),
+                                             (lds_void *)(base + j * NT), 16, 0, 0);
+        }
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-            uint4 v = z;
-            if (active && qq < Lp) v = *(const uint4 *)(q + (size_t)qq * nq * D + (size_t)hq * D + 32 * kk + 8 * kg);
-            qf[qt][kk] = __builtin_bit_cast(bf16x8, v);
+        for (int j = 0; j < V_OPS; ++j) {
+            const int gi = j * NT + tid, e = gi >> 3, c = pf_swz<8>(e, gi & 7) - e * 8;
+            const int key0 = min(k0 + 8 * c, (Lp - 1) & ~7);
+            __builtin_amdgcn_global_load_lds((const void *)(vc + v_offset(kv, nkv, D, slot, kvh, key0, e)),
+                                             (lds_void *)(base + KSTAGE + j * NT), 16, 0, 0);
+        }
+    };
+
+    // Q^T operand: lane l supplies query q0 + l % 32, dims 16 s + 8 (l / 32) .. +7
+    bf16x8 qf[KS];
+    {
+        const int qq = q0 + r32;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            uint4 v = {0u, 0u, 0u, 0u};
+            if (active && qq < Lp) v = *(const uint4 *)(q + (size_t)qq * nq * D + (size_t)hq * D + 16 * ks + 8 * h);
+            qf[ks] = __builtin_bit_cast(bf16x8, v);
         }
     }
-    f32x4 acc[QT][ET];
+    f32x16 acc[DT];
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt)
+    for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int et = 0; et < ET; ++et) acc[qt][et] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    float mrow[QT], lpart[QT];
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-        mrow[qt] = -INFINITY;
-        lpart[qt] = 0.f;
-    }
-    const float scale = 1.0f / sqrtf((float)D);
+        for (int j = 0; j < 16; ++j) acc[dt][j] = 0.f;
+    float mrow = -INFINITY, lpart = 0.f;
+    const float scale2 = 1.4426950408889634f / sqrtf((float)D);   // log2(e) / sqrt(d)
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    const int qq = q0 + r32;
 
-    for (int k0 = 0; k0 <= wg_last_q; k0 += BK) {
-        // stage K rows and transposed V of keys k0 .. k0+63
-        __syncthreads();
-        for (int it = threadIdx.x; it < BK * (D / 8); it += 256) {
-            const int key = it / (D / 8), ch = it % (D / 8);
-            uint4 v = z;
-            if (k0 + key < Lp) v = *(const uint4 *)(kc + kv_offset(kv, nkv, D, slot, kvh, k0 + key) + ch * 8);
-            *(uint4 *)(&Ks[key * KLD + ch * 8]) = v;
-        }
-        for (int it = threadIdx.x; it < D * (BK / 8); it += 256) {
-            // eight consecutive keys of one dimension of the transposed value cache
-            const int e = it / (BK / 8), kc8 = (it % (BK / 8)) * 8;
-            const int key0 = k0 + kc8;
-            uint4 v = z;
-            if (key0 < Lp) {
-                v = *(const uint4 *)(vc + v_offset(kv, nkv, D, slot, kvh, key0, e));
-                const int nv = Lp - key0;           // zero the keys past the prompt
-                uint32_t *w = (uint32_t *)&v;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if (2 * j >= nv) w[j] = 0u;
-                    else if (2 * j + 1 >= nv) w[j] &= 0x0000ffffu;
-                }
+    for (int i = 0; i < P; ++i)
+        if (i < ntiles) issue(i, i * BKT);
+    for (int i = 0; i < ntiles; ++i) {
+        wait_stages<OPS, P - 1>(min(P - 1, ntiles - 1 - i));
+        lds_barrier();
+        const int k0 = i * BKT;
+        uint4 *Kt = ring + (i % NST) * STAGE;
+        uint4 *Vt = Kt + KSTAGE;
+        if (k0 + BKT > Lp) {
+            // last tile: zero the values of keys past the prompt
+            uint16_t *v16 = (uint16_t *)Vt;
+            for (int it = tid; it < D * BKT; it += NT) {
+                const int e = it / BKT, kk = it % BKT;
+                if (k0 + kk >= Lp) v16[pf_swz<8>(e, kk >> 3) * 8 + (kk & 7)] = 0;
             }
-            *(uint4 *)(&Vt[e * VLD + kc8]) = v;
+            lds_barrier();
         }
-        __syncthreads();
-        if (k0 > my_last_q) continue;                 // wave-uniform: all keys of this tile are in our future
+        if (i + P < ntiles) issue((i + P) % NST, (i + P) * BKT);
+        if (k0 > my_last_q) continue;                 // wave-uniform: the whole tile is in this unit's future
 
-        // scores
-        f32x4 st[QT][4];
+        f32x16 st[2];
 #pragma unroll
-        for (int qt = 0; qt < QT; ++qt)
+        for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int t = 0; t < 4; ++t) st[qt][t] = (f32x4){0.f, 0.f, 0.f, 0.f};
+            for (int j = 0; j < 16; ++j) st[kt][j] = 0.f;
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+        for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-            for (int kk = 0; kk < KK; ++kk) {
-                const bf16x8 kf = *(const bf16x8 *)(&Ks[(16 * t + r16) * KLD + 32 * kk + 8 * kg]);
-#pragma unroll
-                for (int qt = 0; qt < QT; ++qt)
-                    st[qt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[qt][kk], st[qt][t], 0, 0, 0);
+            for (int kt = 0; kt < 2; ++kt) {
+                const bf16x8 kf = __builtin_bit_cast(bf16x8, Kt[pf_swz<KCH>(32 * kt + pf_key_of_row(r32), 2 * ks + h)]);
+                st[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], st[kt], 0, 0, 0);
             }
-        // online softmax per query (column l % 16)
-        s16x4 pb[QT][4];
+        // online softmax in base 2; lane holds keys k0 + 32 kt + 16 (j / 8) + 8 h + j % 8
+        // of query qq; only tiles reaching past the wavefront's first query or
+        // past the prompt need the mask
+        float mt = -INFINITY;
+        if (k0 + BKT - 1 > q0 || k0 + BKT > Lp) {
 #pragma unroll
-        for (int qt = 0; qt < QT; ++qt) {
-            const int qq = q0 + 16 * qt + r16;
-            float mt = -INFINITY;
+            for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int key = k0 + 16 * t + 4 * kg + i;
-                    const float sv = key <= qq ? st[qt][t][i] * scale : -INFINITY;
-                    st[qt][t][i] = sv;
+                for (int j = 0; j < 16; ++j) {
+                    const int key = k0 + 32 * kt + 16 * (j >> 3) + 8 * h + (j & 7);
+                    const float sv = (key <= qq && key < Lp) ? st[kt][j] : -INFINITY;
+                    st[kt][j] = sv;
                     mt = fmaxf(mt, sv);
                 }
-            mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-            mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-            const float mnew = fmaxf(mrow[qt], mt);
-            // a query with no visible key yet in this tile keeps mnew = -inf: its p are 0
-            const float alpha = mnew == -INFINITY ? 1.f : __expf(mrow[qt] - mnew);
-            float ls = 0.f;
+        } else {
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                uint16_t pv[4];
+            for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    // rounded to bf16 for the matrix core; summed as rounded
-                    pv[i] = f2bf(mnew == -INFINITY ? 0.f : __expf(st[qt][t][i] - mnew));
-                    ls += bf2f(pv[i]);
-                }
-                pb[qt][t] = (s16x4){(short)pv[0], (short)pv[1], (short)pv[2], (short)pv[3]};
-            }
-            lpart[qt] = lpart[qt] * alpha + ls;
-            mrow[qt] = mnew;
-#pragma unroll
-            for (int et = 0; et < ET; ++et) {
-                acc[qt][et][0] *= alpha;
-                acc[qt][et][1] *= alpha;
-                acc[qt][et][2] *= alpha;
-                acc[qt][et][3] *= alpha;
-            }
+                for (int j = 0; j < 16; ++j) mt = fmaxf(mt, st[kt][j]);
         }
-        // O^T += V^T P^T
+        mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+        // running maximum in scaled units (scale2 > 0 keeps the order)
+        const float mnew = fmaxf(mrow, mt * scale2);
+        // a query with no visible key yet keeps mnew = -inf: its weights are 0
+        const float moff = mnew == -INFINITY ? 0.f : mnew;
+        float ls = 0.f;
+        bf16x8 pf[4];
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+        for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-            for (int et = 0; et < ET; ++et) {
-                const s16x4 vf = *(const s16x4 *)(&Vt[(16 * et + r16) * VLD + 16 * t + 4 * kg]);
+            for (int half = 0; half < 2; ++half) {
+                uint32_t w[4];
 #pragma unroll
-                for (int qt = 0; qt < QT; ++qt)
-                    acc[qt][et] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf, pb[qt][t], acc[qt][et], 0, 0, 0);
+                for (int e = 0; e < 4; ++e) {
+                    w[e] = f2bf2(__builtin_amdgcn_exp2f(__builtin_fmaf(st[kt][8 * half + 2 * e], scale2, -moff)),
+                                 __builtin_amdgcn_exp2f(__builtin_fmaf(st[kt][8 * half + 2 * e + 1], scale2, -moff)));
+                    ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[e]), ones, ls, false);   // the rounded weights
+                }
+                pf[2 * kt + half] = __builtin_bit_cast(bf16x8, (uint4){w[0], w[1], w[2], w[3]});
+            }
+        // rescale only when some lane's maximum moved (alpha == 1 exactly otherwise)
+        if (__ballot(mnew != mrow)) {
+            const float alpha = mnew == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(mrow - mnew);
+            lpart *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int j = 0; j < 16; ++j) acc[dt][j] *= alpha;
+        }
+        lpart += ls;
+        mrow = mnew;
+        // O^T += V^T P^T over the tile's four 16-key steps
+#pragma unroll
+        for (int s16 = 0; s16 < 4; ++s16)
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+                const bf16x8 vf = __builtin_bit_cast(bf16x8, Vt[pf_swz<8>(32 * dt + r32, 2 * s16 + h)]);
+                acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[s16], acc[dt], 0, 0, 0);
             }
     }
-    if (!active) return;
-    // lane l holds O^T[dim 16 et + 4 kg + i][query l % 16]
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-        float L = lpart[qt];
-        L += __shfl_xor(L, 16, 64);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    lds_barrier();                                    // every wavefront is done with the ring
+
+    // lane holds O^T[d = 32 dt + 8 (j / 4) + 4 h + j % 4][query l % 32]:
+    // normalise, round, stage as [query][d] rows, store rows contiguously
+    uint16_t *ost = (uint16_t *)ring + (size_t)wave * QB * OPITCH;
+    {
+        float L = lpart;
         L += __shfl_xor(L, 32, 64);
-        const int qq = q0 + 16 * qt + r16;
-        if (qq >= Lp) continue;
-        uint16_t *orow = o + (size_t)qq * nq * D + (size_t)hq * D;
+        const float inv = 1.0f / L;
 #pragma unroll
-        for (int et = 0; et < ET; ++et)
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) orow[16 * et + 4 * kg + i] = f2bf(acc[qt][et][i] / L);
+            for (int j = 0; j < 16; ++j)
+                ost[r32 * OPITCH + 32 * dt + 8 * (j >> 2) + 4 * h + (j & 3)] = f2bf(acc[dt][j] * inv);
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);               // lgkmcnt(0): this wavefront's staging writes are done
+    if (!active) return;
+#pragma unroll 4
+    for (int it = lane; it < QB * (D / 8); it += 64) {
+        const int qr = it / (D / 8), c8 = it % (D / 8);
+        const int qo = q0 + qr;
+        if (qo < Lp)
+            *(uint4 *)(o + (size_t)qo * nq * D + (size_t)hq * D + 8 * c8) = *(const uint4 *)(ost + qr * OPITCH + 8 * c8);
     }
 }
 
 hipError_t launch_prefill_attn(const uint16_t *q, int Lp, int nq, int nkv, int d, int slot, const uint16_t *kc,
                                const uint16_t *vc, KvView kv, uint16_t *o, hipStream_t st)
 {
+    if (Lp <= 0) return hipErrorInvalidValue;
     const int G = nq / nkv;
-    const int qb = d == 128 ? 32 : 64;
-    const int units = ((Lp + qb - 1) / qb) * G;
-    dim3 grid((units + 3) / 4, nkv);
+    const int units = ((Lp + 31) / 32) * G;
+    dim3 grid(nkv, (units + 7) / 8);
     if (d == 128)
-        hipLaunchKernelGGL((k_prefill_attn<128>), grid, dim3(256), 0, st, q, Lp, nq, nkv, slot, kc, vc, kv, o);
+        hipLaunchKernelGGL((k_prefill_attn<128>), grid, dim3(512), 0, st, q, Lp, nq, nkv, slot, kc, vc, kv, o);
     else if (d == 64)
-        hipLaunchKernelGGL((k_prefill_attn<64>), grid, dim3(256), 0, st, q, Lp, nq, nkv, slot, kc, vc, kv, o);
+        hipLaunchKernelGGL((k_prefill_attn<64>), grid, dim3(512), 0, st, q, Lp, nq, nkv, slot, kc, vc, kv, o);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
