@@ -217,9 +217,10 @@ corun_status corun_check_batch(const corun_model_cfg *cfg, const corun_kv *kv, c
 
 /* The launch plan an engine would use (host-only, no GPU): fills `out` with
  * up to `cap` int32 values -- B, padded M, then (N, K, split_k, k_chunk,
- * m_tile) for the qkv, o, gate_up, down and lm_head projections (m_tile 0 =
- * the skinny kernel), then the attention chunk and its maximum split count.  Returns the count written or
- * a negative corun_status. */
+ * m_tile, n_tile) for the qkv, o, gate_up, down and lm_head projections
+ * (m_tile 0 = the skinny kernel; n_tile 0 = the LDS-tiled kernel, else the
+ * pipelined kernel's N tile), then the attention chunk and its maximum split
+ * count (32 values).  Returns the count written or a negative corun_status. */
 int32_t corun_describe_plan(const corun_model_cfg *cfg, const corun_kv *kv, int32_t B_fixed,
                             const corun_options *opt, int32_t *out, int32_t cap);
 

@@ -162,9 +162,9 @@ def describe_plan(cfg: dict, kv: KV, B: int, opt: Options | None = None) -> dict
     v = out[:n].tolist()
     plan = {"B": v[0], "Mp": v[1]}
     for i, name in enumerate(("qkv", "o", "gate_up", "down", "lm_head")):
-        N, K, S, Kc, bm = v[2 + 5 * i: 7 + 5 * i]
-        plan[name] = {"N": N, "K": K, "split_k": S, "k_chunk": Kc, "m_tile": bm}
-    plan["attn_chunk"], plan["attn_max_splits"] = v[27], v[28]
+        N, K, S, Kc, bm, bn = v[2 + 6 * i: 8 + 6 * i]
+        plan[name] = {"N": N, "K": K, "split_k": S, "k_chunk": Kc, "m_tile": bm, "n_tile": bn}
+    plan["attn_chunk"], plan["attn_max_splits"] = v[32], v[33]
     return plan
 
 

@@ -72,10 +72,12 @@ int mt_for(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 //    about 2048 wavefronts (8 per CU) so enough weight bytes are in flight,
 //    each split keeping at least 256 K elements.
 //  * M > 64, K % 64 == 0: the pipelined kernel (one workgroup per CU) with
-//    M tile 128 (M <= 128) or 256, N tile 128, or 256 x 256 once those tiles
-//    alone fill the GPU (large prefill; never for the argmax epilogue);
-//    split-K up to one round of at most 256 workgroups, each split keeping
-//    at least 512 K elements.
+//    M tile 128 (M <= 128) or 256 and N tile 128; 256 x 256 tiles (eight
+//    wavefronts) once those tiles alone fill the GPU (large prefill) and for
+//    wide decode projections (M <= 256, N >= 16384, at most 128 such tiles,
+//    not the lm_head: measured faster there with 128-column tiles); split-K
+//    up to one round of at most 256 workgroups, each split keeping at least
+//    512 K elements.
 //  * otherwise (or bm_override > 0): the LDS-tiled kernel with a 128-row
 //    tile (or bm_override), split-K to about two workgroups per CU.
 Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_override, bool argmax = false)
@@ -88,7 +90,9 @@ Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_
     if (M > 64 && bm_override <= 0 && K % 64 == 0) {
         p.bm = M <= 128 ? 128 : 256;
         p.bn = 128;
-        if (M > 256 && !argmax && (long long)((M + 255) / 256) * ((N + 255) / 256) >= 256) p.bn = 256;
+        const long long t256 = (long long)((M + 255) / 256) * ((N + 255) / 256);
+        if (M > 256 && t256 >= 256) p.bn = 256;
+        else if (M > 128 && !argmax && N >= 16384 && t256 <= 128) p.bn = 256;
         const long long tiles = (long long)((M + p.bm - 1) / p.bm) * ((N + p.bn - 1) / p.bn);
         S = tiles >= 256 ? 1 : (int)(256 / tiles);
         S = std::min(S, std::max(1, K / 512));
@@ -296,6 +300,7 @@ extern "C" int32_t corun_describe_plan(const corun_model_cfg *c, const corun_kv 
         v.push_back(pr->S);
         v.push_back(pr->Kc);
         v.push_back(pr->bm);
+        v.push_back(pr->bn);
     }
     v.push_back(p.chunk);
     v.push_back(p.max_splits);

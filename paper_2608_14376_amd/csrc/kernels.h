@@ -72,7 +72,7 @@ hipError_t launch_gemm(const uint16_t *A, int lda, const uint16_t *W, const Gemm
 hipError_t launch_gemm_tiled(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, int bm, float *out,
                              long long split_stride, int ldo, hipStream_t st, ArgBest *amax = nullptr);
 // Pipelined large-M variant (direct global -> LDS loads, 32x32 MFMA tiles):
-// K and Kc multiples of 64 (32 for bn == 256); argmax epilogue with bn == 128 only.
+// K and Kc multiples of 64 (32 for bn == 256).
 hipError_t launch_gemm_dma(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
                            long long split_stride, int ldo, hipStream_t st, ArgBest *amax = nullptr);
 inline int gemm_col_blocks(int N) { return (N + 63) / 64; }

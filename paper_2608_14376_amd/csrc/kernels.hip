@@ -552,8 +552,8 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const uint16_t *__restrict__
 // matter: the 64-byte form roughly halves what one CU can pull while its
 // activation and weight loads share the path.
 //
-// Four wavefronts in a WGM x (4 / WGM) grid; wavefront tile (BM / WGM) x
-// (BN / (4 / WGM)) as 32x32 tiles of v_mfma_f32_32x32x16_bf16.  Every output
+// NW wavefronts in a WGM x (NW / WGM) grid; wavefront tile (BM / WGM) x
+// (BN / (NW / WGM)) as 32x32 tiles of v_mfma_f32_32x32x16_bf16.  Every output
 // element's K reduction runs in one order (K steps in order, each the
 // instruction's fixed 16-term product) whatever its row, so rows stay
 // position-invariant.  Rows >= M and columns >= N load clamped (real) rows
@@ -598,17 +598,19 @@ __device__ __forceinline__ int dma_swz(int r, int c)
     else return r * 8 + (c ^ ((r >> 1) & 7));
 }
 
-template <int BM, int BN, int BK, int NST, int WGM>
-__global__ __launch_bounds__(256) void k_gemm_dma(const uint16_t *__restrict__ A, int lda,
+template <int BM, int BN, int BK, int NST, int WGM, int NW = 4>
+__global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict__ A, int lda,
                                                   const uint16_t *__restrict__ W, int M, int N, int K, int Kc,
                                                   float *__restrict__ out, long long split_stride, int ldo,
                                                   ArgBest *__restrict__ amax)
 {
     constexpr int C = BK / 8;                         // 16-byte chunks per row
-    constexpr int WGN = 4 / WGM;
+    constexpr int NT = 64 * NW;                       // threads
+    constexpr int WGN = NW / WGM;
     constexpr int WM = BM / WGM, WN = BN / WGN;
     constexpr int FM = WM / 32, FN = WN / 32;
-    constexpr int A_OPS = BM * C / 256, W_OPS = BN * C / 256;
+    constexpr int A_OPS = BM * C / NT, W_OPS = BN * C / NT;
+    static_assert(A_OPS * NT == BM * C && W_OPS * NT == BN * C, "loads cover the tile");
     constexpr int OPS = A_OPS + W_OPS, P = NST - 1;
     constexpr int STAGE = (BM + BN) * C;             // 16-byte units
     static_assert(P * OPS <= 63, "vmcnt range");
@@ -642,12 +644,12 @@ __global__ __launch_bounds__(256) void k_gemm_dma(const uint16_t *__restrict__ A
     const uint16_t *wsrc[W_OPS];
 #pragma unroll
     for (int j = 0; j < A_OPS; ++j) {
-        const int g = j * 256 + tid, r = g / C, c = dma_swz<C>(r, g % C) - r * C;   // the swizzle is an involution
+        const int g = j * NT + tid, r = g / C, c = dma_swz<C>(r, g % C) - r * C;   // the swizzle is an involution
         asrc[j] = A + (size_t)min(m0 + r, M - 1) * lda + kbeg + 8 * c;
     }
 #pragma unroll
     for (int j = 0; j < W_OPS; ++j) {
-        const int g = j * 256 + tid, r = g / C, c = dma_swz<C>(r, g % C) - r * C;
+        const int g = j * NT + tid, r = g / C, c = dma_swz<C>(r, g % C) - r * C;
         wsrc[j] = W + (size_t)min(n0 + r, N - 1) * K + kbeg + 8 * c;
     }
     typedef __attribute__((address_space(3))) void lds_void;
@@ -655,10 +657,10 @@ __global__ __launch_bounds__(256) void k_gemm_dma(const uint16_t *__restrict__ A
         uint4 *base = ring + slot * STAGE + wave * 64;
 #pragma unroll
         for (int j = 0; j < A_OPS; ++j)
-            __builtin_amdgcn_global_load_lds((const void *)(asrc[j] + kofs), (lds_void *)(base + j * 256), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds((const void *)(asrc[j] + kofs), (lds_void *)(base + j * NT), 16, 0, 0);
 #pragma unroll
         for (int j = 0; j < W_OPS; ++j)
-            __builtin_amdgcn_global_load_lds((const void *)(wsrc[j] + kofs), (lds_void *)(base + BM * C + j * 256), 16,
+            __builtin_amdgcn_global_load_lds((const void *)(wsrc[j] + kofs), (lds_void *)(base + BM * C + j * NT), 16,
                                              0, 0);
     };
 
@@ -771,21 +773,24 @@ __global__ __launch_bounds__(256) void k_gemm_dma(const uint16_t *__restrict__ A
 hipError_t launch_gemm_dma(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
                            long long split_stride, int ldo, hipStream_t st, ArgBest *amax)
 {
+    // 128-column tiles: four wavefronts (2 x 2, 64-row and 64-column wavefront
+    // tiles), 64-element stages; 256 x 256: eight wavefronts (2 x 4, 128 x 64),
+    // two per SIMD, 32-element stages.  Every configuration has 64-column
+    // wavefront tiles, as the argmax epilogue needs.
     const int bk = g.bn == 256 ? 32 : 64;
     if (g.K % bk != 0 || g.Kc % bk != 0 || g.M <= 0) return hipErrorInvalidValue;
-    if (amax != nullptr && g.bn != 128) return hipErrorInvalidValue;   // argmax epilogue needs 64-column wavefront tiles
     const int num_n = (g.N + g.bn - 1) / g.bn;
     const int num_m = (g.M + g.bm - 1) / g.bm;
     dim3 grid(num_m * num_n, g.S);
     if (g.bm == 128 && g.bn == 128)
-        hipLaunchKernelGGL((k_gemm_dma<128, 128, 64, 4, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
-                           split_stride, ldo, amax);
+        hipLaunchKernelGGL((k_gemm_dma<128, 128, 64, 4, 2, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
+                           out, split_stride, ldo, amax);
     else if (g.bm == 256 && g.bn == 128)
-        hipLaunchKernelGGL((k_gemm_dma<256, 128, 64, 3, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
-                           split_stride, ldo, amax);
+        hipLaunchKernelGGL((k_gemm_dma<256, 128, 64, 3, 2, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
+                           out, split_stride, ldo, amax);
     else if (g.bm == 256 && g.bn == 256)
-        hipLaunchKernelGGL((k_gemm_dma<256, 256, 32, 4, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
-                           split_stride, ldo, amax);
+        hipLaunchKernelGGL((k_gemm_dma<256, 256, 32, 4, 2, 8>), grid, dim3(512), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
+                           out, split_stride, ldo, amax);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

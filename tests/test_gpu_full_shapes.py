@@ -1,0 +1,101 @@
+"""GPU parity at the 8B workload's real per-layer shapes (hidden 4096, 32/8
+heads of 128, FFN 12288, vocabulary 151936) on a two-layer slice: the plan
+-- kernel, tile, split-K, attention chunk -- depends on B, the per-layer
+shapes and the cache capacity only, so these launches are the ones the
+decode and prefill benchmarks time, layer count aside.
+
+* decode at B = 256 with the benchmark's context lengths and cache
+  capacity: sampled live rows against the oracle row by row, and a
+  two-slot swap bitwise;
+* prefill of 600 tokens (past the 512 where the 256 x 256 projection tiles
+  start): sampled positions t are recomputed by the oracle's decode row on
+  the GPU-written cache prefix (teacher forcing), which checks the
+  position's whole computation -- its logits at the last position, its
+  cached key and value everywhere -- without an oracle prefill of 600
+  positions."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_14376_amd import corun
+from paper_2608_14376_amd import workload as wl
+from tests.gpu_helpers import DEV, host_model, row_rel_err
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-2
+B = 256
+CAP = 4144          # the decode benchmark's capacity: contexts up to 4096 plus its steps, rounded to 16
+LP = 600
+
+
+@pytest.fixture(scope="module")
+def full():
+    cfg = dict(wl.config("8b"), n_layers=2)
+    Wg = wl.make_weights(cfg, seed=41, device=DEV)
+    return cfg, Wg, host_model(Wg)
+
+
+def row_cache(K, V, r, cap):
+    return oracle.KVCache([wl.bits(k[r:r + 1]) for k in K], [wl.bits(v[r:r + 1]) for v in V],
+                          oracle.KV_CONTIGUOUS, 1, cap)
+
+
+def test_decode_B256_full_shapes(full):
+    cfg, Wg, m = full
+    K, V = wl.make_kv_contiguous(cfg, B, CAP, seed=42, device=DEV)
+    eng = corun.Engine(cfg, Wg, B, K, V)
+    plan = eng.plan()
+    # the benchmark's configurations: 256 x 256 tiles for gate/up, 256 x 128 elsewhere
+    assert (plan["gate_up"]["m_tile"], plan["gate_up"]["n_tile"]) == (256, 256)
+    assert (plan["qkv"]["m_tile"], plan["qkv"]["n_tile"]) == (256, 128)
+    assert plan["lm_head"]["split_k"] == 1
+    b = wl.make_batch(B, cfg["vocab"], seed=43, len_lo=512, len_hi=4096)
+    live = np.nonzero(b.valid)[0]
+    sample = live[:: max(1, len(live) // 5)][:6]
+    K0 = {int(r): [k[r:r + 1].clone() for k in K] for r in sample}
+    V0 = {int(r): [v[r:r + 1].clone() for v in V] for r in sample}
+    logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+    nxt = eng.decode_step(b.tokens, b.valid, b.seq_lens, logits)
+    gl = logits.cpu().numpy()
+    for r in sample:
+        r = int(r)
+        ref = oracle.decode_row(m, row_cache(K0[r], V0[r], 0, CAP), 0, int(b.tokens[r]), int(b.seq_lens[r]))
+        assert row_rel_err(gl[r], ref) <= TOL, (r, row_rel_err(gl[r], ref))
+    # swap two live requests' slots (tokens, lengths, caches): their rows swap bitwise
+    a, c = int(live[0]), int(live[-1])
+    for l in range(cfg["n_layers"]):
+        ka, va = K[l][a].clone(), V[l][a].clone()
+        K[l][a].copy_(K[l][c]); V[l][a].copy_(V[l][c])
+        K[l][c].copy_(ka); V[l][c].copy_(va)
+    t2, s2 = b.tokens.copy(), b.seq_lens.copy()
+    t2[[a, c]], s2[[a, c]] = t2[[c, a]], s2[[c, a]]
+    ref_logits = logits.clone()
+    # the first step appended each row's new key and value at its own length;
+    # the second step appends the same values there again, so the caches agree
+    nxt2 = eng.decode_step(t2, b.valid, s2, logits)
+    assert nxt2[a] == nxt[c] and nxt2[c] == nxt[a]
+    assert torch.equal(logits[a].view(torch.int32), ref_logits[c].view(torch.int32))
+    assert torch.equal(logits[c].view(torch.int32), ref_logits[a].view(torch.int32))
+
+
+def test_prefill_600_full_shapes_teacher_forced(full):
+    cfg, Wg, m = full
+    cap = 608
+    K, V = wl.make_kv_contiguous(cfg, 2, cap, seed=44, device=DEV)
+    eng = corun.Engine(cfg, Wg, 2, K, V, opt=corun.options(max_prefill_len=LP))
+    prompt = wl.make_prompt(cfg["vocab"], LP, seed=45)
+    last = torch.empty(cfg["vocab"], dtype=torch.float32, device=DEV)
+    eng.prefill(prompt, 1, last)
+    gk = [wl.bits(k[1]) for k in K]          # [nkv, cap, d] per layer
+    gv = [wl.bits(v[1]) for v in V]          # [nkv, d, cap]
+    f32 = lambda a: (a.astype(np.uint32) << 16).view(np.float32)
+    for t in (0, 1, 255, 256, 511, 512, LP - 1):
+        kv1 = row_cache(K, V, 1, cap)        # the GPU-written prefix; position t is recomputed
+        ref = oracle.decode_row(m, kv1, 0, int(prompt[t]), t)
+        for l in range(cfg["n_layers"]):
+            ok, ov = f32(kv1.k[l][0, :, t, :]), f32(kv1.v[l][0, :, :, t])
+            assert np.abs(f32(gk[l][:, t, :]) - ok).max() <= TOL * np.abs(ok).max(), (t, l)
+            assert np.abs(f32(gv[l][:, :, t]) - ov).max() <= TOL * np.abs(ov).max(), (t, l)
+        if t == LP - 1:
+            assert row_rel_err(last.cpu().numpy(), ref) <= TOL
