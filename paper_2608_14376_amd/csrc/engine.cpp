@@ -74,13 +74,12 @@ int mt_for(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 //  * M > 64, K % 64 == 0: the pipelined kernel (one workgroup per CU) with
 //    M tile 128 (M <= 128) or 256 and N tile 128; 256 x 256 tiles (eight
 //    wavefronts) once those tiles alone fill the GPU (large prefill) and for
-//    wide decode projections (M <= 256, N >= 16384, at most 128 such tiles,
-//    not the lm_head: measured faster there with 128-column tiles); split-K
-//    up to one round of at most 256 workgroups, each split keeping at least
-//    512 K elements.
+//    wide decode projections (128 < M <= 256, N >= 16384: gate/up, lm_head);
+//    split-K up to one round of at most 256 workgroups, each split keeping
+//    at least 512 K elements.
 //  * otherwise (or bm_override > 0): the LDS-tiled kernel with a 128-row
 //    tile (or bm_override), split-K to about two workgroups per CU.
-Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_override, bool argmax = false)
+Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_override)
 {
     Proj p;
     p.N = N;
@@ -91,8 +90,7 @@ Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_
         p.bm = M <= 128 ? 128 : 256;
         p.bn = 128;
         const long long t256 = (long long)((M + 255) / 256) * ((N + 255) / 256);
-        if (M > 256 && t256 >= 256) p.bn = 256;
-        else if (M > 128 && !argmax && N >= 16384 && t256 <= 128) p.bn = 256;
+        if ((M > 256 && t256 >= 256) || (M > 128 && M <= 256 && N >= 16384)) p.bn = 256;
         const long long tiles = (long long)((M + p.bm - 1) / p.bm) * ((N + p.bn - 1) / p.bn);
         S = tiles >= 256 ? 1 : (int)(256 / tiles);
         S = std::min(S, std::max(1, K / 512));
@@ -154,8 +152,8 @@ Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_
     }
     // lm_head: never split (its epilogue selects the argmax partials) except
     // under the split override test aid; the 64-row tile has no argmax epilogue
-    p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0, bo == 64 ? 0 : bo, true);
-    if (p.lm.bm == 64) p.lm = choose_proj(c->vocab, H, 64, so > 0 ? so : 1, 0, 0, true);
+    p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0, bo == 64 ? 0 : bo);
+    if (p.lm.bm == 64) p.lm = choose_proj(c->vocab, H, 64, so > 0 ? so : 1, 0, 0);
     const int cap = kv_capacity(kv);
     p.chunk = choose_chunk(B, c->n_kv_heads, cap, opt.attn_chunk);
     p.max_splits = (cap + p.chunk - 1) / p.chunk;

@@ -743,29 +743,41 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
                 if (row < M) o[(size_t)row * ldo + col] = acc[a][b][q];
             }
         }
-    if constexpr (WN == 64) {
-        if (amax != nullptr) {   // per row: best over this wavefront's 64 columns (one 64-column block)
-            const int ncb = (N + 63) / 64;
+    // every configuration the launcher uses has 64-column wavefront tiles
+    if (WN == 64 && amax != nullptr) {
+        // per row: best (value, column) over this wavefront's 64 columns (one
+        // 64-column block).  Each 32-row fragment goes through the wavefront's
+        // own padded 32 x 68 float tile in the (now idle) ring; lane l scans
+        // half a row, columns in increasing order, then the two halves meet.
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        lds_barrier();                                // every wavefront is done reading the ring
+        constexpr int TP = 68;
+        static_assert(NW * 32 * TP * 4 <= NST * STAGE * 16, "argmax staging fits the ring");
+        float *T = reinterpret_cast<float *>(ring) + wave * 32 * TP;
+        const int ncb = (N + 63) / 64;
+        const int rr = lane >> 1, hf = lane & 1;
 #pragma unroll
-            for (int a = 0; a < FM; ++a)
+        for (int a = 0; a < FM; ++a) {
 #pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    float bv = -INFINITY;
-                    int bi = 0x7fffffff;
+            for (int b = 0; b < FN; ++b)
 #pragma unroll
-                    for (int b = 0; b < FN; ++b) {
-                        const int col = n0 + wn0 + 32 * b + r32;
-                        if (col < N) better(bv, bi, acc[a][b][q], col);
-                    }
+                for (int q = 0; q < 16; ++q) T[(8 * (q >> 2) + 4 * h + (q & 3)) * TP + 32 * b + r32] = acc[a][b][q];
+            float bv = -INFINITY;
+            int bi = 0x7fffffff;
 #pragma unroll
-                    for (int off = 1; off < 32; off <<= 1) {
-                        const float v2 = __shfl_xor(bv, off, 64);
-                        const int i2 = __shfl_xor(bi, off, 64);
-                        better(bv, bi, v2, i2);
-                    }
-                    const int row = m0 + wm0 + 32 * a + 8 * (q >> 2) + 4 * h + (q & 3);
-                    if (r32 == 0 && row < M && n0 + wn0 < N) amax[(size_t)row * ncb + (n0 + wn0) / 64] = ArgBest{bv, bi};
-                }
+            for (int i = 0; i < 8; ++i) {
+                const float4 v = *reinterpret_cast<const float4 *>(T + rr * TP + 32 * hf + 4 * i);
+                const int col = n0 + wn0 + 32 * hf + 4 * i;
+                if (col + 0 < N) better(bv, bi, v.x, col + 0);
+                if (col + 1 < N) better(bv, bi, v.y, col + 1);
+                if (col + 2 < N) better(bv, bi, v.z, col + 2);
+                if (col + 3 < N) better(bv, bi, v.w, col + 3);
+            }
+            const float v2 = __shfl_xor(bv, 1, 64);
+            const int i2 = __shfl_xor(bi, 1, 64);
+            better(bv, bi, v2, i2);
+            const int row = m0 + wm0 + 32 * a + rr;
+            if (hf == 0 && row < M && n0 + wn0 < N) amax[(size_t)row * ncb + (n0 + wn0) / 64] = ArgBest{bv, bi};
         }
     }
 }

@@ -46,10 +46,11 @@ def test_decode_B256_full_shapes(full):
     K, V = wl.make_kv_contiguous(cfg, B, CAP, seed=42, device=DEV)
     eng = corun.Engine(cfg, Wg, B, K, V)
     plan = eng.plan()
-    # the benchmark's configurations: 256 x 256 tiles for gate/up, 256 x 128 elsewhere
+    # the benchmark's configurations: 256 x 256 tiles for gate/up and the
+    # lm_head (with its argmax epilogue), 256 x 128 elsewhere
     assert (plan["gate_up"]["m_tile"], plan["gate_up"]["n_tile"]) == (256, 256)
+    assert (plan["lm_head"]["m_tile"], plan["lm_head"]["n_tile"], plan["lm_head"]["split_k"]) == (256, 256, 1)
     assert (plan["qkv"]["m_tile"], plan["qkv"]["n_tile"]) == (256, 128)
-    assert plan["lm_head"]["split_k"] == 1
     b = wl.make_batch(B, cfg["vocab"], seed=43, len_lo=512, len_hi=4096)
     live = np.nonzero(b.valid)[0]
     sample = live[:: max(1, len(live) // 5)][:6]
