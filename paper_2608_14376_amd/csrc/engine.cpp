@@ -121,11 +121,12 @@ Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_
 GemmShape shape_of(const Proj &p, int M) { return GemmShape{M, p.N, p.K, p.S, p.Kc, mt_for(M), p.bm, p.bn}; }
 
 // Attention chunk: fixed per engine from (B, kv heads, capacity): enough
-// (row, head, split) blocks to fill the GPU when every row is at capacity.
+// (row, head, split) blocks to fill the GPU when every row is at capacity,
+// and at least 128 tokens.
 int choose_chunk(int B, int nkv, int cap, int override_chunk)
 {
     if (override_chunk > 0) return override_chunk;
-    int chunk = 64;
+    int chunk = 128;   // below 128 tokens some of the four wavefronts get no 32-token block
     while (chunk < 1024 && (long long)B * nkv * ((cap + chunk - 1) / chunk) > 4096) chunk *= 2;
     return chunk;
 }

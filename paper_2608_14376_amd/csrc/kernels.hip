@@ -1154,59 +1154,81 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
 }
 
 // Merge of a row's splits in split order.  Block (kvh, row), 256 threads.
-// Per head: exact maximum over the splits, weights f_s = exp(m_s - M) in
-// LDS, L = sum_s l_s f_s walked in split order by one thread, and each output
-// element's sum over s walked in split order (loads issued 8 ahead).
+// Every split's (max, sum) pair is loaded in one round into LDS; per head
+// the exact maximum M over the splits, weights f_s = exp(m_s - M) and
+// L = sum_s l_s f_s walked in split order by one thread; then each thread
+// folds its E output elements over the splits in split order, eight splits'
+// loads issued ahead of the adds, and writes A / L in bf16.
 template <int D, int G>
 __global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ ws, const uint8_t *__restrict__ valid,
                                                     const int32_t *__restrict__ pos, int nq, int nkv, int chunk,
                                                     int max_splits, uint16_t *__restrict__ o)
 {
+    constexpr int E = (G * D + 255) / 256;           // output elements per thread
     const int kvh = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
     uint16_t *orow = o + (size_t)r * nq * D + (size_t)kvh * G * D;
     if (valid != nullptr && !valid[r]) {
         for (int i = tid; i < G * D; i += 256) orow[i] = 0;
         return;
     }
-    extern __shared__ float fs[];          // [G][max_splits] weights, then [G] sums
-    float *Ls = fs + G * max_splits;
-    __shared__ float red[4];
+    extern __shared__ float fs[];          // [G][ns] maxima then weights, [G][ns] sums, [G] M, [G] L
     const int n = pos[r] + 1;
     const int ns = (n + chunk - 1) / chunk;
+    float *fm = fs, *fl = fs + G * max_splits, *Mg = fl + G * max_splits, *Lg = Mg + G;
     const int stride = G * (D + 2);
     const float *base = ws + ((size_t)r * nkv + kvh) * max_splits * stride;
-    for (int g = 0; g < G; ++g) {
-        float m = -INFINITY;
-        for (int sp = tid; sp < ns; sp += 256) m = fmaxf(m, base[sp * stride + g]);
-        m = wave_max(m);
-        __syncthreads();
-        if ((tid & 63) == 0) red[tid >> 6] = m;
-        __syncthreads();
-        const float M = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-        for (int sp = tid; sp < ns; sp += 256) fs[g * max_splits + sp] = __expf(base[sp * stride + g] - M);
+    for (int idx = tid; idx < G * ns; idx += 256) {
+        const int g = idx / ns, sp = idx - g * ns;
+        fm[idx] = base[(size_t)sp * stride + g];
+        fl[idx] = base[(size_t)sp * stride + G + g];
     }
     __syncthreads();
     if (tid < G) {
-        float L = 0.f;
-        for (int sp = 0; sp < ns; ++sp) L += base[sp * stride + G + tid] * fs[tid * max_splits + sp];
-        Ls[tid] = L;
+        float M = -INFINITY;
+        for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, fm[tid * ns + sp]);
+        Mg[tid] = M;
     }
     __syncthreads();
-    for (int idx = tid; idx < G * D; idx += 256) {
-        const int g = idx / D;
-        const float *a = base + 2 * G + idx;
-        const float *f = fs + g * max_splits;
-        float acc = 0.f;
-        int sp = 0;
-        for (; sp + 8 <= ns; sp += 8) {
-            float v[8];
+    for (int idx = tid; idx < G * ns; idx += 256) fm[idx] = __expf(fm[idx] - Mg[idx / ns]);
+    __syncthreads();
+    if (tid < G) {
+        float L = 0.f;
+        for (int sp = 0; sp < ns; ++sp) L += fl[tid * ns + sp] * fm[tid * ns + sp];
+        Lg[tid] = L;
+    }
+    __syncthreads();
+    float acc[E];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) v[u] = a[(size_t)(sp + u) * stride];
+    for (int e = 0; e < E; ++e) acc[e] = 0.f;
+    const float *a = base + 2 * G;
+    int sp = 0;
+    for (; sp + 8 <= ns; sp += 8) {
+        float v[8][E];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) acc += v[u] * f[sp + u];
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const int idx = tid + 256 * e;
+                v[u][e] = idx < G * D ? a[(size_t)(sp + u) * stride + idx] : 0.f;
+            }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const int idx = tid + 256 * e;
+                if (idx < G * D) acc[e] += v[u][e] * fm[(idx / D) * ns + sp + u];
+            }
+    }
+    for (; sp < ns; ++sp)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int idx = tid + 256 * e;
+            if (idx < G * D) acc[e] += a[(size_t)sp * stride + idx] * fm[(idx / D) * ns + sp];
         }
-        for (; sp < ns; ++sp) acc += a[(size_t)sp * stride] * f[sp];
-        orow[idx] = f2bf(acc / Ls[g]);
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int idx = tid + 256 * e;
+        if (idx < G * D) orow[idx] = f2bf(acc[e] / Lg[idx / D]);
     }
 }
 
@@ -1223,7 +1245,7 @@ template <int D, int G>
 static void launch_merge_dg(const float *ws, int rows, const uint8_t *valid, const int32_t *pos, int nq,
                             int nkv, int chunk, int max_splits, uint16_t *o, hipStream_t st)
 {
-    const size_t shm = sizeof(float) * (G * max_splits + G);
+    const size_t shm = sizeof(float) * (2 * G * max_splits + 2 * G);
     hipLaunchKernelGGL((k_attn_merge<D, G>), dim3(nkv, rows), dim3(256), shm, st, ws, valid, pos, nq, nkv, chunk,
                        max_splits, o);
 }
