@@ -236,6 +236,30 @@ def bitexact_check(cfg, res, n_pairs=2):
     return dict(pairs=n_pairs, identical=ok)
 
 
+def time_sampler(cfg, res, iters=20):
+    """Request-bound seeded sampling of the headline batch's B rows of
+    logits (temperature 0.6, per-row seeds), end to end through
+    corun_sample: host arrays in, tokens and log-probabilities out (H2D,
+    the sampling kernel, D2H, one synchronisation)."""
+    import torch
+    eng, B, med = res["_eng"], res["B"], res["_med"]
+    b = med["batch"]
+    logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device="cuda")
+    eng.decode_step(b.tokens, b.valid, b.seq_lens, logits)
+    pos = (b.seq_lens.astype(np.int64) + 1).astype(np.int32)
+    seeds = np.arange(B, dtype=np.uint64) * np.uint64(2654435761) + np.uint64(42)
+    temp = np.full(B, 0.6, np.float32)
+    eng.sample(logits, b.valid, pos, seeds, temp)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for _ in range(iters):
+        eng.sample(logits, b.valid, pos, seeds, temp)
+    dt = (time.perf_counter() - t) / iters
+    del logits
+    return dict(B=B, rows_live=int(b.valid.sum()), ms_per_call=round(1e3 * dt, 4), temperature=0.6,
+                note="host arrays in, tokens + log-probabilities out; one synchronisation")
+
+
 def cpu_baseline(cfg, W, res, budget_s=12.0):
     """The oracle (plain C, fp64 between bf16 storage points, row by row) on
     a bounded sample: the first 2 of 36 layers plus lm_head for live rows of
@@ -355,6 +379,8 @@ def main():
                  measure_kernels=True)
     bitexact = bitexact_check(cfg, head)
     log(f"[bench] bit-exact across batch mixes: {bitexact}")
+    sampler = time_sampler(cfg, head)
+    log(f"[bench] seeded sampler at B={sampler['B']}: {sampler['ms_per_call']} ms per call")
     cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, W, head)
     if cpu:
         log(f"[bench] cpu oracle: {cpu['value']} tok/s on {cpu['cores']} threads")
@@ -426,6 +452,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "bitexact_across_batch_mixes": bitexact,
+        "sampler": sampler,
         "headline": head,
         "sweep": sweep,
         "extra": extra,

@@ -177,6 +177,33 @@ corun_status corun_decode_run(corun_engine *e, int32_t n_steps, const int32_t *t
 corun_status corun_prefill(corun_engine *e, const int32_t *prompt, int32_t prompt_len, int32_t slot,
                            int32_t *token_out, float *last_logits);
 
+/* Request-bound seeded multinomial sampling (Sec. IV, "Shape-Aligned
+ * Sampling"; y_t = S(l_t, R(s, t)) in Sec. IV, "Determinism Argument"), run on
+ * logits that corun_decode_step (rows = B, the fixed shape) or corun_prefill
+ * (rows = 1) wrote to a caller buffer.  The random variate of row r is a
+ * function of (seeds[r], positions[r], column) only: u_v from Philox4x32-10
+ * (Salmon et al., SC 2011) keyed by the 64-bit seed with counter
+ * (positions[r], v, 0, 0), u = ((w0 >> 6) 2^26 + (w1 >> 6) + 1/2) 2^-52 from
+ * its first two words, so no RNG state exists to be consumed, and
+ * padding rows and co-runners cannot move a request's stream.
+ *  token[r]   = argmax_v ( l[r][v] / T_r + g_v ), g_v = -ln(-ln u_v)
+ *               (the Gumbel-max rule: an exact draw from softmax(l / T));
+ *               greedy (argmax l, lowest index) where T_r <= 0;
+ *  logprob[r] = log softmax(l[r] / T_r)[token[r]] (softmax(l[r]) if greedy),
+ * decided and summed in fp64 with a fixed reduction order.
+ *  logits_dev   device fp32 [rows][ld], ld >= vocab (caller-owned)
+ *  valid        host uint8 [rows]; invalid rows get token -1, logprob 0
+ *  positions    host int32 [rows]: position of the token being sampled
+ *               (seq_len + 1 after a decode step, prompt_len after prefill)
+ *  seeds        host uint64 [rows]; temperature host float [rows]
+ *  tokens_out   host int32 [rows]; logprobs_out host float [rows] or NULL
+ * Errors: CORUN_E_SHAPE for rows outside [1, B] or ld < vocab; CORUN_E_INVAL
+ * for a null pointer, a negative position or a non-finite temperature of a
+ * valid row.  Runs on the engine's stream after the caller's stream. */
+corun_status corun_sample(corun_engine *e, const float *logits_dev, int64_t ld, int32_t rows,
+                          const uint8_t *valid, const int32_t *positions, const uint64_t *seeds,
+                          const float *temperature, int32_t *tokens_out, float *logprobs_out);
+
 /* Kernels that corun_time_kernel can time. */
 enum {
     CORUN_K_QKV_GEMM = 0,     /* QKV projection (split-K partials) */

@@ -95,6 +95,13 @@ def lib():
         L.orc_prefill.restype = C.c_int
         L.orc_prefill.argtypes = [C.POINTER(_Cfg), C.POINTER(_Weights), C.POINTER(_KV), C.c_int,
                                   C.c_void_p, C.c_int, C.c_void_p, C.c_void_p]
+        L.orc_philox4x32_10.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p]
+        L.orc_uniform.restype = C.c_double
+        L.orc_uniform.argtypes = [C.c_uint32, C.c_uint32]
+        L.orc_gumbel.restype = C.c_double
+        L.orc_gumbel.argtypes = [C.c_uint64, C.c_int32, C.c_int32]
+        L.orc_sample.restype = C.c_int
+        L.orc_sample.argtypes = [C.c_void_p, C.c_int, C.c_uint64, C.c_int32, C.c_float, C.c_void_p, C.c_void_p]
         L.orc_set_threads.argtypes = [C.c_int]
         L.orc_get_threads.restype = C.c_int
         _lib = L
@@ -179,6 +186,34 @@ def silu(z: float) -> float:
 def argmax_f32(v: np.ndarray) -> int:
     v = np.ascontiguousarray(v, np.float32)
     return int(lib().orc_argmax_f32(_ptr(v), v.size))
+
+
+def philox4x32_10(ctr, key) -> np.ndarray:
+    """Philox4x32-10 block: four 32-bit counter words, two key words."""
+    c = np.ascontiguousarray(ctr, np.uint32)
+    k = np.ascontiguousarray(key, np.uint32)
+    out = np.empty(4, np.uint32)
+    lib().orc_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def uniform(w0: int, w1: int) -> float:
+    return float(lib().orc_uniform(w0, w1))
+
+
+def gumbel(seed: int, t: int, v: int) -> float:
+    """g_v = -ln(-ln u_v) of R(seed, t)."""
+    return float(lib().orc_gumbel(seed, t, v))
+
+
+def sample(logits: np.ndarray, seed: int, t: int, temperature: float):
+    """S(l, R(seed, t)): (token, log-probability) by the Gumbel-max rule."""
+    l = np.ascontiguousarray(logits, np.float32)
+    tok = np.empty(1, np.int32)
+    lp = np.empty(1, np.float64)
+    if lib().orc_sample(_ptr(l), l.size, seed, t, temperature, _ptr(tok), _ptr(lp)):
+        raise ValueError("empty logits")
+    return int(tok[0]), float(lp[0])
 
 
 def route(logits: np.ndarray, top_k: int):

@@ -490,6 +490,95 @@ int orc_prefill(const orc_cfg *c, const orc_weights *w, const orc_kv *kv, int sl
     return 0;
 }
 
+/* ---------------------------------------------------------------------------
+ * Request-bound seeded sampling (Sec. IV, "Shape-Aligned Sampling"; the
+ * determinism argument's y_t = S(l_t, R(s, t)), Sec. IV "Determinism
+ * Argument").  The paper fixes the properties -- the random variate is a
+ * function of the request's seed s and step t only, padding consumes
+ * nothing, identical logits and variate give the identical token -- but not
+ * the generator or the rule.  Reading used here:
+ *   R(s, t) = { u_v : v < V }, u_v from Philox4x32-10 keyed by the 64-bit
+ *             seed with counter (t, v, 0, 0), t = the position of the token
+ *             being sampled (a function of the request's own state);
+ *   S(l, R) = argmax_v ( l_v / T + g_v ), g_v = -ln(-ln u_v)  (Gumbel-max:
+ *             an exact draw from softmax(l / T)); ties to the lower index;
+ *             T <= 0 is the greedy rule (no noise).
+ * Decision and log-probability in fp64.
+ * ------------------------------------------------------------------------- */
+
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as
+ * easy as 1, 2, 3", SC 2011): ten rounds over four 32-bit words; each round
+ * takes the two 64-bit products M0 c0 and M1 c2 and sets
+ *   (c0, c1, c2, c3) <- (hi(M1 c2) ^ c1 ^ k0, lo(M1 c2), hi(M0 c0) ^ c3 ^ k1, lo(M0 c0)),
+ * the key advancing by the Weyl constants (W0, W1) before every round but
+ * the first. */
+void orc_philox4x32_10(const uint32_t *ctr, const uint32_t *key, uint32_t *out)
+{
+    const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u, W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3], k0 = key[0], k1 = key[1];
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) {
+            k0 += W0;
+            k1 += W1;
+        }
+        const uint64_t p0 = (uint64_t)M0 * c0, p1 = (uint64_t)M1 * c2;
+        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0, n1 = (uint32_t)p1;
+        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1, n3 = (uint32_t)p0;
+        c0 = n0;
+        c1 = n1;
+        c2 = n2;
+        c3 = n3;
+    }
+    out[0] = c0;
+    out[1] = c1;
+    out[2] = c2;
+    out[3] = c3;
+}
+
+/* A uniform double strictly inside (0, 1) from 52 bits of two words:
+ * ((w0 >> 6) 2^26 + (w1 >> 6) + 1/2) 2^-52, in [2^-53, 1 - 2^-53] (every
+ * value exactly representable: the integer part needs 53 bits). */
+double orc_uniform(uint32_t w0, uint32_t w1)
+{
+    return ((double)(w0 >> 6) * 67108864.0 + (double)(w1 >> 6) + 0.5) * (1.0 / 4503599627370496.0);
+}
+
+/* u_v and g_v of R(s, t) for one column v. */
+double orc_gumbel(uint64_t seed, int32_t t, int32_t v)
+{
+    const uint32_t ctr[4] = {(uint32_t)t, (uint32_t)v, 0u, 0u};
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t w[4];
+    orc_philox4x32_10(ctr, key, w);
+    return -log(-log(orc_uniform(w[0], w[1])));
+}
+
+/* S(l, R(s, t)) for one row of V logits; the log-probability of the chosen
+ * token under softmax(l / T) (softmax(l) when T <= 0), sums sequential in v. */
+int orc_sample(const float *logits, int V, uint64_t seed, int32_t t, float temperature, int32_t *token,
+               double *logprob)
+{
+    if (V <= 0) return -1;
+    const int greedy = !(temperature > 0.0f);
+    const double T = greedy ? 1.0 : (double)temperature;
+    int best = 0;
+    double bz = -INFINITY, M = -INFINITY;
+    for (int v = 0; v < V; ++v) {
+        const double x = (double)logits[v] / T;
+        const double z = greedy ? x : x + orc_gumbel(seed, t, v);
+        if (z > bz) {
+            bz = z;
+            best = v;
+        }
+        if (x > M) M = x;
+    }
+    double S = 0.0;
+    for (int v = 0; v < V; ++v) S += exp((double)logits[v] / T - M);
+    *token = best;
+    *logprob = (double)logits[best] / T - M - log(S);
+    return 0;
+}
+
 void orc_set_threads(int n)
 {
 #ifdef _OPENMP

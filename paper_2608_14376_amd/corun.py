@@ -20,7 +20,7 @@ KV_CONTIGUOUS, KV_PAGED = 0, 1
 
 EXPORTS = ("corun_engine_create", "corun_engine_destroy", "corun_decode_step", "corun_decode_run",
            "corun_prefill", "corun_check_config", "corun_check_batch", "corun_describe_plan",
-           "corun_last_error", "corun_time_kernel")
+           "corun_last_error", "corun_time_kernel", "corun_sample")
 
 # kernel ids of corun_time_kernel
 K_QKV_GEMM, K_O_GEMM, K_GATE_UP_GEMM, K_DOWN_GEMM, K_LM_HEAD, K_ATTN_SPLIT, K_ATTN_MERGE, K_RMSNORM, \
@@ -94,6 +94,9 @@ def load():
                                       C.c_void_p, C.c_int32]
     L.corun_time_kernel.restype = st
     L.corun_time_kernel.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_float)]
+    L.corun_sample.restype = st
+    L.corun_sample.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+                               C.c_void_p, C.c_void_p, C.c_void_p]
     L.corun_last_error.restype = C.c_char_p
     L.corun_last_error.argtypes = []
     _lib = L
@@ -166,6 +169,11 @@ def describe_plan(cfg: dict, kv: KV, B: int, opt: Options | None = None) -> dict
         plan[name] = {"N": N, "K": K, "split_k": S, "k_chunk": Kc, "m_tile": bm, "n_tile": bn}
     plan["attn_chunk"], plan["attn_max_splits"] = v[32], v[33]
     return plan
+
+
+def torch_float32():
+    import torch
+    return torch.float32
 
 
 class Engine:
@@ -242,6 +250,23 @@ class Engine:
         us = C.c_float()
         _check(self._L.corun_time_kernel(self._h, kernel, layer, n_iters, C.byref(us)))
         return float(us.value)
+
+    def sample(self, logits, valid, positions, seeds, temperature):
+        """Seeded sampling of the rows of a device fp32 logits tensor
+        ([rows, vocab] or [vocab] for one row): (tokens int32[rows],
+        logprobs float32[rows])."""
+        assert logits.is_cuda and logits.dtype == torch_float32() and logits.is_contiguous()
+        rows = 1 if logits.dim() == 1 else logits.shape[0]
+        ld = logits.shape[-1]
+        vm = _np(valid, np.uint8).reshape(rows)
+        pos = _np(positions, np.int32).reshape(rows)
+        sd = np.ascontiguousarray(np.asarray(seeds, dtype=np.uint64).reshape(rows))
+        tp = np.ascontiguousarray(np.asarray(temperature, dtype=np.float32).reshape(rows))
+        tok = np.empty(rows, np.int32)
+        lp = np.empty(rows, np.float32)
+        _check(self._L.corun_sample(self._h, logits.data_ptr(), ld, rows, vm.ctypes.data, pos.ctypes.data,
+                                    sd.ctypes.data, tp.ctypes.data, tok.ctypes.data, lp.ctypes.data))
+        return tok, lp
 
     def prefill(self, prompt, slot: int, last_logits=None) -> int:
         p = _np(prompt, np.int32)

@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
+#include <cmath>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -201,6 +202,12 @@ struct corun_engine {
     // pinned host staging
     int32_t *h_tok = nullptr, *h_seq = nullptr, *h_next = nullptr, *h_counter = nullptr, *h_hist = nullptr;
     uint8_t *h_valid = nullptr;
+    // seeded sampling: device inputs/outputs [B] and one pinned host block
+    uint8_t *d_svalid = nullptr;
+    int32_t *d_spos = nullptr, *d_stok = nullptr;
+    uint64_t *d_sseed = nullptr;
+    float *d_stemp = nullptr, *d_slp = nullptr;
+    char *h_samp = nullptr;
 
     hipGraph_t graph = nullptr;
     hipGraphExec_t exec = nullptr;
@@ -690,6 +697,12 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
         cv.take(&e->moe_tiles, (size_t)3 * p.moe_slots);
         cv.take(&e->moe_act, na * Fe);
     }
+    cv.take(&e->d_svalid, (size_t)B);
+    cv.take(&e->d_spos, (size_t)B);
+    cv.take(&e->d_stok, (size_t)B);
+    cv.take(&e->d_sseed, (size_t)B);
+    cv.take(&e->d_stemp, (size_t)B);
+    cv.take(&e->d_slp, (size_t)B);
     cv.take(&e->h, (size_t)p.Mp * H);
     cv.take(&e->q, (size_t)B * nq * d);
     cv.take(&e->o, (size_t)p.Mp * nq * d);
@@ -702,6 +715,8 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     rebase(e->p_o, e->ws); rebase(e->p_gu, e->ws); rebase(e->p_down, e->ws); rebase(e->attn_ws, e->ws);
     rebase(e->logits, e->ws); rebase(e->p_lm, e->ws); rebase(e->amax, e->ws); rebase(e->h, e->ws); rebase(e->q, e->ws); rebase(e->o, e->ws); rebase(e->a, e->ws);
     rebase(e->rope, e->ws);
+    rebase(e->d_svalid, e->ws); rebase(e->d_spos, e->ws); rebase(e->d_stok, e->ws); rebase(e->d_sseed, e->ws);
+    rebase(e->d_stemp, e->ws); rebase(e->d_slp, e->ws);
     if (moe) {
         rebase(e->p_router, e->ws); rebase(e->moe_w, e->ws); rebase(e->moe_gu, e->ws); rebase(e->moe_y, e->ws);
         rebase(e->moe_sel, e->ws); rebase(e->moe_list, e->ws); rebase(e->moe_tiles, e->ws); rebase(e->moe_act, e->ws);
@@ -717,7 +732,8 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
 
     if (hipHostMalloc((void **)&e->h_tok, sizeof(int32_t) * B * 4 + 64, 0) != hipSuccess ||
         hipHostMalloc((void **)&e->h_valid, B + 64, 0) != hipSuccess ||
-        hipHostMalloc((void **)&e->h_hist, sizeof(int32_t) * (size_t)e->hist_cap * B, 0) != hipSuccess)
+        hipHostMalloc((void **)&e->h_hist, sizeof(int32_t) * (size_t)e->hist_cap * B, 0) != hipSuccess ||
+        hipHostMalloc((void **)&e->h_samp, (size_t)B * 32 + 256, 0) != hipSuccess)
         return bail(fail(CORUN_E_HIP, "pinned staging allocation failed"));
     e->h_seq = e->h_tok + B;
     e->h_next = e->h_tok + 2 * B;
@@ -744,6 +760,7 @@ extern "C" void corun_engine_destroy(corun_engine *e)
     if (e->h_tok) (void)hipHostFree(e->h_tok);
     if (e->h_valid) (void)hipHostFree(e->h_valid);
     if (e->h_hist) (void)hipHostFree(e->h_hist);
+    if (e->h_samp) (void)hipHostFree(e->h_samp);
     if (e->ev) (void)hipEventDestroy(e->ev);
     if (e->st) (void)hipStreamDestroy(e->st);
     delete e;
@@ -896,6 +913,52 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
         HIP_TRY(hipMemcpyAsync(last_logits, e->pf_logits, sizeof(float) * c.vocab, hipMemcpyDeviceToDevice, st));
     HIP_TRY(hipStreamSynchronize(st));
     *token_out = e->h_next[0];
+    return CORUN_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Seeded sampling
+// ---------------------------------------------------------------------------
+
+extern "C" corun_status corun_sample(corun_engine *e, const float *logits_dev, int64_t ld, int32_t rows,
+                                     const uint8_t *valid, const int32_t *positions, const uint64_t *seeds,
+                                     const float *temperature, int32_t *tokens_out, float *logprobs_out)
+{
+    if (!e || !logits_dev || !valid || !positions || !seeds || !temperature || !tokens_out)
+        return fail(CORUN_E_INVAL, "null argument");
+    if (rows < 1 || rows > e->B) return fail(CORUN_E_SHAPE, "rows %d outside [1, B = %d]", rows, e->B);
+    if (ld < e->c.vocab) return fail(CORUN_E_SHAPE, "row stride %lld below the vocabulary %d", (long long)ld, e->c.vocab);
+    for (int r = 0; r < rows; ++r) {
+        if (!valid[r]) continue;
+        if (positions[r] < 0) return fail(CORUN_E_INVAL, "row %d: negative position %d", r, positions[r]);
+        if (std::isnan(temperature[r]) || std::isinf(temperature[r]))
+            return fail(CORUN_E_INVAL, "row %d: temperature is not finite", r);
+    }
+    ST_TRY(enter(e));
+    // pinned staging: seeds [B] u64, positions [B], temperatures [B], tokens [B], logprobs [B], valid [B]
+    char *hs = e->h_samp;
+    uint64_t *hseed = reinterpret_cast<uint64_t *>(hs);
+    int32_t *hpos = reinterpret_cast<int32_t *>(hs + 8 * (size_t)e->B);
+    float *htemp = reinterpret_cast<float *>(hs + 12 * (size_t)e->B);
+    int32_t *htok = reinterpret_cast<int32_t *>(hs + 16 * (size_t)e->B);
+    float *hlp = reinterpret_cast<float *>(hs + 20 * (size_t)e->B);
+    uint8_t *hval = reinterpret_cast<uint8_t *>(hs + 24 * (size_t)e->B);
+    std::memcpy(hseed, seeds, sizeof(uint64_t) * rows);
+    std::memcpy(hpos, positions, sizeof(int32_t) * rows);
+    std::memcpy(htemp, temperature, sizeof(float) * rows);
+    std::memcpy(hval, valid, rows);
+    hipStream_t st = e->st;
+    HIP_TRY(hipMemcpyAsync(e->d_sseed, hseed, sizeof(uint64_t) * rows, hipMemcpyHostToDevice, st));
+    HIP_TRY(hipMemcpyAsync(e->d_spos, hpos, sizeof(int32_t) * rows, hipMemcpyHostToDevice, st));
+    HIP_TRY(hipMemcpyAsync(e->d_stemp, htemp, sizeof(float) * rows, hipMemcpyHostToDevice, st));
+    HIP_TRY(hipMemcpyAsync(e->d_svalid, hval, rows, hipMemcpyHostToDevice, st));
+    HIP_TRY(launch_sample(logits_dev, ld, rows, e->c.vocab, e->d_svalid, e->d_spos, e->d_sseed, e->d_stemp,
+                          e->d_stok, e->d_slp, st));
+    HIP_TRY(hipMemcpyAsync(htok, e->d_stok, sizeof(int32_t) * rows, hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipMemcpyAsync(hlp, e->d_slp, sizeof(float) * rows, hipMemcpyDeviceToHost, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    std::memcpy(tokens_out, htok, sizeof(int32_t) * rows);
+    if (logprobs_out) std::memcpy(logprobs_out, hlp, sizeof(float) * rows);
     return CORUN_OK;
 }
 

@@ -105,6 +105,13 @@ hipError_t launch_attn_merge(const float *ws, int rows, const uint8_t *valid, co
                              int nq, int nkv, int d, int chunk, int max_splits, uint16_t *o,
                              hipStream_t st);
 
+// Seeded sampling of rows of fp32 logits (row stride ld): token[r] =
+// argmax_v (l_v / temp[r] + g_v) with g_v from Philox4x32-10 keyed by seed[r],
+// counter (pos[r], v, 0, 0); greedy where temp[r] <= 0; logprob[r] of the
+// chosen token; padding rows get -1 / 0.
+hipError_t launch_sample(const float *logits, long long ld, int rows, int V, const uint8_t *valid, const int32_t *pos,
+                         const uint64_t *seed, const float *temp, int32_t *token, float *logprob, hipStream_t st);
+
 // Causal attention of the isolated prefill: q (bf16 [Lp][nq d]) against keys
 // 0..t of `slot` for query position t, o (bf16 [Lp][nq d]).  Sized by Lp only.
 hipError_t launch_prefill_attn(const uint16_t *q, int Lp, int nq, int nkv, int d, int slot, const uint16_t *kc,

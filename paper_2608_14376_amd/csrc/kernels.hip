@@ -1981,6 +1981,127 @@ hipError_t launch_prefill_attn(const uint16_t *q, int Lp, int nq, int nkv, int d
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Request-bound seeded sampling: token = argmax_v (l_v / T + g_v) (the
+// Gumbel-max rule, an exact draw from softmax(l / T)), g_v = -ln(-ln u_v),
+// u_v from Philox4x32-10 keyed by the request's 64-bit seed with counter
+// (t, v, 0, 0), t = the position of the token being sampled.  The variate is
+// a function of (seed, t, v) only: no state is consumed, so padding rows and
+// co-runners cannot shift a request's stream.  T <= 0 is greedy.  Decision
+// and log-probability (of the chosen token under softmax(l / T), softmax(l)
+// when greedy) in fp64; reductions in a fixed tree over 1024 threads:
+// sequential per thread over its columns, then the 64-lane butterfly, then
+// the 16 wavefronts in order.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1)
+{
+    // Salmon et al., SC 2011: per round (c0, c1, c2, c3) <- (hi(M1 c2) ^ c1 ^ k0,
+    // lo(M1 c2), hi(M0 c0) ^ c3 ^ k1, lo(M0 c0)); key += (W0, W1) between rounds
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r > 0) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint32_t lo0 = 0xD2511F53u * c[0], hi0 = __umulhi(0xD2511F53u, c[0]);
+        const uint32_t lo1 = 0xCD9E8D57u * c[2], hi1 = __umulhi(0xCD9E8D57u, c[2]);
+        const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+        c[0] = n0;
+        c[1] = lo1;
+        c[2] = n2;
+        c[3] = lo0;
+    }
+}
+
+__device__ __forceinline__ double gumbel_noise(uint32_t k0, uint32_t k1, int t, int v)
+{
+    uint32_t c[4] = {(uint32_t)t, (uint32_t)v, 0u, 0u};
+    philox4x32_10(c, k0, k1);
+    // u strictly inside (0, 1): ((c0 >> 6) 2^26 + (c1 >> 6) + 1/2) 2^-52, in
+    // [2^-53, 1 - 2^-53], every value exact (53-bit integer part)
+    const double u = ((double)(c[0] >> 6) * 67108864.0 + (double)(c[1] >> 6) + 0.5) * (1.0 / 4503599627370496.0);
+    return -log(-log(u));
+}
+
+__device__ __forceinline__ void better_d(double &v, int &i, double v2, int i2)
+{
+    if (v2 > v || (v2 == v && i2 < i)) {
+        v = v2;
+        i = i2;
+    }
+}
+
+__global__ __launch_bounds__(1024) void k_sample(const float *__restrict__ logits, long long ld, int V,
+                                                 const uint8_t *__restrict__ valid, const int32_t *__restrict__ pos,
+                                                 const uint64_t *__restrict__ seed, const float *__restrict__ temp,
+                                                 int32_t *__restrict__ token, float *__restrict__ logprob)
+{
+    const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (!valid[r]) {
+        if (tid == 0) {
+            token[r] = -1;
+            logprob[r] = 0.f;
+        }
+        return;
+    }
+    __shared__ double sz[16], sm[16];
+    __shared__ int si[16];
+    const float *l = logits + (size_t)r * ld;
+    const float tf = temp[r];
+    const bool greedy = !(tf > 0.0f);
+    const double T = greedy ? 1.0 : (double)tf;
+    const uint32_t k0 = (uint32_t)seed[r], k1 = (uint32_t)(seed[r] >> 32);
+    const int t = pos[r];
+    double bz = -INFINITY, M = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int v = tid; v < V; v += 1024) {
+        const double x = (double)l[v] / T;
+        const double z = greedy ? x : x + gumbel_noise(k0, k1, t, v);
+        better_d(bz, bi, z, v);
+        M = fmax(M, x);
+    }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        better_d(bz, bi, __shfl_xor(bz, off, 64), __shfl_xor(bi, off, 64));
+        M = fmax(M, __shfl_xor(M, off, 64));
+    }
+    if (lane == 0) {
+        sz[wave] = bz;
+        si[wave] = bi;
+        sm[wave] = M;
+    }
+    __syncthreads();
+    bz = sz[0];
+    bi = si[0];
+    M = sm[0];
+    for (int w = 1; w < 16; ++w) {
+        better_d(bz, bi, sz[w], si[w]);
+        M = fmax(M, sm[w]);
+    }
+    double S = 0.0;
+    for (int v = tid; v < V; v += 1024) S += exp((double)l[v] / T - M);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) S += __shfl_xor(S, off, 64);
+    __syncthreads();                                  // every thread has read sz/si/sm
+    if (lane == 0) sm[wave] = S;
+    __syncthreads();
+    if (tid == 0) {
+        double Ssum = 0.0;
+        for (int w = 0; w < 16; ++w) Ssum += sm[w];
+        token[r] = bi;
+        logprob[r] = (float)((double)l[bi] / T - M - log(Ssum));
+    }
+}
+
+hipError_t launch_sample(const float *logits, long long ld, int rows, int V, const uint8_t *valid, const int32_t *pos,
+                         const uint64_t *seed, const float *temp, int32_t *token, float *logprob, hipStream_t st)
+{
+    if (rows <= 0 || V <= 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_sample, dim3(rows), dim3(1024), 0, st, logits, ld, V, valid, pos, seed, temp, token,
+                       logprob);
+    return hipGetLastError();
+}
+
 hipError_t launch_proj(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
                        long long split_stride, int ldo, hipStream_t st, ArgBest *amax)
 {
