@@ -209,6 +209,37 @@ def bench_prefill(cfg, W, lens, args):
     return out
 
 
+def bench_scheduler(cfg, W, n_req=64, B=32, in_len=512, out_len=64):
+    """The host scheduler end to end on a synthetic in=512/out=64 workload:
+    every request prefilled alone (Algorithms 1 and 2), decoded at the
+    fixed B with request-bound sampling (temperature 0.6, own seeds)."""
+    import torch
+
+    from paper_2608_14376_amd import corun
+    from paper_2608_14376_amd import workload as wl
+    cap = (in_len + out_len + 15) // 16 * 16
+    K, V = wl.make_kv_contiguous(cfg, B, cap, seed=5000, device="cuda")
+    eng = corun.Engine(cfg, W, B, K, V, opt=corun.options(max_prefill_len=in_len))
+    s = corun.Scheduler(eng, max_num_reqs=B)
+    for i in range(2):                                   # warm-up: graph capture, first prefill
+        s.add_request(-1 - i, wl.make_prompt(cfg["vocab"], in_len, seed=9000 + i), 2, 1, 0.6)
+    s.run_until_idle()
+    for i in range(n_req):
+        s.add_request(i, wl.make_prompt(cfg["vocab"], in_len, seed=7000 + i), out_len, 1000 + i, 0.6)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    events = s.run_until_idle()
+    dt = time.perf_counter() - t
+    s.close()
+    eng.close()
+    del K, V
+    out = dict(requests=n_req, B=B, input_len=in_len, output_len=out_len, seconds=round(dt, 3),
+               output_tok_s=round(n_req * out_len / dt, 1), prefills=events.count(1), decode_steps=events.count(2))
+    log(f"[bench] scheduler in={in_len}/out={out_len} x{n_req} at B={B}: {dt:.2f} s, "
+        f"{out['output_tok_s']:.0f} output tok/s ({out['prefills']} prefills, {out['decode_steps']} decode steps)")
+    return out
+
+
 def bitexact_check(cfg, res, n_pairs=2):
     """One live request placed in two different batch mixes at two different
     slots: logits rows must be bit-identical."""
@@ -400,6 +431,8 @@ def main():
     if not args.no_extra:
         # prefill on the same 8B weights
         extra["prefill_8b"] = bench_prefill(cfg, W, [512, 2048, 8192, 32768], args)
+        torch.cuda.empty_cache()
+        extra["scheduler_8b"] = bench_scheduler(cfg, W)
         del W
         torch.cuda.empty_cache()
         # 32B-shaped dense decode at long context on the paged cache

@@ -177,6 +177,11 @@ corun_status corun_decode_run(corun_engine *e, int32_t n_steps, const int32_t *t
 corun_status corun_prefill(corun_engine *e, const int32_t *prompt, int32_t prompt_len, int32_t slot,
                            int32_t *token_out, float *last_logits);
 
+/* The engine's fixed batch size, model configuration and KV description
+ * (copies; the k/v/page-table pointers are the caller's borrowed ones).
+ * Any out pointer may be NULL. */
+corun_status corun_engine_info(const corun_engine *e, int32_t *B_fixed, corun_model_cfg *cfg, corun_kv *kv);
+
 /* Request-bound seeded multinomial sampling (Sec. IV, "Shape-Aligned
  * Sampling"; y_t = S(l_t, R(s, t)) in Sec. IV, "Determinism Argument"), run on
  * logits that corun_decode_step (rows = B, the fixed shape) or corun_prefill
@@ -203,6 +208,49 @@ corun_status corun_prefill(corun_engine *e, const int32_t *prompt, int32_t promp
 corun_status corun_sample(corun_engine *e, const float *logits_dev, int64_t ld, int32_t rows,
                           const uint8_t *valid, const int32_t *positions, const uint64_t *seeds,
                           const float *temperature, int32_t *tokens_out, float *logprobs_out);
+
+/* ---------------------------------------------------------------------------
+ * Host scheduler (Sec. IV, "Isolated Prefill", Algorithms 1 and 2, around the
+ * fixed-shape batched decode and the request-bound sampler): a
+ * continuous-batching loop with slot reuse, a concurrency limit and
+ * full-sequence KV admission, driving corun_prefill, corun_decode_step and
+ * corun_sample.  Each corun_sched_step() runs one iteration: the isolated
+ * prefill of the request Algorithm 1 selects (the head of `running` whose
+ * prefill is unfinished, else the head of `waiting` if fewer than
+ * max_num_reqs are running and its prompt plus max_new_tokens fit the KV
+ * cache now), else one decode step of every running request padded to B.
+ * Requests leave at max_new_tokens, returning their slot (the lowest free one
+ * is reused) and pages.  With a paged cache the scheduler owns the page-table
+ * rows of the slots: all pages of the full sequence are taken at admission.
+ * engine NULL is a dry run: the same scheduling, no model, tokens 0.  Not
+ * thread-safe; one scheduler per engine.
+ * ------------------------------------------------------------------------- */
+typedef struct corun_sched corun_sched;
+typedef struct {
+    int32_t max_num_reqs;       /* concurrency limit, <= B (0 = B) */
+    /* dry run only (engine NULL): the slots and cache; page_size 0 = contiguous */
+    int32_t n_slots, max_seq_len, page_size, num_pages, max_pages_per_seq;
+} corun_sched_cfg;
+
+corun_status corun_sched_create(corun_engine *e, const corun_sched_cfg *cfg, corun_sched **out);
+void corun_sched_destroy(corun_sched *s);
+/* Queue one request (FIFO).  prompt: host int32 [prompt_len], copied.
+ * temperature <= 0 is greedy.  CORUN_E_CAPACITY if prompt + max_new_tokens
+ * can never fit one slot; CORUN_E_INVAL for a reused id or bad sizes. */
+corun_status corun_sched_add_request(corun_sched *s, int64_t id, const int32_t *prompt, int32_t prompt_len,
+                                     int32_t max_new_tokens, uint64_t seed, float temperature);
+/* One iteration; event: 0 idle, 1 isolated prefill, 2 decode step. */
+corun_status corun_sched_step(corun_sched *s, int32_t *event);
+/* A request's generated tokens and their log-probabilities so far (up to
+ * cap), their count and whether it finished. */
+corun_status corun_sched_output(const corun_sched *s, int64_t id, int32_t *tokens, float *logprobs, int32_t cap,
+                                int32_t *n_generated, int32_t *finished);
+/* Queue lengths, free slots and pages, and slot_owner [B] (request id, -1
+ * free).  Any out pointer may be NULL. */
+corun_status corun_sched_state(const corun_sched *s, int32_t *n_running, int32_t *n_waiting, int32_t *free_slots,
+                               int32_t *free_pages, int64_t *slot_owner);
+/* Message of the last failed scheduler call (engine failures included). */
+const char *corun_sched_last_error(void);
 
 /* Kernels that corun_time_kernel can time. */
 enum {

@@ -20,7 +20,9 @@ KV_CONTIGUOUS, KV_PAGED = 0, 1
 
 EXPORTS = ("corun_engine_create", "corun_engine_destroy", "corun_decode_step", "corun_decode_run",
            "corun_prefill", "corun_check_config", "corun_check_batch", "corun_describe_plan",
-           "corun_last_error", "corun_time_kernel", "corun_sample")
+           "corun_last_error", "corun_time_kernel", "corun_sample", "corun_engine_info",
+           "corun_sched_create", "corun_sched_destroy", "corun_sched_add_request", "corun_sched_step",
+           "corun_sched_output", "corun_sched_state", "corun_sched_last_error")
 
 # kernel ids of corun_time_kernel
 K_QKV_GEMM, K_O_GEMM, K_GATE_UP_GEMM, K_DOWN_GEMM, K_LM_HEAD, K_ATTN_SPLIT, K_ATTN_MERGE, K_RMSNORM, \
@@ -97,6 +99,25 @@ def load():
     L.corun_sample.restype = st
     L.corun_sample.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
                                C.c_void_p, C.c_void_p, C.c_void_p]
+    L.corun_engine_info.restype = st
+    L.corun_engine_info.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+    L.corun_sched_create.restype = st
+    L.corun_sched_create.argtypes = [C.c_void_p, C.POINTER(SchedCfg), C.POINTER(C.c_void_p)]
+    L.corun_sched_destroy.restype = None
+    L.corun_sched_destroy.argtypes = [C.c_void_p]
+    L.corun_sched_add_request.restype = st
+    L.corun_sched_add_request.argtypes = [C.c_void_p, C.c_int64, C.c_void_p, C.c_int32, C.c_int32, C.c_uint64,
+                                          C.c_float]
+    L.corun_sched_step.restype = st
+    L.corun_sched_step.argtypes = [C.c_void_p, C.POINTER(C.c_int32)]
+    L.corun_sched_output.restype = st
+    L.corun_sched_output.argtypes = [C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p, C.c_int32,
+                                     C.POINTER(C.c_int32), C.POINTER(C.c_int32)]
+    L.corun_sched_state.restype = st
+    L.corun_sched_state.argtypes = [C.c_void_p, C.POINTER(C.c_int32), C.POINTER(C.c_int32), C.POINTER(C.c_int32),
+                                    C.POINTER(C.c_int32), C.c_void_p]
+    L.corun_sched_last_error.restype = C.c_char_p
+    L.corun_sched_last_error.argtypes = []
     L.corun_last_error.restype = C.c_char_p
     L.corun_last_error.argtypes = []
     _lib = L
@@ -169,6 +190,82 @@ def describe_plan(cfg: dict, kv: KV, B: int, opt: Options | None = None) -> dict
         plan[name] = {"N": N, "K": K, "split_k": S, "k_chunk": Kc, "m_tile": bm, "n_tile": bn}
     plan["attn_chunk"], plan["attn_max_splits"] = v[32], v[33]
     return plan
+
+
+class SchedCfg(C.Structure):
+    _fields_ = [("max_num_reqs", C.c_int32), ("n_slots", C.c_int32), ("max_seq_len", C.c_int32),
+                ("page_size", C.c_int32), ("num_pages", C.c_int32), ("max_pages_per_seq", C.c_int32)]
+
+
+class Scheduler:
+    """Host scheduler over an Engine (or a dry run with engine=None):
+    isolated prefill (Algorithms 1 and 2), fixed-shape decode and
+    request-bound sampling, with slot reuse and full-sequence admission."""
+
+    IDLE, PREFILL, DECODE = 0, 1, 2
+
+    def __init__(self, engine=None, max_num_reqs=0, n_slots=0, max_seq_len=0, page_size=0, num_pages=0,
+                 max_pages_per_seq=0):
+        self._L = load()
+        self.engine = engine
+        cfg = SchedCfg(max_num_reqs, n_slots, max_seq_len, page_size, num_pages, max_pages_per_seq)
+        h = C.c_void_p()
+        st = self._L.corun_sched_create(engine._h if engine is not None else None, C.byref(cfg), C.byref(h))
+        if st != 0:
+            raise CorunError(st, self._L.corun_sched_last_error().decode())
+        self._h = h
+        self.B = engine.B if engine is not None else n_slots
+
+    def _ok(self, st):
+        if st != 0:
+            raise CorunError(st, self._L.corun_sched_last_error().decode())
+
+    def add_request(self, rid: int, prompt, max_new_tokens: int, seed: int = 0, temperature: float = 0.0):
+        p = _np(prompt, np.int32)
+        self._ok(self._L.corun_sched_add_request(self._h, rid, p.ctypes.data, p.size, max_new_tokens, seed,
+                                                 temperature))
+
+    def step(self) -> int:
+        ev = C.c_int32()
+        self._ok(self._L.corun_sched_step(self._h, C.byref(ev)))
+        return ev.value
+
+    def output(self, rid: int):
+        n = C.c_int32()
+        fin = C.c_int32()
+        self._ok(self._L.corun_sched_output(self._h, rid, None, None, 0, C.byref(n), C.byref(fin)))
+        tok = np.empty(max(n.value, 1), np.int32)
+        lp = np.empty(max(n.value, 1), np.float32)
+        self._ok(self._L.corun_sched_output(self._h, rid, tok.ctypes.data, lp.ctypes.data, n.value, C.byref(n),
+                                            C.byref(fin)))
+        return tok[:n.value], lp[:n.value], bool(fin.value)
+
+    def state(self) -> dict:
+        r, w, fs, fp = C.c_int32(), C.c_int32(), C.c_int32(), C.c_int32()
+        owner = np.empty(self.B, np.int64)
+        self._ok(self._L.corun_sched_state(self._h, C.byref(r), C.byref(w), C.byref(fs), C.byref(fp),
+                                           owner.ctypes.data))
+        return dict(running=r.value, waiting=w.value, free_slots=fs.value, free_pages=fp.value, slot_owner=owner)
+
+    def run_until_idle(self, max_steps: int = 1 << 20) -> list:
+        events = []
+        for _ in range(max_steps):
+            ev = self.step()
+            if ev == self.IDLE:
+                return events
+            events.append(ev)
+        raise RuntimeError("scheduler did not drain")
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._L.corun_sched_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def torch_float32():

@@ -916,6 +916,15 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
     return CORUN_OK;
 }
 
+extern "C" corun_status corun_engine_info(const corun_engine *e, int32_t *B_fixed, corun_model_cfg *cfg, corun_kv *kv)
+{
+    if (!e) return fail(CORUN_E_INVAL, "null engine");
+    if (B_fixed) *B_fixed = e->B;
+    if (cfg) *cfg = e->c;
+    if (kv) *kv = e->kv;
+    return CORUN_OK;
+}
+
 // ---------------------------------------------------------------------------
 // Seeded sampling
 // ---------------------------------------------------------------------------
