@@ -240,6 +240,120 @@ def bench_scheduler(cfg, W, n_req=64, B=32, in_len=512, out_len=64):
     return out
 
 
+def bench_bi_tradeoff(cfg, W, K, V, args):
+    """The paper's trade-off on this GPU (Sec. I, Fig. 2 and Fig. 4b; Sec. V,
+    "Ablation Study"), on the 8B-shaped model and the headline cache:
+
+    * step: one decode step of 32 live requests with contexts U[512, 4096]
+      under STD (the default plan at B = 32: no padding), BI (batch-invariant
+      kernels at B = 32) and CoRun (the default plan at the fixed B = 256,
+      224 padding rows), each with its per-kernel-class breakdown;
+    * padding: one live request (context 2048) under CoRun at padded sizes
+      1..256 against BI at B = 1 (STD is CoRun at B = 1);
+    * gemm: each projection's launch time under the default and the
+      batch-invariant plan at M = 1..256 (the MatMul panel of Fig. 2);
+    * split_kv: the fixed B = 256 step with split-KV on and off, for ragged
+      (U[512, 4096]) and similar (U[2000, 2100]) contexts."""
+    import torch
+
+    from paper_2608_14376_amd import corun
+    from paper_2608_14376_amd import workload as wl
+
+    groups = {"matmul": (corun.K_QKV_GEMM, corun.K_O_GEMM, corun.K_GATE_UP_GEMM, corun.K_DOWN_GEMM,
+                         corun.K_LM_HEAD),
+              "attention": (corun.K_ATTN_SPLIT, corun.K_ATTN_MERGE), "rmsnorm": (corun.K_RMSNORM,),
+              "other": (corun.K_QKV_POST, corun.K_SWIGLU, corun.K_ARGMAX)}
+    gemms = {"qkv": corun.K_QKV_GEMM, "o": corun.K_O_GEMM, "gate_up": corun.K_GATE_UP_GEMM,
+             "down": corun.K_DOWN_GEMM, "lm_head": corun.K_LM_HEAD}
+    cap = K[0].shape[2]
+
+    def timed(B, b, opt=None, breakdown=False, gemm_times=False, rows=None):
+        eng = corun.Engine(cfg, W, B, K, V, opt=opt)
+        if rows is not None:       # the listed rows' logits of one step, before any timing
+            lg = torch.empty(B, cfg["vocab"], dtype=torch.float32, device="cuda")
+            eng.decode_step(b.tokens, b.valid, b.seq_lens, lg)
+            rows_out = lg[rows].cpu()
+            del lg
+        eng.decode_run(args.warmup, b.tokens, b.valid, b.seq_lens)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        eng.decode_run(args.steps, b.tokens, b.valid, b.seq_lens)
+        torch.cuda.synchronize()
+        r = dict(step_ms=round(1e3 * (time.perf_counter() - t) / args.steps, 4))
+        if breakdown or gemm_times:
+            eng.decode_run(1, b.tokens, b.valid, b.seq_lens)
+            _, per_step = kernel_bytes_flops(cfg, B, b.seq_lens[b.valid == 1].tolist())
+        if breakdown:
+            r["breakdown_ms"] = {g: round(sum(eng.time_kernel(k, 0, args.kernel_iters) * per_step[k] for k in ks) / 1e3, 3)
+                                 for g, ks in groups.items()}
+        if gemm_times:
+            r["gemm_us"] = {n: round(eng.time_kernel(k, 0, args.kernel_iters), 2) for n, k in gemms.items()}
+        eng.close()
+        if rows is not None:
+            r["_rows"] = rows_out
+        return r
+
+    def batch_at(B, slots, lens, seed):
+        r = np.random.default_rng(seed)
+        valid = np.zeros(B, np.uint8)
+        valid[slots] = 1
+        seq = r.integers(0, 1 << 30, B).astype(np.int32)          # padding rows: garbage
+        seq[slots] = lens
+        tok = r.integers(0, cfg["vocab"], B).astype(np.int32)
+        return wl.Batch(tok, valid, seq)
+
+    bi = corun.options(batch_invariant=True)
+    out = {}
+    # Fig. 4b: 32 live requests, ragged contexts, in slots 0..31 of the cache
+    # under every mode, so each mode sees the same 32 requests
+    lens32 = np.random.default_rng(11).integers(LEN_LO, LEN_HI + 1, 32)
+    live = np.arange(32)
+    b32 = batch_at(32, live, lens32, 12)
+    b256 = batch_at(256, live, lens32, 14)
+    b256.tokens[:32] = b32.tokens
+    s = dict(std=timed(32, b32, breakdown=True, rows=live), bi=timed(32, b32, bi, breakdown=True, rows=live),
+             corun_B256=timed(256, b256, breakdown=True, rows=live), bi_B256=timed(256, b256, bi, rows=live))
+    same = lambda a, b: int(sum(torch.equal(a["_rows"][i].view(torch.int32), b["_rows"][i].view(torch.int32))
+                                for i in range(32)))
+    s["identical_rows_of_32"] = dict(default_B32_vs_B256=same(s["std"], s["corun_B256"]),
+                                     bi_B32_vs_B256=same(s["bi"], s["bi_B256"]))
+    for v in s.values():
+        v.pop("_rows", None)
+    out["step_32_live"] = s
+    log(f"[bench] 32 live requests: STD {s['std']['step_ms']} ms, BI {s['bi']['step_ms']} ms, "
+        f"CoRun(B=256) {s['corun_B256']['step_ms']} ms; rows bit-identical between B=32 and B=256: "
+        f"default {s['identical_rows_of_32']['default_B32_vs_B256']}/32, "
+        f"BI {s['identical_rows_of_32']['bi_B32_vs_B256']}/32")
+    # decode padding: one live request; GEMM launch times at each M
+    pad, gemm = {}, {}
+    for B in (1, 2, 4, 8, 16, 32, 64, 128, 256):
+        b = batch_at(B, [B - 1], [2048], 20 + B)
+        r = timed(B, b, gemm_times=B in (1, 8, 32, 64, 128, 256))
+        pad[B] = dict(step_ms=r["step_ms"], tok_s=round(1e3 / r["step_ms"], 1))
+        if "gemm_us" in r:
+            rb = timed(B, b, bi, gemm_times=True)
+            gemm[B] = dict(std=r["gemm_us"], bi=rb["gemm_us"],
+                           bi_over_std={n: round(rb["gemm_us"][n] / r["gemm_us"][n], 2) for n in gemms})
+            if B == 1:
+                pad["bi_B1"] = dict(step_ms=rb["step_ms"], tok_s=round(1e3 / rb["step_ms"], 1))
+    out["padding_1_live"] = pad
+    out["gemm_std_vs_bi_us"] = gemm
+    log(f"[bench] one live request: CoRun B=1 {pad[1]['tok_s']} tok/s, B=256 {pad[256]['tok_s']} tok/s, "
+        f"BI B=1 {pad['bi_B1']['tok_s']} tok/s")
+    # split-KV on/off at the fixed B = 256
+    sk = {}
+    off = corun.options(attn_chunk=(cap + 63) // 64 * 64)
+    for name, lo, hi in (("ragged", LEN_LO, LEN_HI), ("similar", 2000, 2100)):
+        b = wl.make_batch(256, cfg["vocab"], seed=30, len_lo=lo, len_hi=hi)
+        on_ms, off_ms = timed(256, b)["step_ms"], timed(256, b, off)["step_ms"]
+        sk[name] = dict(n_live=int(b.valid.sum()), split_on_ms=on_ms, split_off_ms=off_ms,
+                        off_cost=round(off_ms / on_ms - 1, 4))
+    out["split_kv_B256"] = sk
+    log(f"[bench] split-KV off at B=256: ragged +{100 * sk['ragged']['off_cost']:.1f}%, "
+        f"similar +{100 * sk['similar']['off_cost']:.1f}%")
+    return out
+
+
 def bitexact_check(cfg, res, n_pairs=2):
     """One live request placed in two different batch mixes at two different
     slots: logits rows must be bit-identical."""
@@ -415,6 +529,7 @@ def main():
     cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, W, head)
     if cpu:
         log(f"[bench] cpu oracle: {cpu['value']} tok/s on {cpu['cores']} threads")
+    tradeoff = None if args.no_extra else bench_bi_tradeoff(cfg, W, head["_K"], head["_V"], args)
     _drop(head)
     torch.cuda.empty_cache()
 
@@ -428,6 +543,8 @@ def main():
         torch.cuda.empty_cache()
 
     extra = {}
+    if tradeoff is not None:
+        extra["bi_tradeoff_8b"] = tradeoff
     if not args.no_extra:
         # prefill on the same 8B weights
         extra["prefill_8b"] = bench_prefill(cfg, W, [512, 2048, 8192, 32768], args)

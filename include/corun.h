@@ -113,13 +113,20 @@ typedef struct {
 
 /* Creation options; pass NULL for defaults (all fields 0). */
 typedef struct {
-    int32_t attn_chunk;        /* split-KV chunk in tokens (multiple of 64); 0 = chosen from (model, B, capacity) */
+    int32_t attn_chunk;        /* split-KV chunk in tokens (multiple of 64); 0 = chosen from (model, B, capacity);
+                                  a chunk >= the capacity turns split-KV off (one split per row) */
     int32_t max_prefill_len;   /* prefill workspace in tokens; 0 = none (corun_prefill returns CORUN_E_STATE) */
     int32_t no_graph;          /* 1 = launch the step's kernels eagerly instead of replaying the captured graph */
     int32_t poison_workspace;  /* 1 = fill the workspace with NaN bit patterns at creation (test aid) */
     int32_t split_k_override;  /* >0: force this split-K factor on every projection (test aid; changes the plan) */
     int32_t gemm_bm;           /* 0 = automatic; 64/128/256 = force the LDS-tiled projection kernel with this
                                   M tile (tuning aid; changes the plan) */
+    int32_t batch_invariant;   /* 1 = batch-invariant kernels, the baseline CoRun is measured against (Sec. III,
+                                  "Batch-Dependent GPU Reductions", Fig. 3b, and Definition 1): every projection, in
+                                  decode and prefill, uses one kernel and tile whatever B or the prompt length
+                                  (128 x 128, no split-K), and decode attention runs with split-KV off (one
+                                  split covers the whole cache), so a row's results depend on neither its
+                                  position nor B.  Requires attn_chunk, split_k_override and gemm_bm = 0. */
 } corun_options;
 
 /* Create an engine for one fixed padded batch size B_fixed (Sec. IV,

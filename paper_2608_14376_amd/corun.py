@@ -54,7 +54,8 @@ class KV(C.Structure):
 
 class Options(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
-        "attn_chunk", "max_prefill_len", "no_graph", "poison_workspace", "split_k_override", "gemm_bm")]
+        "attn_chunk", "max_prefill_len", "no_graph", "poison_workspace", "split_k_override", "gemm_bm",
+        "batch_invariant")]
 
 
 class CorunError(RuntimeError):
@@ -155,8 +156,9 @@ def kv_struct(layout: int, n_slots: int, k, v, keep, max_seq_len=0, page_size=0,
 
 
 def options(attn_chunk=0, max_prefill_len=0, no_graph=False, poison_workspace=False, split_k_override=0,
-            gemm_bm=0):
-    return Options(attn_chunk, max_prefill_len, int(no_graph), int(poison_workspace), split_k_override, gemm_bm)
+            gemm_bm=0, batch_invariant=False):
+    return Options(attn_chunk, max_prefill_len, int(no_graph), int(poison_workspace), split_k_override, gemm_bm,
+                   int(batch_invariant))
 
 
 def _np(a, dt):

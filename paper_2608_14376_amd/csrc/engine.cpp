@@ -80,13 +80,24 @@ int mt_for(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 //    at least 512 K elements.
 //  * otherwise (or bm_override > 0): the LDS-tiled kernel with a 128-row
 //    tile (or bm_override), split-K to about two workgroups per CU.
-Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_override)
+// Batch-invariant mode (bi) ignores M: the pipelined kernel's 128 x 128 tile
+// (the LDS-tiled kernel's 128-row tile when K % 64 != 0) and no split-K, so
+// every output element is one MFMA chain over K in the same order whatever
+// the batch size.
+Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_override, bool bi = false)
 {
     Proj p;
     p.N = N;
     p.K = K;
     if (N <= 0 || K <= 0 || M <= 0) return p;   // no such projection
     int S, align;
+    if (bi) {
+        p.bm = 128;
+        p.bn = K % 64 == 0 ? 128 : 0;
+        p.Kc = (K + 63) / 64 * 64;
+        p.S = 1;
+        return p;
+    }
     if (M > 64 && bm_override <= 0 && K % 64 == 0) {
         p.bm = M <= 128 ? 128 : 256;
         p.bn = 128;
@@ -141,23 +152,25 @@ Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_
     const int H = c->hidden, d = c->head_dim;
     const int nqkv = (c->n_heads + 2 * c->n_kv_heads) * d;
     const int so = opt.split_k_override, bo = opt.gemm_bm;
-    p.qkv = choose_proj(nqkv, H, B, so, 0, bo);
-    p.o = choose_proj(H, c->n_heads * d, B, so, 0, bo);
+    const bool bi = opt.batch_invariant != 0;
+    p.qkv = choose_proj(nqkv, H, B, so, 0, bo, bi);
+    p.o = choose_proj(H, c->n_heads * d, B, so, 0, bo, bi);
     if (c->n_experts == 0) {
-        p.gu = choose_proj(2 * c->ffn, H, B, so, 0, bo);
-        p.down = choose_proj(H, c->ffn, B, so, 0, bo);
+        p.gu = choose_proj(2 * c->ffn, H, B, so, 0, bo, bi);
+        p.down = choose_proj(H, c->ffn, B, so, 0, bo, bi);
     } else {
-        p.router = choose_proj(c->n_experts, H, B, so, 0, bo);
+        p.router = choose_proj(c->n_experts, H, B, so, 0, bo, bi);
         p.gu = Proj{2 * c->expert_ffn, H, 1, H, 0};
         p.down = Proj{H, c->expert_ffn, 1, c->expert_ffn, 0};
         p.moe_slots = c->n_experts + (B * c->top_k + 15) / 16;
     }
     // lm_head: never split (its epilogue selects the argmax partials) except
     // under the split override test aid; the 64-row tile has no argmax epilogue
-    p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0, bo == 64 ? 0 : bo);
+    p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0, bo == 64 ? 0 : bo, bi);
     if (p.lm.bm == 64) p.lm = choose_proj(c->vocab, H, 64, so > 0 ? so : 1, 0, 0);
     const int cap = kv_capacity(kv);
-    p.chunk = choose_chunk(B, c->n_kv_heads, cap, opt.attn_chunk);
+    // batch-invariant mode turns split-KV off: one split covers the capacity
+    p.chunk = bi ? (cap + 63) / 64 * 64 : choose_chunk(B, c->n_kv_heads, cap, opt.attn_chunk);
     p.max_splits = (cap + p.chunk - 1) / p.chunk;
     return p;
 }
@@ -291,6 +304,20 @@ extern "C" corun_status corun_check_batch(const corun_model_cfg *c, const corun_
     return CORUN_OK;
 }
 
+static corun_status check_options(const corun_options &o)
+{
+    if (o.attn_chunk < 0 || o.attn_chunk % 64 != 0)
+        return fail(CORUN_E_INVAL, "attn_chunk must be a non-negative multiple of 64");
+    if (o.max_prefill_len < 0) return fail(CORUN_E_INVAL, "negative max_prefill_len");
+    if (o.split_k_override < 0) return fail(CORUN_E_INVAL, "negative split_k_override");
+    if (!(o.gemm_bm == 0 || o.gemm_bm == 64 || o.gemm_bm == 128 || o.gemm_bm == 256))
+        return fail(CORUN_E_INVAL, "gemm_bm must be 0, 64, 128 or 256");
+    if (o.batch_invariant != 0 && o.batch_invariant != 1) return fail(CORUN_E_INVAL, "batch_invariant must be 0 or 1");
+    if (o.batch_invariant && (o.attn_chunk || o.split_k_override || o.gemm_bm))
+        return fail(CORUN_E_INVAL, "batch_invariant fixes the plan: attn_chunk, split_k_override and gemm_bm must be 0");
+    return CORUN_OK;
+}
+
 extern "C" int32_t corun_describe_plan(const corun_model_cfg *c, const corun_kv *kv, int32_t B,
                                        const corun_options *opt, int32_t *out, int32_t cap)
 {
@@ -298,6 +325,8 @@ extern "C" int32_t corun_describe_plan(const corun_model_cfg *c, const corun_kv 
     if (s != CORUN_OK) return s;
     corun_options o{};
     if (opt) o = *opt;
+    s = check_options(o);
+    if (s != CORUN_OK) return s;
     Plan p = make_plan(c, kv, B, o);
     std::vector<int32_t> v = {p.B, p.Mp};
     for (const Proj *pr : {&p.qkv, &p.o, &p.gu, &p.down, &p.lm}) {
@@ -616,11 +645,7 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     if (kv->layout == CORUN_KV_PAGED && !kv->page_table) return fail(CORUN_E_INVAL, "paged cache needs page_table");
     corun_options o{};
     if (opt) o = *opt;
-    if (o.attn_chunk < 0 || o.attn_chunk % 64 != 0 || o.attn_chunk > 1024)
-        return fail(CORUN_E_INVAL, "attn_chunk must be a multiple of 64 in [64, 1024]");
-    if (o.max_prefill_len < 0) return fail(CORUN_E_INVAL, "negative max_prefill_len");
-    if (!(o.gemm_bm == 0 || o.gemm_bm == 64 || o.gemm_bm == 128 || o.gemm_bm == 256))
-        return fail(CORUN_E_INVAL, "gemm_bm must be 0, 64, 128 or 256");
+    ST_TRY(check_options(o));
 
     corun_engine *e = new corun_engine();
     e->c = *cfg;
@@ -862,12 +887,13 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
     const int nqkv = (nq + 2 * nkv) * d;
     hipStream_t st = e->st;
     const int cap_rows = std::max(1, e->pf_max / Lp);
-    const Proj pq = choose_proj(nqkv, H, Lp, 0, cap_rows, 0);
-    const Proj po = choose_proj(H, nq * d, Lp, 0, cap_rows, 0);
-    const Proj pg = e->moe ? Proj{} : choose_proj(2 * F, H, Lp, 0, cap_rows, 0);
-    const Proj pd = e->moe ? Proj{} : choose_proj(H, F, Lp, 0, cap_rows, 0);
-    const Proj pl = choose_proj(c.vocab, H, 1, 1, 0, 0);
-    const Proj pr = e->moe ? choose_proj(c.n_experts, H, Lp, 0, cap_rows, 0) : Proj{};
+    const bool bi = e->opt.batch_invariant != 0;
+    const Proj pq = choose_proj(nqkv, H, Lp, 0, cap_rows, 0, bi);
+    const Proj po = choose_proj(H, nq * d, Lp, 0, cap_rows, 0, bi);
+    const Proj pg = e->moe ? Proj{} : choose_proj(2 * F, H, Lp, 0, cap_rows, 0, bi);
+    const Proj pd = e->moe ? Proj{} : choose_proj(H, F, Lp, 0, cap_rows, 0, bi);
+    const Proj pl = choose_proj(c.vocab, H, 1, 1, 0, 0, bi);
+    const Proj pr = e->moe ? choose_proj(c.n_experts, H, Lp, 0, cap_rows, 0, bi) : Proj{};
     const int dense_S = e->moe ? 0 : pd.S;
     const MoeBufs pmb{nullptr, e->pf_part, e->pf_moe_w, e->pf_moe_gu, e->pf_moe_y, e->pf_moe_sel, e->pf_moe_list,
                       e->pf_moe_tiles, e->pf_moe_act, e->moe ? c.n_experts + (Lp * c.top_k + 15) / 16 : 0};

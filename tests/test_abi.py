@@ -110,3 +110,32 @@ def test_plan_is_a_function_of_shape_only():
     assert plans[1]["qkv"]["split_k"] >= plans[256]["qkv"]["split_k"]
     forced = corun.describe_plan(c, _kv(n_slots=256, max_seq_len=4224), 16, corun.options(split_k_override=3))
     assert forced["qkv"]["split_k"] == 3 and forced["down"]["split_k"] == 3
+
+
+def test_batch_invariant_plan_ignores_the_batch_size():
+    """Batch-invariant mode (Sec. III, Fig. 3b and Definition 1): one
+    projection tile, no split-K and split-KV off for every B, so the plans
+    of all batch sizes agree except for B itself; the default plans do not."""
+    for name in ("8b", "tiny", "32b"):
+        c = wl.config(name)
+        kv = _kv(n_slots=256, max_seq_len=4224)
+        bi = corun.options(batch_invariant=True)
+        plans = [corun.describe_plan(c, kv, B, bi) for B in (1, 3, 8, 64, 65, 200, 256)]
+        strip = [{k: v for k, v in p.items() if k not in ("B", "Mp")} for p in plans]
+        assert all(s == strip[0] for s in strip), name
+        p = plans[0]
+        for proj in ("qkv", "o", "gate_up", "down", "lm_head"):
+            pr = p[proj]
+            assert pr["split_k"] == 1 and pr["m_tile"] == 128
+            assert pr["n_tile"] == (128 if pr["K"] % 64 == 0 else 0)
+        assert p["attn_max_splits"] == 1 and p["attn_chunk"] >= 4224
+    std = [corun.describe_plan(wl.config("8b"), _kv(n_slots=256, max_seq_len=4224), B) for B in (1, 256)]
+    assert std[0]["qkv"] != std[1]["qkv"] and std[0]["attn_chunk"] != std[1]["attn_chunk"]
+
+
+def test_batch_invariant_rejects_plan_overrides():
+    c = wl.config("tiny")
+    kv = _kv(n_slots=4, max_seq_len=128)
+    for extra in (dict(attn_chunk=128), dict(split_k_override=2), dict(gemm_bm=128)):
+        with pytest.raises(corun.CorunError):
+            corun.describe_plan(c, kv, 4, corun.options(batch_invariant=True, **extra))
