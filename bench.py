@@ -205,6 +205,22 @@ def bench_prefill(cfg, W, lens, args):
         out.append(dict(Lp=Lp, ms=round(1e3 * dt, 3), tok_s=round(Lp / dt, 1),
                         tflops=round(flops / dt / 1e12, 1), mfma_frac=round(flops / dt / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)))
         log(f"[bench] prefill Lp={Lp}: {1e3 * dt:.1f} ms, {Lp / dt:.0f} tok/s, {flops / dt / 1e12:.0f} TFLOP/s")
+    # chunked prefill of the longest prompt: fixed chunks run alone, in order
+    prompt = wl.make_prompt(cfg["vocab"], Lmax, seed=Lmax)
+    for C in (2048, 8192):
+        if C >= Lmax:
+            continue
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for start in range(0, Lmax, C):
+            n = min(C, Lmax - start)
+            eng.prefill_chunk(prompt[start:start + n], start, 0, want_token=start + n == Lmax)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t
+        whole = next(o for o in out if o["Lp"] == Lmax)["ms"]
+        out.append(dict(Lp=Lmax, chunk=C, ms=round(1e3 * dt, 3), tok_s=round(Lmax / dt, 1),
+                        vs_whole=round(1e3 * dt / whole, 3)))
+        log(f"[bench] prefill Lp={Lmax} in chunks of {C}: {1e3 * dt:.1f} ms ({1e3 * dt / whole:.2f}x the whole prompt)")
     eng.close()
     return out
 

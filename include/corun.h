@@ -184,6 +184,26 @@ corun_status corun_decode_run(corun_engine *e, int32_t n_steps, const int32_t *t
 corun_status corun_prefill(corun_engine *e, const int32_t *prompt, int32_t prompt_len, int32_t slot,
                            int32_t *token_out, float *last_logits);
 
+/* One chunk of a chunked isolated prefill (Sec. IV, "Isolated Prefill": a
+ * long prompt divided into fixed-size chunks that run alone, one iteration
+ * each, in order; Algorithm 1 continues them before admitting other work).
+ * Runs prompt positions start .. start+n-1 alone: their k, v are appended
+ * at those positions of `slot` in every layer, and their queries attend to
+ * positions 0 .. t of the slot's cache, the first `start` of which the
+ * caller must already have written (the prompt's earlier chunks, in order).
+ * The launch plan depends on (n, start) only, so with a chunk size fixed per
+ * deployment a prompt always runs as the same sequence of shapes.
+ *  tokens      host int32 [n]: the prompt's tokens at those positions
+ *  token_out   host int32 out, or NULL: greedy token from position
+ *              start+n-1 (the first generated token if this is the last chunk)
+ *  last_logits device fp32 [vocab] out, or NULL: that position's logits
+ * With token_out and last_logits both NULL the final norm and lm_head are
+ * skipped (an inner chunk).  corun_prefill is the single chunk at start 0.
+ * Errors: CORUN_E_STATE without a prefill workspace, CORUN_E_CAPACITY if n
+ * exceeds it or start+n the slot's cache, CORUN_E_INVAL otherwise. */
+corun_status corun_prefill_chunk(corun_engine *e, const int32_t *tokens, int32_t n, int32_t start, int32_t slot,
+                                 int32_t *token_out, float *last_logits);
+
 /* The engine's fixed batch size, model configuration and KV description
  * (copies; the k/v/page-table pointers are the caller's borrowed ones).
  * Any out pointer may be NULL. */
@@ -237,6 +257,8 @@ typedef struct {
     int32_t max_num_reqs;       /* concurrency limit, <= B (0 = B) */
     /* dry run only (engine NULL): the slots and cache; page_size 0 = contiguous */
     int32_t n_slots, max_seq_len, page_size, num_pages, max_pages_per_seq;
+    int32_t prefill_chunk;      /* > 0: prefill prompts in chunks of this many tokens (the last one shorter),
+                                   one isolated iteration each (corun_prefill_chunk); 0 = whole prompts */
 } corun_sched_cfg;
 
 corun_status corun_sched_create(corun_engine *e, const corun_sched_cfg *cfg, corun_sched **out);
@@ -246,7 +268,8 @@ void corun_sched_destroy(corun_sched *s);
  * can never fit one slot; CORUN_E_INVAL for a reused id or bad sizes. */
 corun_status corun_sched_add_request(corun_sched *s, int64_t id, const int32_t *prompt, int32_t prompt_len,
                                      int32_t max_new_tokens, uint64_t seed, float temperature);
-/* One iteration; event: 0 idle, 1 isolated prefill, 2 decode step. */
+/* One iteration; event: 0 idle, 1 isolated prefill (a whole prompt or one
+ * chunk of it), 2 decode step. */
 corun_status corun_sched_step(corun_sched *s, int32_t *event);
 /* A request's generated tokens and their log-probabilities so far (up to
  * cap), their count and whether it finished. */

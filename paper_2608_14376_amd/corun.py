@@ -19,7 +19,7 @@ OK, E_INVAL, E_SHAPE, E_CAPACITY, E_HIP, E_STATE = 0, -1, -2, -3, -4, -5
 KV_CONTIGUOUS, KV_PAGED = 0, 1
 
 EXPORTS = ("corun_engine_create", "corun_engine_destroy", "corun_decode_step", "corun_decode_run",
-           "corun_prefill", "corun_check_config", "corun_check_batch", "corun_describe_plan",
+           "corun_prefill", "corun_prefill_chunk", "corun_check_config", "corun_check_batch", "corun_describe_plan",
            "corun_last_error", "corun_time_kernel", "corun_sample", "corun_engine_info",
            "corun_sched_create", "corun_sched_destroy", "corun_sched_add_request", "corun_sched_step",
            "corun_sched_output", "corun_sched_state", "corun_sched_last_error")
@@ -87,6 +87,9 @@ def load():
     L.corun_decode_run.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
     L.corun_prefill.restype = st
     L.corun_prefill.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]
+    L.corun_prefill_chunk.restype = st
+    L.corun_prefill_chunk.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
+                                      C.c_void_p]
     L.corun_check_config.restype = st
     L.corun_check_config.argtypes = [C.POINTER(ModelCfg), C.POINTER(KV), C.c_int32]
     L.corun_check_batch.restype = st
@@ -196,7 +199,8 @@ def describe_plan(cfg: dict, kv: KV, B: int, opt: Options | None = None) -> dict
 
 class SchedCfg(C.Structure):
     _fields_ = [("max_num_reqs", C.c_int32), ("n_slots", C.c_int32), ("max_seq_len", C.c_int32),
-                ("page_size", C.c_int32), ("num_pages", C.c_int32), ("max_pages_per_seq", C.c_int32)]
+                ("page_size", C.c_int32), ("num_pages", C.c_int32), ("max_pages_per_seq", C.c_int32),
+                ("prefill_chunk", C.c_int32)]
 
 
 class Scheduler:
@@ -207,10 +211,10 @@ class Scheduler:
     IDLE, PREFILL, DECODE = 0, 1, 2
 
     def __init__(self, engine=None, max_num_reqs=0, n_slots=0, max_seq_len=0, page_size=0, num_pages=0,
-                 max_pages_per_seq=0):
+                 max_pages_per_seq=0, prefill_chunk=0):
         self._L = load()
         self.engine = engine
-        cfg = SchedCfg(max_num_reqs, n_slots, max_seq_len, page_size, num_pages, max_pages_per_seq)
+        cfg = SchedCfg(max_num_reqs, n_slots, max_seq_len, page_size, num_pages, max_pages_per_seq, prefill_chunk)
         h = C.c_void_p()
         st = self._L.corun_sched_create(engine._h if engine is not None else None, C.byref(cfg), C.byref(h))
         if st != 0:
@@ -373,3 +377,15 @@ class Engine:
         _check(self._L.corun_prefill(self._h, p.ctypes.data, p.size, slot, tok.ctypes.data,
                                      None if last_logits is None else last_logits.data_ptr()))
         return int(tok[0])
+
+    def prefill_chunk(self, tokens, start: int, slot: int, last_logits=None, want_token=True):
+        """Positions start .. start+len(tokens)-1 of a prompt whose earlier
+        positions are already cached in `slot`; returns the greedy token of
+        the chunk's last position (None for an inner chunk: want_token False
+        and no last_logits)."""
+        p = _np(tokens, np.int32)
+        tok = np.empty(1, np.int32)
+        _check(self._L.corun_prefill_chunk(self._h, p.ctypes.data, p.size, start, slot,
+                                           tok.ctypes.data if want_token else None,
+                                           None if last_logits is None else last_logits.data_ptr()))
+        return int(tok[0]) if want_token else None

@@ -610,7 +610,7 @@ static corun_status alloc_prefill(corun_engine *e)
         cv.take(&e->pf_moe_tiles, (size_t)3 * (c.n_experts + (na + 15) / 16));
         cv.take(&e->pf_moe_act, na * Fe);
     }
-    cv.take(&e->pf_pos, (size_t)L);
+    cv.take(&e->pf_pos, (size_t)std::max(L, kv_capacity(&e->kv)));   // positions of any chunk
     cv.take(&e->pf_tok, (size_t)L);
     cv.take(&e->pf_amax, (size_t)gemm_col_blocks(c.vocab));
     size_t total = cv.take(&e->pf_next, 16);
@@ -626,7 +626,7 @@ static corun_status alloc_prefill(corun_engine *e)
         rebase(e->pf_moe_act, e->pws);
     }
     rebase(e->pf_pos, e->pws); rebase(e->pf_tok, e->pws); rebase(e->pf_amax, e->pws); rebase(e->pf_next, e->pws);
-    HIP_TRY(launch_iota(e->pf_pos, L, e->st));
+    HIP_TRY(launch_iota(e->pf_pos, std::max(L, kv_capacity(&e->kv)), e->st));
     return CORUN_OK;
 }
 
@@ -857,26 +857,30 @@ extern "C" corun_status corun_decode_run(corun_engine *e, int32_t n_steps, const
 }
 
 // ---------------------------------------------------------------------------
-// Isolated prefill: every launch is sized by prompt_len alone.
+// Isolated prefill: every launch is sized by the chunk's length and start
+// alone (the whole prompt is one chunk at start 0).
 // ---------------------------------------------------------------------------
 
-extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, int32_t Lp, int32_t slot,
-                                      int32_t *token_out, float *last_logits)
+extern "C" corun_status corun_prefill_chunk(corun_engine *e, const int32_t *tokens, int32_t n, int32_t start,
+                                            int32_t slot, int32_t *token_out, float *last_logits)
 {
-    if (!e || !prompt || !token_out) return fail(CORUN_E_INVAL, "null argument");
+    if (!e || !tokens) return fail(CORUN_E_INVAL, "null argument");
     if (e->pf_max <= 0) return fail(CORUN_E_STATE, "engine was created without a prefill workspace");
-    if (Lp < 1) return fail(CORUN_E_INVAL, "prompt_len must be >= 1");
-    if (Lp > e->pf_max) return fail(CORUN_E_CAPACITY, "prompt_len %d exceeds the prefill workspace %d", Lp, e->pf_max);
+    if (n < 1) return fail(CORUN_E_INVAL, "chunk length must be >= 1");
+    if (start < 0) return fail(CORUN_E_INVAL, "negative chunk start");
+    if (n > e->pf_max) return fail(CORUN_E_CAPACITY, "chunk length %d exceeds the prefill workspace %d", n, e->pf_max);
     if (slot < 0 || slot >= e->kv.n_slots) return fail(CORUN_E_INVAL, "slot %d outside [0, %d)", slot, e->kv.n_slots);
-    if (Lp > kv_capacity(&e->kv)) return fail(CORUN_E_CAPACITY, "prompt_len %d exceeds the cache capacity", Lp);
-    for (int t = 0; t < Lp; ++t)
-        if (prompt[t] < 0 || prompt[t] >= e->c.vocab)
-            return fail(CORUN_E_INVAL, "prompt[%d] = %d outside [0, %d)", t, prompt[t], e->c.vocab);
+    const int cap = kv_capacity(&e->kv);
+    if ((int64_t)start + n > cap)
+        return fail(CORUN_E_CAPACITY, "positions %d..%d exceed the cache capacity %d", start, start + n - 1, cap);
+    for (int t = 0; t < n; ++t)
+        if (tokens[t] < 0 || tokens[t] >= e->c.vocab)
+            return fail(CORUN_E_INVAL, "token[%d] = %d outside [0, %d)", t, tokens[t], e->c.vocab);
     if (e->kv.layout == CORUN_KV_PAGED) {
         std::vector<int32_t> pt(e->kv.max_pages_per_seq);
         HIP_TRY(hipMemcpy(pt.data(), e->kv.page_table + (size_t)slot * e->kv.max_pages_per_seq,
                           pt.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
-        for (int j = 0; j <= (Lp - 1) / e->kv.page_size; ++j)
+        for (int j = 0; j <= (start + n - 1) / e->kv.page_size; ++j)
             if (pt[j] < 0 || pt[j] >= e->kv.num_pages)
                 return fail(CORUN_E_CAPACITY, "slot %d: page %d maps to %d outside [0, %d)", slot, j, pt[j],
                             e->kv.num_pages);
@@ -886,6 +890,7 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
     const int H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn;
     const int nqkv = (nq + 2 * nkv) * d;
     hipStream_t st = e->st;
+    const int Lp = n;     // rows of every projection: the chunk's tokens
     const int cap_rows = std::max(1, e->pf_max / Lp);
     const bool bi = e->opt.batch_invariant != 0;
     const Proj pq = choose_proj(nqkv, H, Lp, 0, cap_rows, 0, bi);
@@ -898,15 +903,15 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
     const MoeBufs pmb{nullptr, e->pf_part, e->pf_moe_w, e->pf_moe_gu, e->pf_moe_y, e->pf_moe_sel, e->pf_moe_list,
                       e->pf_moe_tiles, e->pf_moe_act, e->moe ? c.n_experts + (Lp * c.top_k + 15) / 16 : 0};
 
-    HIP_TRY(hipMemcpyAsync(e->pf_tok, prompt, sizeof(int32_t) * Lp, hipMemcpyHostToDevice, st));
+    HIP_TRY(hipMemcpyAsync(e->pf_tok, tokens, sizeof(int32_t) * Lp, hipMemcpyHostToDevice, st));
     HIP_TRY(launch_embed(e->embed, e->pf_tok, nullptr, Lp, H, e->pf_x, st));
     for (int l = 0; l < c.n_layers; ++l) {
         HIP_TRY(launch_rmsnorm(e->pf_x, l ? e->pf_part : nullptr, l ? dense_S : 0, (long long)Lp * H, Lp, H,
                                e->attn_norm[l], c.rms_eps, e->pf_h, st, fold_of(e, pmb, l)));
         HIP_TRY(launch_proj(e->pf_h, H, e->w_qkv[l], shape_of(pq, Lp), e->pf_part, (long long)Lp * nqkv, nqkv, st));
-        HIP_TRY(launch_qkv_post(e->pf_part, pq.S, (long long)Lp * nqkv, Lp, nullptr, e->pf_pos, nullptr, slot, nq, nkv,
-                                d, e->rope, e->pf_q, e->kc[l], e->vc[l], e->view, st));
-        HIP_TRY(launch_prefill_attn(e->pf_q, Lp, nq, nkv, d, slot, e->kc[l], e->vc[l], e->view, e->pf_o, st));
+        HIP_TRY(launch_qkv_post(e->pf_part, pq.S, (long long)Lp * nqkv, Lp, nullptr, e->pf_pos + start, nullptr, slot,
+                                nq, nkv, d, e->rope, e->pf_q, e->kc[l], e->vc[l], e->view, st));
+        HIP_TRY(launch_prefill_attn(e->pf_q, Lp, start, nq, nkv, d, slot, e->kc[l], e->vc[l], e->view, e->pf_o, st));
         HIP_TRY(launch_proj(e->pf_o, nq * d, e->w_o[l], shape_of(po, Lp), e->pf_part, (long long)Lp * H, H, st));
         HIP_TRY(launch_rmsnorm(e->pf_x, e->pf_part, po.S, (long long)Lp * H, Lp, H, e->mlp_norm[l], c.rms_eps,
                                e->pf_h, st));
@@ -923,6 +928,10 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
             HIP_TRY(launch_proj(e->pf_a, F, e->w_down[l], shape_of(pd, Lp), e->pf_part, (long long)Lp * H, H, st));
         }
     }
+    if (!token_out && !last_logits) {   // an inner chunk: its KV is the product
+        HIP_TRY(hipStreamSynchronize(st));
+        return CORUN_OK;
+    }
     // last position only: fold its down partials, final norm, lm_head, argmax
     const size_t last = (size_t)(Lp - 1) * H;
     MoeFold lf = fold_of(e, pmb, c.n_layers);
@@ -938,8 +947,18 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
     if (last_logits)
         HIP_TRY(hipMemcpyAsync(last_logits, e->pf_logits, sizeof(float) * c.vocab, hipMemcpyDeviceToDevice, st));
     HIP_TRY(hipStreamSynchronize(st));
-    *token_out = e->h_next[0];
+    if (token_out) *token_out = e->h_next[0];
     return CORUN_OK;
+}
+
+extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, int32_t Lp, int32_t slot,
+                                      int32_t *token_out, float *last_logits)
+{
+    if (!token_out) return fail(CORUN_E_INVAL, "null argument");
+    if (e && e->pf_max > 0 && Lp > e->pf_max)
+        return fail(CORUN_E_CAPACITY, "prompt_len %d exceeds the prefill workspace %d", Lp, e->pf_max);
+    if (e && Lp > kv_capacity(&e->kv)) return fail(CORUN_E_CAPACITY, "prompt_len %d exceeds the cache capacity", Lp);
+    return corun_prefill_chunk(e, prompt, Lp, 0, slot, token_out, last_logits);
 }
 
 extern "C" corun_status corun_engine_info(const corun_engine *e, int32_t *B_fixed, corun_model_cfg *cfg, corun_kv *kv)

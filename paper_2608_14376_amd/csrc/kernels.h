@@ -112,9 +112,11 @@ hipError_t launch_attn_merge(const float *ws, int rows, const uint8_t *valid, co
 hipError_t launch_sample(const float *logits, long long ld, int rows, int V, const uint8_t *valid, const int32_t *pos,
                          const uint64_t *seed, const float *temp, int32_t *token, float *logprob, hipStream_t st);
 
-// Causal attention of the isolated prefill: q (bf16 [Lp][nq d]) against keys
-// 0..t of `slot` for query position t, o (bf16 [Lp][nq d]).  Sized by Lp only.
-hipError_t launch_prefill_attn(const uint16_t *q, int Lp, int nq, int nkv, int d, int slot, const uint16_t *kc,
+// Causal attention of the isolated prefill: q (bf16 [n][nq d], row i = query
+// position p0 + i) against keys 0..t of `slot` for query position t, o (bf16
+// [n][nq d]).  Keys before p0 are read from the cache (earlier chunks of the
+// prompt).  Sized by (n, p0) only.
+hipError_t launch_prefill_attn(const uint16_t *q, int n, int p0, int nq, int nkv, int d, int slot, const uint16_t *kc,
                                const uint16_t *vc, KvView kv, uint16_t *o, hipStream_t st);
 
 // a[m][j] = bf16(silu(bf16(sum_s gate)) * bf16(sum_s up)) over the partials

@@ -1731,6 +1731,9 @@ hipError_t launch_moe_gemm(const uint16_t *A, int lda, int row_div, const uint16
 // Causal attention of the isolated prefill (flash-style, no split): the
 // prompt runs alone, so any fixed order is allowed; this one takes, for every
 // query, the keys in tiles of 64 in increasing order with the online softmax.
+// A chunk of a longer prompt (chunked prefill) has its queries at positions
+// p0 .. p0 + n - 1 and reads the keys of positions before p0 from the cache,
+// where the prompt's earlier chunks wrote them; p0 = 0 is the whole prompt.
 //
 // Work units of one KV head: (block of 32 queries, one query head of the
 // group).  A workgroup of eight wavefronts (two per SIMD, so one wavefront's
@@ -1767,7 +1770,7 @@ __device__ __forceinline__ int pf_swz(int r, int c)
 }
 
 template <int D>
-__global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict__ q, int Lp, int nq, int nkv,
+__global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict__ q, int n, int p0, int nq, int nkv,
                                                       int slot, const uint16_t *__restrict__ kc,
                                                       const uint16_t *__restrict__ vc, KvView kv,
                                                       uint16_t *__restrict__ o)
@@ -1786,21 +1789,25 @@ __global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict
     typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
     const int G = nq / nkv;
+    // queries are the n positions p0 .. p0 + n - 1 (q and o rows 0 .. n - 1);
+    // keys are positions 0 .. Lk - 1 of the slot's cache, the first p0 of
+    // them written by earlier chunks of the same prompt
+    const int Lk = p0 + n;
     // grid (kv head, unit group): workgroups are dispatched x fastest, so the
     // groups with the latest (longest) query blocks of every kv head go first
     const int kvh = blockIdx.x, grp = blockIdx.y;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int r32 = lane & 31, h = lane >> 5;
-    const int nqb = (Lp + QB - 1) / QB;
+    const int nqb = (n + QB - 1) / QB;
     const int units = nqb * G;
     const int u = units - 1 - (grp * NW + wave);                // latest blocks first
     const bool active = u >= 0;
     const int qb = active ? u / G : 0, g = active ? u % G : 0;
     const int hq = kvh * G + g;
-    const int q0 = qb * QB;
+    const int q0 = qb * QB;                                     // chunk row of the block's first query
     const int u_first = units - 1 - grp * NW;
-    const int wg_last_q = min(Lp, (u_first / G + 1) * QB) - 1;
-    const int my_last_q = active ? min(Lp, q0 + QB) - 1 : -1;
+    const int wg_last_q = p0 + min(n, (u_first / G + 1) * QB) - 1;
+    const int my_last_q = active ? p0 + min(n, q0 + QB) - 1 : -1;
     const int ntiles = wg_last_q / BKT + 1;
 
     // tile loads: op j of thread t is 16-byte unit 512 j + t of the K part
@@ -1811,14 +1818,14 @@ __global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict
 #pragma unroll
         for (int j = 0; j < K_OPS; ++j) {
             const int gi = j * NT + tid, r = gi / KCH, c = pf_swz<KCH>(r, gi % KCH) - r * KCH;
-            const int key = min(k0 + r, Lp - 1);
+            const int key = min(k0 + r, Lk - 1);
             __builtin_amdgcn_global_load_lds((const void *)(kc + kv_offset(kv, nkv, D, slot, kvh, key) + 8 * c),
                                              (lds_void *)(base + j * NT), 16, 0, 0);
         }
 #pragma unroll
         for (int j = 0; j < V_OPS; ++j) {
             const int gi = j * NT + tid, e = gi >> 3, c = pf_swz<8>(e, gi & 7) - e * 8;
-            const int key0 = min(k0 + 8 * c, (Lp - 1) & ~7);
+            const int key0 = min(k0 + 8 * c, (Lk - 1) & ~7);
             __builtin_amdgcn_global_load_lds((const void *)(vc + v_offset(kv, nkv, D, slot, kvh, key0, e)),
                                              (lds_void *)(base + KSTAGE + j * NT), 16, 0, 0);
         }
@@ -1831,7 +1838,7 @@ __global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             uint4 v = {0u, 0u, 0u, 0u};
-            if (active && qq < Lp) v = *(const uint4 *)(q + (size_t)qq * nq * D + (size_t)hq * D + 16 * ks + 8 * h);
+            if (active && qq < n) v = *(const uint4 *)(q + (size_t)qq * nq * D + (size_t)hq * D + 16 * ks + 8 * h);
             qf[ks] = __builtin_bit_cast(bf16x8, v);
         }
     }
@@ -1843,7 +1850,7 @@ __global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict
     float mrow = -INFINITY, lpart = 0.f;
     const float scale2 = 1.4426950408889634f / sqrtf((float)D);   // log2(e) / sqrt(d)
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
-    const int qq = q0 + r32;
+    const int qq = p0 + q0 + r32;                     // this lane's query position
 
 #pragma unroll
     for (int i = 0; i < P; ++i)
@@ -1854,12 +1861,12 @@ __global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict
         const int k0 = i * BKT;
         uint4 *Kt = ring + (i % NST) * STAGE;
         uint4 *Vt = Kt + KSTAGE;
-        if (k0 + BKT > Lp) {
+        if (k0 + BKT > Lk) {
             // last tile: zero the values of keys past the prompt
             uint16_t *v16 = (uint16_t *)Vt;
             for (int it = tid; it < D * BKT; it += NT) {
                 const int e = it / BKT, kk = it % BKT;
-                if (k0 + kk >= Lp) v16[pf_swz<8>(e, kk >> 3) * 8 + (kk & 7)] = 0;
+                if (k0 + kk >= Lk) v16[pf_swz<8>(e, kk >> 3) * 8 + (kk & 7)] = 0;
             }
             lds_barrier();
         }
@@ -1882,13 +1889,13 @@ __global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict
         // of query qq; only tiles reaching past the wavefront's first query or
         // past the prompt need the mask
         float mt = -INFINITY;
-        if (k0 + BKT - 1 > q0 || k0 + BKT > Lp) {
+        if (k0 + BKT - 1 > p0 + q0 || k0 + BKT > Lk) {
 #pragma unroll
             for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
                 for (int j = 0; j < 16; ++j) {
                     const int key = k0 + 32 * kt + 16 * (j >> 3) + 8 * h + (j & 7);
-                    const float sv = (key <= qq && key < Lp) ? st[kt][j] : -INFINITY;
+                    const float sv = (key <= qq && key < Lk) ? st[kt][j] : -INFINITY;
                     st[kt][j] = sv;
                     mt = fmaxf(mt, sv);
                 }
@@ -1960,22 +1967,22 @@ __global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict
     for (int it = lane; it < QB * (D / 8); it += 64) {
         const int qr = it / (D / 8), c8 = it % (D / 8);
         const int qo = q0 + qr;
-        if (qo < Lp)
+        if (qo < n)
             *(uint4 *)(o + (size_t)qo * nq * D + (size_t)hq * D + 8 * c8) = *(const uint4 *)(ost + qr * OPITCH + 8 * c8);
     }
 }
 
-hipError_t launch_prefill_attn(const uint16_t *q, int Lp, int nq, int nkv, int d, int slot, const uint16_t *kc,
+hipError_t launch_prefill_attn(const uint16_t *q, int n, int p0, int nq, int nkv, int d, int slot, const uint16_t *kc,
                                const uint16_t *vc, KvView kv, uint16_t *o, hipStream_t st)
 {
-    if (Lp <= 0) return hipErrorInvalidValue;
+    if (n <= 0 || p0 < 0) return hipErrorInvalidValue;
     const int G = nq / nkv;
-    const int units = ((Lp + 31) / 32) * G;
+    const int units = ((n + 31) / 32) * G;
     dim3 grid(nkv, (units + 7) / 8);
     if (d == 128)
-        hipLaunchKernelGGL((k_prefill_attn<128>), grid, dim3(512), 0, st, q, Lp, nq, nkv, slot, kc, vc, kv, o);
+        hipLaunchKernelGGL((k_prefill_attn<128>), grid, dim3(512), 0, st, q, n, p0, nq, nkv, slot, kc, vc, kv, o);
     else if (d == 64)
-        hipLaunchKernelGGL((k_prefill_attn<64>), grid, dim3(512), 0, st, q, Lp, nq, nkv, slot, kc, vc, kv, o);
+        hipLaunchKernelGGL((k_prefill_attn<64>), grid, dim3(512), 0, st, q, n, p0, nq, nkv, slot, kc, vc, kv, o);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();

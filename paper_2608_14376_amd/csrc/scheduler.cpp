@@ -4,7 +4,7 @@
 // IV, "Shape-Aligned Sampling"), as a continuous-batching loop with slot
 // reuse, a concurrency limit and full-sequence KV admission.
 //
-// The scheduler is a client of the engine's C ABI: corun_prefill,
+// The scheduler is a client of the engine's C ABI: corun_prefill_chunk,
 // corun_decode_step and corun_sample.  Each schedule() call runs one
 // iteration, either the isolated prefill of one request or one decode step
 // of every running request, padded to the engine's fixed B.
@@ -54,7 +54,7 @@ struct Request {
     int32_t max_new = 0;
     uint64_t seed = 0;
     float temperature = 0.f;
-    int32_t num_computed = 0;           // prompt tokens whose KV is cached (prefill runs whole: 0 or prompt_len)
+    int32_t num_computed = 0;           // prompt tokens whose KV is cached (chunks done so far)
     int32_t slot = -1;
     std::vector<int32_t> pages;
     std::vector<int32_t> tokens;        // generated
@@ -67,6 +67,7 @@ struct Request {
 struct corun_sched {
     corun_engine *e = nullptr;          // null: dry run
     int B = 0, max_num_reqs = 0, vocab = 0;
+    int32_t chunk = 0;                  // prefill chunk (0 = whole prompts)
     corun_kv kv{};
     bool paged = false;
     std::unordered_map<int64_t, Request> reqs;
@@ -165,23 +166,30 @@ corun_status append(corun_sched *s, Request &r, int32_t tok, float lp)
     return CORUN_OK;
 }
 
-// Prefill of one request alone (its own shape), then its first token sampled
-// from the last position's logits (one sampling row).
+// Prefill of one request alone (its own shape): the whole prompt, or its next
+// fixed-size chunk.  After the prompt's last position its first token is
+// sampled from that position's logits (one sampling row).
 corun_status run_prefill(corun_sched *s, Request &r)
 {
+    const int32_t L = (int32_t)r.prompt.size(), start = r.num_computed;
+    const int32_t n = s->chunk > 0 ? std::min(s->chunk, L - start) : L - start;
+    const bool last = start + n == L;
     int32_t tok = 0;
     float lp = 0.f;
     if (s->e) {
-        corun_status st = corun_prefill(s->e, r.prompt.data(), (int32_t)r.prompt.size(), r.slot, &tok, s->last);
+        corun_status st = corun_prefill_chunk(s->e, r.prompt.data() + start, n, start, r.slot,
+                                              last ? &tok : nullptr, last ? s->last : nullptr);
         if (st != CORUN_OK) return from_engine(st);
-        const uint8_t one = 1;
-        const int32_t pos = (int32_t)r.prompt.size();
-        st = corun_sample(s->e, s->last, s->vocab, 1, &one, &pos, &r.seed, &r.temperature, &tok, &lp);
-        if (st != CORUN_OK) return from_engine(st);
+        if (last) {
+            const uint8_t one = 1;
+            const int32_t pos = L;
+            st = corun_sample(s->e, s->last, s->vocab, 1, &one, &pos, &r.seed, &r.temperature, &tok, &lp);
+            if (st != CORUN_OK) return from_engine(st);
+        }
     }
-    r.num_computed = (int32_t)r.prompt.size();
+    r.num_computed = start + n;
     ++s->n_prefill;
-    return append(s, r, tok, lp);
+    return last ? append(s, r, tok, lp) : CORUN_OK;
 }
 
 // One fixed-shape decode step of every running request, padded to B, then
@@ -195,6 +203,7 @@ corun_status run_decode(corun_sched *s)
     std::vector<float> temp(B, 0.f), lps(B, 0.f);
     for (int64_t id : s->running) {
         const Request &r = s->reqs.at(id);
+        if (r.tokens.empty()) continue;   // prefill unfinished (Algorithm 1 runs it first): not in this step
         tokens[r.slot] = r.tokens.back();
         seq[r.slot] = (int32_t)r.prompt.size() + (int32_t)r.tokens.size() - 1;   // cached tokens
         pos[r.slot] = seq[r.slot] + 1;                                           // the sampled token's position
@@ -214,6 +223,7 @@ corun_status run_decode(corun_sched *s)
     ++s->n_decode;
     for (int64_t id : s->running) {
         Request &r = s->reqs.at(id);
+        if (r.tokens.empty()) continue;
         corun_status st = append(s, r, next[r.slot], lps[r.slot]);
         if (st != CORUN_OK) return st;
     }
@@ -307,6 +317,11 @@ extern "C" corun_status corun_sched_create(corun_engine *e, const corun_sched_cf
     }
     s->paged = s->kv.layout == CORUN_KV_PAGED;
     s->max_num_reqs = cfg->max_num_reqs > 0 ? std::min(cfg->max_num_reqs, s->B) : s->B;
+    if (cfg->prefill_chunk < 0) {
+        delete s;
+        return sfail(CORUN_E_INVAL, "negative prefill_chunk");
+    }
+    s->chunk = cfg->prefill_chunk;
     if (s->B <= 0 || (!s->paged && s->kv.max_seq_len <= 0) ||
         (s->paged && (s->kv.page_size <= 0 || s->kv.num_pages <= 0 || s->kv.max_pages_per_seq <= 0))) {
         delete s;

@@ -46,11 +46,11 @@ def engine(cfg, Wg, paged=False):
     return eng, (K, V, pt)
 
 
-def run(cfg, Wg, reqs, order, arrive_at=None, paged=False, max_num_reqs=6):
+def run(cfg, Wg, reqs, order, arrive_at=None, paged=False, max_num_reqs=6, chunk=0):
     """Feed `reqs` in `order`; request k arrives before step arrive_at[k]
     (all at once by default).  Returns {id: (tokens, logprob bits)}."""
     eng, keep = engine(cfg, Wg, paged)
-    s = corun.Scheduler(eng, max_num_reqs=max_num_reqs)
+    s = corun.Scheduler(eng, max_num_reqs=max_num_reqs, prefill_chunk=chunk)
     arrive_at = arrive_at or [0] * len(order)
     pending = sorted(zip(arrive_at, range(len(order))))
     step, k = 0, 0
@@ -99,3 +99,22 @@ def test_paged_cache_gives_the_same_outputs(setup):
     a = run(cfg, Wg, reqs, list(range(n)))
     b = run(cfg, Wg, reqs, list(range(n))[::-1], paged=True)
     assert a == b
+
+
+def test_chunked_prefill_outputs_do_not_depend_on_arrival(setup):
+    """Prompts of 4..40 tokens in chunks of 16 (Algorithm 1 continues a
+    partially prefilled head first): every request's tokens and
+    log-probability bits are the same across arrival orders, concurrency
+    limits, alone, and on a paged cache."""
+    cfg, Wg, reqs = setup
+    n = len(reqs)
+    base = run(cfg, Wg, reqs, list(range(n)), chunk=16)
+    rng = np.random.default_rng(85)
+    shuffled = list(rng.permutation(n))
+    timed = run(cfg, Wg, reqs, shuffled, arrive_at=sorted(rng.integers(0, 40, n).tolist()), chunk=16)
+    tight = run(cfg, Wg, reqs, shuffled[::-1], max_num_reqs=2, chunk=16)
+    paged = run(cfg, Wg, reqs, list(range(n))[::-1], paged=True, chunk=16)
+    for rid, v in base.items():
+        assert timed[rid] == v and tight[rid] == v and paged[rid] == v, rid
+    for i in (0, 5):
+        assert run(cfg, Wg, reqs, [i], chunk=16)[reqs[i]["id"]] == base[reqs[i]["id"]], i

@@ -110,3 +110,35 @@ def test_every_request_generates_its_output_length():
     for i, n in want.items():
         tok, lp, fin = s.output(i)
         assert len(tok) == n and fin
+
+
+def test_chunked_prefill_runs_the_head_to_completion_first():
+    """Algorithm 1's first branch: a running head whose prompt is not fully
+    computed continues before anything else.  A (2-token prompt) is running;
+    B's 10-token prompt in chunks of 4 takes three isolated iterations in a
+    row -- no decode and no other admission in between -- and only its last
+    chunk yields a token."""
+    s = corun.Scheduler(None, max_num_reqs=3, n_slots=4, max_seq_len=64, prefill_chunk=4)
+    s.add_request(0, [1] * 2, max_new_tokens=6)
+    assert s.step() == P
+    s.add_request(1, [1] * 10, max_new_tokens=2)
+    s.add_request(2, [1] * 3, max_new_tokens=2)
+    for k in range(3):
+        assert s.step() == P
+        assert len(s.output(0)[0]) == 1                       # A was not decoded
+        assert len(s.output(1)[0]) == (1 if k == 2 else 0)    # B's token after its last chunk
+        assert len(s.output(2)[0]) == 0                       # C not admitted meanwhile
+    assert s.step() == P                                      # C: one chunk
+    assert s.step() == D
+    assert len(s.output(0)[0]) == 2 and len(s.output(1)[0]) == 2 and len(s.output(2)[0]) == 2
+
+
+def test_chunk_count_per_prompt():
+    s = corun.Scheduler(None, max_num_reqs=1, n_slots=2, max_seq_len=128, prefill_chunk=16)
+    lens = [1, 15, 16, 17, 48, 100]
+    for i, L in enumerate(lens):
+        s.add_request(i, [5] * L, max_new_tokens=1)
+    ev = s.run_until_idle()
+    assert ev.count(P) == sum((L + 15) // 16 for L in lens) and ev.count(D) == 0
+    with pytest.raises(corun.CorunError):
+        corun.Scheduler(None, n_slots=2, max_seq_len=64, prefill_chunk=-1)
