@@ -538,8 +538,9 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const uint16_t *__restrict__
 // ---------------------------------------------------------------------------
 // Large-M projection, pipelined: both operands stream global -> LDS with the
 // direct 16-byte LDS loads of gfx950 (no register staging) through a ring of
-// NST stages of BK (32 or 64) K elements, NST - 1 stages in flight while one
-// feeds the matrix cores.  The loads of a stage are the only vector-memory
+// NST stages of BK (32 or 64) K elements: while the matrix cores run stage i
+// from registers, stage i + 1 is read from LDS and NST - 1 stages are in
+// flight.  The loads of a stage are the only vector-memory
 // operations of the loop, so "stage i has landed" is a fixed vmcnt: the
 // number of loads issued after it.
 //
@@ -611,7 +612,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
     constexpr int FM = WM / 32, FN = WN / 32;
     constexpr int A_OPS = BM * C / NT, W_OPS = BN * C / NT;
     static_assert(A_OPS * NT == BM * C && W_OPS * NT == BN * C, "loads cover the tile");
-    constexpr int OPS = A_OPS + W_OPS, P = NST - 1;
+    constexpr int OPS = A_OPS + W_OPS, P = NST;       // every slot of the ring is a stage in flight
     constexpr int STAGE = (BM + BN) * C;             // 16-byte units
     static_assert(P * OPS <= 63, "vmcnt range");
     __shared__ __attribute__((aligned(16))) uint4 ring[NST * STAGE];
@@ -698,14 +699,16 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
                 for (int j = 0; j < FN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[ks][i], f.w[ks][j], acc[i][j], 0, 0, 0);
     };
-    // Stage i: make stage i + 1 visible, refill the slot freed by stage i - 1
-    // with stage i + P, read stage i + 1's fragments into `nxt`, then run
-    // stage i's products from `cur` while those reads are in flight.  The
-    // freed slot was read two steps ago, before the products of step i - 1
-    // that precede this step's barrier.
+    // Stage i: make stage i + 1 visible, refill stage i's slot with stage
+    // i + P, read stage i + 1's fragments into `nxt`, then run stage i's
+    // products from `cur` while those reads and P - 1 stages of loads are in
+    // flight.  Stage i's fragments were read into registers during step
+    // i - 1; each wavefront waits for its LDS reads (lgkmcnt 0) before the
+    // barrier, so no read of the slot is pending when its refill is issued.
     auto step = [&](int i, const Frags &cur, Frags &nxt) {
         if (i + 1 < nk) {
             wait_stages<OPS, P - 1>(min(P - 2, nk - 2 - i));
+            __builtin_amdgcn_s_waitcnt(0xC07F);       // lgkmcnt(0): this wavefront's LDS reads are done
             lds_barrier();
             if (i + P < nk) issue((i + P) % NST, (i + P) * BK);
             read(nxt, (i + 1) % NST);
