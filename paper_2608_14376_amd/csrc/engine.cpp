@@ -69,9 +69,15 @@ struct Plan {
 int mt_for(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 
 // Kernel, tile and split-K factor from the projection shape and M only.
-//  * M <= 64: the skinny kernel (weights streamed to registers); aim for
-//    about 2048 wavefronts (8 per CU) so enough weight bytes are in flight,
-//    each split keeping at least 256 K elements.
+//  * M <= 8 (or K % 64 != 0 and M <= 64): the skinny kernel (weights
+//    streamed to registers); aim for about 2048 wavefronts (8 per CU) so
+//    enough weight bytes are in flight, each split keeping at least 256 K
+//    elements.
+//  * 8 < M <= 64, K % 64 == 0: the pipelined kernel with a 32- or 64-row
+//    tile and 128 columns, split-K to about 256 workgroups (each split at
+//    least 512 K elements).  The skinny kernel's register loads read 16 rows
+//    x 64 bytes per instruction, which caps its weight stream; at these M it
+//    also repeats each weight tile's loads per 16-row tile.
 //  * M > 64, K % 64 == 0: the pipelined kernel (one workgroup per CU) with
 //    M tile 128 (M <= 128) or 256 and N tile 128; 256 x 256 tiles (eight
 //    wavefronts) once those tiles alone fill the GPU (large prefill) and for
@@ -98,7 +104,14 @@ Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_
         p.S = 1;
         return p;
     }
-    if (M > 64 && bm_override <= 0 && K % 64 == 0) {
+    if (M > 8 && M <= 64 && bm_override <= 0 && K % 64 == 0) {
+        p.bm = M <= 32 ? 32 : 64;
+        p.bn = 128;
+        const int tiles = (N + 127) / 128;
+        S = std::max(1, 256 / tiles);
+        S = std::min(S, std::max(1, K / 512));
+        align = 64;
+    } else if (M > 64 && bm_override <= 0 && K % 64 == 0) {
         p.bm = M <= 128 ? 128 : 256;
         p.bn = 128;
         const long long t256 = (long long)((M + 255) / 256) * ((N + 255) / 256);
@@ -167,7 +180,7 @@ Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_
     // lm_head: never split (its epilogue selects the argmax partials) except
     // under the split override test aid; the 64-row tile has no argmax epilogue
     p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0, bo == 64 ? 0 : bo, bi);
-    if (p.lm.bm == 64) p.lm = choose_proj(c->vocab, H, 64, so > 0 ? so : 1, 0, 0);
+    if (p.lm.bm == 64 && p.lm.bn == 0) p.lm = choose_proj(c->vocab, H, 64, so > 0 ? so : 1, 0, 0);
     const int cap = kv_capacity(kv);
     // batch-invariant mode turns split-KV off: one split covers the capacity
     p.chunk = bi ? (cap + 63) / 64 * 64 : choose_chunk(B, c->n_kv_heads, cap, opt.attn_chunk);

@@ -788,16 +788,24 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
 hipError_t launch_gemm_dma(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
                            long long split_stride, int ldo, hipStream_t st, ArgBest *amax)
 {
-    // 128-column tiles: four wavefronts (2 x 2, 64-row and 64-column wavefront
-    // tiles), 64-element stages; 256 x 256: eight wavefronts (2 x 4, 128 x 64),
-    // two per SIMD, 32-element stages.  Every configuration has 64-column
-    // wavefront tiles, as the argmax epilogue needs.
+    // 32 or 64 x 128 (small batches): two wavefronts side by side (32- or
+    // 64-row, 64-column wavefront tiles); 128-column tiles: four wavefronts
+    // (2 x 2, 64-row and 64-column wavefront tiles), 64-element stages;
+    // 256 x 256: eight wavefronts (2 x 4, 128 x 64), two per SIMD, 32-element
+    // stages.  Every configuration has 64-column wavefront tiles, as the
+    // argmax epilogue needs.
     const int bk = g.bn == 256 ? 32 : 64;
     if (g.K % bk != 0 || g.Kc % bk != 0 || g.M <= 0) return hipErrorInvalidValue;
     const int num_n = (g.N + g.bn - 1) / g.bn;
     const int num_m = (g.M + g.bm - 1) / g.bm;
     dim3 grid(num_m * num_n, g.S);
-    if (g.bm == 128 && g.bn == 128)
+    if (g.bm == 32 && g.bn == 128)
+        hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
+                           out, split_stride, ldo, amax);
+    else if (g.bm == 64 && g.bn == 128)
+        hipLaunchKernelGGL((k_gemm_dma<64, 128, 64, 4, 1, 2>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
+                           out, split_stride, ldo, amax);
+    else if (g.bm == 128 && g.bn == 128)
         hipLaunchKernelGGL((k_gemm_dma<128, 128, 64, 4, 2, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
                            out, split_stride, ldo, amax);
     else if (g.bm == 256 && g.bn == 128)
