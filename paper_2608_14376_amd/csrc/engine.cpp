@@ -69,15 +69,14 @@ struct Plan {
 int mt_for(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 
 // Kernel, tile and split-K factor from the projection shape and M only.
-//  * M <= 8 (or K % 64 != 0 and M <= 64): the skinny kernel (weights
-//    streamed to registers); aim for about 2048 wavefronts (8 per CU) so
-//    enough weight bytes are in flight, each split keeping at least 256 K
-//    elements.
-//  * 8 < M <= 64, K % 64 == 0: the pipelined kernel with a 32- or 64-row
-//    tile and 128 columns, split-K to about 256 workgroups (each split at
-//    least 512 K elements).  The skinny kernel's register loads read 16 rows
-//    x 64 bytes per instruction, which caps its weight stream; at these M it
-//    also repeats each weight tile's loads per 16-row tile.
+//  * M <= 64, K % 64 == 0: the pipelined kernel with a 32- or 64-row tile
+//    and 128 columns, split-K to about 256 workgroups (each split at least
+//    512 K elements).  Against the skinny kernel it streams weights in
+//    whole lines and needs a third to a quarter of the split-K partials that
+//    the next kernel folds.
+//  * M <= 64, K % 64 != 0: the skinny kernel (weights streamed to
+//    registers); aim for about 2048 wavefronts (8 per CU) so enough weight
+//    bytes are in flight, each split keeping at least 256 K elements.
 //  * M > 64, K % 64 == 0: the pipelined kernel (one workgroup per CU) with
 //    M tile 128 (M <= 128) or 256 and N tile 128; 256 x 256 tiles (eight
 //    wavefronts) once those tiles alone fill the GPU (large prefill) and for
@@ -104,7 +103,7 @@ Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_
         p.S = 1;
         return p;
     }
-    if (M > 8 && M <= 64 && bm_override <= 0 && K % 64 == 0) {
+    if (M <= 64 && bm_override <= 0 && K % 64 == 0) {
         p.bm = M <= 32 ? 32 : 64;
         p.bn = 128;
         const int tiles = (N + 127) / 128;
