@@ -225,18 +225,23 @@ def bench_prefill(cfg, W, lens, args):
     return out
 
 
-def bench_scheduler(cfg, W, n_req=64, B=32, in_len=512, out_len=64):
+def bench_scheduler(cfg, W, n_req=64, B=32, in_len=512, out_len=64, batch_tokens=None):
     """The host scheduler end to end on a synthetic in=512/out=64 workload:
-    every request prefilled alone (Algorithms 1 and 2), decoded at the
-    fixed B with request-bound sampling (temperature 0.6, own seeds)."""
+    Algorithms 1 and 2 around the fixed-B decode with request-bound sampling
+    (temperature 0.6, own seeds).  batch_tokens None: every request
+    prefilled alone with the default prefill plan; else a batch-invariant
+    prefill engine, 0 = one prompt per prefill iteration, > 0 = batched
+    prefill of up to that many prompt tokens per iteration."""
     import torch
 
     from paper_2608_14376_amd import corun
     from paper_2608_14376_amd import workload as wl
     cap = (in_len + out_len + 15) // 16 * 16
     K, V = wl.make_kv_contiguous(cfg, B, cap, seed=5000, device="cuda")
-    eng = corun.Engine(cfg, W, B, K, V, opt=corun.options(max_prefill_len=in_len))
-    s = corun.Scheduler(eng, max_num_reqs=B)
+    bi = batch_tokens is not None
+    pf = max(in_len, batch_tokens or 0, 4096)         # the same prefill workspace in every mode
+    eng = corun.Engine(cfg, W, B, K, V, opt=corun.options(max_prefill_len=pf, bi_prefill=bi))
+    s = corun.Scheduler(eng, max_num_reqs=B, prefill_batch_tokens=batch_tokens or 0)
     for i in range(2):                                   # warm-up: graph capture, first prefill
         s.add_request(-1 - i, wl.make_prompt(cfg["vocab"], in_len, seed=9000 + i), 2, 1, 0.6)
     s.run_until_idle()
@@ -249,10 +254,15 @@ def bench_scheduler(cfg, W, n_req=64, B=32, in_len=512, out_len=64):
     s.close()
     eng.close()
     del K, V
-    out = dict(requests=n_req, B=B, input_len=in_len, output_len=out_len, seconds=round(dt, 3),
-               output_tok_s=round(n_req * out_len / dt, 1), prefills=events.count(1), decode_steps=events.count(2))
-    log(f"[bench] scheduler in={in_len}/out={out_len} x{n_req} at B={B}: {dt:.2f} s, "
-        f"{out['output_tok_s']:.0f} output tok/s ({out['prefills']} prefills, {out['decode_steps']} decode steps)")
+    mode = ("isolated prefill" if not bi else
+            "batch-invariant prefill, " + ("one prompt per iteration" if not batch_tokens else
+                                           f"batched up to {batch_tokens} tokens"))
+    out = dict(mode=mode, requests=n_req, B=B, input_len=in_len, output_len=out_len, seconds=round(dt, 3),
+               output_tok_s=round(n_req * out_len / dt, 1), prefill_iterations=events.count(1),
+               decode_steps=events.count(2))
+    log(f"[bench] scheduler in={in_len}/out={out_len} x{n_req} at B={B}, {mode}: {dt:.2f} s, "
+        f"{out['output_tok_s']:.0f} output tok/s ({out['prefill_iterations']} prefill iterations, "
+        f"{out['decode_steps']} decode steps)")
     return out
 
 
@@ -566,6 +576,8 @@ def main():
         extra["prefill_8b"] = bench_prefill(cfg, W, [512, 2048, 8192, 32768], args)
         torch.cuda.empty_cache()
         extra["scheduler_8b"] = bench_scheduler(cfg, W)
+        extra["scheduler_8b_bi_prefill"] = bench_scheduler(cfg, W, batch_tokens=0)
+        extra["scheduler_8b_batched_prefill"] = bench_scheduler(cfg, W, batch_tokens=4096)
         del W
         torch.cuda.empty_cache()
         # 32B-shaped dense decode at long context on the paged cache

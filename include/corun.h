@@ -123,10 +123,16 @@ typedef struct {
                                   M tile (tuning aid; changes the plan) */
     int32_t batch_invariant;   /* 1 = batch-invariant kernels, the baseline CoRun is measured against (Sec. III,
                                   "Batch-Dependent GPU Reductions", Fig. 3b, and Definition 1): every projection, in
-                                  decode and prefill, uses one kernel and tile whatever B or the prompt length
-                                  (128 x 128, no split-K), and decode attention runs with split-KV off (one
-                                  split covers the whole cache), so a row's results depend on neither its
-                                  position nor B.  Requires attn_chunk, split_k_override and gemm_bm = 0. */
+                                  decode and prefill, runs without split-K on one kernel whatever B or the prompt
+                                  length (each output element one MFMA chain over K in order; the tile, which
+                                  changes no element's arithmetic, still follows M), and decode attention runs
+                                  with split-KV off (one split covers the whole cache), so a row's results depend
+                                  on neither its position nor B.  Requires attn_chunk, split_k_override and
+                                  gemm_bm = 0. */
+    int32_t bi_prefill;        /* 1 = batch-invariant prefill only (Sec. VIII, "Batch-Invariant Kernels for
+                                  Prefill": the hybrid of batch-invariant prefill and position-invariant
+                                  fixed-shape decode): every prefill uses the plan of batch_invariant, and
+                                  corun_prefill_batch is enabled; decode keeps its fixed-B plan. */
 } corun_options;
 
 /* Create an engine for one fixed padded batch size B_fixed (Sec. IV,
@@ -204,6 +210,28 @@ corun_status corun_prefill(corun_engine *e, const int32_t *prompt, int32_t promp
 corun_status corun_prefill_chunk(corun_engine *e, const int32_t *tokens, int32_t n, int32_t start, int32_t slot,
                                  int32_t *token_out, float *last_logits);
 
+/* Most prompts one corun_prefill_batch call takes. */
+#define CORUN_MAX_PREFILL_BATCH 64
+
+/* Batched prefill of several whole prompts in one pass (Sec. VIII,
+ * "Batch-Invariant Kernels for Prefill"): the prompts' tokens run as one
+ * batch of rows through batch-invariant kernels -- one projection tile and
+ * no split-K for any number of rows, row-wise norms, per-prompt causal
+ * attention with each prompt's own plan -- so every prompt's k, v and
+ * last-position logits are bit-identical to its own corun_prefill on the
+ * same engine, whatever the other prompts are.  Requires an engine created
+ * with bi_prefill or batch_invariant (else CORUN_E_STATE).
+ *  tokens      host int32 [sum of lens]: the prompts back to back
+ *  lens        host int32 [n], each >= 1; their sum at most max_prefill_len
+ *  slots       host int32 [n]: distinct cache slots
+ *  n           1 .. CORUN_MAX_PREFILL_BATCH
+ *  tokens_out  host int32 [n] out: each prompt's greedy first token
+ *  last_logits device fp32 [n, vocab] out, or NULL
+ * Errors: CORUN_E_CAPACITY (sum of lens beyond the workspace, a prompt
+ * beyond its slot's cache), CORUN_E_INVAL (bad sizes, slots, tokens). */
+corun_status corun_prefill_batch(corun_engine *e, const int32_t *tokens, const int32_t *lens, const int32_t *slots,
+                                 int32_t n, int32_t *tokens_out, float *last_logits);
+
 /* The engine's fixed batch size, model configuration and KV description
  * (copies; the k/v/page-table pointers are the caller's borrowed ones).
  * Any out pointer may be NULL. */
@@ -259,6 +287,12 @@ typedef struct {
     int32_t n_slots, max_seq_len, page_size, num_pages, max_pages_per_seq;
     int32_t prefill_chunk;      /* > 0: prefill prompts in chunks of this many tokens (the last one shorter),
                                    one isolated iteration each (corun_prefill_chunk); 0 = whole prompts */
+    int32_t prefill_batch_tokens; /* > 0: batched prefill (Sec. VIII, batch-invariant prefill): a prefill
+                                   iteration takes the request Algorithm 1 selects and the waiting requests
+                                   behind it, in order, while each passes admission and the prompts total at
+                                   most this many tokens, through one corun_prefill_batch (the engine needs
+                                   bi_prefill; keep this within its max_prefill_len).  Excludes
+                                   prefill_chunk.  0 = one prompt per prefill iteration. */
 } corun_sched_cfg;
 
 corun_status corun_sched_create(corun_engine *e, const corun_sched_cfg *cfg, corun_sched **out);

@@ -19,7 +19,7 @@ OK, E_INVAL, E_SHAPE, E_CAPACITY, E_HIP, E_STATE = 0, -1, -2, -3, -4, -5
 KV_CONTIGUOUS, KV_PAGED = 0, 1
 
 EXPORTS = ("corun_engine_create", "corun_engine_destroy", "corun_decode_step", "corun_decode_run",
-           "corun_prefill", "corun_prefill_chunk", "corun_check_config", "corun_check_batch", "corun_describe_plan",
+           "corun_prefill", "corun_prefill_chunk", "corun_prefill_batch", "corun_check_config", "corun_check_batch", "corun_describe_plan",
            "corun_last_error", "corun_time_kernel", "corun_sample", "corun_engine_info",
            "corun_sched_create", "corun_sched_destroy", "corun_sched_add_request", "corun_sched_step",
            "corun_sched_output", "corun_sched_state", "corun_sched_last_error")
@@ -55,7 +55,7 @@ class KV(C.Structure):
 class Options(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "attn_chunk", "max_prefill_len", "no_graph", "poison_workspace", "split_k_override", "gemm_bm",
-        "batch_invariant")]
+        "batch_invariant", "bi_prefill")]
 
 
 class CorunError(RuntimeError):
@@ -87,6 +87,9 @@ def load():
     L.corun_decode_run.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
     L.corun_prefill.restype = st
     L.corun_prefill.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p]
+    L.corun_prefill_batch.restype = st
+    L.corun_prefill_batch.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p,
+                                      C.c_void_p]
     L.corun_prefill_chunk.restype = st
     L.corun_prefill_chunk.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
                                       C.c_void_p]
@@ -159,9 +162,9 @@ def kv_struct(layout: int, n_slots: int, k, v, keep, max_seq_len=0, page_size=0,
 
 
 def options(attn_chunk=0, max_prefill_len=0, no_graph=False, poison_workspace=False, split_k_override=0,
-            gemm_bm=0, batch_invariant=False):
+            gemm_bm=0, batch_invariant=False, bi_prefill=False):
     return Options(attn_chunk, max_prefill_len, int(no_graph), int(poison_workspace), split_k_override, gemm_bm,
-                   int(batch_invariant))
+                   int(batch_invariant), int(bi_prefill))
 
 
 def _np(a, dt):
@@ -200,7 +203,7 @@ def describe_plan(cfg: dict, kv: KV, B: int, opt: Options | None = None) -> dict
 class SchedCfg(C.Structure):
     _fields_ = [("max_num_reqs", C.c_int32), ("n_slots", C.c_int32), ("max_seq_len", C.c_int32),
                 ("page_size", C.c_int32), ("num_pages", C.c_int32), ("max_pages_per_seq", C.c_int32),
-                ("prefill_chunk", C.c_int32)]
+                ("prefill_chunk", C.c_int32), ("prefill_batch_tokens", C.c_int32)]
 
 
 class Scheduler:
@@ -211,10 +214,11 @@ class Scheduler:
     IDLE, PREFILL, DECODE = 0, 1, 2
 
     def __init__(self, engine=None, max_num_reqs=0, n_slots=0, max_seq_len=0, page_size=0, num_pages=0,
-                 max_pages_per_seq=0, prefill_chunk=0):
+                 max_pages_per_seq=0, prefill_chunk=0, prefill_batch_tokens=0):
         self._L = load()
         self.engine = engine
-        cfg = SchedCfg(max_num_reqs, n_slots, max_seq_len, page_size, num_pages, max_pages_per_seq, prefill_chunk)
+        cfg = SchedCfg(max_num_reqs, n_slots, max_seq_len, page_size, num_pages, max_pages_per_seq, prefill_chunk,
+                       prefill_batch_tokens)
         h = C.c_void_p()
         st = self._L.corun_sched_create(engine._h if engine is not None else None, C.byref(cfg), C.byref(h))
         if st != 0:
@@ -377,6 +381,20 @@ class Engine:
         _check(self._L.corun_prefill(self._h, p.ctypes.data, p.size, slot, tok.ctypes.data,
                                      None if last_logits is None else last_logits.data_ptr()))
         return int(tok[0])
+
+    def prefill_batch(self, prompts, slots, last_logits=None) -> np.ndarray:
+        """Several whole prompts in one batch-invariant pass (engine created
+        with bi_prefill or batch_invariant); returns their first tokens.
+        last_logits: a device fp32 tensor [len(prompts), vocab], or None."""
+        ps = [_np(p, np.int32) for p in prompts]
+        toks = np.ascontiguousarray(np.concatenate(ps), np.int32)
+        lens = np.array([p.size for p in ps], np.int32)
+        sl = _np(slots, np.int32)
+        out = np.empty(len(ps), np.int32)
+        _check(self._L.corun_prefill_batch(self._h, toks.ctypes.data, lens.ctypes.data, sl.ctypes.data, len(ps),
+                                           out.ctypes.data,
+                                           None if last_logits is None else last_logits.data_ptr()))
+        return out
 
     def prefill_chunk(self, tokens, start: int, slot: int, last_logits=None, want_token=True):
         """Positions start .. start+len(tokens)-1 of a prompt whose earlier

@@ -85,10 +85,11 @@ int mt_for(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 //    at least 512 K elements.
 //  * otherwise (or bm_override > 0): the LDS-tiled kernel with a 128-row
 //    tile (or bm_override), split-K to about two workgroups per CU.
-// Batch-invariant mode (bi) ignores M: the pipelined kernel's 128 x 128 tile
-// (the LDS-tiled kernel's 128-row tile when K % 64 != 0) and no split-K, so
-// every output element is one MFMA chain over K in the same order whatever
-// the batch size.
+// Batch-invariant mode (bi): no split-K and, when K % 64 == 0, the
+// pipelined kernel for every M (else the LDS-tiled kernel's 128-row tile),
+// so every output element is one chain of v_mfma_f32_32x32x16_bf16 over K in
+// order whatever the batch size.  The tile still follows M (occupancy): an
+// element's arithmetic does not depend on the tile it sits in.
 Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_override, bool bi = false)
 {
     Proj p;
@@ -97,8 +98,9 @@ Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_
     if (N <= 0 || K <= 0 || M <= 0) return p;   // no such projection
     int S, align;
     if (bi) {
+        if (K % 64 == 0) return choose_proj(N, K, M, 0, 1, 0, false);
         p.bm = 128;
-        p.bn = K % 64 == 0 ? 128 : 0;
+        p.bn = 0;
         p.Kc = (K + 63) / 64 * 64;
         p.S = 1;
         return p;
@@ -115,9 +117,18 @@ Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_
         p.bn = 128;
         const long long t256 = (long long)((M + 255) / 256) * ((N + 255) / 256);
         if ((M > 256 && t256 >= 256) || (M > 128 && M <= 256 && N >= 16384)) p.bn = 256;
-        const long long tiles = (long long)((M + p.bm - 1) / p.bm) * ((N + p.bn - 1) / p.bn);
+        long long tiles = (long long)((M + p.bm - 1) / p.bm) * ((N + p.bn - 1) / p.bn);
         S = tiles >= 256 ? 1 : (int)(256 / tiles);
         S = std::min(S, std::max(1, K / 512));
+        if (max_split > 0 && S > max_split && p.bm == 256 && tiles * max_split < 256) {
+            // the workspace leaves too little room for split-K: fill the GPU
+            // with 128 x 128 tiles instead
+            p.bm = 128;
+            p.bn = 128;
+            tiles = (long long)((M + 127) / 128) * ((N + 127) / 128);
+            S = tiles >= 256 ? 1 : (int)(256 / tiles);
+            S = std::min(S, std::max(1, K / 512));
+        }
         align = 64;
     } else if (M <= 64 && bm_override <= 0) {
         const int col_waves = (N + 63) / 64;
@@ -244,6 +255,7 @@ struct corun_engine {
     float *pf_x = nullptr, *pf_part = nullptr, *pf_logits = nullptr;
     uint16_t *pf_h = nullptr, *pf_q = nullptr, *pf_o = nullptr, *pf_a = nullptr, *pf_hlast = nullptr;
     int32_t *pf_pos = nullptr, *pf_tok = nullptr, *pf_next = nullptr;
+    int32_t *pf_rowpos = nullptr, *pf_rowslot = nullptr, *pf_seq = nullptr;   // batched prefill
     ArgBest *pf_amax = nullptr;
     size_t pf_part_elems = 0;
 };
@@ -325,6 +337,7 @@ static corun_status check_options(const corun_options &o)
     if (!(o.gemm_bm == 0 || o.gemm_bm == 64 || o.gemm_bm == 128 || o.gemm_bm == 256))
         return fail(CORUN_E_INVAL, "gemm_bm must be 0, 64, 128 or 256");
     if (o.batch_invariant != 0 && o.batch_invariant != 1) return fail(CORUN_E_INVAL, "batch_invariant must be 0 or 1");
+    if (o.bi_prefill != 0 && o.bi_prefill != 1) return fail(CORUN_E_INVAL, "bi_prefill must be 0 or 1");
     if (o.batch_invariant && (o.attn_chunk || o.split_k_override || o.gemm_bm))
         return fail(CORUN_E_INVAL, "batch_invariant fixes the plan: attn_chunk, split_k_override and gemm_bm must be 0");
     return CORUN_OK;
@@ -606,7 +619,9 @@ static corun_status alloc_prefill(corun_engine *e)
     Carver cv;
     cv.take(&e->pf_x, (size_t)L * H);
     cv.take(&e->pf_part, e->pf_part_elems);
-    cv.take(&e->pf_logits, (size_t)c.vocab);
+    const bool bi_pf = e->opt.batch_invariant || e->opt.bi_prefill;
+    const int lrows = bi_pf ? CORUN_MAX_PREFILL_BATCH : 1;   // last positions a prefill call reports
+    cv.take(&e->pf_logits, (size_t)lrows * c.vocab);
     cv.take(&e->pf_h, (size_t)Lp64 * H);
     cv.take(&e->pf_q, (size_t)L * nq * d);
     cv.take(&e->pf_o, (size_t)Lp64 * nq * d);
@@ -624,8 +639,11 @@ static corun_status alloc_prefill(corun_engine *e)
     }
     cv.take(&e->pf_pos, (size_t)std::max(L, kv_capacity(&e->kv)));   // positions of any chunk
     cv.take(&e->pf_tok, (size_t)L);
-    cv.take(&e->pf_amax, (size_t)gemm_col_blocks(c.vocab));
-    size_t total = cv.take(&e->pf_next, 16);
+    cv.take(&e->pf_amax, (size_t)lrows * gemm_col_blocks(c.vocab));
+    cv.take(&e->pf_rowpos, bi_pf ? (size_t)L : 1);
+    cv.take(&e->pf_rowslot, bi_pf ? (size_t)L : 1);
+    cv.take(&e->pf_seq, (size_t)4 * CORUN_MAX_PREFILL_BATCH);
+    size_t total = cv.take(&e->pf_next, CORUN_MAX_PREFILL_BATCH);
     e->pws_bytes = total;
     HIP_TRY(hipMalloc(&e->pws, total));
     HIP_TRY(hipMemsetAsync(e->pws, 0, total, e->st));
@@ -638,6 +656,7 @@ static corun_status alloc_prefill(corun_engine *e)
         rebase(e->pf_moe_act, e->pws);
     }
     rebase(e->pf_pos, e->pws); rebase(e->pf_tok, e->pws); rebase(e->pf_amax, e->pws); rebase(e->pf_next, e->pws);
+    rebase(e->pf_rowpos, e->pws); rebase(e->pf_rowslot, e->pws); rebase(e->pf_seq, e->pws);
     HIP_TRY(launch_iota(e->pf_pos, std::max(L, kv_capacity(&e->kv)), e->st));
     return CORUN_OK;
 }
@@ -904,7 +923,7 @@ extern "C" corun_status corun_prefill_chunk(corun_engine *e, const int32_t *toke
     hipStream_t st = e->st;
     const int Lp = n;     // rows of every projection: the chunk's tokens
     const int cap_rows = std::max(1, e->pf_max / Lp);
-    const bool bi = e->opt.batch_invariant != 0;
+    const bool bi = e->opt.batch_invariant != 0 || e->opt.bi_prefill != 0;
     const Proj pq = choose_proj(nqkv, H, Lp, 0, cap_rows, 0, bi);
     const Proj po = choose_proj(H, nq * d, Lp, 0, cap_rows, 0, bi);
     const Proj pg = e->moe ? Proj{} : choose_proj(2 * F, H, Lp, 0, cap_rows, 0, bi);
@@ -971,6 +990,118 @@ extern "C" corun_status corun_prefill(corun_engine *e, const int32_t *prompt, in
         return fail(CORUN_E_CAPACITY, "prompt_len %d exceeds the prefill workspace %d", Lp, e->pf_max);
     if (e && Lp > kv_capacity(&e->kv)) return fail(CORUN_E_CAPACITY, "prompt_len %d exceeds the cache capacity", Lp);
     return corun_prefill_chunk(e, prompt, Lp, 0, slot, token_out, last_logits);
+}
+
+extern "C" corun_status corun_prefill_batch(corun_engine *e, const int32_t *tokens, const int32_t *lens,
+                                            const int32_t *slots, int32_t n, int32_t *tokens_out, float *last_logits)
+{
+    if (!e || !tokens || !lens || !slots || !tokens_out) return fail(CORUN_E_INVAL, "null argument");
+    if (!(e->opt.batch_invariant || e->opt.bi_prefill))
+        return fail(CORUN_E_STATE, "batched prefill needs an engine created with bi_prefill or batch_invariant");
+    if (e->pf_max <= 0) return fail(CORUN_E_STATE, "engine was created without a prefill workspace");
+    if (n < 1 || n > CORUN_MAX_PREFILL_BATCH)
+        return fail(CORUN_E_INVAL, "n = %d outside [1, %d]", n, CORUN_MAX_PREFILL_BATCH);
+    const int cap = kv_capacity(&e->kv);
+    long long M = 0;
+    for (int i = 0; i < n; ++i) {
+        if (lens[i] < 1) return fail(CORUN_E_INVAL, "lens[%d] = %d", i, lens[i]);
+        if (lens[i] > cap) return fail(CORUN_E_CAPACITY, "prompt %d (%d tokens) exceeds the cache capacity", i, lens[i]);
+        if (slots[i] < 0 || slots[i] >= e->kv.n_slots)
+            return fail(CORUN_E_INVAL, "slots[%d] = %d outside [0, %d)", i, slots[i], e->kv.n_slots);
+        for (int j = 0; j < i; ++j)
+            if (slots[j] == slots[i]) return fail(CORUN_E_INVAL, "slot %d given twice", slots[i]);
+        M += lens[i];
+    }
+    if (M > e->pf_max) return fail(CORUN_E_CAPACITY, "%lld prompt tokens exceed the prefill workspace %d", M, e->pf_max);
+    for (long long t = 0; t < M; ++t)
+        if (tokens[t] < 0 || tokens[t] >= e->c.vocab)
+            return fail(CORUN_E_INVAL, "tokens[%lld] = %d outside [0, %d)", t, tokens[t], e->c.vocab);
+    if (e->kv.layout == CORUN_KV_PAGED) {
+        std::vector<int32_t> pt(e->kv.max_pages_per_seq);
+        for (int i = 0; i < n; ++i) {
+            HIP_TRY(hipMemcpy(pt.data(), e->kv.page_table + (size_t)slots[i] * e->kv.max_pages_per_seq,
+                              pt.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+            for (int j = 0; j <= (lens[i] - 1) / e->kv.page_size; ++j)
+                if (pt[j] < 0 || pt[j] >= e->kv.num_pages)
+                    return fail(CORUN_E_CAPACITY, "slot %d: page %d maps to %d outside [0, %d)", slots[i], j, pt[j],
+                                e->kv.num_pages);
+        }
+    }
+    ST_TRY(enter(e));
+    const corun_model_cfg &c = e->c;
+    const int H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn;
+    const int nqkv = (nq + 2 * nkv) * d;
+    const int G = nq / nkv;
+    const int Lp = (int)M;   // rows of every projection: all prompts' tokens
+    hipStream_t st = e->st;
+    // every row's position within its prompt and its cache slot; per prompt
+    // (first row, length, slot, first attention unit group)
+    std::vector<int32_t> rowpos(Lp), rowslot(Lp), seq(4 * n);
+    int groups = 0;
+    for (int i = 0, r0 = 0; i < n; r0 += lens[i], ++i) {
+        for (int t = 0; t < lens[i]; ++t) {
+            rowpos[r0 + t] = t;
+            rowslot[r0 + t] = slots[i];
+        }
+        seq[4 * i] = r0;
+        seq[4 * i + 1] = lens[i];
+        seq[4 * i + 2] = slots[i];
+        seq[4 * i + 3] = groups;
+        groups += (((lens[i] + 31) / 32) * G + 7) / 8;
+    }
+    const int cap_rows = std::max(1, e->pf_max / Lp);
+    const Proj pq = choose_proj(nqkv, H, Lp, 0, cap_rows, 0, true);
+    const Proj po = choose_proj(H, nq * d, Lp, 0, cap_rows, 0, true);
+    const Proj pg = e->moe ? Proj{} : choose_proj(2 * F, H, Lp, 0, cap_rows, 0, true);
+    const Proj pd = e->moe ? Proj{} : choose_proj(H, F, Lp, 0, cap_rows, 0, true);
+    const Proj pl = choose_proj(c.vocab, H, n, 1, 0, 0, true);
+    const Proj pr = e->moe ? choose_proj(c.n_experts, H, Lp, 0, cap_rows, 0, true) : Proj{};
+    const int dense_S = e->moe ? 0 : pd.S;
+    const MoeBufs pmb{nullptr, e->pf_part, e->pf_moe_w, e->pf_moe_gu, e->pf_moe_y, e->pf_moe_sel, e->pf_moe_list,
+                      e->pf_moe_tiles, e->pf_moe_act, e->moe ? c.n_experts + (Lp * c.top_k + 15) / 16 : 0};
+
+    HIP_TRY(hipMemcpyAsync(e->pf_tok, tokens, sizeof(int32_t) * Lp, hipMemcpyHostToDevice, st));
+    HIP_TRY(hipMemcpyAsync(e->pf_rowpos, rowpos.data(), sizeof(int32_t) * Lp, hipMemcpyHostToDevice, st));
+    HIP_TRY(hipMemcpyAsync(e->pf_rowslot, rowslot.data(), sizeof(int32_t) * Lp, hipMemcpyHostToDevice, st));
+    HIP_TRY(hipMemcpyAsync(e->pf_seq, seq.data(), sizeof(int32_t) * 4 * n, hipMemcpyHostToDevice, st));
+    HIP_TRY(launch_embed(e->embed, e->pf_tok, nullptr, Lp, H, e->pf_x, st));
+    for (int l = 0; l < c.n_layers; ++l) {
+        HIP_TRY(launch_rmsnorm(e->pf_x, l ? e->pf_part : nullptr, l ? dense_S : 0, (long long)Lp * H, Lp, H,
+                               e->attn_norm[l], c.rms_eps, e->pf_h, st, fold_of(e, pmb, l)));
+        HIP_TRY(launch_proj(e->pf_h, H, e->w_qkv[l], shape_of(pq, Lp), e->pf_part, (long long)Lp * nqkv, nqkv, st));
+        HIP_TRY(launch_qkv_post(e->pf_part, pq.S, (long long)Lp * nqkv, Lp, nullptr, e->pf_rowpos, e->pf_rowslot, -1,
+                                nq, nkv, d, e->rope, e->pf_q, e->kc[l], e->vc[l], e->view, st));
+        HIP_TRY(launch_prefill_attn_multi(e->pf_q, e->pf_seq, n, groups, nq, nkv, d, e->kc[l], e->vc[l], e->view,
+                                          e->pf_o, st));
+        HIP_TRY(launch_proj(e->pf_o, nq * d, e->w_o[l], shape_of(po, Lp), e->pf_part, (long long)Lp * H, H, st));
+        HIP_TRY(launch_rmsnorm(e->pf_x, e->pf_part, po.S, (long long)Lp * H, Lp, H, e->mlp_norm[l], c.rms_eps,
+                               e->pf_h, st));
+        if (e->moe) {
+            const int Fe = c.expert_ffn;
+            ST_TRY(moe_router(e, pmb, e->pf_h, Lp, pr, l));
+            ST_TRY(moe_expert_gate_up(e, pmb, e->pf_h, l));
+            HIP_TRY(launch_swiglu(e->pf_moe_gu, 1, 0, Lp * c.top_k, Fe, e->pf_moe_act, Fe, st));
+            ST_TRY(moe_expert_down(e, pmb, l));
+        } else {
+            HIP_TRY(launch_proj(e->pf_h, H, e->w_gu[l], shape_of(pg, Lp), e->pf_part, (long long)Lp * 2 * F, 2 * F,
+                                st));
+            HIP_TRY(launch_swiglu(e->pf_part, pg.S, (long long)Lp * 2 * F, Lp, F, e->pf_a, F, st));
+            HIP_TRY(launch_proj(e->pf_a, F, e->w_down[l], shape_of(pd, Lp), e->pf_part, (long long)Lp * H, H, st));
+        }
+    }
+    // final norm of every row (the same row-wise arithmetic as one prompt's
+    // last row), then the prompts' last rows through lm_head and argmax
+    HIP_TRY(launch_rmsnorm(e->pf_x, e->pf_part, dense_S, (long long)Lp * H, Lp, H, e->final_norm, c.rms_eps, e->pf_h,
+                           st, fold_of(e, pmb, c.n_layers)));
+    HIP_TRY(launch_gather_last_rows(e->pf_h, e->pf_seq, n, H, e->pf_hlast, st));
+    HIP_TRY(launch_proj(e->pf_hlast, H, e->lm_head, shape_of(pl, n), e->pf_logits, 0, c.vocab, st, e->pf_amax));
+    HIP_TRY(launch_argmax_partials(e->pf_amax, n, gemm_col_blocks(c.vocab), nullptr, e->pf_next, st));
+    HIP_TRY(hipMemcpyAsync(tokens_out, e->pf_next, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
+    if (last_logits)
+        HIP_TRY(hipMemcpyAsync(last_logits, e->pf_logits, sizeof(float) * (size_t)n * c.vocab,
+                               hipMemcpyDeviceToDevice, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    return CORUN_OK;
 }
 
 extern "C" corun_status corun_engine_info(const corun_engine *e, int32_t *B_fixed, corun_model_cfg *cfg, corun_kv *kv)

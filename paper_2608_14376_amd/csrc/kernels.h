@@ -119,6 +119,17 @@ hipError_t launch_sample(const float *logits, long long ld, int rows, int V, con
 hipError_t launch_prefill_attn(const uint16_t *q, int n, int p0, int nq, int nkv, int d, int slot, const uint16_t *kc,
                                const uint16_t *vc, KvView kv, uint16_t *o, hipStream_t st);
 
+// The same attention for several prompts in one launch: seq (device int32
+// [nseq][4]) = (first row in q/o, length, cache slot, first unit group),
+// total_groups = the sum over prompts of ceil(ceil(len / 32) G / 8).  Each
+// prompt's results are bit-identical to its own launch with p0 = 0.
+// dst row i (bf16 [n][H]) = src row seq[i][0] + seq[i][1] - 1.
+hipError_t launch_gather_last_rows(const uint16_t *src, const int32_t *seq, int n, int H, uint16_t *dst, hipStream_t st);
+
+hipError_t launch_prefill_attn_multi(const uint16_t *q, const int32_t *seq, int nseq, int total_groups, int nq,
+                                     int nkv, int d, const uint16_t *kc, const uint16_t *vc, KvView kv, uint16_t *o,
+                                     hipStream_t st);
+
 // a[m][j] = bf16(silu(bf16(sum_s gate)) * bf16(sum_s up)) over the partials
 // of the [2F] gate/up projection (gate columns first).
 hipError_t launch_swiglu(const float *part, int S, long long part_stride, int rows, int F,

@@ -1843,11 +1843,12 @@ __device__ __forceinline__ int pf_swz(int r, int c)
     else return r * 8 + (c ^ ((r >> 1) & 7));
 }
 
+// One workgroup of the kernel: kv head kvh, unit group grp of one prompt.
 template <int D>
-__global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict__ q, int n, int p0, int nq, int nkv,
-                                                      int slot, const uint16_t *__restrict__ kc,
-                                                      const uint16_t *__restrict__ vc, KvView kv,
-                                                      uint16_t *__restrict__ o)
+__device__ __forceinline__ void prefill_attn_block(const uint16_t *__restrict__ q, int n, int p0, int nq, int nkv,
+                                                   int slot, const uint16_t *__restrict__ kc,
+                                                   const uint16_t *__restrict__ vc, const KvView &kv,
+                                                   uint16_t *__restrict__ o, int kvh, int grp)
 {
     constexpr int NW = 8, NT = 64 * NW;              // wavefronts, threads
     constexpr int QB = 32, BKT = 64;                  // queries per wavefront, keys per tile
@@ -1869,7 +1870,6 @@ __global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict
     const int Lk = p0 + n;
     // grid (kv head, unit group): workgroups are dispatched x fastest, so the
     // groups with the latest (longest) query blocks of every kv head go first
-    const int kvh = blockIdx.x, grp = blockIdx.y;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int r32 = lane & 31, h = lane >> 5;
     const int nqb = (n + QB - 1) / QB;
@@ -2044,6 +2044,68 @@ __global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict
         if (qo < n)
             *(uint4 *)(o + (size_t)qo * nq * D + (size_t)hq * D + 8 * c8) = *(const uint4 *)(ost + qr * OPITCH + 8 * c8);
     }
+}
+
+template <int D>
+__global__ __launch_bounds__(512) void k_prefill_attn(const uint16_t *__restrict__ q, int n, int p0, int nq, int nkv,
+                                                      int slot, const uint16_t *__restrict__ kc,
+                                                      const uint16_t *__restrict__ vc, KvView kv,
+                                                      uint16_t *__restrict__ o)
+{
+    prefill_attn_block<D>(q, n, p0, nq, nkv, slot, kc, vc, kv, o, blockIdx.x, blockIdx.y);
+}
+
+// Several prompts in one launch (batched prefill): prompt i owns rows
+// seq[i].row0 .. + len of q and o and the cache of seq[i].slot; the unit
+// groups of all prompts follow one another along the grid's y, prompt i's
+// starting at seq[i].grp0.  Each workgroup runs exactly the arithmetic of the
+// same unit in the prompt's own launch.
+template <int D>
+__global__ __launch_bounds__(512) void k_prefill_attn_multi(const uint16_t *__restrict__ q,
+                                                            const int32_t *__restrict__ seq, int nseq, int nq,
+                                                            int nkv, const uint16_t *__restrict__ kc,
+                                                            const uint16_t *__restrict__ vc, KvView kv,
+                                                            uint16_t *__restrict__ o)
+{
+    const int g = blockIdx.y;
+    int i = 0;
+    while (i + 1 < nseq && seq[4 * (i + 1) + 3] <= g) ++i;
+    const int row0 = seq[4 * i], len = seq[4 * i + 1], slot = seq[4 * i + 2], grp = g - seq[4 * i + 3];
+    const size_t ofs = (size_t)row0 * nq * D;
+    prefill_attn_block<D>(q + ofs, len, 0, nq, nkv, slot, kc, vc, kv, o + ofs, blockIdx.x, grp);
+}
+
+hipError_t launch_prefill_attn_multi(const uint16_t *q, const int32_t *seq, int nseq, int total_groups, int nq,
+                                     int nkv, int d, const uint16_t *kc, const uint16_t *vc, KvView kv, uint16_t *o,
+                                     hipStream_t st)
+{
+    if (nseq <= 0 || total_groups <= 0) return hipErrorInvalidValue;
+    dim3 grid(nkv, total_groups);
+    if (d == 128)
+        hipLaunchKernelGGL((k_prefill_attn_multi<128>), grid, dim3(512), 0, st, q, seq, nseq, nq, nkv, kc, vc, kv, o);
+    else if (d == 64)
+        hipLaunchKernelGGL((k_prefill_attn_multi<64>), grid, dim3(512), 0, st, q, seq, nseq, nq, nkv, kc, vc, kv, o);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
+// Row seq[i].row0 + seq[i].len - 1 of src (bf16 [.][H]) to row i of dst: the
+// last position of every prompt of a batched prefill.
+__global__ __launch_bounds__(256) void k_gather_last_rows(const uint16_t *__restrict__ src, const int32_t *__restrict__ seq,
+                                                          int H, uint16_t *__restrict__ dst)
+{
+    const int i = blockIdx.x;
+    const size_t row = (size_t)seq[4 * i] + seq[4 * i + 1] - 1;
+    for (int c = threadIdx.x; c < H / 8; c += 256)
+        *(uint4 *)(dst + (size_t)i * H + 8 * c) = *(const uint4 *)(src + row * H + 8 * c);
+}
+
+hipError_t launch_gather_last_rows(const uint16_t *src, const int32_t *seq, int n, int H, uint16_t *dst, hipStream_t st)
+{
+    if (n <= 0 || H % 8) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_gather_last_rows, dim3(n), dim3(256), 0, st, src, seq, H, dst);
+    return hipGetLastError();
 }
 
 hipError_t launch_prefill_attn(const uint16_t *q, int n, int p0, int nq, int nkv, int d, int slot, const uint16_t *kc,

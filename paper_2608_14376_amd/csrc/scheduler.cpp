@@ -68,6 +68,8 @@ struct corun_sched {
     corun_engine *e = nullptr;          // null: dry run
     int B = 0, max_num_reqs = 0, vocab = 0;
     int32_t chunk = 0;                  // prefill chunk (0 = whole prompts)
+    int32_t batch_tokens = 0;           // batched prefill: most prompt tokens per prefill iteration (0 = one prompt)
+    float *blogits = nullptr;           // device [n][vocab]: a batched prefill's last-position logits
     corun_kv kv{};
     bool paged = false;
     std::unordered_map<int64_t, Request> reqs;
@@ -286,6 +288,77 @@ void remove_id(std::deque<int64_t> &q, int64_t id)
     q.erase(std::remove(q.begin(), q.end(), id), q.end());
 }
 
+// Batched prefill iteration (batch-invariant prefill, Sec. VIII): the
+// request Algorithm 1 selected from `waiting` and the requests behind it, in
+// order, while each passes the same admission checks (concurrency limit, a
+// free slot, its full sequence in the cache after its batch-mates') and the
+// batch's prompt tokens stay within batch_tokens.  They are admitted, run
+// through one corun_prefill_batch -- each prompt's result bit-identical to
+// its own prefill -- and each samples its first token; the batch then heads
+// `running` in order, as Algorithm 2 puts an isolated request there.
+corun_status run_prefill_batch(corun_sched *s, int64_t det, int32_t *event)
+{
+    std::vector<int64_t> batch = {det};
+    int64_t tokens = (int64_t)s->reqs.at(det).prompt.size();
+    int free_slots = (int)std::count(s->slot_owner.begin(), s->slot_owner.end(), (int64_t)-1) - 1;
+    int64_t free_pages = s->paged ? (int64_t)s->free_pages.size() - pages_for(s, s->reqs.at(det)) : 0;
+    auto it = std::find(s->waiting.begin(), s->waiting.end(), det);
+    for (++it; it != s->waiting.end(); ++it) {
+        const Request &r = s->reqs.at(*it);
+        if ((int)batch.size() >= CORUN_MAX_PREFILL_BATCH) break;
+        if ((int)(s->running.size() + batch.size()) >= s->max_num_reqs) break;
+        if (tokens + (int64_t)r.prompt.size() > s->batch_tokens) break;
+        if (free_slots < 1) break;
+        if (!s->paged && (int64_t)r.prompt.size() + r.max_new > s->kv.max_seq_len) break;
+        if (s->paged && (pages_for(s, r) > s->kv.max_pages_per_seq || pages_for(s, r) > free_pages)) break;
+        batch.push_back(r.id);
+        tokens += (int64_t)r.prompt.size();
+        --free_slots;
+        if (s->paged) free_pages -= pages_for(s, r);
+    }
+    std::vector<int32_t> toks, lens, slots;
+    for (int64_t id : batch) {
+        remove_id(s->waiting, id);
+        Request &r = s->reqs.at(id);
+        corun_status st = admit(s, r);
+        if (st != CORUN_OK) return st;
+        toks.insert(toks.end(), r.prompt.begin(), r.prompt.end());
+        lens.push_back((int32_t)r.prompt.size());
+        slots.push_back(r.slot);
+    }
+    const int n = (int)batch.size();
+    std::vector<int32_t> first(n, 0), pos(n);
+    std::vector<float> lps(n, 0.f);
+    std::vector<uint64_t> seeds(n);
+    std::vector<float> temps(n);
+    std::vector<uint8_t> valid(n, 1);
+    for (int i = 0; i < n; ++i) {
+        const Request &r = s->reqs.at(batch[i]);
+        pos[i] = (int32_t)r.prompt.size();
+        seeds[i] = r.seed;
+        temps[i] = r.temperature;
+    }
+    if (s->e) {
+        corun_status st = corun_prefill_batch(s->e, toks.data(), lens.data(), slots.data(), n, first.data(), s->blogits);
+        if (st != CORUN_OK) return from_engine(st);
+        st = corun_sample(s->e, s->blogits, s->vocab, n, valid.data(), pos.data(), seeds.data(), temps.data(),
+                          first.data(), lps.data());
+        if (st != CORUN_OK) return from_engine(st);
+    }
+    std::deque<int64_t> running(batch.begin(), batch.end());
+    for (int64_t id : s->running) running.push_back(id);
+    s->running.swap(running);
+    for (int i = 0; i < n; ++i) {
+        Request &r = s->reqs.at(batch[i]);
+        r.num_computed = (int32_t)r.prompt.size();
+        corun_status st = append(s, r, first[i], lps[i]);
+        if (st != CORUN_OK) return st;
+    }
+    ++s->n_prefill;
+    *event = 1;
+    return CORUN_OK;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -322,6 +395,11 @@ extern "C" corun_status corun_sched_create(corun_engine *e, const corun_sched_cf
         return sfail(CORUN_E_INVAL, "negative prefill_chunk");
     }
     s->chunk = cfg->prefill_chunk;
+    if (cfg->prefill_batch_tokens < 0 || (cfg->prefill_batch_tokens > 0 && cfg->prefill_chunk > 0)) {
+        delete s;
+        return sfail(CORUN_E_INVAL, "prefill_batch_tokens must be >= 0 and excludes prefill_chunk");
+    }
+    s->batch_tokens = cfg->prefill_batch_tokens;
     if (s->B <= 0 || (!s->paged && s->kv.max_seq_len <= 0) ||
         (s->paged && (s->kv.page_size <= 0 || s->kv.num_pages <= 0 || s->kv.max_pages_per_seq <= 0))) {
         delete s;
@@ -331,8 +409,10 @@ extern "C" corun_status corun_sched_create(corun_engine *e, const corun_sched_cf
     if (s->paged)
         for (int32_t p = s->kv.num_pages - 1; p >= 0; --p) s->free_pages.push_back(p);
     if (e) {
+        const size_t brows = s->batch_tokens > 0 ? (size_t)std::min(s->B, CORUN_MAX_PREFILL_BATCH) : 1;
         if (hipMalloc(&s->logits, sizeof(float) * (size_t)s->B * s->vocab) != hipSuccess ||
-            hipMalloc(&s->last, sizeof(float) * (size_t)s->vocab) != hipSuccess) {
+            hipMalloc(&s->last, sizeof(float) * (size_t)s->vocab) != hipSuccess ||
+            hipMalloc(&s->blogits, sizeof(float) * brows * s->vocab) != hipSuccess) {
             corun_sched_destroy(s);
             return sfail(CORUN_E_HIP, "logits buffers");
         }
@@ -346,6 +426,7 @@ extern "C" void corun_sched_destroy(corun_sched *s)
     if (!s) return;
     if (s->logits) (void)hipFree(s->logits);
     if (s->last) (void)hipFree(s->last);
+    if (s->blogits) (void)hipFree(s->blogits);
     delete s;
 }
 
@@ -383,6 +464,8 @@ extern "C" corun_status corun_sched_step(corun_sched *s, int32_t *event)
     corun_status st;
     if (det < 0) {
         st = schedule_origin(s, event);
+    } else if (s->batch_tokens > 0 && std::find(s->waiting.begin(), s->waiting.end(), det) != s->waiting.end()) {
+        st = run_prefill_batch(s, det, event);
     } else {
         std::deque<int64_t> stashed_running = s->running, stashed_waiting = s->waiting;
         s->waiting.clear();

@@ -1,7 +1,8 @@
 """Batch-invariant mode (`batch_invariant` option), the baseline CoRun is
 measured against (Sec. III, "Batch-Dependent GPU Reductions", Fig. 3b, and
-Definition 1): one projection tile and no split-K for every batch size,
-split-KV off in decode attention.
+Definition 1): no split-K and one MFMA instruction chain per output element
+for every batch size (the tile follows B: 32-, 64-, 128- and 256-row tiles
+across the batch sizes below), split-KV off in decode attention.
 
 * A request's logits, greedy token and appended k/v are bit-identical across
   engines of different B (1, 5, 72, 130) and slots, among other co-runners:

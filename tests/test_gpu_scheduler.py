@@ -30,12 +30,13 @@ def setup():
     return cfg, Wg, reqs
 
 
-def engine(cfg, Wg, paged=False):
+def engine(cfg, Wg, paged=False, bi_prefill=False):
     if not paged:
         K, V = wl.make_kv_contiguous(cfg, B, CAP, seed=82)
         K = [k.to(DEV) for k in K]
         V = [v.to(DEV) for v in V]
-        return corun.Engine(cfg, Wg, B, K, V, opt=corun.options(max_prefill_len=48)), (K, V)
+        pf = 160 if bi_prefill else 48
+        return corun.Engine(cfg, Wg, B, K, V, opt=corun.options(max_prefill_len=pf, bi_prefill=bi_prefill)), (K, V)
     ps, num_pages, mpp = 16, 24, CAP // 16
     K, V = wl.make_kv_paged(cfg, num_pages, ps, seed=83)
     K = [k.to(DEV) for k in K]
@@ -46,11 +47,13 @@ def engine(cfg, Wg, paged=False):
     return eng, (K, V, pt)
 
 
-def run(cfg, Wg, reqs, order, arrive_at=None, paged=False, max_num_reqs=6, chunk=0):
+def run(cfg, Wg, reqs, order, arrive_at=None, paged=False, max_num_reqs=6, chunk=0, batch_tokens=None):
     """Feed `reqs` in `order`; request k arrives before step arrive_at[k]
-    (all at once by default).  Returns {id: (tokens, logprob bits)}."""
-    eng, keep = engine(cfg, Wg, paged)
-    s = corun.Scheduler(eng, max_num_reqs=max_num_reqs, prefill_chunk=chunk)
+    (all at once by default).  batch_tokens: None = a plain engine; else a
+    batch-invariant-prefill engine with that prefill batch size (0 = one
+    prompt per prefill).  Returns {id: (tokens, logprob bits)}."""
+    eng, keep = engine(cfg, Wg, paged, bi_prefill=batch_tokens is not None)
+    s = corun.Scheduler(eng, max_num_reqs=max_num_reqs, prefill_chunk=chunk, prefill_batch_tokens=batch_tokens or 0)
     arrive_at = arrive_at or [0] * len(order)
     pending = sorted(zip(arrive_at, range(len(order))))
     step, k = 0, 0
@@ -118,3 +121,23 @@ def test_chunked_prefill_outputs_do_not_depend_on_arrival(setup):
         assert timed[rid] == v and tight[rid] == v and paged[rid] == v, rid
     for i in (0, 5):
         assert run(cfg, Wg, reqs, [i], chunk=16)[reqs[i]["id"]] == base[reqs[i]["id"]], i
+
+
+def test_batched_prefill_outputs_match_one_prompt_at_a_time(setup):
+    """A batch-invariant-prefill engine: batching prompts (up to 120 tokens
+    per prefill iteration) gives every request the tokens and
+    log-probability bits it gets with one prompt per prefill iteration, and
+    those do not depend on arrival order or time, the concurrency limit, or
+    running alone."""
+    cfg, Wg, reqs = setup
+    n = len(reqs)
+    one = run(cfg, Wg, reqs, list(range(n)), batch_tokens=0)
+    batched = run(cfg, Wg, reqs, list(range(n)), batch_tokens=120)
+    rng = np.random.default_rng(86)
+    shuffled = list(rng.permutation(n))
+    timed = run(cfg, Wg, reqs, shuffled, arrive_at=sorted(rng.integers(0, 30, n).tolist()), batch_tokens=120)
+    tight = run(cfg, Wg, reqs, shuffled[::-1], max_num_reqs=3, batch_tokens=120)
+    for rid, v in one.items():
+        assert batched[rid] == v and timed[rid] == v and tight[rid] == v, rid
+    for i in (2, 9):
+        assert run(cfg, Wg, reqs, [i], batch_tokens=120)[reqs[i]["id"]] == one[reqs[i]["id"]], i

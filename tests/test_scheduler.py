@@ -142,3 +142,40 @@ def test_chunk_count_per_prompt():
     assert ev.count(P) == sum((L + 15) // 16 for L in lens) and ev.count(D) == 0
     with pytest.raises(corun.CorunError):
         corun.Scheduler(None, n_slots=2, max_seq_len=64, prefill_chunk=-1)
+
+
+def test_batched_prefill_takes_the_fitting_requests_in_order():
+    """prefill_batch_tokens = 25, prompts of 10 tokens: a prefill iteration
+    takes the selected head and the next waiting requests while the prompts
+    total at most 25 tokens (two at a time), within the concurrency limit;
+    all of a batch get their first token in that iteration."""
+    s = corun.Scheduler(None, max_num_reqs=5, n_slots=6, max_seq_len=64, prefill_batch_tokens=25)
+    for i in range(6):
+        s.add_request(i, [1] * 10, max_new_tokens=3)
+    assert s.step() == P
+    assert [len(s.output(i)[0]) for i in range(6)] == [1, 1, 0, 0, 0, 0]
+    assert s.step() == P
+    assert [len(s.output(i)[0]) for i in range(6)] == [1, 1, 1, 1, 0, 0]
+    assert s.step() == P                                   # the limit of 5 cuts the third batch to one
+    assert [len(s.output(i)[0]) for i in range(6)] == [1, 1, 1, 1, 1, 0]
+    assert s.state()["running"] == 5
+    assert s.step() == D
+    s.run_until_idle()
+    for i in range(6):
+        assert s.output(i)[2] and len(s.output(i)[0]) == 3
+
+
+def test_batched_prefill_respects_pages_and_fifo():
+    """Eight 16-token pages: the head needs 4 (40 + 20 tokens), the next 3,
+    the third 2: only the first two fit together, and the third waits
+    although the token budget would allow it."""
+    s = corun.Scheduler(None, max_num_reqs=4, n_slots=4, page_size=16, num_pages=8, max_pages_per_seq=4,
+                        prefill_batch_tokens=1000)
+    s.add_request(0, [1] * 40, max_new_tokens=20)
+    s.add_request(1, [1] * 30, max_new_tokens=10)
+    s.add_request(2, [1] * 20, max_new_tokens=10)
+    assert s.step() == P
+    st = s.state()
+    assert st["running"] == 2 and st["waiting"] == 1 and st["free_pages"] == 1
+    with pytest.raises(corun.CorunError):
+        corun.Scheduler(None, n_slots=2, max_seq_len=64, prefill_chunk=16, prefill_batch_tokens=64)
