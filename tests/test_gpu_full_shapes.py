@@ -47,10 +47,11 @@ def test_decode_B256_full_shapes(full):
     eng = corun.Engine(cfg, Wg, B, K, V)
     plan = eng.plan()
     # the benchmark's configurations: 256 x 256 tiles for gate/up and the
-    # lm_head (with its argmax epilogue), 256 x 128 elsewhere
+    # lm_head (with its argmax epilogue), 128 x 128 (two M tiles) elsewhere
     assert (plan["gate_up"]["m_tile"], plan["gate_up"]["n_tile"]) == (256, 256)
     assert (plan["lm_head"]["m_tile"], plan["lm_head"]["n_tile"], plan["lm_head"]["split_k"]) == (256, 256, 1)
-    assert (plan["qkv"]["m_tile"], plan["qkv"]["n_tile"]) == (256, 128)
+    for name in ("qkv", "o", "down"):
+        assert (plan[name]["m_tile"], plan[name]["n_tile"]) == (128, 128), name
     b = wl.make_batch(B, cfg["vocab"], seed=43, len_lo=512, len_hi=4096)
     live = np.nonzero(b.valid)[0]
     sample = live[:: max(1, len(live) // 5)][:6]
