@@ -69,9 +69,10 @@ typedef struct {
 } corun_model_cfg;
 
 /* Weights: device bf16 buffers, caller-owned, borrowed for the engine's
- * lifetime.  Per-layer fields are HOST arrays of n_layers DEVICE pointers
- * (copied at creation).  Dense models leave the three expert fields NULL;
- * MoE models leave w_gate_up / w_down NULL. */
+ * lifetime and not to be changed during it (the engine may keep packed
+ * copies: corun_options.no_weight_pack).  Per-layer fields are HOST arrays
+ * of n_layers DEVICE pointers (copied at creation).  Dense models leave the
+ * three expert fields NULL; MoE models leave w_gate_up / w_down NULL. */
 typedef struct {
     const void *embed;                 /* [vocab, hidden] */
     const void *final_norm;            /* [hidden] */
@@ -133,6 +134,12 @@ typedef struct {
                                   Prefill": the hybrid of batch-invariant prefill and position-invariant
                                   fixed-shape decode): every prefill uses the plan of batch_invariant, and
                                   corun_prefill_batch is enabled; decode keeps its fixed-B plan. */
+    int32_t no_weight_pack;    /* 0 (default) = at creation the engine copies every projection weight whose
+                                  decode plan streams it with the small-M kernel (B_fixed <= 64) into a layout of
+                                  contiguous 128 x 64 tiles, in memory it owns (one more copy of those weights),
+                                  and reads that copy from then on, in decode and in prefill projections of up to
+                                  64 rows; results are bit-identical either way.  The weights must not change
+                                  after creation.  1 = no copies: read the caller's row-major weights. */
 } corun_options;
 
 /* Create an engine for one fixed padded batch size B_fixed (Sec. IV,

@@ -203,6 +203,11 @@ Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_
 
 }  // namespace
 
+namespace {
+// Projection weights, for the tile-packed copies the engine may hold.
+enum WeightId { W_QKV, W_O, W_GATE_UP, W_DOWN, W_ROUTER, W_LM_HEAD, W_COUNT };
+}  // namespace
+
 struct corun_engine {
     corun_model_cfg c{};
     corun_kv kv{};
@@ -214,6 +219,12 @@ struct corun_engine {
 
     const uint16_t *embed = nullptr, *final_norm = nullptr, *lm_head = nullptr;
     std::vector<const uint16_t *> attn_norm, w_qkv, w_o, mlp_norm, w_gu, w_down, w_router, w_egu, w_edown;
+    // tile-packed copies (per layer; one for lm_head) of the projections
+    // whose decode plan streams weights with the small-M pipelined kernel;
+    // empty = that projection reads the row-major weight only
+    std::vector<const uint16_t *> packed[W_COUNT];
+    char *pk_buf = nullptr;
+    size_t pk_bytes = 0;
     bool moe = false;
     // mixture-of-experts workspace (decode)
     float *p_router = nullptr, *moe_w = nullptr, *moe_gu = nullptr, *moe_y = nullptr;
@@ -341,6 +352,7 @@ static corun_status check_options(const corun_options &o)
         return fail(CORUN_E_INVAL, "gemm_bm must be 0, 64, 128 or 256");
     if (o.batch_invariant != 0 && o.batch_invariant != 1) return fail(CORUN_E_INVAL, "batch_invariant must be 0 or 1");
     if (o.bi_prefill != 0 && o.bi_prefill != 1) return fail(CORUN_E_INVAL, "bi_prefill must be 0 or 1");
+    if (o.no_weight_pack != 0 && o.no_weight_pack != 1) return fail(CORUN_E_INVAL, "no_weight_pack must be 0 or 1");
     if (o.batch_invariant && (o.attn_chunk || o.split_k_override || o.gemm_bm))
         return fail(CORUN_E_INVAL, "batch_invariant fixes the plan: attn_chunk, split_k_override and gemm_bm must be 0");
     return CORUN_OK;
@@ -399,6 +411,38 @@ void rebase(T *&p, char *base)
 
 size_t proj_part_elems(const Proj &p, int M) { return (size_t)p.S * M * p.N; }
 
+const uint16_t *row_major_weight(const corun_engine *e, int w, int l)
+{
+    switch (w) {
+    case W_QKV: return e->w_qkv[l];
+    case W_O: return e->w_o[l];
+    case W_GATE_UP: return e->w_gu[l];
+    case W_DOWN: return e->w_down[l];
+    case W_ROUTER: return e->w_router[l];
+    default: return e->lm_head;
+    }
+}
+
+// Whether a plan's kernel reads tile-packed weights: the pipelined kernel's
+// small-M configurations (32 or 64 x 128 tiles, 64-element stages).
+bool takes_packed(const Proj &p) { return p.bn == 128 && (p.bm == 32 || p.bm == 64) && p.K % 64 == 0; }
+
+// Projection `w` of layer l over `rows` rows of A: from the engine's
+// tile-packed copy where it holds one and the plan's kernel takes it (the
+// results are bit-identical), else from the caller's row-major weight.
+hipError_t proj(corun_engine *e, const uint16_t *A, int lda, int w, int l, const Proj &pr, int rows, float *out,
+                long long split_stride, int ldo, ArgBest *amax = nullptr)
+{
+    GemmShape g = shape_of(pr, rows);
+    const uint16_t *W = row_major_weight(e, w, l);
+    const std::vector<const uint16_t *> &pk = e->packed[w];
+    if (!pk.empty() && takes_packed(pr)) {
+        g.pk = 1;
+        W = pk[w == W_LM_HEAD ? 0 : l];
+    }
+    return launch_proj(A, lda, W, g, out, split_stride, ldo, e->st, amax);
+}
+
 // Buffers of one mixture-of-experts layer run over `rows` rows.
 struct MoeBufs {
     const uint8_t *valid;
@@ -411,8 +455,7 @@ struct MoeBufs {
 corun_status moe_router(corun_engine *e, const MoeBufs &m, const uint16_t *h, int rows, const Proj &pr, int l)
 {
     const corun_model_cfg &c = e->c;
-    HIP_TRY(launch_proj(h, c.hidden, e->w_router[l], shape_of(pr, rows), m.router_part, (long long)rows * c.n_experts,
-                        c.n_experts, e->st));
+    HIP_TRY(proj(e, h, c.hidden, W_ROUTER, l, pr, rows, m.router_part, (long long)rows * c.n_experts, c.n_experts));
     HIP_TRY(launch_moe_route(m.router_part, pr.S, (long long)rows * c.n_experts, rows, c.n_experts, c.top_k, m.valid,
                              m.sel, m.w, e->st));
     HIP_TRY(launch_moe_dispatch(m.sel, rows * c.top_k, c.n_experts, m.slots, m.list, m.tiles, e->st));
@@ -467,7 +510,7 @@ corun_status launch_one(corun_engine *e, int which, int l)
     hipStream_t st = e->st;
     switch (which) {
     case CORUN_K_QKV_GEMM: {
-        HIP_TRY(launch_proj(e->h, H, e->w_qkv[l], shape_of(p.qkv, B), e->p_qkv, (long long)B * nqkv, nqkv, st));
+        HIP_TRY(proj(e, e->h, H, W_QKV, l, p.qkv, B, e->p_qkv, (long long)B * nqkv, nqkv));
         break;
     }
     case CORUN_K_QKV_POST:
@@ -482,7 +525,7 @@ corun_status launch_one(corun_engine *e, int which, int l)
         HIP_TRY(launch_attn_merge(e->attn_ws, B, e->d_valid, e->d_seq, nq, nkv, d, p.chunk, p.max_splits, e->o, st));
         break;
     case CORUN_K_O_GEMM: {
-        HIP_TRY(launch_proj(e->o, nq * d, e->w_o[l], shape_of(p.o, B), e->p_o, (long long)B * H, H, st));
+        HIP_TRY(proj(e, e->o, nq * d, W_O, l, p.o, B, e->p_o, (long long)B * H, H));
         break;
     }
     case CORUN_K_RMSNORM:   // the post-attention norm (folds the O partials)
@@ -496,7 +539,7 @@ corun_status launch_one(corun_engine *e, int which, int l)
         if (e->moe) {
             ST_TRY(moe_expert_gate_up(e, decode_moe(e), e->h, l));
         } else {
-            HIP_TRY(launch_proj(e->h, H, e->w_gu[l], shape_of(p.gu, B), e->p_gu, (long long)B * 2 * F, 2 * F, st));
+            HIP_TRY(proj(e, e->h, H, W_GATE_UP, l, p.gu, B, e->p_gu, (long long)B * 2 * F, 2 * F));
         }
         break;
     case CORUN_K_SWIGLU:
@@ -511,15 +554,14 @@ corun_status launch_one(corun_engine *e, int which, int l)
         if (e->moe) {
             ST_TRY(moe_expert_down(e, decode_moe(e), l));
         } else {
-            HIP_TRY(launch_proj(e->a, F, e->w_down[l], shape_of(p.down, B), e->p_down, (long long)B * H, H, st));
+            HIP_TRY(proj(e, e->a, F, W_DOWN, l, p.down, B, e->p_down, (long long)B * H, H));
         }
         break;
     case CORUN_K_LM_HEAD:
         if (p.lm.S == 1) {
-            HIP_TRY(launch_proj(e->h, H, e->lm_head, shape_of(p.lm, B), e->logits, 0, c.vocab, st, e->amax));
+            HIP_TRY(proj(e, e->h, H, W_LM_HEAD, 0, p.lm, B, e->logits, 0, c.vocab, e->amax));
         } else {   // test aid only: a split lm_head, reduced in split order
-            HIP_TRY(launch_proj(e->h, H, e->lm_head, shape_of(p.lm, B), e->p_lm, (long long)B * c.vocab, c.vocab,
-                                st));
+            HIP_TRY(proj(e, e->h, H, W_LM_HEAD, 0, p.lm, B, e->p_lm, (long long)B * c.vocab, c.vocab));
             HIP_TRY(launch_reduce_splits(e->p_lm, p.lm.S, (long long)B * c.vocab, (long long)B * c.vocab, e->logits,
                                          st));
         }
@@ -664,6 +706,48 @@ static corun_status alloc_prefill(corun_engine *e)
     return CORUN_OK;
 }
 
+// Tile-packed copies of the projections whose decode plan takes them
+// (batches of up to 64 rows), made on the engine's stream after the caller's
+// stream has reached this point.  Prefill projections of up to 64 rows use
+// them as well.
+static corun_status pack_weights(corun_engine *e)
+{
+    const Plan &p = e->plan;
+    const int L = e->c.n_layers;
+    struct Item {
+        int w;
+        const Proj *pr;
+        int count;
+    };
+    const Item items[] = {{W_QKV, &p.qkv, L},
+                          {W_O, &p.o, L},
+                          {W_GATE_UP, &p.gu, e->moe ? 0 : L},
+                          {W_DOWN, &p.down, e->moe ? 0 : L},
+                          {W_ROUTER, &p.router, e->moe ? L : 0},
+                          {W_LM_HEAD, &p.lm, 1}};
+    size_t total = 0;   // each copy is a whole number of 16 KB tiles
+    for (const Item &it : items)
+        if (it.count && takes_packed(*it.pr)) total += (size_t)it.count * packed_weight_elems(it.pr->N, it.pr->K) * 2;
+    if (total == 0) return CORUN_OK;
+    if (hipMalloc(&e->pk_buf, total) != hipSuccess)
+        return fail(CORUN_E_HIP, "packed weight copies (%zu bytes) do not fit; no_weight_pack = 1 reads the row-major "
+                    "weights instead", total);
+    e->pk_bytes = total;
+    HIP_TRY(hipEventRecord(e->ev, e->user));
+    HIP_TRY(hipStreamWaitEvent(e->st, e->ev, 0));
+    char *q = e->pk_buf;
+    for (const Item &it : items) {
+        if (!it.count || !takes_packed(*it.pr)) continue;
+        const size_t bytes = packed_weight_elems(it.pr->N, it.pr->K) * 2;
+        for (int l = 0; l < it.count; ++l) {
+            HIP_TRY(launch_pack_weights(row_major_weight(e, it.w, l), it.pr->N, it.pr->K, (uint16_t *)q, e->st));
+            e->packed[it.w].push_back((const uint16_t *)q);
+            q += bytes;
+        }
+    }
+    return CORUN_OK;
+}
+
 extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const corun_weights *w, const corun_kv *kv,
                                             int32_t B, const corun_options *opt, void *stream, corun_engine **out)
 {
@@ -803,6 +887,10 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
         corun_status s = alloc_prefill(e);
         if (s != CORUN_OK) return bail(s);
     }
+    if (!o.no_weight_pack) {
+        corun_status s = pack_weights(e);
+        if (s != CORUN_OK) return bail(s);
+    }
     if (hipStreamSynchronize(e->st) != hipSuccess) return bail(fail(CORUN_E_HIP, "initialisation failed"));
     *out = e;
     return CORUN_OK;
@@ -816,6 +904,7 @@ extern "C" void corun_engine_destroy(corun_engine *e)
     if (e->graph) (void)hipGraphDestroy(e->graph);
     if (e->ws) (void)hipFree(e->ws);
     if (e->pws) (void)hipFree(e->pws);
+    if (e->pk_buf) (void)hipFree(e->pk_buf);
     if (e->h_tok) (void)hipHostFree(e->h_tok);
     if (e->h_valid) (void)hipHostFree(e->h_valid);
     if (e->h_hist) (void)hipHostFree(e->h_hist);
@@ -942,11 +1031,11 @@ extern "C" corun_status corun_prefill_chunk(corun_engine *e, const int32_t *toke
     for (int l = 0; l < c.n_layers; ++l) {
         HIP_TRY(launch_rmsnorm(e->pf_x, l ? e->pf_part : nullptr, l ? dense_S : 0, (long long)Lp * H, Lp, H,
                                e->attn_norm[l], c.rms_eps, e->pf_h, st, fold_of(e, pmb, l)));
-        HIP_TRY(launch_proj(e->pf_h, H, e->w_qkv[l], shape_of(pq, Lp), e->pf_part, (long long)Lp * nqkv, nqkv, st));
+        HIP_TRY(proj(e, e->pf_h, H, W_QKV, l, pq, Lp, e->pf_part, (long long)Lp * nqkv, nqkv));
         HIP_TRY(launch_qkv_post(e->pf_part, pq.S, (long long)Lp * nqkv, Lp, nullptr, e->pf_pos + start, nullptr, slot,
                                 nq, nkv, d, e->rope, e->pf_q, e->kc[l], e->vc[l], e->view, st));
         HIP_TRY(launch_prefill_attn(e->pf_q, Lp, start, nq, nkv, d, slot, e->kc[l], e->vc[l], e->view, e->pf_o, st));
-        HIP_TRY(launch_proj(e->pf_o, nq * d, e->w_o[l], shape_of(po, Lp), e->pf_part, (long long)Lp * H, H, st));
+        HIP_TRY(proj(e, e->pf_o, nq * d, W_O, l, po, Lp, e->pf_part, (long long)Lp * H, H));
         HIP_TRY(launch_rmsnorm(e->pf_x, e->pf_part, po.S, (long long)Lp * H, Lp, H, e->mlp_norm[l], c.rms_eps,
                                e->pf_h, st));
         if (e->moe) {
@@ -956,10 +1045,9 @@ extern "C" corun_status corun_prefill_chunk(corun_engine *e, const int32_t *toke
             HIP_TRY(launch_swiglu(e->pf_moe_gu, 1, 0, Lp * c.top_k, Fe, e->pf_moe_act, Fe, st));
             ST_TRY(moe_expert_down(e, pmb, l));
         } else {
-            HIP_TRY(launch_proj(e->pf_h, H, e->w_gu[l], shape_of(pg, Lp), e->pf_part, (long long)Lp * 2 * F, 2 * F,
-                                st));
+            HIP_TRY(proj(e, e->pf_h, H, W_GATE_UP, l, pg, Lp, e->pf_part, (long long)Lp * 2 * F, 2 * F));
             HIP_TRY(launch_swiglu(e->pf_part, pg.S, (long long)Lp * 2 * F, Lp, F, e->pf_a, F, st));
-            HIP_TRY(launch_proj(e->pf_a, F, e->w_down[l], shape_of(pd, Lp), e->pf_part, (long long)Lp * H, H, st));
+            HIP_TRY(proj(e, e->pf_a, F, W_DOWN, l, pd, Lp, e->pf_part, (long long)Lp * H, H));
         }
     }
     if (!token_out && !last_logits) {   // an inner chunk: its KV is the product
@@ -975,7 +1063,7 @@ extern "C" corun_status corun_prefill_chunk(corun_engine *e, const int32_t *toke
     }
     HIP_TRY(launch_rmsnorm(e->pf_x + last, e->pf_part + last, dense_S, (long long)Lp * H, 1, H, e->final_norm,
                            c.rms_eps, e->pf_hlast, st, lf));
-    HIP_TRY(launch_proj(e->pf_hlast, H, e->lm_head, shape_of(pl, 1), e->pf_logits, 0, c.vocab, st, e->pf_amax));
+    HIP_TRY(proj(e, e->pf_hlast, H, W_LM_HEAD, 0, pl, 1, e->pf_logits, 0, c.vocab, e->pf_amax));
     HIP_TRY(launch_argmax_partials(e->pf_amax, 1, gemm_col_blocks(c.vocab), nullptr, e->pf_next, st));
     HIP_TRY(hipMemcpyAsync(e->h_next, e->pf_next, sizeof(int32_t), hipMemcpyDeviceToHost, st));
     if (last_logits)
@@ -1071,12 +1159,12 @@ extern "C" corun_status corun_prefill_batch(corun_engine *e, const int32_t *toke
     for (int l = 0; l < c.n_layers; ++l) {
         HIP_TRY(launch_rmsnorm(e->pf_x, l ? e->pf_part : nullptr, l ? dense_S : 0, (long long)Lp * H, Lp, H,
                                e->attn_norm[l], c.rms_eps, e->pf_h, st, fold_of(e, pmb, l)));
-        HIP_TRY(launch_proj(e->pf_h, H, e->w_qkv[l], shape_of(pq, Lp), e->pf_part, (long long)Lp * nqkv, nqkv, st));
+        HIP_TRY(proj(e, e->pf_h, H, W_QKV, l, pq, Lp, e->pf_part, (long long)Lp * nqkv, nqkv));
         HIP_TRY(launch_qkv_post(e->pf_part, pq.S, (long long)Lp * nqkv, Lp, nullptr, e->pf_rowpos, e->pf_rowslot, -1,
                                 nq, nkv, d, e->rope, e->pf_q, e->kc[l], e->vc[l], e->view, st));
         HIP_TRY(launch_prefill_attn_multi(e->pf_q, e->pf_seq, n, groups, nq, nkv, d, e->kc[l], e->vc[l], e->view,
                                           e->pf_o, st));
-        HIP_TRY(launch_proj(e->pf_o, nq * d, e->w_o[l], shape_of(po, Lp), e->pf_part, (long long)Lp * H, H, st));
+        HIP_TRY(proj(e, e->pf_o, nq * d, W_O, l, po, Lp, e->pf_part, (long long)Lp * H, H));
         HIP_TRY(launch_rmsnorm(e->pf_x, e->pf_part, po.S, (long long)Lp * H, Lp, H, e->mlp_norm[l], c.rms_eps,
                                e->pf_h, st));
         if (e->moe) {
@@ -1086,10 +1174,9 @@ extern "C" corun_status corun_prefill_batch(corun_engine *e, const int32_t *toke
             HIP_TRY(launch_swiglu(e->pf_moe_gu, 1, 0, Lp * c.top_k, Fe, e->pf_moe_act, Fe, st));
             ST_TRY(moe_expert_down(e, pmb, l));
         } else {
-            HIP_TRY(launch_proj(e->pf_h, H, e->w_gu[l], shape_of(pg, Lp), e->pf_part, (long long)Lp * 2 * F, 2 * F,
-                                st));
+            HIP_TRY(proj(e, e->pf_h, H, W_GATE_UP, l, pg, Lp, e->pf_part, (long long)Lp * 2 * F, 2 * F));
             HIP_TRY(launch_swiglu(e->pf_part, pg.S, (long long)Lp * 2 * F, Lp, F, e->pf_a, F, st));
-            HIP_TRY(launch_proj(e->pf_a, F, e->w_down[l], shape_of(pd, Lp), e->pf_part, (long long)Lp * H, H, st));
+            HIP_TRY(proj(e, e->pf_a, F, W_DOWN, l, pd, Lp, e->pf_part, (long long)Lp * H, H));
         }
     }
     // final norm of every row (the same row-wise arithmetic as one prompt's
@@ -1097,7 +1184,7 @@ extern "C" corun_status corun_prefill_batch(corun_engine *e, const int32_t *toke
     HIP_TRY(launch_rmsnorm(e->pf_x, e->pf_part, dense_S, (long long)Lp * H, Lp, H, e->final_norm, c.rms_eps, e->pf_h,
                            st, fold_of(e, pmb, c.n_layers)));
     HIP_TRY(launch_gather_last_rows(e->pf_h, e->pf_seq, n, H, e->pf_hlast, st));
-    HIP_TRY(launch_proj(e->pf_hlast, H, e->lm_head, shape_of(pl, n), e->pf_logits, 0, c.vocab, st, e->pf_amax));
+    HIP_TRY(proj(e, e->pf_hlast, H, W_LM_HEAD, 0, pl, n, e->pf_logits, 0, c.vocab, e->pf_amax));
     HIP_TRY(launch_argmax_partials(e->pf_amax, n, gemm_col_blocks(c.vocab), nullptr, e->pf_next, st));
     HIP_TRY(hipMemcpyAsync(tokens_out, e->pf_next, sizeof(int32_t) * n, hipMemcpyDeviceToHost, st));
     if (last_logits)

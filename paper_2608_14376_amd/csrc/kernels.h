@@ -59,6 +59,7 @@ struct GemmShape {
     int mt;         // skinny kernel: 16-row M tiles per wave: 1, 2 or 4
     int bm;         // 0 = skinny kernel; 64, 128, 256 = LDS-tiled kernel with this M tile
     int bn;         // > 0: pipelined kernel with bm x bn tiles (128 x 128, 256 x 128, 256 x 256)
+    int pk;         // 1: W is the tile-packed copy (launch_pack_weights); bm 32 or 64, bn 128 only
 };
 // Dispatch on g.bm.
 hipError_t launch_proj(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
@@ -156,6 +157,11 @@ hipError_t launch_rope_table(float2 *tab, int max_pos, int d, double theta, hipS
 
 // fill n bytes with the byte value v (graph-safe replacement for memset)
 hipError_t launch_fill_u32(uint32_t *p, long long n_words, uint32_t v, hipStream_t st);
+// Tile-packed copy of a row-major [N, K] bf16 weight (K % 64 == 0) for the
+// pipelined kernel's 128 x 64 weight tiles: [ceil(N / 128)][K / 64][128][64],
+// rows past N zero; packed_weight_elems(N, K) elements.
+size_t packed_weight_elems(int N, int K);
+hipError_t launch_pack_weights(const uint16_t *W, int N, int K, uint16_t *P, hipStream_t st);
 
 // prefill helpers: pos[t] = t for t < n
 hipError_t launch_iota(int32_t *p, int n, hipStream_t st);

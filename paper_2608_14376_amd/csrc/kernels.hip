@@ -561,6 +561,14 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const uint16_t *__restrict__
 // and are never stored; K and the split chunk are multiples of BK, so no
 // stage is partial.
 //
+// Packed weights (PKW, 128 x 64 tiles only): W is the tile-packed copy that
+// launch_pack_weights writes, [ceil(N / 128)][K / 64][128][64], each 16 KB
+// tile contiguous and rows past N zero.  A workgroup then streams one
+// contiguous run of K / 64 tiles instead of 128 rows 2 K bytes apart; the
+// same elements meet the same instructions in the same order, so the results
+// are bit-identical to the row-major layout.  At small M, where the kernel
+// streams weights, this is 5-20% faster.
+//
 // Tile order: with several M tiles, workgroups are handed to the eight XCDs
 // in turn, so each XCD gets a contiguous run of tiles, walked in groups of
 // eight M tiles per N tile: the workgroups sharing a weight tile or an
@@ -599,7 +607,7 @@ __device__ __forceinline__ int dma_swz(int r, int c)
     else return r * 8 + (c ^ ((r >> 1) & 7));
 }
 
-template <int BM, int BN, int BK, int NST, int WGM, int NW = 4>
+template <int BM, int BN, int BK, int NST, int WGM, int NW = 4, bool PKW = false>
 __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict__ A, int lda,
                                                   const uint16_t *__restrict__ W, int M, int N, int K, int Kc,
                                                   float *__restrict__ out, long long split_stride, int ldo,
@@ -615,6 +623,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
     constexpr int OPS = A_OPS + W_OPS, P = NST;       // every slot of the ring is a stage in flight
     constexpr int STAGE = (BM + BN) * C;             // 16-byte units
     static_assert(P * OPS <= 63, "vmcnt range");
+    static_assert(!PKW || (BN == 128 && BK == 64), "packed weights come in 128 x 64 tiles");
     __shared__ __attribute__((aligned(16))) uint4 ring[NST * STAGE];
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -651,8 +660,11 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
 #pragma unroll
     for (int j = 0; j < W_OPS; ++j) {
         const int g = j * NT + tid, r = g / C, c = dma_swz<C>(r, g % C) - r * C;
-        wsrc[j] = W + (size_t)min(n0 + r, N - 1) * K + kbeg + 8 * c;
+        if constexpr (PKW) wsrc[j] = W + ((size_t)nt * (K / BK) + kbeg / BK) * (BN * BK) + r * BK + 8 * c;
+        else wsrc[j] = W + (size_t)min(n0 + r, N - 1) * K + kbeg + 8 * c;
     }
+    // a stage kofs K elements in: kofs further along a row, or kofs / BK tiles on
+    constexpr int WSTEP = PKW ? BN : 1;
     typedef __attribute__((address_space(3))) void lds_void;
     auto issue = [&](int slot, int kofs) {
         uint4 *base = ring + slot * STAGE + wave * 64;
@@ -661,8 +673,8 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
             __builtin_amdgcn_global_load_lds((const void *)(asrc[j] + kofs), (lds_void *)(base + j * NT), 16, 0, 0);
 #pragma unroll
         for (int j = 0; j < W_OPS; ++j)
-            __builtin_amdgcn_global_load_lds((const void *)(wsrc[j] + kofs), (lds_void *)(base + BM * C + j * NT), 16,
-                                             0, 0);
+            __builtin_amdgcn_global_load_lds((const void *)(wsrc[j] + (size_t)kofs * WSTEP),
+                                             (lds_void *)(base + BM * C + j * NT), 16, 0, 0);
     };
 
     f32x16 acc[FM][FN];
@@ -799,6 +811,17 @@ hipError_t launch_gemm_dma(const uint16_t *A, int lda, const uint16_t *W, const 
     const int num_n = (g.N + g.bn - 1) / g.bn;
     const int num_m = (g.M + g.bm - 1) / g.bm;
     dim3 grid(num_m * num_n, g.S);
+    if (g.pk) {   // tile-packed weights: the small-M configurations only
+        if (g.bm == 32 && g.bn == 128)
+            hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, true>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N,
+                               g.K, g.Kc, out, split_stride, ldo, amax);
+        else if (g.bm == 64 && g.bn == 128)
+            hipLaunchKernelGGL((k_gemm_dma<64, 128, 64, 4, 1, 2, true>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N,
+                               g.K, g.Kc, out, split_stride, ldo, amax);
+        else
+            return hipErrorInvalidValue;
+        return hipGetLastError();
+    }
     if (g.bm == 32 && g.bn == 128)
         hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
                            out, split_stride, ldo, amax);
@@ -1549,6 +1572,37 @@ hipError_t launch_fill_u32(uint32_t *p, long long n_words, uint32_t v, hipStream
     long long blocks = (n_words + 255) / 256;
     if (blocks > 65536) blocks = 65536;
     hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)blocks), dim3(256), 0, st, p, n_words, v);
+    return hipGetLastError();
+}
+
+// Tile-packed copy of a row-major [N, K] weight: P[nt][kb][r][c] =
+// W[nt * 128 + r][kb * 64 + c], zero for rows past N.  One thread per
+// 16 bytes of P.
+__global__ void k_pack_weights(const uint16_t *__restrict__ W, int N, int K, uint16_t *__restrict__ P,
+                               long long units)
+{
+    const int kt = K / 64;
+    for (long long u = (long long)blockIdx.x * blockDim.x + threadIdx.x; u < units;
+         u += (long long)gridDim.x * blockDim.x) {
+        const int c8 = (int)(u & 7), r = (int)((u >> 3) & 127);
+        const long long tile = u >> 10;
+        const int kb = (int)(tile % kt);
+        const long long row = tile / kt * 128 + r;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (row < N) v = *reinterpret_cast<const uint4 *>(W + row * K + kb * 64 + 8 * c8);
+        reinterpret_cast<uint4 *>(P)[u] = v;
+    }
+}
+
+size_t packed_weight_elems(int N, int K) { return (size_t)(N + 127) / 128 * 128 * K; }
+
+hipError_t launch_pack_weights(const uint16_t *W, int N, int K, uint16_t *P, hipStream_t st)
+{
+    if (N <= 0 || K <= 0 || K % 64 != 0) return hipErrorInvalidValue;
+    const long long units = (long long)packed_weight_elems(N, K) / 8;
+    long long blocks = (units + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    hipLaunchKernelGGL(k_pack_weights, dim3((unsigned)blocks), dim3(256), 0, st, W, N, K, P, units);
     return hipGetLastError();
 }
 
