@@ -334,7 +334,8 @@ enum {
     CORUN_K_ATTN_MERGE = 6,   /* fixed-order split merge */
     CORUN_K_RMSNORM = 7,      /* residual fold + RMSNorm */
     CORUN_K_QKV_POST = 8,     /* QKV epilogue: RoPE + KV append */
-    CORUN_K_SWIGLU = 9,       /* SwiGLU epilogue */
+    CORUN_K_SWIGLU = 9,       /* SwiGLU epilogue (no kernel where the gate/up projection's epilogue applies it:
+                                 packed weights without split-K) */
     CORUN_K_ARGMAX = 10,      /* greedy argmax */
     CORUN_K_MOE_ROUTER = 11,  /* MoE: router projection, top-k routing and dispatch (3 kernels) */
     CORUN_K_COUNT = 12

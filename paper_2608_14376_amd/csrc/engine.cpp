@@ -225,6 +225,7 @@ struct corun_engine {
     std::vector<const uint16_t *> packed[W_COUNT];
     char *pk_buf = nullptr;
     size_t pk_bytes = 0;
+    bool gu_fused = false;   // the gate/up copy is interleaved for the fused SwiGLU epilogue
     bool moe = false;
     // mixture-of-experts workspace (decode)
     float *p_router = nullptr, *moe_w = nullptr, *moe_gu = nullptr, *moe_y = nullptr;
@@ -436,11 +437,25 @@ hipError_t proj(corun_engine *e, const uint16_t *A, int lda, int w, int l, const
     GemmShape g = shape_of(pr, rows);
     const uint16_t *W = row_major_weight(e, w, l);
     const std::vector<const uint16_t *> &pk = e->packed[w];
-    if (!pk.empty() && takes_packed(pr)) {
+    if (!pk.empty() && takes_packed(pr) && !(w == W_GATE_UP && e->gu_fused)) {
         g.pk = 1;
         W = pk[w == W_LM_HEAD ? 0 : l];
     }
     return launch_proj(A, lda, W, g, out, split_stride, ldo, e->st, amax);
+}
+
+// Whether gate/up and SwiGLU run as one kernel for this plan: the engine
+// holds the gate/up-interleaved packed copy and the plan takes it without
+// split-K.  The epilogue computes what the SwiGLU kernel computes from the
+// same fp32 sums, so both paths give the same bits.
+bool gu_fuses(const corun_engine *e, const Proj &pr) { return e->gu_fused && takes_packed(pr) && pr.S == 1; }
+
+// gate/up of layer l over `rows` rows of A with SwiGLU into act [rows][ffn]
+hipError_t gate_up_swiglu(corun_engine *e, const uint16_t *A, int l, const Proj &pr, int rows, uint16_t *act)
+{
+    GemmShape g = shape_of(pr, rows);
+    g.pk = 1;
+    return launch_gemm_dma(A, e->c.hidden, e->packed[W_GATE_UP][l], g, nullptr, 0, e->c.ffn, e->st, nullptr, act);
 }
 
 // Buffers of one mixture-of-experts layer run over `rows` rows.
@@ -538,15 +553,17 @@ corun_status launch_one(corun_engine *e, int which, int l)
     case CORUN_K_GATE_UP_GEMM:
         if (e->moe) {
             ST_TRY(moe_expert_gate_up(e, decode_moe(e), e->h, l));
+        } else if (gu_fuses(e, p.gu)) {
+            HIP_TRY(gate_up_swiglu(e, e->h, l, p.gu, B, e->a));
         } else {
             HIP_TRY(proj(e, e->h, H, W_GATE_UP, l, p.gu, B, e->p_gu, (long long)B * 2 * F, 2 * F));
         }
         break;
-    case CORUN_K_SWIGLU:
+    case CORUN_K_SWIGLU:   // nothing to launch when the gate/up projection's epilogue does it
         if (e->moe) {
             const int Fe = c.expert_ffn;
             HIP_TRY(launch_swiglu(e->moe_gu, 1, 0, B * c.top_k, Fe, e->moe_act, Fe, st));
-        } else {
+        } else if (!gu_fuses(e, p.gu)) {
             HIP_TRY(launch_swiglu(e->p_gu, p.gu.S, (long long)B * 2 * F, B, F, e->a, F, st));
         }
         break;
@@ -735,16 +752,21 @@ static corun_status pack_weights(corun_engine *e)
     e->pk_bytes = total;
     HIP_TRY(hipEventRecord(e->ev, e->user));
     HIP_TRY(hipStreamWaitEvent(e->st, e->ev, 0));
+    // gate/up without split-K: interleave gate and up rows of the same
+    // features so that the projection's epilogue can apply SwiGLU
+    const bool interleave = !e->moe && takes_packed(p.gu) && p.gu.S == 1 && p.gu.N % 128 == 0;
     char *q = e->pk_buf;
     for (const Item &it : items) {
         if (!it.count || !takes_packed(*it.pr)) continue;
         const size_t bytes = packed_weight_elems(it.pr->N, it.pr->K) * 2;
         for (int l = 0; l < it.count; ++l) {
-            HIP_TRY(launch_pack_weights(row_major_weight(e, it.w, l), it.pr->N, it.pr->K, (uint16_t *)q, e->st));
+            HIP_TRY(launch_pack_weights(row_major_weight(e, it.w, l), it.pr->N, it.pr->K, (uint16_t *)q, e->st,
+                                        it.w == W_GATE_UP && interleave));
             e->packed[it.w].push_back((const uint16_t *)q);
             q += bytes;
         }
     }
+    e->gu_fused = interleave;
     return CORUN_OK;
 }
 
@@ -1045,8 +1067,12 @@ extern "C" corun_status corun_prefill_chunk(corun_engine *e, const int32_t *toke
             HIP_TRY(launch_swiglu(e->pf_moe_gu, 1, 0, Lp * c.top_k, Fe, e->pf_moe_act, Fe, st));
             ST_TRY(moe_expert_down(e, pmb, l));
         } else {
-            HIP_TRY(proj(e, e->pf_h, H, W_GATE_UP, l, pg, Lp, e->pf_part, (long long)Lp * 2 * F, 2 * F));
-            HIP_TRY(launch_swiglu(e->pf_part, pg.S, (long long)Lp * 2 * F, Lp, F, e->pf_a, F, st));
+            if (gu_fuses(e, pg)) {
+                HIP_TRY(gate_up_swiglu(e, e->pf_h, l, pg, Lp, e->pf_a));
+            } else {
+                HIP_TRY(proj(e, e->pf_h, H, W_GATE_UP, l, pg, Lp, e->pf_part, (long long)Lp * 2 * F, 2 * F));
+                HIP_TRY(launch_swiglu(e->pf_part, pg.S, (long long)Lp * 2 * F, Lp, F, e->pf_a, F, st));
+            }
             HIP_TRY(proj(e, e->pf_a, F, W_DOWN, l, pd, Lp, e->pf_part, (long long)Lp * H, H));
         }
     }
@@ -1174,8 +1200,12 @@ extern "C" corun_status corun_prefill_batch(corun_engine *e, const int32_t *toke
             HIP_TRY(launch_swiglu(e->pf_moe_gu, 1, 0, Lp * c.top_k, Fe, e->pf_moe_act, Fe, st));
             ST_TRY(moe_expert_down(e, pmb, l));
         } else {
-            HIP_TRY(proj(e, e->pf_h, H, W_GATE_UP, l, pg, Lp, e->pf_part, (long long)Lp * 2 * F, 2 * F));
-            HIP_TRY(launch_swiglu(e->pf_part, pg.S, (long long)Lp * 2 * F, Lp, F, e->pf_a, F, st));
+            if (gu_fuses(e, pg)) {
+                HIP_TRY(gate_up_swiglu(e, e->pf_h, l, pg, Lp, e->pf_a));
+            } else {
+                HIP_TRY(proj(e, e->pf_h, H, W_GATE_UP, l, pg, Lp, e->pf_part, (long long)Lp * 2 * F, 2 * F));
+                HIP_TRY(launch_swiglu(e->pf_part, pg.S, (long long)Lp * 2 * F, Lp, F, e->pf_a, F, st));
+            }
             HIP_TRY(proj(e, e->pf_a, F, W_DOWN, l, pd, Lp, e->pf_part, (long long)Lp * H, H));
         }
     }

@@ -74,8 +74,13 @@ hipError_t launch_gemm_tiled(const uint16_t *A, int lda, const uint16_t *W, cons
                              long long split_stride, int ldo, hipStream_t st, ArgBest *amax = nullptr);
 // Pipelined large-M variant (direct global -> LDS loads, 32x32 MFMA tiles):
 // K and Kc multiples of 64 (32 for bn == 256).
+// With act != nullptr (g.pk, S == 1, N % 128 == 0): W is the gate/up-
+// interleaved packed copy of a [2F, K] gate/up weight (launch_pack_weights
+// with interleave) and the kernel writes act[m * ldo + j] = SwiGLU of
+// feature j (bf16) instead of fp32 outputs; out and amax are unused.
 hipError_t launch_gemm_dma(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
-                           long long split_stride, int ldo, hipStream_t st, ArgBest *amax = nullptr);
+                           long long split_stride, int ldo, hipStream_t st, ArgBest *amax = nullptr,
+                           uint16_t *act = nullptr);
 inline int gemm_col_blocks(int N) { return (N + 63) / 64; }
 // next[r] = best index over the np column-block partials of row r (-1 for padding rows).
 hipError_t launch_argmax_partials(const ArgBest *part, int rows, int np, const uint8_t *valid, int32_t *next,
@@ -160,8 +165,10 @@ hipError_t launch_fill_u32(uint32_t *p, long long n_words, uint32_t v, hipStream
 // Tile-packed copy of a row-major [N, K] bf16 weight (K % 64 == 0) for the
 // pipelined kernel's 128 x 64 weight tiles: [ceil(N / 128)][K / 64][128][64],
 // rows past N zero; packed_weight_elems(N, K) elements.
+// With interleave (N % 128 == 0), tile nt holds rows 64 nt .. 64 nt + 63 of
+// each half of W: a gate/up weight's gate and up rows of the same features.
 size_t packed_weight_elems(int N, int K);
-hipError_t launch_pack_weights(const uint16_t *W, int N, int K, uint16_t *P, hipStream_t st);
+hipError_t launch_pack_weights(const uint16_t *W, int N, int K, uint16_t *P, hipStream_t st, bool interleave = false);
 
 // prefill helpers: pos[t] = t for t < n
 hipError_t launch_iota(int32_t *p, int n, hipStream_t st);

@@ -30,7 +30,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
-// fp32 -> bf16, round to nearest even; NaN stays NaN (quieted).
 // fp32 -> bf16, round to nearest even, NaN quieted: gfx950's v_cvt_pk_bf16_f32
 // (bit-identical, over all 2^32 inputs, to adding 0x7fff + lsb and truncating,
 // with (u >> 16) | 0x40 for NaN)
@@ -41,6 +40,18 @@ __device__ __forceinline__ uint32_t f2bf2(float a, float b)
     typedef float f32x2_t __attribute__((ext_vector_type(2)));
     typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
+
+// SwiGLU of one feature from its fp32 gate and up sums: both rounded to
+// bf16 (the projection's output precision), silu(g) u rounded to bf16.  The
+// SwiGLU kernel and the gate/up projection's fused epilogue share it, so the
+// two paths agree bit for bit.
+__device__ __forceinline__ uint16_t swiglu_bf16(float gs, float us)
+{
+    const float g = bf2f(f2bf(gs));
+    const float u = bf2f(f2bf(us));
+    const float silu = g / (1.0f + __expf(-g));
+    return f2bf(silu * u);
 }
 
 // Fixed butterfly over the 64 lanes, then lane 0's value to every lane.
@@ -607,11 +618,11 @@ __device__ __forceinline__ int dma_swz(int r, int c)
     else return r * 8 + (c ^ ((r >> 1) & 7));
 }
 
-template <int BM, int BN, int BK, int NST, int WGM, int NW = 4, bool PKW = false>
+template <int BM, int BN, int BK, int NST, int WGM, int NW = 4, bool PKW = false, bool SWIGLU = false>
 __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict__ A, int lda,
                                                   const uint16_t *__restrict__ W, int M, int N, int K, int Kc,
                                                   float *__restrict__ out, long long split_stride, int ldo,
-                                                  ArgBest *__restrict__ amax)
+                                                  ArgBest *__restrict__ amax, uint16_t *__restrict__ act)
 {
     constexpr int C = BK / 8;                         // 16-byte chunks per row
     constexpr int NT = 64 * NW;                       // threads
@@ -624,6 +635,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
     constexpr int STAGE = (BM + BN) * C;             // 16-byte units
     static_assert(P * OPS <= 63, "vmcnt range");
     static_assert(!PKW || (BN == 128 && BK == 64), "packed weights come in 128 x 64 tiles");
+    static_assert(!SWIGLU || (PKW && NW == 2 && WGM == 1), "SwiGLU pairs the two wavefronts' 64 columns");
     __shared__ __attribute__((aligned(16))) uint4 ring[NST * STAGE];
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -744,6 +756,40 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
     if (i < nk) step(i, f0, f1);
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));   // nothing may land in LDS after the workgroup ends
 
+    if constexpr (SWIGLU) {
+        // Tile nt of the interleaved copy: wavefront 0 holds gate features
+        // 64 nt .. 64 nt + 63, wavefront 1 the matching up features.  Up goes
+        // through the idle ring; wavefront 0 writes act[row][64 nt + j].
+        constexpr int TP = 68;
+        static_assert(BM * TP * 4 <= NST * STAGE * 16, "SwiGLU staging fits the ring");
+        float *T = reinterpret_cast<float *>(ring);
+        __syncthreads();                              // every wavefront is done reading the ring
+        if (wave == 1)
+#pragma unroll
+            for (int a = 0; a < FM; ++a)
+#pragma unroll
+                for (int b = 0; b < FN; ++b)
+#pragma unroll
+                    for (int q = 0; q < 16; ++q)
+                        T[(32 * a + 8 * (q >> 2) + 4 * h + (q & 3)) * TP + 32 * b + r32] = acc[a][b][q];
+        __syncthreads();
+        if (wave == 0) {
+            const int F = N / 2;
+#pragma unroll
+            for (int a = 0; a < FM; ++a)
+#pragma unroll
+                for (int b = 0; b < FN; ++b) {
+                    const int j = nt * 64 + 32 * b + r32;
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) {
+                        const int rl = 32 * a + 8 * (q >> 2) + 4 * h + (q & 3), row = m0 + rl;
+                        if (row < M && j < F) act[(size_t)row * ldo + j] = swiglu_bf16(0.f + acc[a][b][q], 0.f + T[rl * TP + 32 * b + r32]);
+                    }
+                }
+        }
+        return;
+    }
+
     // lane holds, per 32x32 tile, column r32 and rows 8 (q / 4) + 4 h + q % 4
     float *o = out + (size_t)s * split_stride;
 #pragma unroll
@@ -798,7 +844,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
 }
 
 hipError_t launch_gemm_dma(const uint16_t *A, int lda, const uint16_t *W, const GemmShape &g, float *out,
-                           long long split_stride, int ldo, hipStream_t st, ArgBest *amax)
+                           long long split_stride, int ldo, hipStream_t st, ArgBest *amax, uint16_t *act)
 {
     // 32 or 64 x 128 (small batches): two wavefronts side by side (32- or
     // 64-row, 64-column wavefront tiles); 128-column tiles: four wavefronts
@@ -812,31 +858,43 @@ hipError_t launch_gemm_dma(const uint16_t *A, int lda, const uint16_t *W, const 
     const int num_m = (g.M + g.bm - 1) / g.bm;
     dim3 grid(num_m * num_n, g.S);
     if (g.pk) {   // tile-packed weights: the small-M configurations only
+        if (act != nullptr) {   // gate/up-interleaved copy, SwiGLU epilogue, no split-K
+            if (g.S != 1 || g.N % 128 != 0) return hipErrorInvalidValue;
+            if (g.bm == 32 && g.bn == 128)
+                hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, true, true>), grid, dim3(128), 0, st, A, lda, W,
+                                   g.M, g.N, g.K, g.Kc, nullptr, 0, ldo, nullptr, act);
+            else if (g.bm == 64 && g.bn == 128)
+                hipLaunchKernelGGL((k_gemm_dma<64, 128, 64, 4, 1, 2, true, true>), grid, dim3(128), 0, st, A, lda, W,
+                                   g.M, g.N, g.K, g.Kc, nullptr, 0, ldo, nullptr, act);
+            else
+                return hipErrorInvalidValue;
+            return hipGetLastError();
+        }
         if (g.bm == 32 && g.bn == 128)
             hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, true>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N,
-                               g.K, g.Kc, out, split_stride, ldo, amax);
+                               g.K, g.Kc, out, split_stride, ldo, amax, nullptr);
         else if (g.bm == 64 && g.bn == 128)
             hipLaunchKernelGGL((k_gemm_dma<64, 128, 64, 4, 1, 2, true>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N,
-                               g.K, g.Kc, out, split_stride, ldo, amax);
+                               g.K, g.Kc, out, split_stride, ldo, amax, nullptr);
         else
             return hipErrorInvalidValue;
         return hipGetLastError();
     }
     if (g.bm == 32 && g.bn == 128)
         hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
-                           out, split_stride, ldo, amax);
+                           out, split_stride, ldo, amax, nullptr);
     else if (g.bm == 64 && g.bn == 128)
         hipLaunchKernelGGL((k_gemm_dma<64, 128, 64, 4, 1, 2>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
-                           out, split_stride, ldo, amax);
+                           out, split_stride, ldo, amax, nullptr);
     else if (g.bm == 128 && g.bn == 128)
         hipLaunchKernelGGL((k_gemm_dma<128, 128, 64, 4, 2, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
-                           out, split_stride, ldo, amax);
+                           out, split_stride, ldo, amax, nullptr);
     else if (g.bm == 256 && g.bn == 128)
         hipLaunchKernelGGL((k_gemm_dma<256, 128, 64, 3, 2, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
-                           out, split_stride, ldo, amax);
+                           out, split_stride, ldo, amax, nullptr);
     else if (g.bm == 256 && g.bn == 256)
         hipLaunchKernelGGL((k_gemm_dma<256, 256, 32, 4, 2, 8>), grid, dim3(512), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
-                           out, split_stride, ldo, amax);
+                           out, split_stride, ldo, amax, nullptr);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
@@ -1405,10 +1463,7 @@ __global__ void k_swiglu(const float *__restrict__ part, int S, long long part_s
         gs += p[s * part_stride + j];
         us += p[s * part_stride + F + j];
     }
-    const float g = bf2f(f2bf(gs));
-    const float u = bf2f(f2bf(us));
-    const float silu = g / (1.0f + __expf(-g));
-    a[(size_t)r * lda + j] = f2bf(silu * u);
+    a[(size_t)r * lda + j] = swiglu_bf16(gs, us);
 }
 
 hipError_t launch_swiglu(const float *part, int S, long long part_stride, int rows, int F, uint16_t *a, int lda,
@@ -1579,15 +1634,17 @@ hipError_t launch_fill_u32(uint32_t *p, long long n_words, uint32_t v, hipStream
 // W[nt * 128 + r][kb * 64 + c], zero for rows past N.  One thread per
 // 16 bytes of P.
 __global__ void k_pack_weights(const uint16_t *__restrict__ W, int N, int K, uint16_t *__restrict__ P,
-                               long long units)
+                               long long units, int half)
 {
     const int kt = K / 64;
     for (long long u = (long long)blockIdx.x * blockDim.x + threadIdx.x; u < units;
          u += (long long)gridDim.x * blockDim.x) {
         const int c8 = (int)(u & 7), r = (int)((u >> 3) & 127);
-        const long long tile = u >> 10;
+        const long long tile = u >> 10, nt = tile / kt;
         const int kb = (int)(tile % kt);
-        const long long row = tile / kt * 128 + r;
+        // interleaved: rows 0..63 of tile nt are rows 64 nt.. of the first
+        // half, rows 64..127 the same rows of the second half
+        const long long row = half > 0 ? (r < 64 ? 0 : half) + nt * 64 + (r & 63) : nt * 128 + r;
         uint4 v = make_uint4(0, 0, 0, 0);
         if (row < N) v = *reinterpret_cast<const uint4 *>(W + row * K + kb * 64 + 8 * c8);
         reinterpret_cast<uint4 *>(P)[u] = v;
@@ -1596,13 +1653,14 @@ __global__ void k_pack_weights(const uint16_t *__restrict__ W, int N, int K, uin
 
 size_t packed_weight_elems(int N, int K) { return (size_t)(N + 127) / 128 * 128 * K; }
 
-hipError_t launch_pack_weights(const uint16_t *W, int N, int K, uint16_t *P, hipStream_t st)
+hipError_t launch_pack_weights(const uint16_t *W, int N, int K, uint16_t *P, hipStream_t st, bool interleave)
 {
-    if (N <= 0 || K <= 0 || K % 64 != 0) return hipErrorInvalidValue;
+    if (N <= 0 || K <= 0 || K % 64 != 0 || (interleave && N % 128 != 0)) return hipErrorInvalidValue;
     const long long units = (long long)packed_weight_elems(N, K) / 8;
     long long blocks = (units + 255) / 256;
     if (blocks > 65536) blocks = 65536;
-    hipLaunchKernelGGL(k_pack_weights, dim3((unsigned)blocks), dim3(256), 0, st, W, N, K, P, units);
+    hipLaunchKernelGGL(k_pack_weights, dim3((unsigned)blocks), dim3(256), 0, st, W, N, K, P, units,
+                       interleave ? N / 2 : 0);
     return hipGetLastError();
 }
 
