@@ -162,27 +162,26 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float *__restrict__ x, const f
     float *xr = x + (size_t)row * H;
     const float *pr = part + (size_t)row * H;
     float4 v[NG];
+    ushort4 gg[NG];
     float ss = 0.f;
 #pragma unroll
     for (int j = 0; j < NG; ++j) {
         const int i = 4 * (threadIdx.x + nth * j);
         if (i < H) {
+            gg[j] = *(const ushort4 *)(g + i);        // needed after the reduction; loaded with the rest
             v[j] = *(const float4 *)(xr + i);
             // partials are added in split order; their loads are issued in
-            // batches of 8 ahead of the adds
-            int s = 0;
-            for (; s + 8 <= S; s += 8) {
+            // batches of up to 8 ahead of the adds
+            for (int s = 0; s < S; s += 8) {
                 float4 p[8];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) p[u] = *(const float4 *)(pr + (s + u) * part_stride + i);
+                for (int u = 0; u < 8; ++u)
+                    if (s + u < S) p[u] = *(const float4 *)(pr + (s + u) * part_stride + i);
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    v[j].x += p[u].x; v[j].y += p[u].y; v[j].z += p[u].z; v[j].w += p[u].w;
-                }
-            }
-            for (; s < S; ++s) {
-                const float4 p = *(const float4 *)(pr + s * part_stride + i);
-                v[j].x += p.x; v[j].y += p.y; v[j].z += p.z; v[j].w += p.w;
+                for (int u = 0; u < 8; ++u)
+                    if (s + u < S) {
+                        v[j].x += p[u].x; v[j].y += p[u].y; v[j].z += p[u].z; v[j].w += p[u].w;
+                    }
             }
             if (mf.y != nullptr && (mf.valid == nullptr || mf.valid[row])) {
                 // mixture-of-experts combine: sum_r w_r y_r in rank order, then added
@@ -208,12 +207,11 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float *__restrict__ x, const f
     for (int j = 0; j < NG; ++j) {
         const int i = 4 * (threadIdx.x + nth * j);
         if (i < H) {
-            const ushort4 gg = *(const ushort4 *)(g + i);
             ushort4 o;
-            o.x = f2bf(v[j].x * rstd * bf2f(gg.x));
-            o.y = f2bf(v[j].y * rstd * bf2f(gg.y));
-            o.z = f2bf(v[j].z * rstd * bf2f(gg.z));
-            o.w = f2bf(v[j].w * rstd * bf2f(gg.w));
+            o.x = f2bf(v[j].x * rstd * bf2f(gg[j].x));
+            o.y = f2bf(v[j].y * rstd * bf2f(gg[j].y));
+            o.z = f2bf(v[j].z * rstd * bf2f(gg[j].z));
+            o.w = f2bf(v[j].w * rstd * bf2f(gg[j].w));
             *(ushort4 *)(hr + i) = o;
         }
     }
@@ -971,16 +969,30 @@ __global__ void k_qkv_post(const float *__restrict__ part, int S, long long part
     const int p = pos[r];
     const int ncols = (nq + 2 * nkv) * d;
     const int c0 = hd * d + i, c1 = c0 + half;
+    const bool rot = hd < nq + nkv;
+    float2 cs = {1.f, 0.f};
+    if (rot) cs = rope_tab[(size_t)p * half + i];    // issued with the partial loads
+    // partials in split order, loads issued in batches of up to 8
     float x0 = 0.f, x1 = 0.f;
-    for (int s = 0; s < S; ++s) {
-        const float *ps = part + s * part_stride + (size_t)r * ncols;
-        x0 += ps[c0];
-        x1 += ps[c1];
+    const float *pb = part + (size_t)r * ncols;
+    for (int s = 0; s < S; s += 8) {
+        float a0[8], a1[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (s + u < S) {
+                a0[u] = pb[(s + u) * part_stride + c0];
+                a1[u] = pb[(s + u) * part_stride + c1];
+            }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (s + u < S) {
+                x0 += a0[u];
+                x1 += a1[u];
+            }
     }
     x0 = bf2f(f2bf(x0));
     x1 = bf2f(f2bf(x1));
-    if (hd < nq + nkv) {
-        const float2 cs = rope_tab[(size_t)p * half + i];
+    if (rot) {
         const float y0 = x0 * cs.x - x1 * cs.y;
         const float y1 = x1 * cs.x + x0 * cs.y;
         x0 = y0;
@@ -1313,7 +1325,8 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
 // the exact maximum M over the splits, weights f_s = exp(m_s - M) and
 // L = sum_s l_s f_s walked in split order by one thread; then each thread
 // folds its E output elements over the splits in split order, eight splits'
-// loads issued ahead of the adds, and writes A / L in bf16.
+// loads issued ahead of the adds (the first eight with the maxima), and
+// writes A / L in bf16.
 template <int D, int G>
 __global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ ws, const uint8_t *__restrict__ valid,
                                                     const int32_t *__restrict__ pos, int nq, int nkv, int chunk,
@@ -1332,6 +1345,16 @@ __global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ ws
     float *fm = fs, *fl = fs + G * max_splits, *Mg = fl + G * max_splits, *Lg = Mg + G;
     const int stride = G * (D + 2);
     const float *base = ws + ((size_t)r * nkv + kvh) * max_splits * stride;
+    const float *a = base + 2 * G;
+    // the first eight splits' values load with the maxima and sums
+    float v[8][E];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int idx = tid + 256 * e;
+            v[u][e] = idx < G * D && u < ns ? a[(size_t)u * stride + idx] : 0.f;
+        }
     for (int idx = tid; idx < G * ns; idx += 256) {
         const int g = idx / ns, sp = idx - g * ns;
         fm[idx] = base[(size_t)sp * stride + g];
@@ -1355,31 +1378,23 @@ __global__ __launch_bounds__(256) void k_attn_merge(const float *__restrict__ ws
     float acc[E];
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.f;
-    const float *a = base + 2 * G;
-    int sp = 0;
-    for (; sp + 8 <= ns; sp += 8) {
-        float v[8][E];
+    for (int sp = 0; sp < ns; sp += 8) {
+        if (sp > 0)
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const int idx = tid + 256 * e;
+                    v[u][e] = idx < G * D && sp + u < ns ? a[(size_t)(sp + u) * stride + idx] : 0.f;
+                }
 #pragma unroll
         for (int u = 0; u < 8; ++u)
 #pragma unroll
             for (int e = 0; e < E; ++e) {
                 const int idx = tid + 256 * e;
-                v[u][e] = idx < G * D ? a[(size_t)(sp + u) * stride + idx] : 0.f;
-            }
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const int idx = tid + 256 * e;
-                if (idx < G * D) acc[e] += v[u][e] * fm[(idx / D) * ns + sp + u];
+                if (idx < G * D && sp + u < ns) acc[e] += v[u][e] * fm[(idx / D) * ns + sp + u];
             }
     }
-    for (; sp < ns; ++sp)
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            const int idx = tid + 256 * e;
-            if (idx < G * D) acc[e] += a[(size_t)sp * stride + idx] * fm[(idx / D) * ns + sp];
-        }
 #pragma unroll
     for (int e = 0; e < E; ++e) {
         const int idx = tid + 256 * e;
@@ -1458,10 +1473,22 @@ __global__ void k_swiglu(const float *__restrict__ part, int S, long long part_s
     const int j = (blockIdx.x % nb) * 256 + threadIdx.x;
     if (j >= F) return;
     const float *p = part + (size_t)r * 2 * F;
+    // partials in split order, loads issued in batches of up to 8
     float gs = 0.f, us = 0.f;
-    for (int s = 0; s < S; ++s) {
-        gs += p[s * part_stride + j];
-        us += p[s * part_stride + F + j];
+    for (int s = 0; s < S; s += 8) {
+        float a0[8], a1[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (s + u < S) {
+                a0[u] = p[(s + u) * part_stride + j];
+                a1[u] = p[(s + u) * part_stride + F + j];
+            }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (s + u < S) {
+                gs += a0[u];
+                us += a1[u];
+            }
     }
     a[(size_t)r * lda + j] = swiglu_bf16(gs, us);
 }
