@@ -1737,9 +1737,17 @@ __global__ __launch_bounds__(64) void k_moe_route(const float *__restrict__ part
     for (int j = 0; j < EPL; ++j) {
         const int e = lane + 64 * j;
         float v = -INFINITY;
-        if (e < E) {
+        if (e < E) {   // partials in split order, loads issued in batches of up to 8
             v = 0.f;
-            for (int s = 0; s < S; ++s) v += part[s * part_stride + (size_t)b * E + e];
+            for (int s = 0; s < S; s += 8) {
+                float p8[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (s + u < S) p8[u] = part[(s + u) * part_stride + (size_t)b * E + e];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (s + u < S) v += p8[u];
+            }
         }
         l[j] = v;
     }
@@ -1786,55 +1794,77 @@ hipError_t launch_moe_route(const float *part, int S, long long part_stride, int
 }
 
 // tiles[slot] = {expert, first list index, count}; count 0 = unused slot.
+// Dispatch: counts per expert (integer LDS atomics: order-independent), an
+// exclusive scan over experts for list and tile offsets, tiles written by
+// their expert's thread, then assignments ranked 1024 at a time: each
+// expert's assignments of the chunk set their bit in the expert's 1024-bit
+// mask, and an assignment's rank among its expert's is the popcount below
+// its bit plus what earlier chunks placed.  Every output is a function of
+// sel alone.
 __global__ __launch_bounds__(1024) void k_moe_dispatch(const int32_t *__restrict__ sel, int n_assign, int E,
                                                        int n_slots, int32_t *__restrict__ list,
                                                        int32_t *__restrict__ tiles)
 {
-    __shared__ int cnt[256], base[256], csel[1024];
+    __shared__ int cnt[256], base[256], toff[257], scan_v[256], scan_w[256];
+    __shared__ uint32_t mask[256 * 32];
     const int tid = threadIdx.x;
-    for (int e = tid; e < E; e += 1024) cnt[e] = 0;
+    if (tid < 256) cnt[tid] = 0;
     __syncthreads();
-    // per-expert totals (integer counts: order-independent)
     for (int a = tid; a < n_assign; a += 1024) {
         const int e = sel[a];
         if (e >= 0) atomicAdd(&cnt[e], 1);
     }
     __syncthreads();
-    if (tid == 0) {
-        int off = 0, slot = 0;
-        for (int e = 0; e < E; ++e) {
-            base[e] = off;
-            for (int j = 0; j * 16 < cnt[e]; ++j, ++slot) {
-                tiles[3 * slot + 0] = e;
-                tiles[3 * slot + 1] = off + 16 * j;
-                tiles[3 * slot + 2] = min(16, cnt[e] - 16 * j);
-            }
-            off += cnt[e];
+    // exclusive scans of counts and tile counts over the experts (Hillis-Steele)
+    const int c = tid < E ? cnt[tid] : 0, nt = (c + 15) / 16;
+    int v = c, w = nt;
+    for (int off = 1; off < 256; off <<= 1) {
+        if (tid < 256) {
+            scan_v[tid] = v;
+            scan_w[tid] = w;
         }
-        for (; slot < n_slots; ++slot) {
-            tiles[3 * slot + 0] = 0;
-            tiles[3 * slot + 1] = 0;
-            tiles[3 * slot + 2] = 0;
+        __syncthreads();
+        if (tid < 256 && tid >= off) {
+            v += scan_v[tid - off];
+            w += scan_w[tid - off];
         }
+        __syncthreads();
+    }
+    if (tid < 256) {
+        base[tid] = v - c;
+        toff[tid] = w - nt;
+        if (tid == 255) toff[256] = w;
     }
     __syncthreads();
-    // placement in increasing assignment order, one 1024-assignment chunk at a time
+    if (tid < E)
+        for (int j = 0; j < nt; ++j) {
+            const int slot = toff[tid] + j;
+            tiles[3 * slot + 0] = tid;
+            tiles[3 * slot + 1] = base[tid] + 16 * j;
+            tiles[3 * slot + 2] = min(16, c - 16 * j);
+        }
+    for (int slot = toff[256] + tid; slot < n_slots; slot += 1024) {
+        tiles[3 * slot + 0] = 0;
+        tiles[3 * slot + 1] = 0;
+        tiles[3 * slot + 2] = 0;
+    }
     for (int c0 = 0; c0 < n_assign; c0 += 1024) {
+        for (int i = tid; i < 256 * 32; i += 1024) mask[i] = 0u;
+        __syncthreads();
         const int a = c0 + tid;
         const int e = a < n_assign ? sel[a] : -1;
-        csel[tid] = e;
+        if (e >= 0) atomicOr(&mask[e * 32 + (tid >> 5)], 1u << (tid & 31));
         __syncthreads();
         if (e >= 0) {
-            int rank = 0;
-            for (int j = 0; j < tid; ++j) rank += (csel[j] == e);
+            int rank = __popc(mask[e * 32 + (tid >> 5)] & ((1u << (tid & 31)) - 1u));
+            for (int j = 0; j < (tid >> 5); ++j) rank += __popc(mask[e * 32 + j]);
             list[base[e] + rank] = a;
         }
         __syncthreads();
         if (tid < E) {   // advance each expert's base past this chunk's assignments
-            int c = 0;
-            const int n = min(1024, n_assign - c0);
-            for (int j = 0; j < n; ++j) c += (csel[j] == tid);
-            base[tid] += c;
+            int n = 0;
+            for (int j = 0; j < 32; ++j) n += __popc(mask[tid * 32 + j]);
+            base[tid] += n;
         }
         __syncthreads();
     }
