@@ -205,7 +205,7 @@ Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_
 
 namespace {
 // Projection weights, for the tile-packed copies the engine may hold.
-enum WeightId { W_QKV, W_O, W_GATE_UP, W_DOWN, W_ROUTER, W_LM_HEAD, W_COUNT };
+enum WeightId { W_QKV, W_O, W_GATE_UP, W_DOWN, W_ROUTER, W_LM_HEAD, W_EXP_GATE_UP, W_EXP_DOWN, W_COUNT };
 }  // namespace
 
 struct corun_engine {
@@ -226,6 +226,7 @@ struct corun_engine {
     char *pk_buf = nullptr;
     size_t pk_bytes = 0;
     bool gu_fused = false;   // the gate/up copy is interleaved for the fused SwiGLU epilogue
+    bool egu_fused = false;  // likewise for every expert's gate/up (mixture of experts)
     bool moe = false;
     // mixture-of-experts workspace (decode)
     float *p_router = nullptr, *moe_w = nullptr, *moe_gu = nullptr, *moe_y = nullptr;
@@ -420,6 +421,8 @@ const uint16_t *row_major_weight(const corun_engine *e, int w, int l)
     case W_GATE_UP: return e->w_gu[l];
     case W_DOWN: return e->w_down[l];
     case W_ROUTER: return e->w_router[l];
+    case W_EXP_GATE_UP: return e->w_egu[l];
+    case W_EXP_DOWN: return e->w_edown[l];
     default: return e->lm_head;
     }
 }
@@ -477,21 +480,40 @@ corun_status moe_router(corun_engine *e, const MoeBufs &m, const uint16_t *h, in
     return CORUN_OK;
 }
 
+// Expert gate/up on the pipelined kernel (hidden is a multiple of 64), from
+// the packed copies when the engine holds them; with interleaved copies the
+// epilogue applies SwiGLU into m.act and no SwiGLU kernel runs.
 corun_status moe_expert_gate_up(corun_engine *e, const MoeBufs &m, const uint16_t *h, int l)
 {
     const corun_model_cfg &c = e->c;
     const int Fe = c.expert_ffn, H = c.hidden;
-    HIP_TRY(launch_moe_gemm(h, H, c.top_k, e->w_egu[l], (long long)2 * Fe * H, 2 * Fe, H, m.list, m.tiles, m.slots,
-                            m.gu, 2 * Fe, e->st));
+    const std::vector<const uint16_t *> &pk = e->packed[W_EXP_GATE_UP];
+    if (!pk.empty())
+        HIP_TRY(launch_moe_gemm_dma(h, H, c.top_k, pk[l], (long long)packed_weight_elems(2 * Fe, H), true, 2 * Fe, H,
+                                    m.list, m.tiles, m.slots, m.gu, e->egu_fused ? m.act : nullptr,
+                                    e->egu_fused ? Fe : 2 * Fe, e->st));
+    else
+        HIP_TRY(launch_moe_gemm_dma(h, H, c.top_k, e->w_egu[l], (long long)2 * Fe * H, false, 2 * Fe, H, m.list,
+                                    m.tiles, m.slots, m.gu, nullptr, 2 * Fe, e->st));
     return CORUN_OK;
 }
 
+// Expert down: the pipelined kernel when expert_ffn is a multiple of 64
+// (packed or row-major), else the register-streaming kernel.
 corun_status moe_expert_down(corun_engine *e, const MoeBufs &m, int l)
 {
     const corun_model_cfg &c = e->c;
     const int Fe = c.expert_ffn, H = c.hidden;
-    HIP_TRY(launch_moe_gemm(m.act, Fe, 1, e->w_edown[l], (long long)H * Fe, H, Fe, m.list, m.tiles, m.slots, m.y, H,
-                            e->st));
+    const std::vector<const uint16_t *> &pk = e->packed[W_EXP_DOWN];
+    if (!pk.empty())
+        HIP_TRY(launch_moe_gemm_dma(m.act, Fe, 1, pk[l], (long long)packed_weight_elems(H, Fe), true, H, Fe, m.list,
+                                    m.tiles, m.slots, m.y, nullptr, H, e->st));
+    else if (Fe % 64 == 0)
+        HIP_TRY(launch_moe_gemm_dma(m.act, Fe, 1, e->w_edown[l], (long long)H * Fe, false, H, Fe, m.list, m.tiles,
+                                    m.slots, m.y, nullptr, H, e->st));
+    else
+        HIP_TRY(launch_moe_gemm(m.act, Fe, 1, e->w_edown[l], (long long)H * Fe, H, Fe, m.list, m.tiles, m.slots, m.y,
+                                H, e->st));
     return CORUN_OK;
 }
 
@@ -562,7 +584,7 @@ corun_status launch_one(corun_engine *e, int which, int l)
     case CORUN_K_SWIGLU:   // nothing to launch when the gate/up projection's epilogue does it
         if (e->moe) {
             const int Fe = c.expert_ffn;
-            HIP_TRY(launch_swiglu(e->moe_gu, 1, 0, B * c.top_k, Fe, e->moe_act, Fe, st));
+            if (!e->egu_fused) HIP_TRY(launch_swiglu(e->moe_gu, 1, 0, B * c.top_k, Fe, e->moe_act, Fe, st));
         } else if (!gu_fuses(e, p.gu)) {
             HIP_TRY(launch_swiglu(e->p_gu, p.gu.S, (long long)B * 2 * F, B, F, e->a, F, st));
         }
@@ -742,7 +764,14 @@ static corun_status pack_weights(corun_engine *e)
                           {W_DOWN, &p.down, e->moe ? 0 : L},
                           {W_ROUTER, &p.router, e->moe ? L : 0},
                           {W_LM_HEAD, &p.lm, 1}};
-    size_t total = 0;   // each copy is a whole number of 16 KB tiles
+    // experts (any B: an expert tile holds at most 16 assignments): gate/up
+    // always (K = hidden), down when expert_ffn is a multiple of 64
+    const corun_model_cfg &c = e->c;
+    const int E = c.n_experts, Fe = c.expert_ffn, H = c.hidden;
+    const bool pk_egu = e->moe, pk_edown = e->moe && Fe % 64 == 0;
+    const size_t egu_elems = pk_egu ? (size_t)E * packed_weight_elems(2 * Fe, H) : 0;
+    const size_t edown_elems = pk_edown ? (size_t)E * packed_weight_elems(H, Fe) : 0;
+    size_t total = (size_t)L * (egu_elems + edown_elems) * 2;   // each copy is a whole number of 16 KB tiles
     for (const Item &it : items)
         if (it.count && takes_packed(*it.pr)) total += (size_t)it.count * packed_weight_elems(it.pr->N, it.pr->K) * 2;
     if (total == 0) return CORUN_OK;
@@ -767,6 +796,25 @@ static corun_status pack_weights(corun_engine *e)
         }
     }
     e->gu_fused = interleave;
+    // expert stacks, expert by expert; gate/up interleaved when its halves
+    // split into 64-row tiles
+    const bool e_interleave = Fe % 64 == 0;
+    for (int l = 0; pk_egu && l < L; ++l) {
+        for (int x = 0; x < E; ++x)
+            HIP_TRY(launch_pack_weights(e->w_egu[l] + (size_t)x * 2 * Fe * H, 2 * Fe, H,
+                                        (uint16_t *)q + (size_t)x * packed_weight_elems(2 * Fe, H), e->st,
+                                        e_interleave));
+        e->packed[W_EXP_GATE_UP].push_back((const uint16_t *)q);
+        q += egu_elems * 2;
+    }
+    for (int l = 0; pk_edown && l < L; ++l) {
+        for (int x = 0; x < E; ++x)
+            HIP_TRY(launch_pack_weights(e->w_edown[l] + (size_t)x * H * Fe, H, Fe,
+                                        (uint16_t *)q + (size_t)x * packed_weight_elems(H, Fe), e->st));
+        e->packed[W_EXP_DOWN].push_back((const uint16_t *)q);
+        q += edown_elems * 2;
+    }
+    e->egu_fused = pk_egu && e_interleave;
     return CORUN_OK;
 }
 
@@ -1064,7 +1112,7 @@ extern "C" corun_status corun_prefill_chunk(corun_engine *e, const int32_t *toke
             const int Fe = c.expert_ffn;
             ST_TRY(moe_router(e, pmb, e->pf_h, Lp, pr, l));
             ST_TRY(moe_expert_gate_up(e, pmb, e->pf_h, l));
-            HIP_TRY(launch_swiglu(e->pf_moe_gu, 1, 0, Lp * c.top_k, Fe, e->pf_moe_act, Fe, st));
+            if (!e->egu_fused) HIP_TRY(launch_swiglu(e->pf_moe_gu, 1, 0, Lp * c.top_k, Fe, e->pf_moe_act, Fe, st));
             ST_TRY(moe_expert_down(e, pmb, l));
         } else {
             if (gu_fuses(e, pg)) {
@@ -1197,7 +1245,7 @@ extern "C" corun_status corun_prefill_batch(corun_engine *e, const int32_t *toke
             const int Fe = c.expert_ffn;
             ST_TRY(moe_router(e, pmb, e->pf_h, Lp, pr, l));
             ST_TRY(moe_expert_gate_up(e, pmb, e->pf_h, l));
-            HIP_TRY(launch_swiglu(e->pf_moe_gu, 1, 0, Lp * c.top_k, Fe, e->pf_moe_act, Fe, st));
+            if (!e->egu_fused) HIP_TRY(launch_swiglu(e->pf_moe_gu, 1, 0, Lp * c.top_k, Fe, e->pf_moe_act, Fe, st));
             ST_TRY(moe_expert_down(e, pmb, l));
         } else {
             if (gu_fuses(e, pg)) {

@@ -42,6 +42,14 @@ hipError_t launch_moe_dispatch(const int32_t *sel, int n_assign, int E, int n_sl
 hipError_t launch_moe_gemm(const uint16_t *A, int lda, int row_div, const uint16_t *W, long long w_expert_stride, int N,
                            int K, const int32_t *list, const int32_t *tiles, int n_slots, float *out, int ldo,
                            hipStream_t st);
+// The same product on the pipelined kernel (K % 64 == 0): one 32 x 128 tile
+// per (128 columns, tile slot), weights row-major per expert or tile-packed
+// per expert (packed; w_expert_stride in elements of the packed copy).
+// With act (packed gate/up-interleaved copies, N % 128 == 0) the epilogue
+// writes act[a][j] = SwiGLU of feature j (bf16, ld ldo) instead of out.
+hipError_t launch_moe_gemm_dma(const uint16_t *A, int lda, int row_div, const uint16_t *W, long long w_expert_stride,
+                               bool packed, int N, int K, const int32_t *list, const int32_t *tiles, int n_slots,
+                               float *out, uint16_t *act, int ldo, hipStream_t st);
 
 // Projection partials: out[s][m][n] = sum_{k in chunk s} A[m][k] W[n][k]
 // for m < M_store (bf16 MFMA, fp32 accumulate).  A has lda columns and at
@@ -50,6 +58,16 @@ hipError_t launch_moe_gemm(const uint16_t *A, int lda, int row_div, const uint16
 struct ArgBest {
     float v;
     int i;
+};
+
+// Expert tiles of a mixture-of-experts projection (launch_moe_dispatch):
+// slot s holds tiles[3 s + 2] assignments list[tiles[3 s + 1] ..] of expert
+// tiles[3 s]; an assignment's A row is assignment / row_div; expert e's
+// weight starts at W + e w_stride.
+struct ExpertTiles {
+    const int32_t *list = nullptr, *tiles = nullptr;
+    int row_div = 1;
+    long long w_stride = 0;
 };
 
 struct GemmShape {

@@ -616,11 +616,13 @@ __device__ __forceinline__ int dma_swz(int r, int c)
     else return r * 8 + (c ^ ((r >> 1) & 7));
 }
 
-template <int BM, int BN, int BK, int NST, int WGM, int NW = 4, bool PKW = false, bool SWIGLU = false>
+template <int BM, int BN, int BK, int NST, int WGM, int NW = 4, bool PKW = false, bool SWIGLU = false,
+          bool MOE = false>
 __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict__ A, int lda,
                                                   const uint16_t *__restrict__ W, int M, int N, int K, int Kc,
                                                   float *__restrict__ out, long long split_stride, int ldo,
-                                                  ArgBest *__restrict__ amax, uint16_t *__restrict__ act)
+                                                  ArgBest *__restrict__ amax, uint16_t *__restrict__ act,
+                                                  ExpertTiles et)
 {
     constexpr int C = BK / 8;                         // 16-byte chunks per row
     constexpr int NT = 64 * NW;                       // threads
@@ -634,12 +636,24 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
     static_assert(P * OPS <= 63, "vmcnt range");
     static_assert(!PKW || (BN == 128 && BK == 64), "packed weights come in 128 x 64 tiles");
     static_assert(!SWIGLU || (PKW && NW == 2 && WGM == 1), "SwiGLU pairs the two wavefronts' 64 columns");
+    static_assert(!MOE || BM >= 16, "an expert tile holds up to 16 assignments");
     __shared__ __attribute__((aligned(16))) uint4 ring[NST * STAGE];
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int num_m = (M + BM - 1) / BM, num_n = (N + BN - 1) / BN;
     int t = blockIdx.x, mt, nt;
-    if (num_m == 1) {
+    // expert tiles: grid.y walks the tile slots; rows are the slot's
+    // assignments, A row = assignment / row_div, output row = assignment
+    int row_end = M, slot_start = 0;
+    if constexpr (MOE) {
+        const int sl = blockIdx.y;
+        row_end = et.tiles[3 * sl + 2];
+        if (row_end == 0) return;                    // an unused slot (uniform over the workgroup)
+        slot_start = et.tiles[3 * sl + 1];
+        W += (size_t)et.tiles[3 * sl] * et.w_stride;
+        mt = 0;
+        nt = t;
+    } else if (num_m == 1) {
         mt = 0;
         nt = t;
     } else {
@@ -655,9 +669,13 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
         nt = in / gs;
     }
     const int m0 = mt * BM, n0 = nt * BN;
-    const int s = blockIdx.y;
+    const int s = MOE ? 0 : blockIdx.y;
     const int kbeg = s * Kc, kend = min(K, kbeg + Kc);
     const int nk = kend > kbeg ? (kend - kbeg) / BK : 0;
+    auto out_row = [&](int row) -> size_t {
+        if constexpr (MOE) return (size_t)et.list[slot_start + row];
+        else return (size_t)row;
+    };
 
     // per load op j: source row and logical chunk of this thread's 16 bytes
     const uint16_t *asrc[A_OPS];
@@ -665,7 +683,10 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
 #pragma unroll
     for (int j = 0; j < A_OPS; ++j) {
         const int g = j * NT + tid, r = g / C, c = dma_swz<C>(r, g % C) - r * C;   // the swizzle is an involution
-        asrc[j] = A + (size_t)min(m0 + r, M - 1) * lda + kbeg + 8 * c;
+        size_t arow;
+        if constexpr (MOE) arow = (size_t)(et.list[slot_start + min(r, row_end - 1)] / et.row_div);
+        else arow = (size_t)min(m0 + r, M - 1);
+        asrc[j] = A + arow * lda + kbeg + 8 * c;
     }
 #pragma unroll
     for (int j = 0; j < W_OPS; ++j) {
@@ -781,7 +802,8 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
 #pragma unroll
                     for (int q = 0; q < 16; ++q) {
                         const int rl = 32 * a + 8 * (q >> 2) + 4 * h + (q & 3), row = m0 + rl;
-                        if (row < M && j < F) act[(size_t)row * ldo + j] = swiglu_bf16(0.f + acc[a][b][q], 0.f + T[rl * TP + 32 * b + r32]);
+                        if (row < row_end && j < F)
+                            act[out_row(row) * ldo + j] = swiglu_bf16(0.f + acc[a][b][q], 0.f + T[rl * TP + 32 * b + r32]);
                     }
                 }
         }
@@ -799,7 +821,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
 #pragma unroll
             for (int q = 0; q < 16; ++q) {
                 const int row = m0 + wm0 + 32 * a + 8 * (q >> 2) + 4 * h + (q & 3);
-                if (row < M) o[(size_t)row * ldo + col] = acc[a][b][q];
+                if (row < row_end) o[out_row(row) * ldo + col] = acc[a][b][q];
             }
         }
     // every configuration the launcher uses has 64-column wavefront tiles
@@ -860,39 +882,39 @@ hipError_t launch_gemm_dma(const uint16_t *A, int lda, const uint16_t *W, const 
             if (g.S != 1 || g.N % 128 != 0) return hipErrorInvalidValue;
             if (g.bm == 32 && g.bn == 128)
                 hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, true, true>), grid, dim3(128), 0, st, A, lda, W,
-                                   g.M, g.N, g.K, g.Kc, nullptr, 0, ldo, nullptr, act);
+                                   g.M, g.N, g.K, g.Kc, nullptr, 0, ldo, nullptr, act, ExpertTiles{});
             else if (g.bm == 64 && g.bn == 128)
                 hipLaunchKernelGGL((k_gemm_dma<64, 128, 64, 4, 1, 2, true, true>), grid, dim3(128), 0, st, A, lda, W,
-                                   g.M, g.N, g.K, g.Kc, nullptr, 0, ldo, nullptr, act);
+                                   g.M, g.N, g.K, g.Kc, nullptr, 0, ldo, nullptr, act, ExpertTiles{});
             else
                 return hipErrorInvalidValue;
             return hipGetLastError();
         }
         if (g.bm == 32 && g.bn == 128)
             hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, true>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N,
-                               g.K, g.Kc, out, split_stride, ldo, amax, nullptr);
+                               g.K, g.Kc, out, split_stride, ldo, amax, nullptr, ExpertTiles{});
         else if (g.bm == 64 && g.bn == 128)
             hipLaunchKernelGGL((k_gemm_dma<64, 128, 64, 4, 1, 2, true>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N,
-                               g.K, g.Kc, out, split_stride, ldo, amax, nullptr);
+                               g.K, g.Kc, out, split_stride, ldo, amax, nullptr, ExpertTiles{});
         else
             return hipErrorInvalidValue;
         return hipGetLastError();
     }
     if (g.bm == 32 && g.bn == 128)
         hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
-                           out, split_stride, ldo, amax, nullptr);
+                           out, split_stride, ldo, amax, nullptr, ExpertTiles{});
     else if (g.bm == 64 && g.bn == 128)
         hipLaunchKernelGGL((k_gemm_dma<64, 128, 64, 4, 1, 2>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
-                           out, split_stride, ldo, amax, nullptr);
+                           out, split_stride, ldo, amax, nullptr, ExpertTiles{});
     else if (g.bm == 128 && g.bn == 128)
         hipLaunchKernelGGL((k_gemm_dma<128, 128, 64, 4, 2, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
-                           out, split_stride, ldo, amax, nullptr);
+                           out, split_stride, ldo, amax, nullptr, ExpertTiles{});
     else if (g.bm == 256 && g.bn == 128)
         hipLaunchKernelGGL((k_gemm_dma<256, 128, 64, 3, 2, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
-                           out, split_stride, ldo, amax, nullptr);
+                           out, split_stride, ldo, amax, nullptr, ExpertTiles{});
     else if (g.bm == 256 && g.bn == 256)
         hipLaunchKernelGGL((k_gemm_dma<256, 256, 32, 4, 2, 8>), grid, dim3(512), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
-                           out, split_stride, ldo, amax, nullptr);
+                           out, split_stride, ldo, amax, nullptr, ExpertTiles{});
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
@@ -1967,6 +1989,25 @@ hipError_t launch_moe_gemm(const uint16_t *A, int lda, int row_div, const uint16
     const int ncb = (N + 16 * NT - 1) / (16 * NT);
     hipLaunchKernelGGL((k_moe_gemm<NT, 4>), dim3((ncb + 3) / 4, n_slots), dim3(256), 0, st, A, lda, row_div, W,
                        w_expert_stride, N, K, list, tiles, out, ldo);
+    return hipGetLastError();
+}
+
+hipError_t launch_moe_gemm_dma(const uint16_t *A, int lda, int row_div, const uint16_t *W, long long w_expert_stride,
+                               bool packed, int N, int K, const int32_t *list, const int32_t *tiles, int n_slots,
+                               float *out, uint16_t *act, int ldo, hipStream_t st)
+{
+    if (K % 64 != 0 || N <= 0 || (act != nullptr && (!packed || N % 128 != 0))) return hipErrorInvalidValue;
+    const ExpertTiles et{list, tiles, row_div, w_expert_stride};
+    const dim3 grid((N + 127) / 128, n_slots);
+    if (act != nullptr)
+        hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, true, true, true>), grid, dim3(128), 0, st, A, lda, W, 16,
+                           N, K, K, nullptr, 0, ldo, nullptr, act, et);
+    else if (packed)
+        hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, true, false, true>), grid, dim3(128), 0, st, A, lda, W,
+                           16, N, K, K, out, 0, ldo, nullptr, nullptr, et);
+    else
+        hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, false, false, true>), grid, dim3(128), 0, st, A, lda, W,
+                           16, N, K, K, out, 0, ldo, nullptr, nullptr, et);
     return hipGetLastError();
 }
 

@@ -48,6 +48,11 @@ CONFIGS = {
     "tiny_moe": dict(n_layers=2, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64, ffn=0,
                      vocab=1024, n_experts=16, top_k=4, expert_ffn=96, rms_eps=1e-6,
                      rope_theta=10000.0),
+    # small mixture-of-experts decoder whose expert width is a multiple of 64
+    # (the packed expert copies with the fused SwiGLU, as at full size)
+    "small_moe": dict(n_layers=2, hidden=512, n_heads=8, n_kv_heads=2, head_dim=128, ffn=0,
+                      vocab=1024, n_experts=16, top_k=4, expert_ffn=128, rms_eps=1e-6,
+                      rope_theta=1e6),
 }
 
 

@@ -5,8 +5,8 @@ batch-invariant kernels while decode keeps its fixed-shape kernels).
 * Every prompt of a batch gets k/v and last-position logits bit-identical
   to its own corun_prefill on the same engine, in another slot, whatever
   its batch-mates and their order: small128 (head_dim 128, the pipelined
-  projections), tiny (head_dim 64, a K tail) and the tiny mixture of
-  experts.
+  projections), tiny (head_dim 64, a K tail) and the two small mixtures
+  of experts.
 * Against the oracle (relative 2e-2 on the logits, greedy token unless a
   near tie).
 * Refusals: an engine without batch-invariant prefill, a slot given twice,
@@ -28,7 +28,7 @@ B = 10
 LENS = [1, 33, 200, 64, 17]
 
 
-@pytest.fixture(scope="module", params=["small128", "tiny", "tiny_moe"])
+@pytest.fixture(scope="module", params=["small128", "tiny", "tiny_moe", "small_moe"])
 def model(request):
     cfg = wl.config(request.param)
     Wc = wl.make_weights(cfg, seed=51)

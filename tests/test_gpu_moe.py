@@ -1,7 +1,10 @@
 """GPU tests of the mixture-of-experts layer (router, top-k routing,
 drop-free dispatch into fixed tile slots, grouped expert projections,
-rank-order combine) on a small MoE decoder: oracle parity and the
-position-invariance contract."""
+rank-order combine) on two small MoE decoders: oracle parity and the
+position-invariance contract.  tiny_moe (expert width 96) streams the
+expert down projection through the register kernel and applies SwiGLU in
+its own kernel; small_moe (width 128) runs both expert projections from
+tile-packed copies with SwiGLU in the gate/up epilogue."""
 import itertools
 
 import numpy as np
@@ -19,9 +22,9 @@ S_CAP = 160
 TOL = 2e-2
 
 
-@pytest.fixture(scope="module")
-def moe():
-    cfg = wl.config("tiny_moe")
+@pytest.fixture(scope="module", params=["tiny_moe", "small_moe"])
+def moe(request):
+    cfg = wl.config(request.param)
     Wc = wl.make_weights(cfg, seed=11)
     return cfg, Wc, to_device(Wc), host_model(Wc)
 

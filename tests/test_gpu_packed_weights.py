@@ -11,8 +11,10 @@ that reads the caller's row-major weights:
 * the packed copies exist: creating the engine takes the memory they need
   (small128).
 
-small128 (every K a multiple of 64), tiny (down K = 688 stays row-major)
-and the tiny mixture of experts (router, attention and lm_head packed)."""
+small128 (every K a multiple of 64), tiny (down K = 688 stays row-major),
+the tiny mixture of experts (router, attention, lm_head and expert gate/up
+packed) and small_moe (expert down packed too, SwiGLU fused into the expert
+gate/up)."""
 import numpy as np
 import pytest
 import torch
@@ -25,7 +27,7 @@ pytestmark = pytest.mark.gpu
 CAP = 256
 
 
-@pytest.fixture(scope="module", params=["small128", "tiny", "tiny_moe"])
+@pytest.fixture(scope="module", params=["small128", "tiny", "tiny_moe", "small_moe"])
 def model(request):
     cfg = wl.config(request.param)
     return cfg, to_device(wl.make_weights(cfg, seed=61))
