@@ -171,8 +171,12 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float *__restrict__ x, const f
             gg[j] = *(const ushort4 *)(g + i);        // needed after the reduction; loaded with the rest
             v[j] = *(const float4 *)(xr + i);
             // partials are added in split order; their loads are issued in
-            // batches of up to 8 ahead of the adds
-            for (int s = 0; s < S; s += 8) {
+            // batches of up to 8 ahead of the adds (one split without the
+            // predication)
+            if (S == 1) {
+                const float4 p = *(const float4 *)(pr + i);
+                v[j].x += p.x; v[j].y += p.y; v[j].z += p.z; v[j].w += p.w;
+            } else for (int s = 0; s < S; s += 8) {
                 float4 p[8];
 #pragma unroll
                 for (int u = 0; u < 8; ++u)
@@ -994,10 +998,14 @@ __global__ void k_qkv_post(const float *__restrict__ part, int S, long long part
     const bool rot = hd < nq + nkv;
     float2 cs = {1.f, 0.f};
     if (rot) cs = rope_tab[(size_t)p * half + i];    // issued with the partial loads
-    // partials in split order, loads issued in batches of up to 8
+    // partials in split order, loads issued in batches of up to 8 (one
+    // split without the predication)
     float x0 = 0.f, x1 = 0.f;
     const float *pb = part + (size_t)r * ncols;
-    for (int s = 0; s < S; s += 8) {
+    if (S == 1) {
+        x0 += pb[c0];
+        x1 += pb[c1];
+    } else for (int s = 0; s < S; s += 8) {
         float a0[8], a1[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
@@ -1495,9 +1503,13 @@ __global__ void k_swiglu(const float *__restrict__ part, int S, long long part_s
     const int j = (blockIdx.x % nb) * 256 + threadIdx.x;
     if (j >= F) return;
     const float *p = part + (size_t)r * 2 * F;
-    // partials in split order, loads issued in batches of up to 8
+    // partials in split order, loads issued in batches of up to 8 (one
+    // split, the usual prefill case, without the predication)
     float gs = 0.f, us = 0.f;
-    for (int s = 0; s < S; s += 8) {
+    if (S == 1) {
+        gs += p[j];
+        us += p[F + j];
+    } else for (int s = 0; s < S; s += 8) {
         float a0[8], a1[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u)
