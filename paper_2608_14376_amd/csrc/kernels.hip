@@ -162,30 +162,27 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float *__restrict__ x, const f
     float *xr = x + (size_t)row * H;
     const float *pr = part + (size_t)row * H;
     float4 v[NG];
-    ushort4 gg[NG];
     float ss = 0.f;
 #pragma unroll
     for (int j = 0; j < NG; ++j) {
         const int i = 4 * (threadIdx.x + nth * j);
         if (i < H) {
-            gg[j] = *(const ushort4 *)(g + i);        // needed after the reduction; loaded with the rest
             v[j] = *(const float4 *)(xr + i);
             // partials are added in split order; their loads are issued in
-            // batches of up to 8 ahead of the adds (one split without the
-            // predication)
-            if (S == 1) {
-                const float4 p = *(const float4 *)(pr + i);
-                v[j].x += p.x; v[j].y += p.y; v[j].z += p.z; v[j].w += p.w;
-            } else for (int s = 0; s < S; s += 8) {
+            // batches of 8 ahead of the adds
+            int s = 0;
+            for (; s + 8 <= S; s += 8) {
                 float4 p[8];
 #pragma unroll
-                for (int u = 0; u < 8; ++u)
-                    if (s + u < S) p[u] = *(const float4 *)(pr + (s + u) * part_stride + i);
+                for (int u = 0; u < 8; ++u) p[u] = *(const float4 *)(pr + (s + u) * part_stride + i);
 #pragma unroll
-                for (int u = 0; u < 8; ++u)
-                    if (s + u < S) {
-                        v[j].x += p[u].x; v[j].y += p[u].y; v[j].z += p[u].z; v[j].w += p[u].w;
-                    }
+                for (int u = 0; u < 8; ++u) {
+                    v[j].x += p[u].x; v[j].y += p[u].y; v[j].z += p[u].z; v[j].w += p[u].w;
+                }
+            }
+            for (; s < S; ++s) {
+                const float4 p = *(const float4 *)(pr + s * part_stride + i);
+                v[j].x += p.x; v[j].y += p.y; v[j].z += p.z; v[j].w += p.w;
             }
             if (mf.y != nullptr && (mf.valid == nullptr || mf.valid[row])) {
                 // mixture-of-experts combine: sum_r w_r y_r in rank order, then added
@@ -211,11 +208,12 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float *__restrict__ x, const f
     for (int j = 0; j < NG; ++j) {
         const int i = 4 * (threadIdx.x + nth * j);
         if (i < H) {
+            const ushort4 gg = *(const ushort4 *)(g + i);
             ushort4 o;
-            o.x = f2bf(v[j].x * rstd * bf2f(gg[j].x));
-            o.y = f2bf(v[j].y * rstd * bf2f(gg[j].y));
-            o.z = f2bf(v[j].z * rstd * bf2f(gg[j].z));
-            o.w = f2bf(v[j].w * rstd * bf2f(gg[j].w));
+            o.x = f2bf(v[j].x * rstd * bf2f(gg.x));
+            o.y = f2bf(v[j].y * rstd * bf2f(gg.y));
+            o.z = f2bf(v[j].z * rstd * bf2f(gg.z));
+            o.w = f2bf(v[j].w * rstd * bf2f(gg.w));
             *(ushort4 *)(hr + i) = o;
         }
     }
@@ -1503,26 +1501,10 @@ __global__ void k_swiglu(const float *__restrict__ part, int S, long long part_s
     const int j = (blockIdx.x % nb) * 256 + threadIdx.x;
     if (j >= F) return;
     const float *p = part + (size_t)r * 2 * F;
-    // partials in split order, loads issued in batches of up to 8 (one
-    // split, the usual prefill case, without the predication)
     float gs = 0.f, us = 0.f;
-    if (S == 1) {
-        gs += p[j];
-        us += p[F + j];
-    } else for (int s = 0; s < S; s += 8) {
-        float a0[8], a1[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if (s + u < S) {
-                a0[u] = p[(s + u) * part_stride + j];
-                a1[u] = p[(s + u) * part_stride + F + j];
-            }
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if (s + u < S) {
-                gs += a0[u];
-                us += a1[u];
-            }
+    for (int s = 0; s < S; ++s) {
+        gs += p[s * part_stride + j];
+        us += p[s * part_stride + F + j];
     }
     a[(size_t)r * lda + j] = swiglu_bf16(gs, us);
 }
