@@ -1348,31 +1348,37 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
     }
 }
 
-// Merge of a row's splits in split order.  Block (query head, row), one
-// thread per dimension.  The head's (max, sum) pair of every split goes to
-// LDS while each thread's values of the first 32 splits load into registers
-// (one round trip for up to 32 splits, the small-batch case); then the exact
-// maximum M over the splits, the weights f_s = exp(m_s - M) and
-// L = sum_s l_s f_s in split order by one thread; each thread folds its
-// dimension over the splits in split order and writes A / L in bf16.
+// Merge of a row's splits in split order (any number of splits; the plans
+// with more than 8).  Block (HB query heads of one kv head, row), one thread per (head, dimension).  Each head's (max, sum) pair
+// of every split goes to LDS while each thread's values of the first 32
+// splits load into registers (one round trip for up to 32 splits, the
+// small-batch case); then, per head, the exact maximum M over the splits,
+// the weights f_s = exp(m_s - M) and L = sum_s l_s f_s in split order by one
+// thread; each thread folds its dimension over the splits in split order
+// and writes A / L in bf16.
 template <int D, int G>
-__global__ __launch_bounds__(D) void k_attn_merge(const float *__restrict__ ws, const uint8_t *__restrict__ valid,
-                                                  const int32_t *__restrict__ pos, int nq, int nkv, int chunk,
-                                                  int max_splits, uint16_t *__restrict__ o)
+constexpr int merge_heads() { return G < 512 / D ? G : 512 / D; }
+
+template <int D, int G>
+__global__ __launch_bounds__((D * merge_heads<D, G>())) void k_attn_merge(
+    const float *__restrict__ ws, const uint8_t *__restrict__ valid, const int32_t *__restrict__ pos, int nq, int nkv,
+    int chunk, int max_splits, uint16_t *__restrict__ o)
 {
     constexpr int PF = 32;                            // splits whose values are in flight at once
-    const int hq = blockIdx.x, r = blockIdx.y, dd = threadIdx.x;
+    constexpr int HB = merge_heads<D, G>();           // divides G
+    const int hl = threadIdx.x / D, dd = threadIdx.x % D;
+    const int hq = blockIdx.x * HB + hl, r = blockIdx.y;
     const int kvh = hq / G, g = hq - kvh * G;
     uint16_t *orow = o + (size_t)r * nq * D + (size_t)hq * D;
     if (valid != nullptr && !valid[r]) {
         orow[dd] = 0;
         return;
     }
-    extern __shared__ float fs[];                     // [max_splits] maxima then weights, [max_splits] sums
-    __shared__ float ML[2];
+    extern __shared__ float fs[];                     // per head: [max_splits] maxima then weights, [max_splits] sums
+    __shared__ float ML[HB][2];
     const int n = pos[r] + 1;
     const int ns = (n + chunk - 1) / chunk;
-    float *fm = fs, *fl = fs + max_splits;
+    float *fm = fs + (size_t)hl * 2 * max_splits, *fl = fm + max_splits;
     const int stride = G * (D + 2);
     const float *base = ws + ((size_t)r * nkv + kvh) * max_splits * stride;
     const float *a = base + 2 * G + g * D + dd;
@@ -1388,15 +1394,15 @@ __global__ __launch_bounds__(D) void k_attn_merge(const float *__restrict__ ws, 
     if (dd == 0) {
         float M = -INFINITY;
         for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, fm[sp]);
-        ML[0] = M;
+        ML[hl][0] = M;
     }
     __syncthreads();
-    for (int sp = dd; sp < ns; sp += D) fm[sp] = __expf(fm[sp] - ML[0]);
+    for (int sp = dd; sp < ns; sp += D) fm[sp] = __expf(fm[sp] - ML[hl][0]);
     __syncthreads();
     if (dd == 0) {
         float L = 0.f;
         for (int sp = 0; sp < ns; ++sp) L += fl[sp] * fm[sp];
-        ML[1] = L;
+        ML[hl][1] = L;
     }
     __syncthreads();
     float acc = 0.f;
@@ -1409,7 +1415,89 @@ __global__ __launch_bounds__(D) void k_attn_merge(const float *__restrict__ ws, 
         for (int u = 0; u < PF; ++u)
             if (sp + u < ns) acc += v[u] * fm[sp + u];
     }
-    orow[dd] = f2bf(acc / ML[1]);
+    orow[dd] = f2bf(acc / ML[hl][1]);
+}
+
+// Merge of a row's splits in split order, for few splits (up to 8, the
+// large-batch plans).  Block (kvh, row), 256 threads.  Every split's (max,
+// sum) pair is loaded in one round into LDS; per head
+// the exact maximum M over the splits, weights f_s = exp(m_s - M) and
+// L = sum_s l_s f_s walked in split order by one thread; then each thread
+// folds its E output elements over the splits in split order, eight splits'
+// loads issued ahead of the adds, and writes A / L in bf16: the arithmetic
+// of k_attn_merge, in the same order.  A plan uses one of the two for all
+// its rows.
+template <int D, int G>
+__global__ __launch_bounds__(256) void k_attn_merge_kv(const float *__restrict__ ws, const uint8_t *__restrict__ valid,
+                                                    const int32_t *__restrict__ pos, int nq, int nkv, int chunk,
+                                                    int max_splits, uint16_t *__restrict__ o)
+{
+    constexpr int E = (G * D + 255) / 256;           // output elements per thread
+    const int kvh = blockIdx.x, r = blockIdx.y, tid = threadIdx.x;
+    uint16_t *orow = o + (size_t)r * nq * D + (size_t)kvh * G * D;
+    if (valid != nullptr && !valid[r]) {
+        for (int i = tid; i < G * D; i += 256) orow[i] = 0;
+        return;
+    }
+    extern __shared__ float fs[];          // [G][ns] maxima then weights, [G][ns] sums, [G] M, [G] L
+    const int n = pos[r] + 1;
+    const int ns = (n + chunk - 1) / chunk;
+    float *fm = fs, *fl = fs + G * max_splits, *Mg = fl + G * max_splits, *Lg = Mg + G;
+    const int stride = G * (D + 2);
+    const float *base = ws + ((size_t)r * nkv + kvh) * max_splits * stride;
+    for (int idx = tid; idx < G * ns; idx += 256) {
+        const int g = idx / ns, sp = idx - g * ns;
+        fm[idx] = base[(size_t)sp * stride + g];
+        fl[idx] = base[(size_t)sp * stride + G + g];
+    }
+    __syncthreads();
+    if (tid < G) {
+        float M = -INFINITY;
+        for (int sp = 0; sp < ns; ++sp) M = fmaxf(M, fm[tid * ns + sp]);
+        Mg[tid] = M;
+    }
+    __syncthreads();
+    for (int idx = tid; idx < G * ns; idx += 256) fm[idx] = __expf(fm[idx] - Mg[idx / ns]);
+    __syncthreads();
+    if (tid < G) {
+        float L = 0.f;
+        for (int sp = 0; sp < ns; ++sp) L += fl[tid * ns + sp] * fm[tid * ns + sp];
+        Lg[tid] = L;
+    }
+    __syncthreads();
+    float acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0.f;
+    const float *a = base + 2 * G;
+    int sp = 0;
+    for (; sp + 8 <= ns; sp += 8) {
+        float v[8][E];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const int idx = tid + 256 * e;
+                v[u][e] = idx < G * D ? a[(size_t)(sp + u) * stride + idx] : 0.f;
+            }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const int idx = tid + 256 * e;
+                if (idx < G * D) acc[e] += v[u][e] * fm[(idx / D) * ns + sp + u];
+            }
+    }
+    for (; sp < ns; ++sp)
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int idx = tid + 256 * e;
+            if (idx < G * D) acc[e] += a[(size_t)sp * stride + idx] * fm[(idx / D) * ns + sp];
+        }
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int idx = tid + 256 * e;
+        if (idx < G * D) orow[idx] = f2bf(acc[e] / Lg[idx / D]);
+    }
 }
 
 template <int D, int G>
@@ -1425,9 +1513,16 @@ template <int D, int G>
 static void launch_merge_dg(const float *ws, int rows, const uint8_t *valid, const int32_t *pos, int nq,
                             int nkv, int chunk, int max_splits, uint16_t *o, hipStream_t st)
 {
-    const size_t shm = sizeof(float) * 2 * max_splits;
-    hipLaunchKernelGGL((k_attn_merge<D, G>), dim3(nq, rows), dim3(D), shm, st, ws, valid, pos, nq, nkv, chunk,
-                       max_splits, o);
+    if (max_splits <= 8) {   // one round trip either way: the per-kv-head layout launches fewer wavefronts
+        const size_t shm = sizeof(float) * (2 * G * max_splits + 2 * G);
+        hipLaunchKernelGGL((k_attn_merge_kv<D, G>), dim3(nkv, rows), dim3(256), shm, st, ws, valid, pos, nq, nkv,
+                           chunk, max_splits, o);
+        return;
+    }
+    constexpr int HB = merge_heads<D, G>();
+    const size_t shm = sizeof(float) * 2 * HB * max_splits;
+    hipLaunchKernelGGL((k_attn_merge<D, G>), dim3(nq / HB, rows), dim3(D * HB), shm, st, ws, valid, pos, nq, nkv,
+                       chunk, max_splits, o);
 }
 
 #define CORUN_ATTN_DISPATCH(FN, ...)                                                \
