@@ -140,6 +140,10 @@ typedef struct {
                                   and reads that copy from then on, in decode and in prefill projections of up to
                                   64 rows; results are bit-identical either way.  The weights must not change
                                   after creation.  1 = no copies: read the caller's row-major weights. */
+    int32_t qkv_epilogue;      /* where the decode step applies the QKV epilogue (RoPE, KV append): 0 = chosen
+                                  from B (inside the attention kernel for B_fixed <= 8, where it saves a launch;
+                                  its own kernel above, where recomputing q in every attention block costs
+                                  more); 1 = its own kernel; 2 = inside attention.  Bit-identical results. */
 } corun_options;
 
 /* Create an engine for one fixed padded batch size B_fixed (Sec. IV,
@@ -333,7 +337,8 @@ enum {
     CORUN_K_ATTN_SPLIT = 5,   /* split-KV decode attention */
     CORUN_K_ATTN_MERGE = 6,   /* fixed-order split merge */
     CORUN_K_RMSNORM = 7,      /* residual fold + RMSNorm */
-    CORUN_K_QKV_POST = 8,     /* QKV epilogue: RoPE + KV append */
+    CORUN_K_QKV_POST = 8,     /* QKV epilogue: RoPE + KV append (no kernel where the attention kernel
+                                 applies it: corun_options.qkv_epilogue) */
     CORUN_K_SWIGLU = 9,       /* SwiGLU epilogue (no kernel where the gate/up projection's epilogue applies it:
                                  packed weights without split-K) */
     CORUN_K_ARGMAX = 10,      /* greedy argmax */

@@ -227,6 +227,7 @@ struct corun_engine {
     size_t pk_bytes = 0;
     bool gu_fused = false;   // the gate/up copy is interleaved for the fused SwiGLU epilogue
     bool egu_fused = false;  // likewise for every expert's gate/up (mixture of experts)
+    bool qkv_in_attn = false;   // decode attention applies the QKV epilogue (no k_qkv_post launch)
     bool moe = false;
     // mixture-of-experts workspace (decode)
     float *p_router = nullptr, *moe_w = nullptr, *moe_gu = nullptr, *moe_y = nullptr;
@@ -355,6 +356,7 @@ static corun_status check_options(const corun_options &o)
     if (o.batch_invariant != 0 && o.batch_invariant != 1) return fail(CORUN_E_INVAL, "batch_invariant must be 0 or 1");
     if (o.bi_prefill != 0 && o.bi_prefill != 1) return fail(CORUN_E_INVAL, "bi_prefill must be 0 or 1");
     if (o.no_weight_pack != 0 && o.no_weight_pack != 1) return fail(CORUN_E_INVAL, "no_weight_pack must be 0 or 1");
+    if (o.qkv_epilogue < 0 || o.qkv_epilogue > 2) return fail(CORUN_E_INVAL, "qkv_epilogue must be 0, 1 or 2");
     if (o.batch_invariant && (o.attn_chunk || o.split_k_override || o.gemm_bm))
         return fail(CORUN_E_INVAL, "batch_invariant fixes the plan: attn_chunk, split_k_override and gemm_bm must be 0");
     return CORUN_OK;
@@ -550,13 +552,16 @@ corun_status launch_one(corun_engine *e, int which, int l)
         HIP_TRY(proj(e, e->h, H, W_QKV, l, p.qkv, B, e->p_qkv, (long long)B * nqkv, nqkv));
         break;
     }
-    case CORUN_K_QKV_POST:
+    case CORUN_K_QKV_POST:   // nothing to launch when attention applies the epilogue
+        if (e->qkv_in_attn) break;
         HIP_TRY(launch_qkv_post(e->p_qkv, p.qkv.S, (long long)B * nqkv, B, e->d_valid, e->d_seq, nullptr, -1, nq,
                                 nkv, d, e->rope, e->q, e->kc[l], e->vc[l], e->view, st));
         break;
     case CORUN_K_ATTN_SPLIT:
         HIP_TRY(launch_attn_split(e->q, B, e->d_valid, e->d_seq, nullptr, -1, nq, nkv, d, e->kc[l], e->vc[l],
-                                  e->view, p.chunk, p.max_splits, e->attn_ws, st));
+                                  e->view, p.chunk, p.max_splits, e->attn_ws, st,
+                                  e->qkv_in_attn ? QkvIn{e->p_qkv, p.qkv.S, (long long)B * nqkv, e->rope}
+                                                 : QkvIn{}));
         break;
     case CORUN_K_ATTN_MERGE:
         HIP_TRY(launch_attn_merge(e->attn_ws, B, e->d_valid, e->d_seq, nq, nkv, d, p.chunk, p.max_splits, e->o, st));
@@ -869,6 +874,11 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     e->view.page_table = kv->page_table;
     e->plan = make_plan(cfg, kv, B, o);
     const Plan &p = e->plan;
+    // Inside attention every block rebuilds its group's q from the split
+    // partials: one launch fewer, which pays where launches dominate (B = 1:
+    // about 3%) and costs where many blocks repeat the work (B = 256: the
+    // attention kernel 187 -> 206 us against 7 us for the epilogue kernel).
+    e->qkv_in_attn = o.qkv_epilogue == 2 || (o.qkv_epilogue == 0 && B <= 8);
 
     auto bail = [&](corun_status s) {
         corun_engine_destroy(e);

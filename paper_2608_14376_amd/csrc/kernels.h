@@ -60,6 +60,16 @@ struct ArgBest {
     int i;
 };
 
+// The QKV projection's split partials for an attention kernel that applies
+// the QKV epilogue itself (launch_attn_split): part [S][rows][(nq + 2 nkv) d]
+// with split stride `stride`, and the RoPE table.
+struct QkvIn {
+    const float *part = nullptr;
+    int S = 0;
+    long long stride = 0;
+    const float2 *rope = nullptr;
+};
+
 // Expert tiles of a mixture-of-experts projection (launch_moe_dispatch):
 // slot s holds tiles[3 s + 2] assignments list[tiles[3 s + 1] ..] of expert
 // tiles[3 s]; an assignment's A row is assignment / row_div; expert e's
@@ -121,10 +131,14 @@ hipError_t launch_qkv_post(const float *part, int S, long long part_stride, int 
 // attending keys 0..pos[r]) is cut into chunks of `chunk` tokens; block
 // (split, kvh, r) writes the chunk's (max, sum, unnormalised acc) for the G
 // query heads of kv head kvh.  Merge combines the splits in index order.
+// With qi.part set, q is not read: every block applies the QKV epilogue of
+// launch_qkv_post to its group's q from the split partials, and the block
+// holding the new token (position pos[r]) also makes its k and v, appends
+// them to the cache and uses them -- the same bits launch_qkv_post writes.
 hipError_t launch_attn_split(const uint16_t *q, int rows, const uint8_t *valid, const int32_t *pos,
                              const int32_t *slot_of_row, int slot_const, int nq, int nkv, int d,
-                             const uint16_t *kc, const uint16_t *vc, KvView kv, int chunk,
-                             int max_splits, float *ws, hipStream_t st);
+                             uint16_t *kc, uint16_t *vc, KvView kv, int chunk,
+                             int max_splits, float *ws, hipStream_t st, QkvIn qi = QkvIn{});
 hipError_t launch_attn_merge(const float *ws, int rows, const uint8_t *valid, const int32_t *pos,
                              int nq, int nkv, int d, int chunk, int max_splits, uint16_t *o,
                              hipStream_t st);

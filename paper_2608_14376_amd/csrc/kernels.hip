@@ -979,6 +979,45 @@ hipError_t launch_gemm(const uint16_t *A, int lda, const uint16_t *W, const Gemm
 // row's own position, bf16 rounding, KV append.  Block (head, row); thread i
 // owns the rotation pair (i, i + d/2).
 // ---------------------------------------------------------------------------
+// The QKV epilogue of one rotation pair (elements i and i + d/2 of a head):
+// the split partials at columns c0 and c0 + half folded in split order (loads
+// of up to eight splits issued together), both sums rounded to bf16, rotated
+// by (cos, sin) when rot, rounded again.  k_qkv_post and the attention
+// kernel's fused epilogue both run this, so they write the same bits.
+__device__ __forceinline__ void qkv_pair(const float *__restrict__ pb, long long stride, int S, int c0, int half,
+                                         bool rot, float2 cs, uint16_t &b0, uint16_t &b1)
+{
+    float x0 = 0.f, x1 = 0.f;
+    if (S == 1) {
+        x0 += pb[c0];
+        x1 += pb[c0 + half];
+    } else for (int s = 0; s < S; s += 8) {
+        float a0[8], a1[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (s + u < S) {
+                a0[u] = pb[(s + u) * stride + c0];
+                a1[u] = pb[(s + u) * stride + c0 + half];
+            }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (s + u < S) {
+                x0 += a0[u];
+                x1 += a1[u];
+            }
+    }
+    x0 = bf2f(f2bf(x0));
+    x1 = bf2f(f2bf(x1));
+    if (rot) {
+        const float y0 = __builtin_fmaf(x0, cs.x, -(x1 * cs.y));
+        const float y1 = __builtin_fmaf(x1, cs.x, x0 * cs.y);
+        x0 = y0;
+        x1 = y1;
+    }
+    b0 = f2bf(x0);
+    b1 = f2bf(x1);
+}
+
 __global__ void k_qkv_post(const float *__restrict__ part, int S, long long part_stride,
                            const uint8_t *__restrict__ valid, const int32_t *__restrict__ pos,
                            const int32_t *__restrict__ slot_of_row, int slot_const, int nq, int nkv, int d,
@@ -992,41 +1031,12 @@ __global__ void k_qkv_post(const float *__restrict__ part, int S, long long part
     if (valid != nullptr && !valid[r]) return;
     const int p = pos[r];
     const int ncols = (nq + 2 * nkv) * d;
-    const int c0 = hd * d + i, c1 = c0 + half;
     const bool rot = hd < nq + nkv;
     float2 cs = {1.f, 0.f};
     if (rot) cs = rope_tab[(size_t)p * half + i];    // issued with the partial loads
-    // partials in split order, loads issued in batches of up to 8 (one
-    // split without the predication)
-    float x0 = 0.f, x1 = 0.f;
-    const float *pb = part + (size_t)r * ncols;
-    if (S == 1) {
-        x0 += pb[c0];
-        x1 += pb[c1];
-    } else for (int s = 0; s < S; s += 8) {
-        float a0[8], a1[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if (s + u < S) {
-                a0[u] = pb[(s + u) * part_stride + c0];
-                a1[u] = pb[(s + u) * part_stride + c1];
-            }
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if (s + u < S) {
-                x0 += a0[u];
-                x1 += a1[u];
-            }
-    }
-    x0 = bf2f(f2bf(x0));
-    x1 = bf2f(f2bf(x1));
-    if (rot) {
-        const float y0 = x0 * cs.x - x1 * cs.y;
-        const float y1 = x1 * cs.x + x0 * cs.y;
-        x0 = y0;
-        x1 = y1;
-    }
-    const uint16_t b0 = f2bf(x0), b1 = f2bf(x1);
+    uint16_t b0, b1;
+    qkv_pair(part + (size_t)r * ncols, part_stride, S, hd * d + i, half, rot, cs, b0, b1);
+    const int c0 = hd * d + i, c1 = c0 + half;
     if (hd < nq) {
         q[(size_t)r * nq * d + c0] = b0;
         q[(size_t)r * nq * d + c1] = b1;
@@ -1113,9 +1123,9 @@ template <int D, int G>
 __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__ q, const uint8_t *__restrict__ valid,
                                                     const int32_t *__restrict__ pos,
                                                     const int32_t *__restrict__ slot_of_row, int slot_const,
-                                                    int nq, int nkv, const uint16_t *__restrict__ kc,
-                                                    const uint16_t *__restrict__ vc, KvView kv, int chunk,
-                                                    int max_splits, float *__restrict__ ws)
+                                                    int nq, int nkv, uint16_t *__restrict__ kc,
+                                                    uint16_t *__restrict__ vc, KvView kv, int chunk,
+                                                    int max_splits, float *__restrict__ ws, QkvIn qi)
 {
     constexpr int ET = D / 16;
     constexpr int KCH = D / 8;                        // 16-byte chunks per key row
@@ -1127,6 +1137,8 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
     __shared__ __attribute__((aligned(16))) uint4 tile[KU + VU];
     __shared__ float cm[4][16], cl[4][16];
     __shared__ int32_t pgs[2][64];                    // paged: the pages of a step, fetched one step ahead
+    __shared__ __attribute__((aligned(16))) uint16_t qs[G * D];     // fused epilogue: the group's q
+    __shared__ __attribute__((aligned(16))) uint16_t kvn[2 * D];    // fused epilogue: the new token's k, v
     typedef __attribute__((address_space(3))) void lds_void;
 
     const int split = blockIdx.x, kvh = blockIdx.y, r = blockIdx.z;
@@ -1138,16 +1150,19 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
     const int t1 = min(n, t0 + chunk);
     const int slot = row_slot(slot_of_row, slot_const, r);
     const int hl = lane & 15, kg = lane >> 4;
+    const bool fused = qi.part != nullptr;
+    const int pnew = n - 1;                           // the new token's position
+    const bool owns_new = fused && t1 == n;           // the split that holds it appends and patches it
 
     // q^T fragments (B operand of the scores): lane l supplies head l % 16,
-    // dims 32 kk + 8 (l / 16) .. +7
+    // dims 32 kk + 8 (l / 16) .. +7; from q, or (fused) from qs below
     bf16x8 qf[D / 32];
-    {
+    const uint4 zq = {0u, 0u, 0u, 0u};
+    if (!fused) {
         const uint16_t *qr = q + (size_t)r * nq * D + ((size_t)kvh * G + hl) * D + kg * 8;
-        const uint4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int kk = 0; kk < D / 32; ++kk) {
-            uint4 v = z;
+            uint4 v = zq;
             if (hl < G) v = *(const uint4 *)(qr + 32 * kk);
             qf[kk] = __builtin_bit_cast(bf16x8, v);
         }
@@ -1207,8 +1222,77 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
         if (st_i > 0) lds_barrier();                  // every wavefront is done with the previous step
         issue(tb0, st_i & 1);
         if (st_i + 1 < nsteps) fetch_pages(tb0 + STEP, (st_i + 1) & 1);
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        if (fused && st_i == 0) {
+            // The QKV epilogue while the first step's loads are in flight:
+            // pair pi < G d/2 is q (head pi / (d/2)); the owner of the new
+            // token also makes its k (rotated) and v pairs, appends them to
+            // the cache and keeps them in kvn for the patch below.
+            const int nqkv = (nq + 2 * nkv) * D, nqp = G * (D / 2);
+            const float *pb = qi.part + (size_t)r * nqkv;
+            const float2 *rt = qi.rope + (size_t)pnew * (D / 2);
+            const int npairs = nqp + (owns_new ? D : 0);
+            for (int pi = tid; pi < npairs; pi += 256) {
+                int i, c0, which;                     // 0: q, 1: k, 2: v
+                if (pi < nqp) {
+                    i = pi % (D / 2);
+                    c0 = (kvh * G + pi / (D / 2)) * D + i;
+                    which = 0;
+                } else if (pi < nqp + D / 2) {
+                    i = pi - nqp;
+                    c0 = (nq + kvh) * D + i;
+                    which = 1;
+                } else {
+                    i = pi - nqp - D / 2;
+                    c0 = (nq + nkv + kvh) * D + i;
+                    which = 2;
+                }
+                float2 cs = {1.f, 0.f};
+                if (which < 2) cs = rt[i];
+                uint16_t b0, b1;
+                qkv_pair(pb, qi.stride, qi.S, c0, D / 2, which < 2, cs, b0, b1);
+                if (which == 0) {
+                    const int hh = pi / (D / 2);
+                    qs[hh * D + i] = b0;
+                    qs[hh * D + i + D / 2] = b1;
+                } else if (which == 1) {
+                    kvn[i] = b0;
+                    kvn[i + D / 2] = b1;
+                    uint16_t *dst = kc + kv_offset(kv, nkv, D, slot, kvh, pnew);
+                    dst[i] = b0;
+                    dst[i + D / 2] = b1;
+                } else {
+                    kvn[D + i] = b0;
+                    kvn[D + i + D / 2] = b1;
+                    vc[v_offset(kv, nkv, D, slot, kvh, pnew, i)] = b0;
+                    vc[v_offset(kv, nkv, D, slot, kvh, pnew, i + D / 2)] = b1;
+                }
+            }
+        }
+        if (fused && st_i == 0) __builtin_amdgcn_s_waitcnt(0);   // also the qs / kvn stores
+        else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
         lds_barrier();                                // the step (and the next step's pages) are in LDS
+        if (fused && st_i == 0) {
+            const uint16_t *qr = qs + hl * D + kg * 8;
+#pragma unroll
+            for (int kk = 0; kk < D / 32; ++kk) {
+                uint4 v = zq;
+                if (hl < G) v = *(const uint4 *)(qr + 32 * kk);
+                qf[kk] = __builtin_bit_cast(bf16x8, v);
+            }
+        }
+        if (owns_new && pnew >= tb0 && pnew < tb0 + STEP) {
+            // the step holds the new token: its cache entries may have
+            // landed before the append, so its tile slots take kvn
+            const int tl = pnew - tb0;
+            if (tid < KCH) {
+                tile[tl * KCH + (tid ^ attn_kswz<KCH>(tl))] = reinterpret_cast<const uint4 *>(kvn)[tid];
+            } else if (tid >= 64 && tid < 64 + D) {
+                const int e = tid - 64;
+                reinterpret_cast<uint16_t *>(&tile[KU + e * 16 + ((tl >> 3) ^ (e & 15))])[tl & 7] = kvn[D + e];
+            }
+            __builtin_amdgcn_s_waitcnt(0);
+            lds_barrier();
+        }
         const int tb = tb0 + 32 * wave;
         if (tb >= t1) continue;                       // wave-uniform: no token of this block is real
         const int wt1 = t1;
@@ -1502,11 +1586,11 @@ __global__ __launch_bounds__(256) void k_attn_merge_kv(const float *__restrict__
 
 template <int D, int G>
 static void launch_attn_dg(const uint16_t *q, int rows, const uint8_t *valid, const int32_t *pos,
-                           const int32_t *slot_of_row, int slot_const, int nq, int nkv, const uint16_t *kc,
-                           const uint16_t *vc, KvView kv, int chunk, int max_splits, float *ws, hipStream_t st)
+                           const int32_t *slot_of_row, int slot_const, int nq, int nkv, uint16_t *kc,
+                           uint16_t *vc, KvView kv, int chunk, int max_splits, float *ws, hipStream_t st, QkvIn qi)
 {
     hipLaunchKernelGGL((k_attn_split<D, G>), dim3(max_splits, nkv, rows), dim3(256), 0, st, q, valid, pos,
-                       slot_of_row, slot_const, nq, nkv, kc, vc, kv, chunk, max_splits, ws);
+                       slot_of_row, slot_const, nq, nkv, kc, vc, kv, chunk, max_splits, ws, qi);
 }
 
 template <int D, int G>
@@ -1552,11 +1636,11 @@ static void launch_merge_dg(const float *ws, int rows, const uint8_t *valid, con
 
 hipError_t launch_attn_split(const uint16_t *q, int rows, const uint8_t *valid, const int32_t *pos,
                              const int32_t *slot_of_row, int slot_const, int nq, int nkv, int d,
-                             const uint16_t *kc, const uint16_t *vc, KvView kv, int chunk, int max_splits,
-                             float *ws, hipStream_t st)
+                             uint16_t *kc, uint16_t *vc, KvView kv, int chunk, int max_splits,
+                             float *ws, hipStream_t st, QkvIn qi)
 {
     CORUN_ATTN_DISPATCH(launch_attn_dg, q, rows, valid, pos, slot_of_row, slot_const, nq, nkv, kc, vc, kv, chunk,
-                        max_splits, ws, st);
+                        max_splits, ws, st, qi);
     return hipGetLastError();
 }
 

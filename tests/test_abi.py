@@ -145,13 +145,15 @@ def test_batch_invariant_rejects_plan_overrides():
 
 
 def test_options_take_only_flags():
-    """no_weight_pack, batch_invariant and bi_prefill are 0 or 1."""
+    """no_weight_pack, batch_invariant and bi_prefill are 0 or 1,
+    qkv_epilogue 0, 1 or 2."""
     c = wl.config("tiny")
     kv = _kv(n_slots=4, max_seq_len=128)
-    for bad in (dict(no_weight_pack=2), dict(no_weight_pack=-1), dict(bi_prefill=3)):
+    for bad in (dict(no_weight_pack=2), dict(no_weight_pack=-1), dict(bi_prefill=3), dict(qkv_epilogue=3),
+                dict(qkv_epilogue=-1)):
         opt = corun.options()
         for k, v in bad.items():
             setattr(opt, k, v)
         with pytest.raises(corun.CorunError):
             corun.describe_plan(c, kv, 4, opt)
-    corun.describe_plan(c, kv, 4, corun.options(no_weight_pack=True))
+    corun.describe_plan(c, kv, 4, corun.options(no_weight_pack=True, qkv_epilogue=2))
