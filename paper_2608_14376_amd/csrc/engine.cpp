@@ -77,12 +77,15 @@ int mt_for(int M) { return M <= 16 ? 1 : (M <= 32 ? 2 : 4); }
 //  * M <= 64, K % 64 != 0: the skinny kernel (weights streamed to
 //    registers); aim for about 2048 wavefronts (8 per CU) so enough weight
 //    bytes are in flight, each split keeping at least 256 K elements.
-//  * M > 64, K % 64 == 0: the pipelined kernel (one workgroup per CU) with
-//    M tile 128 (M <= 128) or 256 and N tile 128; 256 x 256 tiles (eight
-//    wavefronts) once those tiles alone fill the GPU (large prefill) and for
-//    wide decode projections (128 < M <= 256, N >= 16384: gate/up, lm_head);
+//  * 64 < M <= 256, K % 64 == 0: the pipelined kernel (one workgroup per
+//    CU) with M tile 128 (M <= 128, and the narrower projections up to 256)
+//    or 256 and N tile 128; 256 x 256 tiles (eight wavefronts) for wide
+//    decode projections (128 < M <= 256, N >= 16384: gate/up, lm_head);
 //    split-K up to one round of at most 256 workgroups, each split keeping
 //    at least 512 K elements.
+//  * M > 256 (prefill), K % 64 == 0: the pipelined kernel with the tile
+//    (256 x 256, 256 x 128, 128 x 128) and split-K of least estimated time
+//    (waves of 256 workgroups, per-tile wave costs, the partials' traffic).
 //  * otherwise (or bm_override > 0): the LDS-tiled kernel with a 128-row
 //    tile (or bm_override), split-K to about two workgroups per CU.
 // Batch-invariant mode (bi): no split-K and, when K % 64 == 0, the
@@ -111,6 +114,38 @@ Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_
         const int tiles = (N + 127) / 128;
         S = std::max(1, 256 / tiles);
         S = std::min(S, std::max(1, K / 512));
+        align = 64;
+    } else if (M > 256 && bm_override <= 0 && K % 64 == 0) {
+        // Prefill-sized M: the tile and split-K with the least estimated
+        // time, calibrated on this GPU's pipelined kernel.  A launch runs in
+        // waves of 256 workgroups; a wave costs c x K / S with c = 1.69,
+        // 1.0, 0.62 for 256 x 256, 256 x 128, 128 x 128 tiles (a 256 x 128
+        // wave over 4096 K elements took 68.5 us), and each split beyond the
+        // first adds a set of fp32 partials that is written and folded again
+        // (8 bytes per output at about 5 TB/s).  Against measured times at
+        // M = 512 .. 8192 the estimate picks the fastest tile, or one within
+        // a few percent.
+        struct Cand {
+            int bm, bn;
+            double c;
+        };
+        const Cand cands[] = {{256, 256, 1.69}, {256, 128, 1.0}, {128, 128, 0.62}};
+        const int smax = std::max(1, std::min(K / 512, max_split > 0 ? max_split : 64));
+        double best = 1e300;
+        S = 1;
+        for (const Cand &cd : cands) {
+            const long long tiles = (long long)((M + cd.bm - 1) / cd.bm) * ((N + cd.bn - 1) / cd.bn);
+            for (int s = 1; s <= smax; s *= 2) {
+                const double waves = (double)((tiles * s + 255) / 256);
+                const double t = waves * cd.c * ((double)K / s) * (68.5 / 4096) + (s - 1) * (double)M * N * 8 / 5e6;
+                if (t < best) {
+                    best = t;
+                    p.bm = cd.bm;
+                    p.bn = cd.bn;
+                    S = s;
+                }
+            }
+        }
         align = 64;
     } else if (M > 64 && bm_override <= 0 && K % 64 == 0) {
         // 128-row tiles up to M = 256 for the narrower projections (qkv, o,
