@@ -157,3 +157,25 @@ def test_options_take_only_flags():
         with pytest.raises(corun.CorunError):
             corun.describe_plan(c, kv, 4, opt)
     corun.describe_plan(c, kv, 4, corun.options(no_weight_pack=True, qkv_epilogue=2))
+
+
+def test_prefill_tiles_follow_the_wave_estimate():
+    """Prefill-sized M takes the tile and split-K of least estimated time
+    (waves of 256 workgroups, per-tile wave costs, split partials' traffic):
+    the choices the standalone measurements favour at these 8B shapes."""
+    c = wl.config("8b")
+
+    def plan(M):
+        p = corun.describe_plan(c, _kv(n_slots=M, max_seq_len=4224), M)
+        return {k: (p[k]["m_tile"], p[k]["n_tile"], p[k]["split_k"]) for k in ("qkv", "o", "gate_up", "down")}
+
+    p512, p1024, p2048 = plan(512), plan(1024), plan(2048)
+    assert p512["gate_up"] == (256, 256, 1)          # 192 tiles in one wave beat 384 of 256 x 128
+    assert p512["qkv"] == (256, 128, 2)
+    assert p1024["gate_up"] == (256, 128, 1)         # three full waves beat 1.5 waves of 256 x 256
+    assert p2048["qkv"] == (256, 256, 1)             # 192 tiles in one wave beat two waves of 256 x 128
+    assert p2048["gate_up"] == (256, 256, 1)
+    assert p2048["o"] == (256, 128, 1)
+    for p in (p512, p1024, p2048):                   # every split keeps at least 512 K elements
+        for name, K in (("qkv", 4096), ("o", 4096), ("gate_up", 4096), ("down", 12288)):
+            assert K // p[name][2] >= 512, (name, p[name])
