@@ -191,7 +191,7 @@ Proj choose_proj(int N, int K, int M, int split_override, int max_split, int bm_
     return p;
 }
 
-GemmShape shape_of(const Proj &p, int M) { return GemmShape{M, p.N, p.K, p.S, p.Kc, mt_for(M), p.bm, p.bn}; }
+GemmShape shape_of(const Proj &p, int M) { return GemmShape{M, p.N, p.K, p.S, p.Kc, mt_for(M), p.bm, p.bn, 0}; }
 
 // Attention chunk: fixed per engine from (B, kv heads, capacity): enough
 // (row, head, split) blocks to fill the GPU when every row is at capacity,
@@ -924,7 +924,6 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
         return bail(fail(CORUN_E_HIP, "stream/event creation failed"));
 
     const int H = cfg->hidden, d = cfg->head_dim, nq = cfg->n_heads, nkv = cfg->n_kv_heads, F = cfg->ffn;
-    const int nqkv = (nq + 2 * nkv) * d;
     const int cap = kv_capacity(kv);
     const int rope_len = std::max(cap, o.max_prefill_len);
     e->hist_cap = 4096;
