@@ -12,7 +12,9 @@ decode and prefill benchmarks time, layer count aside.
   the GPU-written cache prefix (teacher forcing), which checks the
   position's whole computation -- its logits at the last position, its
   cached key and value everywhere -- without an oracle prefill of 600
-  positions."""
+  positions;
+* prefill of 32768 tokens (the longest benchmarked prompt), sampled
+  positions checked the same way."""
 import numpy as np
 import pytest
 import torch
@@ -101,3 +103,31 @@ def test_prefill_600_full_shapes_teacher_forced(full):
             assert np.abs(f32(gv[l][:, :, t]) - ov).max() <= TOL * np.abs(ov).max(), (t, l)
         if t == LP - 1:
             assert row_rel_err(last.cpu().numpy(), ref) <= TOL
+
+
+def test_prefill_32768_full_shapes_teacher_forced(full):
+    """The longest benchmarked prompt: its projections take the largest-M
+    tiles and split-K of the prefill plan, and its causal attention spans
+    32768 keys; sampled positions are recomputed as above."""
+    cfg, Wg, m = full
+    lp, cap = 32768, 32784
+    K, V = wl.make_kv_contiguous(cfg, 2, cap, seed=46, device=DEV)
+    eng = corun.Engine(cfg, Wg, 2, K, V, opt=corun.options(max_prefill_len=lp))
+    prompt = wl.make_prompt(cfg["vocab"], lp, seed=47)
+    last = torch.empty(cfg["vocab"], dtype=torch.float32, device=DEV)
+    eng.prefill(prompt, 1, last)
+    eng.close()
+    gk = [wl.bits(k[1]) for k in K]
+    gv = [wl.bits(v[1]) for v in V]
+    f32 = lambda a: (a.astype(np.uint32) << 16).view(np.float32)
+    for t in (0, 4095, 16384, lp - 1):
+        kv1 = row_cache(K, V, 1, cap)
+        ref = oracle.decode_row(m, kv1, 0, int(prompt[t]), t)
+        for l in range(cfg["n_layers"]):
+            ok, ov = f32(kv1.k[l][0, :, t, :]), f32(kv1.v[l][0, :, :, t])
+            assert np.abs(f32(gk[l][:, t, :]) - ok).max() <= TOL * np.abs(ok).max(), (t, l)
+            assert np.abs(f32(gv[l][:, :, t]) - ov).max() <= TOL * np.abs(ov).max(), (t, l)
+        if t == lp - 1:
+            err = row_rel_err(last.cpu().numpy(), ref)
+            print(f"prefill of {lp}: last-position relative logit error {err:.2e}")
+            assert err <= TOL
