@@ -13,8 +13,9 @@ method's cost).
 
 The headline is B = 256 (the paper's capture size); --sweep adds further
 fixed sizes.  Alongside: per-kernel durations measured with HIP events on the
-engine's stream, the roofline of the dominant kernel, a bit-exactness check
-across two batch mixes, and the CPU oracle timed on a bounded sample.
+engine's stream, the roofline of the dominant kernel (against the published
+peak, and against what a plain device copy reaches here), a bit-exactness
+check across two batch mixes, and the CPU oracle timed on a bounded sample.
 Prints one JSON line.
 """
 from __future__ import annotations
@@ -510,6 +511,47 @@ def _cpu_name():
     return "unknown"
 
 
+def achievable_peaks():
+    """What this device reaches on plain vendor work, reported beside the
+    published peaks: HBM reads from a row-wise sum over a 1 GiB fp32 matrix
+    (65536 x 4096; the fastest of torch's plain reductions measured here),
+    HBM read + write from a 1 GiB device-to-device copy, bf16 matrix-core
+    throughput from an 8192^3 bf16 matmul (torch's vendor GEMM); best of 10
+    launches each, timed with HIP events on torch's current stream, where
+    they run.  1 GiB is four times the last-level cache."""
+    import torch
+
+    def best_ms(fn, n=10):
+        fn()
+        best = float("inf")
+        for _ in range(n):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            best = min(best, e0.elapsed_time(e1))
+        return best
+
+    x = torch.ones(65536, 4096, dtype=torch.float32, device="cuda")
+    rd = x.numel() * 4 / (best_ms(lambda: x.sum(1)) * 1e-3) / 1e9
+    del x
+    src = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
+    dst = torch.empty_like(src)
+    cp = 2 * src.numel() * 2 / (best_ms(lambda: dst.copy_(src)) * 1e-3) / 1e9
+    del src, dst
+    n = 8192
+    g = torch.Generator(device="cuda").manual_seed(0)
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16, generator=g)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16, generator=g)
+    mfma = 2 * n ** 3 / (best_ms(lambda: torch.matmul(a, b)) * 1e-3) / 1e12
+    del a, b
+    torch.cuda.empty_cache()
+    return dict(hbm_read_gbs=round(rd, 1), hbm_read_source="row sums of a 65536 x 4096 fp32 matrix (1 GiB read)",
+                hbm_copy_gbs=round(cp, 1), hbm_copy_source="1 GiB device-to-device copy, (read + written bytes) / time",
+                mfma_bf16_tflops=round(mfma, 1), mfma_source="8192^3 bf16 matmul through torch (vendor GEMM)")
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -605,12 +647,21 @@ def main():
         torch.cuda.synchronize()
         log("[bench] calibration copy: 1 GiB read + 1 GiB written")
 
+    peaks = achievable_peaks()
+    log(f"[bench] achievable on this device: HBM read {peaks['hbm_read_gbs']} GB/s (row sums), "
+        f"read + write {peaks['hbm_copy_gbs']} GB/s (device copy), "
+        f"bf16 MFMA {peaks['mfma_bf16_tflops']} TFLOP/s (vendor GEMM)")
+    g = head.get("gemm_phase")
+    if g:
+        g["mfma_frac_of_achievable"] = round(g["mfma_frac"] * MFMA_BF16_PEAK_TFLOPS / peaks["mfma_bf16_tflops"], 4)
+        g["hbm_frac_of_achievable"] = round(g["hbm_frac"] * HBM_PEAK_GBS / peaks["hbm_read_gbs"], 4)
     kern = head["kernels"]
     dom_name, dom = max(kern.items(), key=lambda kv: kv[1]["us"] * kv[1]["per_step"])
     traffic, traffic_src = measured_traffic(dom_name, args.B, head["seeds"][len(head["seeds"]) // 2])
     roof = dict(kernel=dom_name, bound="hbm", achieved=dom["gbs"], peak=HBM_PEAK_GBS, unit="GB/s",
                 frac=round(dom["gbs"] / HBM_PEAK_GBS, 4), traffic=traffic,
-                bytes_per_launch=dom["bytes"], us_per_launch=dom["us"], traffic_source=traffic_src)
+                bytes_per_launch=dom["bytes"], us_per_launch=dom["us"], traffic_source=traffic_src,
+                achievable_peak=peaks["hbm_read_gbs"], frac_of_achievable=round(dom["gbs"] / peaks["hbm_read_gbs"], 4))
     out = {
         "metric": METRIC,
         "value": head["live_tok_s"],
@@ -629,6 +680,7 @@ def main():
                    "weights": "seeded N(0, 0.02) bf16", "steps_per_seed": args.steps, "seeds": args.seeds},
         "roofline": roof,
         "cpu_baseline": cpu,
+        "achievable_peaks": peaks,
         "bitexact_across_batch_mixes": bitexact,
         "sampler": sampler,
         "headline": head,
