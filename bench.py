@@ -651,10 +651,14 @@ def main():
     log(f"[bench] achievable on this device: HBM read {peaks['hbm_read_gbs']} GB/s (row sums), "
         f"read + write {peaks['hbm_copy_gbs']} GB/s (device copy), "
         f"bf16 MFMA {peaks['mfma_bf16_tflops']} TFLOP/s (vendor GEMM)")
+    for r in [head] + sweep:
+        r["step_hbm_frac_of_achievable"] = round(r["step_hbm_frac"] * HBM_PEAK_GBS / peaks["hbm_read_gbs"], 4)
+        gp = r.get("gemm_phase")
+        if gp:
+            gp["hbm_frac_of_achievable"] = round(gp["hbm_frac"] * HBM_PEAK_GBS / peaks["hbm_read_gbs"], 4)
     g = head.get("gemm_phase")
     if g:
         g["mfma_frac_of_achievable"] = round(g["mfma_frac"] * MFMA_BF16_PEAK_TFLOPS / peaks["mfma_bf16_tflops"], 4)
-        g["hbm_frac_of_achievable"] = round(g["hbm_frac"] * HBM_PEAK_GBS / peaks["hbm_read_gbs"], 4)
     kern = head["kernels"]
     dom_name, dom = max(kern.items(), key=lambda kv: kv[1]["us"] * kv[1]["per_step"])
     traffic, traffic_src = measured_traffic(dom_name, args.B, head["seeds"][len(head["seeds"]) // 2])
