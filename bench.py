@@ -567,6 +567,9 @@ def main():
                     help="skip the 32B paged, MoE and prefill workloads")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="also run one plain 1 GiB device copy (reference for HBM traffic counters)")
+    ap.add_argument("--prefill-only", default="",
+                    help="profiling aid: time only the isolated prefill of these prompt lengths (comma list) "
+                         "and print their results as one JSON line instead of the decode benchmark")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -587,6 +590,10 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] weights {wl.streamed_weight_params(cfg) * 2 / 1e9:.2f} GB streamed per step, "
         f"made in {time.time() - t0:.1f}s")
+    if args.prefill_only:
+        lens = [int(x) for x in args.prefill_only.split(",") if x.strip()]
+        print(json.dumps({"prefill_8b": bench_prefill(cfg, W, lens, args)}), flush=True)
+        return
 
     head = run_B(cfg, W, args.B, args, seeds=list(range(args.first_seed, args.first_seed + args.seeds)),
                  measure_kernels=True)
