@@ -647,6 +647,7 @@ def main():
         extra["decode_moe"] = _drop(rm)
         del Wm
         torch.cuda.empty_cache()
+    peaks = achievable_peaks()          # before the calibration copy, which stays the run's last dispatch
     if args.calibrate_copy:
         src = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
         dst = torch.empty_like(src)
@@ -654,7 +655,6 @@ def main():
         torch.cuda.synchronize()
         log("[bench] calibration copy: 1 GiB read + 1 GiB written")
 
-    peaks = achievable_peaks()
     log(f"[bench] achievable on this device: HBM read {peaks['hbm_read_gbs']} GB/s (row sums), "
         f"read + write {peaks['hbm_copy_gbs']} GB/s (device copy), "
         f"bf16 MFMA {peaks['mfma_bf16_tflops']} TFLOP/s (vendor GEMM)")

@@ -279,6 +279,7 @@ struct corun_engine {
     char *ws = nullptr;
     size_t ws_bytes = 0;
     int32_t *d_tokens = nullptr, *d_seq = nullptr, *d_next = nullptr, *d_hist = nullptr, *d_counter = nullptr;
+    int32_t *d_order = nullptr, *h_order = nullptr;   // attention's row dispatch order
     uint8_t *d_valid = nullptr;
     float *x = nullptr, *p_qkv = nullptr, *p_o = nullptr, *p_gu = nullptr, *p_down = nullptr, *attn_ws = nullptr,
           *logits = nullptr, *p_lm = nullptr;
@@ -596,7 +597,8 @@ corun_status launch_one(corun_engine *e, int which, int l)
         HIP_TRY(launch_attn_split(e->q, B, e->d_valid, e->d_seq, nullptr, -1, nq, nkv, d, e->kc[l], e->vc[l],
                                   e->view, p.chunk, p.max_splits, e->attn_ws, st,
                                   e->qkv_in_attn ? QkvIn{e->p_qkv, p.qkv.S, (long long)B * nqkv, e->rope}
-                                                 : QkvIn{}));
+                                                 : QkvIn{},
+                                  e->d_order));
         break;
     case CORUN_K_ATTN_MERGE:
         HIP_TRY(launch_attn_merge(e->attn_ws, B, e->d_valid, e->d_seq, nq, nkv, d, p.chunk, p.max_splits, e->o, st));
@@ -934,6 +936,7 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     cv.take(&e->d_counter, 4);
     cv.take(&e->d_hist, (size_t)e->hist_cap * B);
     cv.take(&e->d_valid, B);
+    cv.take(&e->d_order, B);
     cv.take(&e->x, (size_t)B * H);
     cv.take(&e->p_qkv, proj_part_elems(p.qkv, B));
     cv.take(&e->p_o, proj_part_elems(p.o, B));
@@ -968,7 +971,8 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     e->ws_bytes = total;
     if (hipMalloc(&e->ws, total) != hipSuccess) return bail(fail(CORUN_E_HIP, "workspace allocation of %zu bytes", total));
     rebase(e->d_tokens, e->ws); rebase(e->d_seq, e->ws); rebase(e->d_next, e->ws); rebase(e->d_counter, e->ws);
-    rebase(e->d_hist, e->ws); rebase(e->d_valid, e->ws); rebase(e->x, e->ws); rebase(e->p_qkv, e->ws);
+    rebase(e->d_hist, e->ws); rebase(e->d_valid, e->ws); rebase(e->d_order, e->ws); rebase(e->x, e->ws);
+    rebase(e->p_qkv, e->ws);
     rebase(e->p_o, e->ws); rebase(e->p_gu, e->ws); rebase(e->p_down, e->ws); rebase(e->attn_ws, e->ws);
     rebase(e->logits, e->ws); rebase(e->p_lm, e->ws); rebase(e->amax, e->ws); rebase(e->h, e->ws); rebase(e->q, e->ws); rebase(e->o, e->ws); rebase(e->a, e->ws);
     rebase(e->rope, e->ws);
@@ -984,10 +988,11 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     const size_t rope_off = (size_t)((char *)e->rope - e->ws);
     if (launch_fill_u32((uint32_t *)e->ws, (long long)(rope_off / 4), fillv, e->st) != hipSuccess ||
         launch_fill_u32((uint32_t *)e->d_counter, 1, (uint32_t)e->hist_cap, e->st) != hipSuccess ||
-        launch_rope_table(e->rope, rope_len, d, (double)cfg->rope_theta, e->st) != hipSuccess)
+        launch_rope_table(e->rope, rope_len, d, (double)cfg->rope_theta, e->st) != hipSuccess ||
+        launch_iota(e->d_order, B, e->st) != hipSuccess)   // a valid row order before the first upload
         return bail(fail(CORUN_E_HIP, "workspace initialisation failed"));
 
-    if (hipHostMalloc((void **)&e->h_tok, sizeof(int32_t) * B * 4 + 64, 0) != hipSuccess ||
+    if (hipHostMalloc((void **)&e->h_tok, sizeof(int32_t) * B * 5 + 64, 0) != hipSuccess ||
         hipHostMalloc((void **)&e->h_valid, B + 64, 0) != hipSuccess ||
         hipHostMalloc((void **)&e->h_hist, sizeof(int32_t) * (size_t)e->hist_cap * B, 0) != hipSuccess ||
         hipHostMalloc((void **)&e->h_samp, (size_t)B * 32 + 256, 0) != hipSuccess)
@@ -995,6 +1000,7 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     e->h_seq = e->h_tok + B;
     e->h_next = e->h_tok + 2 * B;
     e->h_counter = e->h_tok + 3 * B;
+    e->h_order = e->h_tok + 4 * B;
 
     if (o.max_prefill_len > 0) {
         e->pf_max = o.max_prefill_len;
@@ -1040,6 +1046,15 @@ static corun_status upload_inputs(corun_engine *e, const int32_t *tokens, const 
     std::memcpy(e->h_seq, seq_lens, sizeof(int32_t) * B);
     std::memcpy(e->h_valid, valid, B);
     *e->h_counter = counter;
+    // attention dispatches live rows longest first, padding rows last; the
+    // order moves only work between workgroups, never a row's arithmetic
+    for (int r = 0; r < B; ++r) e->h_order[r] = r;
+    std::stable_sort(e->h_order, e->h_order + B, [&](int32_t a, int32_t b) {
+        const bool va = valid[a] != 0, vb = valid[b] != 0;
+        if (va != vb) return va;
+        return va && seq_lens[a] > seq_lens[b];
+    });
+    HIP_TRY(hipMemcpyAsync(e->d_order, e->h_order, sizeof(int32_t) * B, hipMemcpyHostToDevice, e->st));
     HIP_TRY(hipMemcpyAsync(e->d_tokens, e->h_tok, sizeof(int32_t) * B, hipMemcpyHostToDevice, e->st));
     HIP_TRY(hipMemcpyAsync(e->d_seq, e->h_seq, sizeof(int32_t) * B, hipMemcpyHostToDevice, e->st));
     HIP_TRY(hipMemcpyAsync(e->d_valid, e->h_valid, B, hipMemcpyHostToDevice, e->st));

@@ -138,7 +138,8 @@ hipError_t launch_qkv_post(const float *part, int S, long long part_stride, int 
 hipError_t launch_attn_split(const uint16_t *q, int rows, const uint8_t *valid, const int32_t *pos,
                              const int32_t *slot_of_row, int slot_const, int nq, int nkv, int d,
                              uint16_t *kc, uint16_t *vc, KvView kv, int chunk,
-                             int max_splits, float *ws, hipStream_t st, QkvIn qi = QkvIn{});
+                             int max_splits, float *ws, hipStream_t st, QkvIn qi = QkvIn{},
+                             const int32_t *row_order = nullptr);
 hipError_t launch_attn_merge(const float *ws, int rows, const uint8_t *valid, const int32_t *pos,
                              int nq, int nkv, int d, int chunk, int max_splits, uint16_t *o,
                              hipStream_t st);

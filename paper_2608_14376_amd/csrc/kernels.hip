@@ -1125,7 +1125,8 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
                                                     const int32_t *__restrict__ slot_of_row, int slot_const,
                                                     int nq, int nkv, uint16_t *__restrict__ kc,
                                                     uint16_t *__restrict__ vc, KvView kv, int chunk,
-                                                    int max_splits, float *__restrict__ ws, QkvIn qi)
+                                                    int max_splits, float *__restrict__ ws, QkvIn qi,
+                                                    const int32_t *__restrict__ row_order)
 {
     constexpr int ET = D / 16;
     constexpr int KCH = D / 8;                        // 16-byte chunks per key row
@@ -1145,7 +1146,7 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
     // so the concurrently streamed value rows (2 max_seq_len bytes apart
     // within a head) spread over the memory channels; with the splits of one
     // head side by side instead, a load-only replica streamed 11% slower
-    const int kvh = blockIdx.x, split = blockIdx.y, r = blockIdx.z;
+    const int kvh = blockIdx.x, split = blockIdx.y, r = row_order != nullptr ? row_order[blockIdx.z] : blockIdx.z;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     if (valid != nullptr && !valid[r]) return;
     const int n = pos[r] + 1;
@@ -1591,10 +1592,11 @@ __global__ __launch_bounds__(256) void k_attn_merge_kv(const float *__restrict__
 template <int D, int G>
 static void launch_attn_dg(const uint16_t *q, int rows, const uint8_t *valid, const int32_t *pos,
                            const int32_t *slot_of_row, int slot_const, int nq, int nkv, uint16_t *kc,
-                           uint16_t *vc, KvView kv, int chunk, int max_splits, float *ws, hipStream_t st, QkvIn qi)
+                           uint16_t *vc, KvView kv, int chunk, int max_splits, float *ws, hipStream_t st, QkvIn qi,
+                           const int32_t *row_order)
 {
     hipLaunchKernelGGL((k_attn_split<D, G>), dim3(nkv, max_splits, rows), dim3(256), 0, st, q, valid, pos,
-                       slot_of_row, slot_const, nq, nkv, kc, vc, kv, chunk, max_splits, ws, qi);
+                       slot_of_row, slot_const, nq, nkv, kc, vc, kv, chunk, max_splits, ws, qi, row_order);
 }
 
 template <int D, int G>
@@ -1641,10 +1643,10 @@ static void launch_merge_dg(const float *ws, int rows, const uint8_t *valid, con
 hipError_t launch_attn_split(const uint16_t *q, int rows, const uint8_t *valid, const int32_t *pos,
                              const int32_t *slot_of_row, int slot_const, int nq, int nkv, int d,
                              uint16_t *kc, uint16_t *vc, KvView kv, int chunk, int max_splits,
-                             float *ws, hipStream_t st, QkvIn qi)
+                             float *ws, hipStream_t st, QkvIn qi, const int32_t *row_order)
 {
     CORUN_ATTN_DISPATCH(launch_attn_dg, q, rows, valid, pos, slot_of_row, slot_const, nq, nkv, kc, vc, kv, chunk,
-                        max_splits, ws, st, qi);
+                        max_splits, ws, st, qi, row_order);
     return hipGetLastError();
 }
 
