@@ -376,8 +376,8 @@ def bench_bi_tradeoff(cfg, W, K, V, args):
         sk[name] = dict(n_live=int(b.valid.sum()), split_on_ms=on_ms, split_off_ms=off_ms,
                         off_cost=round(off_ms / on_ms - 1, 4))
     out["split_kv_B256"] = sk
-    log(f"[bench] split-KV off at B=256: ragged +{100 * sk['ragged']['off_cost']:.1f}%, "
-        f"similar +{100 * sk['similar']['off_cost']:.1f}%")
+    log(f"[bench] split-KV off at B=256: ragged {100 * sk['ragged']['off_cost']:+.1f}%, "
+        f"similar {100 * sk['similar']['off_cost']:+.1f}%")
     return out
 
 
