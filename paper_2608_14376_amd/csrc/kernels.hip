@@ -1145,7 +1145,9 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
     // grid (kv head, split, row): the kv heads of a split run side by side,
     // so the concurrently streamed value rows (2 max_seq_len bytes apart
     // within a head) spread over the memory channels; with the splits of one
-    // head side by side instead, a load-only replica streamed 11% slower
+    // head side by side instead, a load-only replica streamed 11% slower.
+    // Grid z takes the rows in row_order when given (the host puts live rows
+    // longest first): any permutation of 0..rows-1 gives the same results.
     const int kvh = blockIdx.x, split = blockIdx.y, r = row_order != nullptr ? row_order[blockIdx.z] : blockIdx.z;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     if (valid != nullptr && !valid[r]) return;
