@@ -123,3 +123,27 @@ def test_prefill_fills_the_workspace(model):
     with pytest.raises(corun.CorunError):
         eng.prefill(wl.make_prompt(cfg["vocab"], L + 1, seed=91), 0)
     eng.close()
+
+
+@pytest.mark.parametrize("poison", [False, True])
+def test_attention_before_the_first_step(poison):
+    """The attention kernel's row order is valid from creation: timing it on
+    a fresh engine, before any step has uploaded inputs, runs (the cleared or
+    poisoned workspace makes every block exit at once), and a step afterwards
+    still matches a fresh engine's bit for bit."""
+    cfg = wl.config("tiny")
+    Wg = to_device(wl.make_weights(cfg, seed=71))
+    B = 4
+    K, V = wl.make_kv_contiguous(cfg, B, 160, seed=72, device=DEV)
+    b = wl.make_batch(B, cfg["vocab"], seed=73, len_lo=16, len_hi=128)
+    outs = []
+    for timed_first in (True, False):
+        eng = corun.Engine(cfg, Wg, B, [k.clone() for k in K], [v.clone() for v in V],
+                           opt=corun.options(poison_workspace=poison))
+        if timed_first:
+            assert eng.time_kernel(corun.K_ATTN_SPLIT, 0, 3) > 0
+        logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+        eng.decode_step(b.tokens, b.valid, b.seq_lens, logits)
+        outs.append(logits.cpu().numpy().view(np.int32)[b.valid == 1])
+        eng.close()
+    assert np.array_equal(outs[0], outs[1])
