@@ -144,6 +144,10 @@ typedef struct {
                                   from B (inside the attention kernel for B_fixed <= 8, where it saves a launch;
                                   its own kernel above, where recomputing q in every attention block costs
                                   more); 1 = its own kernel; 2 = inside attention.  Bit-identical results. */
+    int32_t record_routing;    /* 1 = mixture-of-experts engines keep, for every layer, each row's chosen experts
+                                  and the router logits they were chosen from, for the last decode step and the
+                                  last prefill call (corun_routing_trace).  Extra workspace of
+                                  n_layers x rows x (top_k + n_experts) x 4 bytes; results are unchanged. */
 } corun_options;
 
 /* Create an engine for one fixed padded batch size B_fixed (Sec. IV,
@@ -189,7 +193,8 @@ corun_status corun_decode_run(corun_engine *e, int32_t n_steps, const int32_t *t
 
 /* Isolated prefill of one prompt into `slot` (Sec. IV, "Isolated Prefill";
  * the base case of the determinism argument): the prompt runs alone, with a
- * launch plan that depends only on prompt_len, writes k, v for positions
+ * launch plan that depends only on prompt_len (not on the engine's max_prefill_len;
+ * corun_describe_prefill_plan), writes k, v for positions
  * 0..prompt_len-1 of the slot in every layer, and samples the first token
  * greedily from the last position's logits (Sec. IV, "Shape-Aligned
  * Sampling": one sampling row).
@@ -208,8 +213,9 @@ corun_status corun_prefill(corun_engine *e, const int32_t *prompt, int32_t promp
  * at those positions of `slot` in every layer, and their queries attend to
  * positions 0 .. t of the slot's cache, the first `start` of which the
  * caller must already have written (the prompt's earlier chunks, in order).
- * The launch plan depends on (n, start) only, so with a chunk size fixed per
- * deployment a prompt always runs as the same sequence of shapes.
+ * The launch plan depends on n only (corun_describe_prefill_plan), so with a
+ * chunk size fixed per deployment a prompt always runs as the same sequence
+ * of shapes, on any engine of the model.
  *  tokens      host int32 [n]: the prompt's tokens at those positions
  *  token_out   host int32 out, or NULL: greedy token from position
  *              start+n-1 (the first generated token if this is the last chunk)
@@ -247,6 +253,20 @@ corun_status corun_prefill_batch(corun_engine *e, const int32_t *tokens, const i
  * (copies; the k/v/page-table pointers are the caller's borrowed ones).
  * Any out pointer may be NULL. */
 corun_status corun_engine_info(const corun_engine *e, int32_t *B_fixed, corun_model_cfg *cfg, corun_kv *kv);
+
+/* Routing record of a mixture-of-experts engine created with record_routing
+ * (Sec. VII names the router as the fragile point of a mixture of experts: a
+ * top-k choice is a comparison of floating-point logits).  source 0 = the
+ * last decode step (rows = B_fixed), 1 = the last prefill call (rows = its
+ * row count: prompt_len, the chunk length, or the batch's total tokens).
+ *  sel     host int32 [n_layers][rows][top_k] out, or NULL: the experts each
+ *          row was routed to in rank order (-1 for decode padding rows)
+ *  logits  host fp32 [n_layers][rows][n_experts] out, or NULL: the router
+ *          logits the choice was made from (unspecified for padding rows)
+ *  rows_out host int32 out
+ * Waits for the engine's stream.  Errors: CORUN_E_STATE (dense model, no
+ * record_routing, or source 1 without a prefill workspace), CORUN_E_INVAL. */
+corun_status corun_routing_trace(corun_engine *e, int32_t source, int32_t *sel, float *logits, int32_t *rows_out);
 
 /* Request-bound seeded multinomial sampling (Sec. IV, "Shape-Aligned
  * Sampling"; y_t = S(l_t, R(s, t)) in Sec. IV, "Determinism Argument"), run on
@@ -351,12 +371,15 @@ enum {
 /* Measurement aid: launch one kernel of the decode step n_iters times back
  * to back on the engine's stream, launch i using layer (layer + i) mod
  * n_layers (so weights and cache stream from HBM as in the step) and the
- * engine's current workspace and inputs (as left by the last step), and
- * return the mean duration per launch in microseconds, measured with HIP
- * events around the launches.  Call after at least one decode step.
- * Re-running a kernel rewrites the same workspace values it wrote in the
- * step (the residual-folding RMSNorm adds its partials again; the next step
- * recomputes the residual from the embedding). */
+ * engine's current workspace (as left by the last step), and return the mean
+ * duration per launch in microseconds, measured with HIP events around the
+ * launches.  The launches run on the inputs of the last decode step (tokens,
+ * valid mask, positions as validated by the call that ran it, uploaded again
+ * first: the step itself advanced the positions), so a kernel that appends
+ * to the cache rewrites the value that step wrote at that position.  Re-running a kernel rewrites the workspace
+ * values it wrote in the step (the residual-folding RMSNorm adds its
+ * partials again; the next step recomputes the residual from the
+ * embedding).  CORUN_E_STATE before the engine's first decode step. */
 corun_status corun_time_kernel(corun_engine *e, int32_t kernel, int32_t layer, int32_t n_iters, float *avg_us);
 
 /* Host-only checks, usable without a GPU: the shape rules of
@@ -375,6 +398,17 @@ corun_status corun_check_batch(const corun_model_cfg *cfg, const corun_kv *kv, c
  * count (32 values).  Returns the count written or a negative corun_status. */
 int32_t corun_describe_plan(const corun_model_cfg *cfg, const corun_kv *kv, int32_t B_fixed,
                             const corun_options *opt, int32_t *out, int32_t cap);
+
+/* The projection plan of a prefill call over n rows (host-only, no GPU):
+ * (N, K, split_k, k_chunk, m_tile, n_tile) for the qkv, o, gate_up, down and
+ * router projections (zeros where the model has none), 30 values.  It is a
+ * function of (cfg, n, batch_invariant or bi_prefill) only -- not of the
+ * engine's max_prefill_len, whose workspace holds the partials of any plan
+ * up to that length (Sec. IV, "Isolated Prefill": a prompt's prefill shape
+ * is fixed by the prompt).  Returns the count written or a negative
+ * corun_status. */
+int32_t corun_describe_prefill_plan(const corun_model_cfg *cfg, int32_t n, const corun_options *opt, int32_t *out,
+                                    int32_t cap);
 
 /* Message for the calling thread's last non-OK status ("" if none). */
 const char *corun_last_error(void);

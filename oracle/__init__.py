@@ -86,9 +86,16 @@ def lib():
         L.orc_decode_row.restype = C.c_int
         L.orc_decode_row.argtypes = [C.POINTER(_Cfg), C.POINTER(_Weights), C.POINTER(_KV),
                                      C.c_int, C.c_int, C.c_int, C.c_void_p]
-        L.orc_decode_row_margin.restype = C.c_int
-        L.orc_decode_row_margin.argtypes = [C.POINTER(_Cfg), C.POINTER(_Weights), C.POINTER(_KV),
-                                            C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p]
+        L.orc_decode_row_routed.restype = C.c_int
+        L.orc_decode_row_routed.argtypes = [C.POINTER(_Cfg), C.POINTER(_Weights), C.POINTER(_KV),
+                                            C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p,
+                                            C.c_void_p]
+        L.orc_prefill_routed.restype = C.c_int
+        L.orc_prefill_routed.argtypes = [C.POINTER(_Cfg), C.POINTER(_Weights), C.POINTER(_KV), C.c_int,
+                                         C.c_void_p, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                         C.c_void_p]
+        L.orc_route_forced.restype = C.c_int
+        L.orc_route_forced.argtypes = [C.c_void_p, C.c_int, C.c_int, C.c_void_p, C.c_void_p]
         L.orc_decode_batch.restype = C.c_int
         L.orc_decode_batch.argtypes = [C.POINTER(_Cfg), C.POINTER(_Weights), C.POINTER(_KV), C.c_int,
                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
@@ -224,6 +231,17 @@ def route(logits: np.ndarray, top_k: int):
     return sel, w
 
 
+def route_forced(logits: np.ndarray, force) -> np.ndarray:
+    """Weights of a given expert set: softmax over all experts, renormalised
+    over the set, in the set's order."""
+    logits = np.ascontiguousarray(logits, np.float64)
+    f = np.ascontiguousarray(force, np.int32)
+    w = np.empty(f.size, np.float64)
+    if lib().orc_route_forced(_ptr(logits), logits.size, f.size, _ptr(f), _ptr(w)):
+        raise ValueError("malformed expert set")
+    return w
+
+
 # --------------------------------------------------------------------------
 # Whole model
 # --------------------------------------------------------------------------
@@ -310,17 +328,44 @@ def decode_row(m: Model, kv: KVCache, slot: int, token: int, pos: int) -> np.nda
     return logits
 
 
-def decode_row_margin(m: Model, kv: KVCache, slot: int, token: int, pos: int):
-    """decode_row plus the smallest top-k routing margin over the MoE layers
-    (the gap between the k-th and (k+1)-th router logits; inf if dense)."""
+def decode_row_routed(m: Model, kv: KVCache, slot: int, token: int, pos: int, force=None):
+    """decode_row of a mixture of experts with its routing exposed:
+    (logits [V], router logits [L, E] fp64, own top-k [L, k]).  force
+    ([L, k] int32, optional) makes layer l follow that expert set instead of
+    its own top-k (the records still hold the oracle's own choice)."""
+    c = m.cfg
+    L, E, k = c["n_layers"], c["n_experts"], c["top_k"]
     b = _Bound(m, kv)
-    logits = np.empty(m.cfg["vocab"], np.float64)
-    mg = np.empty(1, np.float64)
-    rc = lib().orc_decode_row_margin(C.byref(b.cfg), C.byref(b.w), C.byref(b.kv), slot, token, pos,
-                                     _ptr(logits), _ptr(mg))
+    logits = np.empty(c["vocab"], np.float64)
+    rl = np.empty((L, E), np.float64)
+    own = np.empty((L, k), np.int32)
+    f = None if force is None else np.ascontiguousarray(force, np.int32).reshape(L, k)
+    rc = lib().orc_decode_row_routed(C.byref(b.cfg), C.byref(b.w), C.byref(b.kv), slot, token, pos,
+                                     _ptr(logits), None if f is None else _ptr(f), _ptr(rl), _ptr(own))
     if rc:
-        raise ValueError("oracle rejected the row")
-    return logits, float(mg[0])
+        raise ValueError("oracle rejected the row or the forced routing")
+    return logits, rl, own
+
+
+def prefill_routed(m: Model, kv: KVCache, slot: int, prompt, force=None):
+    """prefill of a mixture of experts with its routing exposed: (logits of
+    the last position [V], token, router logits [L, Lp, E], own top-k
+    [L, Lp, k]); force [L, Lp, k] optional, as in decode_row_routed."""
+    c = m.cfg
+    L, E, k = c["n_layers"], c["n_experts"], c["top_k"]
+    prompt = np.ascontiguousarray(prompt, np.int32)
+    Lp = prompt.size
+    b = _Bound(m, kv)
+    logits = np.empty(c["vocab"], np.float64)
+    tok = np.empty(1, np.int32)
+    rl = np.empty((L, Lp, E), np.float64)
+    own = np.empty((L, Lp, k), np.int32)
+    f = None if force is None else np.ascontiguousarray(force, np.int32).reshape(L, Lp, k)
+    rc = lib().orc_prefill_routed(C.byref(b.cfg), C.byref(b.w), C.byref(b.kv), slot, _ptr(prompt), Lp,
+                                  _ptr(logits), _ptr(tok), None if f is None else _ptr(f), _ptr(rl), _ptr(own))
+    if rc:
+        raise ValueError("oracle rejected the prompt or the forced routing")
+    return logits, int(tok[0]), rl, own
 
 
 def decode_batch(m: Model, kv: KVCache, tokens, valid, seq_lens):

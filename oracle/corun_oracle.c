@@ -338,29 +338,48 @@ void orc_route(const double *logits, int E, int top_k, int32_t *sel, double *wse
     free(p); free(used);
 }
 
-/* Gap between the top_k-th and the (top_k+1)-th largest router logits: how
- * far the routing decision is from a tie (diagnostic; +inf when E == top_k). */
-static double route_margin(const double *logits, int E, int top_k)
+/* Routing that follows a given expert set instead of the top_k: the same
+ * softmax over all experts, the chosen experts' probabilities renormalised
+ * over the given set, combined in the given order.  (A top-k choice is a
+ * comparison of floating-point logits; where two logits are closer than a
+ * computation's error, either choice is a correct result, and a test uses
+ * this to follow the choice another computation made.)  Returns -1 unless
+ * the set holds top_k distinct ids in [0, E). */
+int orc_route_forced(const double *logits, int E, int top_k, const int32_t *force, double *wsel)
 {
-    double kth = INFINITY, next = -INFINITY;
-    char *used = calloc((size_t)E, 1);
-    for (int r = 0; r <= top_k && r < E; ++r) {
-        int best = -1;
-        for (int e = 0; e < E; ++e)
-            if (!used[e] && (best < 0 || logits[e] > logits[best])) best = e;
-        used[best] = 1;
-        if (r == top_k - 1) kth = logits[best];
-        if (r == top_k) next = logits[best];
+    for (int r = 0; r < top_k; ++r) {
+        if (force[r] < 0 || force[r] >= E) return -1;
+        for (int q = 0; q < r; ++q)
+            if (force[q] == force[r]) return -1;
     }
-    free(used);
-    return kth - next;
+    double m = -INFINITY;
+    for (int e = 0; e < E; ++e) if (logits[e] > m) m = logits[e];
+    double z = 0.0;
+    for (int e = 0; e < E; ++e) z += exp(logits[e] - m);
+    double s = 0.0;
+    for (int r = 0; r < top_k; ++r) {
+        wsel[r] = exp(logits[force[r]] - m) / z;
+        s += wsel[r];
+    }
+    for (int r = 0; r < top_k; ++r) wsel[r] /= s;
+    return 0;
 }
+
+/* Per-row routing controls and records of one MoE layer (all optional):
+ * force [top_k] = follow this expert set; logits_out [E] = the router
+ * logits; sel_out [top_k] = the oracle's own top_k choice. */
+typedef struct {
+    const int32_t *force;
+    double *logits_out;
+    int32_t *sel_out;
+} orc_route_io;
 
 /* Feed-forward sub-layer for one row: RMSNorm, then either the dense SwiGLU
  * MLP or the routed mixture of SwiGLU experts, added to the residual x.
- * margin (optional) receives the minimum routing margin seen. */
-static void mlp_block(const orc_cfg *c, const orc_weights *w, int layer, float *x, double *margin)
+ * Returns -1 if a forced expert set is malformed. */
+static int mlp_block(const orc_cfg *c, const orc_weights *w, int layer, float *x, orc_route_io io)
 {
+    int rc = 0;
     int H = c->hidden;
     uint16_t *h = malloc(sizeof(uint16_t) * H);
     double *y = malloc(sizeof(double) * H);
@@ -375,11 +394,13 @@ static void mlp_block(const orc_cfg *c, const orc_weights *w, int layer, float *
         double *ws = malloc(sizeof(double) * K);
         double *acc = calloc((size_t)H, sizeof(double));
         orc_linear(h, H, w->w_router[layer], E, rl);
-        if (margin) {
-            double mg = route_margin(rl, E, K);
-            if (mg < *margin) *margin = mg;
-        }
         orc_route(rl, E, K, sel, ws);
+        if (io.logits_out) memcpy(io.logits_out, rl, sizeof(double) * E);
+        if (io.sel_out) memcpy(io.sel_out, sel, sizeof(int32_t) * K);
+        if (io.force) {
+            rc = orc_route_forced(rl, E, K, io.force, ws);
+            memcpy(sel, io.force, sizeof(int32_t) * K);
+        }
         for (int r = 0; r < K; ++r) {     /* combine in rank order */
             int e = sel[r];
             swiglu_mlp(h, H, Fe, w->w_exp_gate_up[layer] + (int64_t)e * 2 * Fe * H,
@@ -390,6 +411,7 @@ static void mlp_block(const orc_cfg *c, const orc_weights *w, int layer, float *
         free(rl); free(sel); free(ws); free(acc);
     }
     free(h); free(y);
+    return rc;
 }
 
 static void lm_head(const orc_cfg *c, const orc_weights *w, const float *x, double *logits)
@@ -405,29 +427,35 @@ static void lm_head(const orc_cfg *c, const orc_weights *w, const float *x, doub
 /* one token of one request at position pos (= tokens already cached),      */
 /* appending its k, v at pos in every layer and returning fp64 logits.      */
 /* ------------------------------------------------------------------------ */
-/* As orc_decode_row; route_margin (optional) receives the smallest top-k
- * routing margin over the MoE layers (+inf for a dense model). */
-int orc_decode_row_margin(const orc_cfg *c, const orc_weights *w, const orc_kv *kv,
-                          int slot, int token, int pos, double *logits, double *route_margin_out)
+/* As orc_decode_row, for a mixture of experts with routing controls per
+ * layer (each optional): force [L][top_k] = the expert set layer l follows
+ * (its own top_k where NULL), router_logits [L][E] and own_sel [L][top_k]
+ * receive each layer's router logits and own top_k choice. */
+int orc_decode_row_routed(const orc_cfg *c, const orc_weights *w, const orc_kv *kv, int slot, int token,
+                          int pos, double *logits, const int32_t *force, double *router_logits,
+                          int32_t *own_sel)
 {
     if (token < 0 || token >= c->vocab || pos < 0) return -1;
-    int H = c->hidden;
+    int H = c->hidden, E = c->n_experts, K = c->top_k;
     float *x = malloc(sizeof(float) * H);
-    if (route_margin_out) *route_margin_out = INFINITY;
+    int rc = 0;
     for (int i = 0; i < H; ++i) x[i] = (float)bf(w->embed[(int64_t)token * H + i]);
-    for (int l = 0; l < c->n_layers; ++l) {
+    for (int l = 0; l < c->n_layers && !rc; ++l) {
+        orc_route_io io = {force ? force + (int64_t)l * K : NULL,
+                           router_logits ? router_logits + (int64_t)l * E : NULL,
+                           own_sel ? own_sel + (int64_t)l * K : NULL};
         attn_block(c, w, kv, l, slot, pos, x);
-        mlp_block(c, w, l, x, route_margin_out);
+        rc = mlp_block(c, w, l, x, io);
     }
-    lm_head(c, w, x, logits);
+    if (!rc) lm_head(c, w, x, logits);
     free(x);
-    return 0;
+    return rc;
 }
 
 int orc_decode_row(const orc_cfg *c, const orc_weights *w, const orc_kv *kv,
                    int slot, int token, int pos, double *logits)
 {
-    return orc_decode_row_margin(c, w, kv, slot, token, pos, logits, NULL);
+    return orc_decode_row_routed(c, w, kv, slot, token, pos, logits, NULL, NULL, NULL);
 }
 
 /* The padded decode step at batch size B, computed row by row: each live row
@@ -464,22 +492,36 @@ int orc_decode_batch(const orc_cfg *c, const orc_weights *w, const orc_kv *kv, i
 /* sums run in the same order as in orc_decode_row, so prefill(p ++ [t]) at  */
 /* its last row equals prefill(p) followed by decode(t), bit for bit.        */
 /* ------------------------------------------------------------------------ */
-int orc_prefill(const orc_cfg *c, const orc_weights *w, const orc_kv *kv, int slot,
-                const int32_t *prompt, int Lp, double *logits, int32_t *token_out)
+/* As orc_prefill, with the routing controls of orc_decode_row_routed for
+ * every (layer, position): force [L][Lp][top_k], router_logits [L][Lp][E],
+ * own_sel [L][Lp][top_k], each optional. */
+int orc_prefill_routed(const orc_cfg *c, const orc_weights *w, const orc_kv *kv, int slot,
+                       const int32_t *prompt, int Lp, double *logits, int32_t *token_out,
+                       const int32_t *force, double *router_logits, int32_t *own_sel)
 {
     if (Lp <= 0) return -1;
     for (int t = 0; t < Lp; ++t)
         if (prompt[t] < 0 || prompt[t] >= c->vocab) return -1;
-    int H = c->hidden;
+    int H = c->hidden, E = c->n_experts, K = c->top_k;
     float *X = malloc(sizeof(float) * (int64_t)Lp * H);
     for (int t = 0; t < Lp; ++t)
         for (int i = 0; i < H; ++i)
             X[(int64_t)t * H + i] = (float)bf(w->embed[(int64_t)prompt[t] * H + i]);
-    for (int l = 0; l < c->n_layers; ++l) {
+    int rc = 0;
+    for (int l = 0; l < c->n_layers && !rc; ++l) {
         /* positions in order: position t reads keys 0..t of this layer,
          * which positions 0..t have already written */
         for (int t = 0; t < Lp; ++t) attn_block(c, w, kv, l, slot, t, X + (int64_t)t * H);
-        for (int t = 0; t < Lp; ++t) mlp_block(c, w, l, X + (int64_t)t * H, NULL);
+        for (int t = 0; t < Lp && !rc; ++t) {
+            int64_t at = (int64_t)l * Lp + t;
+            orc_route_io io = {force ? force + at * K : NULL, router_logits ? router_logits + at * E : NULL,
+                               own_sel ? own_sel + at * K : NULL};
+            rc = mlp_block(c, w, l, X + (int64_t)t * H, io);
+        }
+    }
+    if (rc) {
+        free(X);
+        return rc;
     }
     lm_head(c, w, X + (int64_t)(Lp - 1) * H, logits);
     float *lf = malloc(sizeof(float) * c->vocab);
@@ -488,6 +530,12 @@ int orc_prefill(const orc_cfg *c, const orc_weights *w, const orc_kv *kv, int sl
     free(lf);
     free(X);
     return 0;
+}
+
+int orc_prefill(const orc_cfg *c, const orc_weights *w, const orc_kv *kv, int slot,
+                const int32_t *prompt, int Lp, double *logits, int32_t *token_out)
+{
+    return orc_prefill_routed(c, w, kv, slot, prompt, Lp, logits, token_out, NULL, NULL, NULL);
 }
 
 /* ---------------------------------------------------------------------------

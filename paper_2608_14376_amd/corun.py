@@ -19,8 +19,9 @@ OK, E_INVAL, E_SHAPE, E_CAPACITY, E_HIP, E_STATE = 0, -1, -2, -3, -4, -5
 KV_CONTIGUOUS, KV_PAGED = 0, 1
 
 EXPORTS = ("corun_engine_create", "corun_engine_destroy", "corun_decode_step", "corun_decode_run",
-           "corun_prefill", "corun_prefill_chunk", "corun_prefill_batch", "corun_check_config", "corun_check_batch", "corun_describe_plan",
-           "corun_last_error", "corun_time_kernel", "corun_sample", "corun_engine_info",
+           "corun_prefill", "corun_prefill_chunk", "corun_prefill_batch", "corun_check_config", "corun_check_batch",
+           "corun_describe_plan", "corun_describe_prefill_plan",
+           "corun_last_error", "corun_time_kernel", "corun_sample", "corun_engine_info", "corun_routing_trace",
            "corun_sched_create", "corun_sched_destroy", "corun_sched_add_request", "corun_sched_step",
            "corun_sched_output", "corun_sched_state", "corun_sched_last_error")
 
@@ -55,7 +56,7 @@ class KV(C.Structure):
 class Options(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "attn_chunk", "max_prefill_len", "no_graph", "poison_workspace", "split_k_override", "gemm_bm",
-        "batch_invariant", "bi_prefill", "no_weight_pack", "qkv_epilogue")]
+        "batch_invariant", "bi_prefill", "no_weight_pack", "qkv_epilogue", "record_routing")]
 
 
 class CorunError(RuntimeError):
@@ -101,6 +102,9 @@ def load():
     L.corun_describe_plan.restype = C.c_int32
     L.corun_describe_plan.argtypes = [C.POINTER(ModelCfg), C.POINTER(KV), C.c_int32, C.POINTER(Options),
                                       C.c_void_p, C.c_int32]
+    L.corun_describe_prefill_plan.restype = C.c_int32
+    L.corun_describe_prefill_plan.argtypes = [C.POINTER(ModelCfg), C.c_int32, C.POINTER(Options), C.c_void_p,
+                                              C.c_int32]
     L.corun_time_kernel.restype = st
     L.corun_time_kernel.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_float)]
     L.corun_sample.restype = st
@@ -108,6 +112,8 @@ def load():
                                C.c_void_p, C.c_void_p, C.c_void_p]
     L.corun_engine_info.restype = st
     L.corun_engine_info.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+    L.corun_routing_trace.restype = st
+    L.corun_routing_trace.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.POINTER(C.c_int32)]
     L.corun_sched_create.restype = st
     L.corun_sched_create.argtypes = [C.c_void_p, C.POINTER(SchedCfg), C.POINTER(C.c_void_p)]
     L.corun_sched_destroy.restype = None
@@ -162,9 +168,11 @@ def kv_struct(layout: int, n_slots: int, k, v, keep, max_seq_len=0, page_size=0,
 
 
 def options(attn_chunk=0, max_prefill_len=0, no_graph=False, poison_workspace=False, split_k_override=0,
-            gemm_bm=0, batch_invariant=False, bi_prefill=False, no_weight_pack=False, qkv_epilogue=0):
+            gemm_bm=0, batch_invariant=False, bi_prefill=False, no_weight_pack=False, qkv_epilogue=0,
+            record_routing=False):
     return Options(attn_chunk, max_prefill_len, int(no_graph), int(poison_workspace), split_k_override, gemm_bm,
-                   int(batch_invariant), int(bi_prefill), int(no_weight_pack), int(qkv_epilogue))
+                   int(batch_invariant), int(bi_prefill), int(no_weight_pack), int(qkv_epilogue),
+                   int(record_routing))
 
 
 def _np(a, dt):
@@ -197,6 +205,22 @@ def describe_plan(cfg: dict, kv: KV, B: int, opt: Options | None = None) -> dict
         N, K, S, Kc, bm, bn = v[2 + 6 * i: 8 + 6 * i]
         plan[name] = {"N": N, "K": K, "split_k": S, "k_chunk": Kc, "m_tile": bm, "n_tile": bn}
     plan["attn_chunk"], plan["attn_max_splits"] = v[32], v[33]
+    return plan
+
+
+def describe_prefill_plan(cfg: dict, n: int, opt: Options | None = None) -> dict:
+    """Projection plan of a prefill call over n rows (a function of the
+    model, n and the batch-invariant flags only)."""
+    c = model_cfg(cfg)
+    out = np.zeros(30, np.int32)
+    k = load().corun_describe_prefill_plan(C.byref(c), n, C.byref(opt) if opt else None, out.ctypes.data, 30)
+    if k < 0:
+        raise CorunError(k, last_error())
+    v = out[:k].tolist()
+    plan = {}
+    for i, name in enumerate(("qkv", "o", "gate_up", "down", "router")):
+        N, K, S, Kc, bm, bn = v[6 * i: 6 * i + 6]
+        plan[name] = {"N": N, "K": K, "split_k": S, "k_chunk": Kc, "m_tile": bm, "n_tile": bn}
     return plan
 
 
@@ -351,6 +375,19 @@ class Engine:
         _check(self._L.corun_decode_run(self._h, n_steps, t.ctypes.data, vm.ctypes.data, s.ctypes.data,
                                         out.ctypes.data))
         return out
+
+    def routing_trace(self, source: int = 0):
+        """(sel int32 [L, rows, top_k], router logits float32 [L, rows, E]) of
+        the last decode step (source 0) or prefill call (source 1); needs an
+        engine created with record_routing."""
+        L, k, E = self.cfg["n_layers"], self.cfg["top_k"], self.cfg["n_experts"]
+        rows = C.c_int32()
+        _check(self._L.corun_routing_trace(self._h, source, None, None, C.byref(rows)))
+        n = rows.value
+        sel = np.empty((L, n, k), np.int32)
+        lg = np.empty((L, n, E), np.float32)
+        _check(self._L.corun_routing_trace(self._h, source, sel.ctypes.data, lg.ctypes.data, C.byref(rows)))
+        return sel, lg
 
     def time_kernel(self, kernel: int, layer: int = 0, n_iters: int = 20) -> float:
         """Mean launch duration in microseconds (HIP events, engine stream)."""

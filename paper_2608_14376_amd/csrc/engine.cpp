@@ -272,6 +272,12 @@ struct corun_engine {
     float *pf_moe_w = nullptr, *pf_moe_gu = nullptr, *pf_moe_y = nullptr;
     int32_t *pf_moe_sel = nullptr, *pf_moe_list = nullptr, *pf_moe_tiles = nullptr;
     uint16_t *pf_moe_act = nullptr;
+    // routing record (record_routing): [L][B] decode rows, [L][max_prefill_len]
+    // prefill rows; pf_trace_rows = the rows of the last prefill call
+    int32_t *rt_sel = nullptr, *rt_pf_sel = nullptr;
+    float *rt_logit = nullptr, *rt_pf_logit = nullptr;
+    int pf_trace_rows = 0;
+    bool decoded = false;   // a decode step has uploaded inputs
     std::vector<uint16_t *> kc, vc;
     KvView view{};
 
@@ -393,6 +399,7 @@ static corun_status check_options(const corun_options &o)
     if (o.bi_prefill != 0 && o.bi_prefill != 1) return fail(CORUN_E_INVAL, "bi_prefill must be 0 or 1");
     if (o.no_weight_pack != 0 && o.no_weight_pack != 1) return fail(CORUN_E_INVAL, "no_weight_pack must be 0 or 1");
     if (o.qkv_epilogue < 0 || o.qkv_epilogue > 2) return fail(CORUN_E_INVAL, "qkv_epilogue must be 0, 1 or 2");
+    if (o.record_routing != 0 && o.record_routing != 1) return fail(CORUN_E_INVAL, "record_routing must be 0 or 1");
     if (o.batch_invariant && (o.attn_chunk || o.split_k_override || o.gemm_bm))
         return fail(CORUN_E_INVAL, "batch_invariant fixes the plan: attn_chunk, split_k_override and gemm_bm must be 0");
     return CORUN_OK;
@@ -506,14 +513,20 @@ struct MoeBufs {
     int32_t *sel, *list, *tiles;
     uint16_t *act;
     int slots;
+    // routing record (corun_options.record_routing): layer l's choice and
+    // router logits at sel_trace + l rows top_k and logit_trace + l rows E
+    int32_t *sel_trace = nullptr;
+    float *logit_trace = nullptr;
 };
 
 corun_status moe_router(corun_engine *e, const MoeBufs &m, const uint16_t *h, int rows, const Proj &pr, int l)
 {
     const corun_model_cfg &c = e->c;
     HIP_TRY(proj(e, h, c.hidden, W_ROUTER, l, pr, rows, m.router_part, (long long)rows * c.n_experts, c.n_experts));
+    int32_t *st_l = m.sel_trace ? m.sel_trace + (size_t)l * rows * c.top_k : nullptr;
+    float *lt_l = m.logit_trace ? m.logit_trace + (size_t)l * rows * c.n_experts : nullptr;
     HIP_TRY(launch_moe_route(m.router_part, pr.S, (long long)rows * c.n_experts, rows, c.n_experts, c.top_k, m.valid,
-                             m.sel, m.w, e->st));
+                             m.sel, m.w, e->st, st_l, lt_l));
     HIP_TRY(launch_moe_dispatch(m.sel, rows * c.top_k, c.n_experts, m.slots, m.list, m.tiles, e->st));
     return CORUN_OK;
 }
@@ -557,8 +570,8 @@ corun_status moe_expert_down(corun_engine *e, const MoeBufs &m, int l)
 
 MoeBufs decode_moe(corun_engine *e)
 {
-    return MoeBufs{e->d_valid, e->p_router, e->moe_w, e->moe_gu, e->moe_y, e->moe_sel, e->moe_list, e->moe_tiles,
-                   e->moe_act, e->plan.moe_slots};
+    return MoeBufs{e->d_valid, e->p_router, e->moe_w,     e->moe_gu,         e->moe_y,         e->moe_sel,
+                   e->moe_list, e->moe_tiles, e->moe_act, e->plan.moe_slots, e->rt_sel, e->rt_logit};
 }
 
 // The residual fold that opens layer l (l = n_layers: the final norm): the
@@ -732,16 +745,71 @@ corun_status check_pages(corun_engine *e, const int32_t *seq_lens, const uint8_t
 // Engine lifetime
 // ---------------------------------------------------------------------------
 
+namespace {
+// The prefill projections of n rows (a prompt, a chunk, or a batch of
+// prompts' tokens): their plan is a function of n and the model alone, so a
+// prompt's bits never depend on the engine's workspace size.
+struct PrefillPlan {
+    Proj qkv, o, gu, down, router;
+};
+
+PrefillPlan prefill_plan(const corun_model_cfg &c, int n, bool bi)
+{
+    const int H = c.hidden, nqkv = (c.n_heads + 2 * c.n_kv_heads) * c.head_dim, F = c.ffn;
+    PrefillPlan p;
+    p.qkv = choose_proj(nqkv, H, n, 0, 0, 0, bi);
+    p.o = choose_proj(H, c.n_heads * c.head_dim, n, 0, 0, 0, bi);
+    if (c.n_experts == 0) {
+        p.gu = choose_proj(2 * F, H, n, 0, 0, 0, bi);
+        p.down = choose_proj(H, F, n, 0, 0, 0, bi);
+    } else {
+        p.router = choose_proj(c.n_experts, H, n, 0, 0, 0, bi);
+    }
+    return p;
+}
+
+// Split-K partials the prefill plans of 1 .. max_rows rows can hold at once:
+// the largest S x n x N over those plans.
+size_t prefill_part_elems(const corun_model_cfg &c, int max_rows, bool bi)
+{
+    size_t most = 1;
+    for (int n = 1; n <= max_rows; ++n) {
+        const PrefillPlan p = prefill_plan(c, n, bi);
+        for (const Proj *pr : {&p.qkv, &p.o, &p.gu, &p.down, &p.router})
+            if (pr->N > 0) most = std::max(most, proj_part_elems(*pr, n));
+    }
+    return most;
+}
+}  // namespace
+
+extern "C" int32_t corun_describe_prefill_plan(const corun_model_cfg *c, int32_t n, const corun_options *opt,
+                                               int32_t *out, int32_t cap)
+{
+    if (!c || !out) return fail(CORUN_E_INVAL, "null argument");
+    if (n < 1) return fail(CORUN_E_INVAL, "n must be >= 1");
+    corun_options o{};
+    if (opt) o = *opt;
+    ST_TRY(check_options(o));
+    const PrefillPlan p = prefill_plan(*c, n, o.batch_invariant || o.bi_prefill);
+    std::vector<int32_t> v;
+    for (const Proj *pr : {&p.qkv, &p.o, &p.gu, &p.down, &p.router})
+        for (int x : {pr->N, pr->K, pr->S, pr->Kc, pr->bm, pr->bn}) v.push_back(x);
+    const int k = std::min<int>((int)v.size(), cap);
+    for (int i = 0; i < k; ++i) out[i] = v[i];
+    return k;
+}
+
 static corun_status alloc_prefill(corun_engine *e)
 {
     const corun_model_cfg &c = e->c;
     const int L = e->pf_max, H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn;
-    const int nqkv = (nq + 2 * nkv) * d;
     const int Lp64 = (L + 63) / 64 * 64;
-    const int maxN = std::max({nqkv, 2 * F, H, c.n_experts});
-    // Split-K for prefill is capped so that S * Lp <= pf_max: the partial
-    // buffer then holds pf_max rows of the widest projection.
-    e->pf_part_elems = (size_t)L * maxN;
+    // The partial buffer holds the split-K partials of any prefill plan of
+    // up to pf_max rows (corun_prefill_batch runs the batch-invariant plans).
+    const bool bi_any = e->opt.batch_invariant || e->opt.bi_prefill;
+    e->pf_part_elems = prefill_part_elems(c, L, e->opt.batch_invariant != 0);
+    if (bi_any) e->pf_part_elems = std::max(e->pf_part_elems, prefill_part_elems(c, L, true));
+    e->pf_part_elems = std::max(e->pf_part_elems, (size_t)L * H);   // the norms' residual folds read [L][H]
     Carver cv;
     cv.take(&e->pf_x, (size_t)L * H);
     cv.take(&e->pf_part, e->pf_part_elems);
@@ -762,6 +830,10 @@ static corun_status alloc_prefill(corun_engine *e)
         cv.take(&e->pf_moe_list, na);
         cv.take(&e->pf_moe_tiles, (size_t)3 * (c.n_experts + (na + 15) / 16));
         cv.take(&e->pf_moe_act, na * Fe);
+        if (e->opt.record_routing) {
+            cv.take(&e->rt_pf_sel, (size_t)c.n_layers * na);
+            cv.take(&e->rt_pf_logit, (size_t)c.n_layers * L * c.n_experts);
+        }
     }
     cv.take(&e->pf_pos, (size_t)std::max(L, kv_capacity(&e->kv)));   // positions of any chunk
     cv.take(&e->pf_tok, (size_t)L);
@@ -780,6 +852,10 @@ static corun_status alloc_prefill(corun_engine *e)
         rebase(e->pf_moe_w, e->pws); rebase(e->pf_moe_gu, e->pws); rebase(e->pf_moe_y, e->pws);
         rebase(e->pf_moe_sel, e->pws); rebase(e->pf_moe_list, e->pws); rebase(e->pf_moe_tiles, e->pws);
         rebase(e->pf_moe_act, e->pws);
+        if (e->opt.record_routing) {
+            rebase(e->rt_pf_sel, e->pws);
+            rebase(e->rt_pf_logit, e->pws);
+        }
     }
     rebase(e->pf_pos, e->pws); rebase(e->pf_tok, e->pws); rebase(e->pf_amax, e->pws); rebase(e->pf_next, e->pws);
     rebase(e->pf_rowpos, e->pws); rebase(e->pf_rowslot, e->pws); rebase(e->pf_seq, e->pws);
@@ -956,6 +1032,10 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
         cv.take(&e->moe_list, na);
         cv.take(&e->moe_tiles, (size_t)3 * p.moe_slots);
         cv.take(&e->moe_act, na * Fe);
+        if (o.record_routing) {
+            cv.take(&e->rt_sel, (size_t)L * na);
+            cv.take(&e->rt_logit, (size_t)L * B * cfg->n_experts);
+        }
     }
     cv.take(&e->d_svalid, (size_t)B);
     cv.take(&e->d_spos, (size_t)B);
@@ -981,6 +1061,10 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     if (moe) {
         rebase(e->p_router, e->ws); rebase(e->moe_w, e->ws); rebase(e->moe_gu, e->ws); rebase(e->moe_y, e->ws);
         rebase(e->moe_sel, e->ws); rebase(e->moe_list, e->ws); rebase(e->moe_tiles, e->ws); rebase(e->moe_act, e->ws);
+        if (o.record_routing) {
+            rebase(e->rt_sel, e->ws);
+            rebase(e->rt_logit, e->ws);
+        }
     }
     // Rows B..Mp-1 of the MFMA A operands (h, o, a) are read but never
     // stored; start everything at zero, or at NaN when poisoning.
@@ -1059,6 +1143,20 @@ static corun_status upload_inputs(corun_engine *e, const int32_t *tokens, const 
     HIP_TRY(hipMemcpyAsync(e->d_seq, e->h_seq, sizeof(int32_t) * B, hipMemcpyHostToDevice, e->st));
     HIP_TRY(hipMemcpyAsync(e->d_valid, e->h_valid, B, hipMemcpyHostToDevice, e->st));
     HIP_TRY(hipMemcpyAsync(e->d_counter, e->h_counter, sizeof(int32_t), hipMemcpyHostToDevice, e->st));
+    e->decoded = true;
+    return CORUN_OK;
+}
+
+// The last validated step inputs (still in the pinned staging) back to the
+// device: the step's feedback advanced every live row's position, possibly to
+// the capacity, and a kernel launched on that state would write past it.
+static corun_status restore_inputs(corun_engine *e)
+{
+    const int B = e->B;
+    HIP_TRY(hipMemcpyAsync(e->d_order, e->h_order, sizeof(int32_t) * B, hipMemcpyHostToDevice, e->st));
+    HIP_TRY(hipMemcpyAsync(e->d_tokens, e->h_tok, sizeof(int32_t) * B, hipMemcpyHostToDevice, e->st));
+    HIP_TRY(hipMemcpyAsync(e->d_seq, e->h_seq, sizeof(int32_t) * B, hipMemcpyHostToDevice, e->st));
+    HIP_TRY(hipMemcpyAsync(e->d_valid, e->h_valid, B, hipMemcpyHostToDevice, e->st));
     return CORUN_OK;
 }
 
@@ -1105,6 +1203,13 @@ extern "C" corun_status corun_decode_run(corun_engine *e, int32_t n_steps, const
         std::memcpy(tokens_out + (size_t)done * B, e->h_hist, sizeof(int32_t) * (size_t)n * B);
         done += n;
     }
+    // the staging now holds the inputs of the run's last step (what its
+    // feedback fed it), for corun_time_kernel
+    for (int b = 0; b < B && n_steps > 1; ++b) {
+        if (!e->h_valid[b]) continue;
+        e->h_seq[b] += n_steps - 1;
+        e->h_tok[b] = tokens_out[(size_t)(n_steps - 2) * B + b];
+    }
     return CORUN_OK;
 }
 
@@ -1143,17 +1248,16 @@ extern "C" corun_status corun_prefill_chunk(corun_engine *e, const int32_t *toke
     const int nqkv = (nq + 2 * nkv) * d;
     hipStream_t st = e->st;
     const int Lp = n;     // rows of every projection: the chunk's tokens
-    const int cap_rows = std::max(1, e->pf_max / Lp);
     const bool bi = e->opt.batch_invariant != 0 || e->opt.bi_prefill != 0;
-    const Proj pq = choose_proj(nqkv, H, Lp, 0, cap_rows, 0, bi);
-    const Proj po = choose_proj(H, nq * d, Lp, 0, cap_rows, 0, bi);
-    const Proj pg = e->moe ? Proj{} : choose_proj(2 * F, H, Lp, 0, cap_rows, 0, bi);
-    const Proj pd = e->moe ? Proj{} : choose_proj(H, F, Lp, 0, cap_rows, 0, bi);
+    const PrefillPlan pp = prefill_plan(c, Lp, bi);   // a function of n alone
+    const Proj &pq = pp.qkv, &po = pp.o, &pg = pp.gu, &pd = pp.down, &pr = pp.router;
     const Proj pl = choose_proj(c.vocab, H, 1, 1, 0, 0, bi);
-    const Proj pr = e->moe ? choose_proj(c.n_experts, H, Lp, 0, cap_rows, 0, bi) : Proj{};
     const int dense_S = e->moe ? 0 : pd.S;
-    const MoeBufs pmb{nullptr, e->pf_part, e->pf_moe_w, e->pf_moe_gu, e->pf_moe_y, e->pf_moe_sel, e->pf_moe_list,
-                      e->pf_moe_tiles, e->pf_moe_act, e->moe ? c.n_experts + (Lp * c.top_k + 15) / 16 : 0};
+    const MoeBufs pmb{nullptr,         e->pf_part,       e->pf_moe_w,   e->pf_moe_gu,
+                      e->pf_moe_y,     e->pf_moe_sel,    e->pf_moe_list, e->pf_moe_tiles,
+                      e->pf_moe_act,   e->moe ? c.n_experts + (Lp * c.top_k + 15) / 16 : 0,
+                      e->rt_pf_sel,    e->rt_pf_logit};
+    e->pf_trace_rows = Lp;
 
     HIP_TRY(hipMemcpyAsync(e->pf_tok, tokens, sizeof(int32_t) * Lp, hipMemcpyHostToDevice, st));
     HIP_TRY(launch_embed(e->embed, e->pf_tok, nullptr, Lp, H, e->pf_x, st));
@@ -1273,16 +1377,15 @@ extern "C" corun_status corun_prefill_batch(corun_engine *e, const int32_t *toke
         seq[4 * i + 3] = groups;
         groups += (((lens[i] + 31) / 32) * G + 7) / 8;
     }
-    const int cap_rows = std::max(1, e->pf_max / Lp);
-    const Proj pq = choose_proj(nqkv, H, Lp, 0, cap_rows, 0, true);
-    const Proj po = choose_proj(H, nq * d, Lp, 0, cap_rows, 0, true);
-    const Proj pg = e->moe ? Proj{} : choose_proj(2 * F, H, Lp, 0, cap_rows, 0, true);
-    const Proj pd = e->moe ? Proj{} : choose_proj(H, F, Lp, 0, cap_rows, 0, true);
+    const PrefillPlan pp = prefill_plan(c, Lp, true);   // batch-invariant: no split-K for any Lp
+    const Proj &pq = pp.qkv, &po = pp.o, &pg = pp.gu, &pd = pp.down, &pr = pp.router;
     const Proj pl = choose_proj(c.vocab, H, n, 1, 0, 0, true);
-    const Proj pr = e->moe ? choose_proj(c.n_experts, H, Lp, 0, cap_rows, 0, true) : Proj{};
     const int dense_S = e->moe ? 0 : pd.S;
-    const MoeBufs pmb{nullptr, e->pf_part, e->pf_moe_w, e->pf_moe_gu, e->pf_moe_y, e->pf_moe_sel, e->pf_moe_list,
-                      e->pf_moe_tiles, e->pf_moe_act, e->moe ? c.n_experts + (Lp * c.top_k + 15) / 16 : 0};
+    const MoeBufs pmb{nullptr,         e->pf_part,       e->pf_moe_w,   e->pf_moe_gu,
+                      e->pf_moe_y,     e->pf_moe_sel,    e->pf_moe_list, e->pf_moe_tiles,
+                      e->pf_moe_act,   e->moe ? c.n_experts + (Lp * c.top_k + 15) / 16 : 0,
+                      e->rt_pf_sel,    e->rt_pf_logit};
+    e->pf_trace_rows = Lp;
 
     HIP_TRY(hipMemcpyAsync(e->pf_tok, tokens, sizeof(int32_t) * Lp, hipMemcpyHostToDevice, st));
     HIP_TRY(hipMemcpyAsync(e->pf_rowpos, rowpos.data(), sizeof(int32_t) * Lp, hipMemcpyHostToDevice, st));
@@ -1340,6 +1443,27 @@ extern "C" corun_status corun_engine_info(const corun_engine *e, int32_t *B_fixe
     return CORUN_OK;
 }
 
+extern "C" corun_status corun_routing_trace(corun_engine *e, int32_t source, int32_t *sel, float *logits,
+                                            int32_t *rows_out)
+{
+    if (!e || !rows_out) return fail(CORUN_E_INVAL, "null argument");
+    if (!e->moe || !e->opt.record_routing)
+        return fail(CORUN_E_STATE, "no routing record: a mixture-of-experts engine created with record_routing");
+    if (source != 0 && source != 1) return fail(CORUN_E_INVAL, "source must be 0 (decode) or 1 (prefill)");
+    if (source == 1 && e->pf_max <= 0) return fail(CORUN_E_STATE, "engine was created without a prefill workspace");
+    const int rows = source == 0 ? e->B : e->pf_trace_rows;
+    *rows_out = rows;
+    const size_t L = (size_t)e->c.n_layers;
+    HIP_TRY(hipStreamSynchronize(e->st));
+    if (sel && rows > 0)
+        HIP_TRY(hipMemcpy(sel, source == 0 ? e->rt_sel : e->rt_pf_sel, sizeof(int32_t) * L * rows * e->c.top_k,
+                          hipMemcpyDeviceToHost));
+    if (logits && rows > 0)
+        HIP_TRY(hipMemcpy(logits, source == 0 ? e->rt_logit : e->rt_pf_logit,
+                          sizeof(float) * L * rows * e->c.n_experts, hipMemcpyDeviceToHost));
+    return CORUN_OK;
+}
+
 // ---------------------------------------------------------------------------
 // Seeded sampling
 // ---------------------------------------------------------------------------
@@ -1393,7 +1517,10 @@ extern "C" corun_status corun_time_kernel(corun_engine *e, int32_t kernel, int32
     if (kernel < 0 || kernel >= CORUN_K_COUNT) return fail(CORUN_E_INVAL, "unknown kernel id %d", kernel);
     if (layer < 0 || layer >= e->c.n_layers) return fail(CORUN_E_INVAL, "layer %d out of range", layer);
     if (n_iters < 1) return fail(CORUN_E_INVAL, "n_iters must be >= 1");
+    if (!e->decoded) return fail(CORUN_E_STATE, "no decode step has run: the kernels have no validated inputs");
     ST_TRY(enter(e));
+    // every timed launch runs on the last step's own (validated) inputs
+    ST_TRY(restore_inputs(e));
     hipEvent_t t0, t1;
     HIP_TRY(hipEventCreate(&t0));
     HIP_TRY(hipEventCreate(&t1));

@@ -29,9 +29,12 @@ hipError_t launch_rmsnorm(float *x, const float *part, int S, long long part_str
 
 // Mixture-of-experts routing: per valid row, top_k experts of the router
 // logits (sum of S split partials [S][rows][E]), ties to the lower id, with
-// renormalised softmax weights; padding rows get sel = -1.
+// renormalised softmax weights; padding rows get sel = -1.  Optionally the
+// choice and the summed router logits are copied to sel_trace [rows][top_k]
+// and logit_trace [rows][E] (valid rows' logits only).
 hipError_t launch_moe_route(const float *part, int S, long long part_stride, int rows, int E, int top_k,
-                            const uint8_t *valid, int32_t *sel, float *wsel, hipStream_t st);
+                            const uint8_t *valid, int32_t *sel, float *wsel, hipStream_t st,
+                            int32_t *sel_trace = nullptr, float *logit_trace = nullptr);
 // Deterministic dispatch of the n_assign = rows * top_k assignments into the
 // fixed pool of n_slots 16-row tiles: list (expert-major, increasing
 // assignment) and tiles[slot] = {expert, first list index, count}.

@@ -1906,13 +1906,15 @@ hipError_t launch_iota(int32_t *p, int n, hipStream_t st)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_moe_route(const float *__restrict__ part, int S, long long part_stride,
                                                   int E, int top_k, const uint8_t *__restrict__ valid,
-                                                  int32_t *__restrict__ sel, float *__restrict__ wsel)
+                                                  int32_t *__restrict__ sel, float *__restrict__ wsel,
+                                                  int32_t *__restrict__ sel_trace, float *__restrict__ logit_trace)
 {
     const int b = blockIdx.x, lane = threadIdx.x;
     if (valid != nullptr && !valid[b]) {
         if (lane < top_k) {
             sel[(size_t)b * top_k + lane] = -1;
             wsel[(size_t)b * top_k + lane] = 0.f;
+            if (sel_trace != nullptr) sel_trace[(size_t)b * top_k + lane] = -1;
         }
         return;
     }
@@ -1935,6 +1937,7 @@ __global__ __launch_bounds__(64) void k_moe_route(const float *__restrict__ part
             }
         }
         l[j] = v;
+        if (logit_trace != nullptr && e < E) logit_trace[(size_t)b * E + e] = v;
     }
     float top_l[16];
     int top_e[16];
@@ -1966,15 +1969,18 @@ __global__ __launch_bounds__(64) void k_moe_route(const float *__restrict__ part
         for (int r = 0; r < top_k; ++r) {
             sel[(size_t)b * top_k + r] = top_e[r];
             wsel[(size_t)b * top_k + r] = ev[r] / z;
+            if (sel_trace != nullptr) sel_trace[(size_t)b * top_k + r] = top_e[r];
         }
     }
 }
 
 hipError_t launch_moe_route(const float *part, int S, long long part_stride, int rows, int E, int top_k,
-                            const uint8_t *valid, int32_t *sel, float *wsel, hipStream_t st)
+                            const uint8_t *valid, int32_t *sel, float *wsel, hipStream_t st, int32_t *sel_trace,
+                            float *logit_trace)
 {
     if (E > 256 || top_k > 16 || top_k > E) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_moe_route, dim3(rows), dim3(64), 0, st, part, S, part_stride, E, top_k, valid, sel, wsel);
+    hipLaunchKernelGGL(k_moe_route, dim3(rows), dim3(64), 0, st, part, S, part_stride, E, top_k, valid, sel, wsel,
+                       sel_trace, logit_trace);
     return hipGetLastError();
 }
 

@@ -61,3 +61,41 @@ def check_tokens(gpu_next, ref_logits, gpu_logits, valid, near_ties: list):
             assert gpu_next[b] == exp, (b, gpu_next[b], exp, top2_gap(ref), err)
         elif gpu_next[b] != exp:
             near_ties.append((b, top2_gap(ref), err))
+
+
+def check_routing(gsel, glog, rl, own, where, tol=2e-2):
+    """The GPU's mixture-of-experts routing of one row against the oracle's
+    records of the same trajectory (the oracle run with force = gsel).
+
+    gsel [L, k], glog [L, E]: the GPU's choice and the fp32 router logits it
+    was made from; rl [L, E], own [L, k]: the oracle's fp64 router logits and
+    its own top-k on that trajectory.  Per layer:
+      * exact: gsel is the top-k of glog, ties to the lower expert id;
+      * the router logits agree within tol of the layer's largest |logit|;
+      * where the two expert sets differ, the oracle's logits admit the GPU's
+        set as a top-k under the measured error eps = max |glog - rl|: every
+        chosen expert's logit is at least every other's minus 2 eps (each of
+        the two logits can be off by eps).  Such a layer is a routing
+        near-tie: both choices are correct results.
+    Returns the near-ties as (where, layer, gap, eps)."""
+    near = []
+    L, k = gsel.shape
+    for l in range(L):
+        g = glog[l].astype(np.float64)
+        top = np.lexsort((np.arange(g.size), -g))[:k]
+        assert list(gsel[l]) == list(top), (where, l, list(gsel[l]), list(top))
+        eps = float(np.abs(g - rl[l]).max())
+        assert eps <= tol * np.abs(rl[l]).max(), (where, l, eps)
+        if set(gsel[l].tolist()) != set(own[l].tolist()):
+            chosen = rl[l][list(gsel[l])].min()
+            other = np.delete(rl[l], list(gsel[l])).max()
+            assert chosen >= other - 2 * eps, (where, l, float(chosen), float(other), eps)
+            near.append((where, l, float(other - chosen), eps))
+    return near
+
+
+def routed_decode_row(m, okv, slot, token, pos, gsel, glog, where):
+    """Oracle logits of one decode row following the GPU's expert sets
+    (checked by check_routing); returns (logits, routing near-ties)."""
+    ref, rl, own = oracle.decode_row_routed(m, okv, slot, token, pos, force=gsel)
+    return ref, check_routing(gsel, glog, rl, own, where)

@@ -179,3 +179,25 @@ def test_prefill_tiles_follow_the_wave_estimate():
     for p in (p512, p1024):                          # every split keeps at least 512 K elements
         for name, K in (("qkv", 4096), ("o", 4096), ("gate_up", 4096), ("down", 12288)):
             assert K // p[name][2] >= 512, (name, p[name])
+
+
+def test_prefill_plan_is_a_function_of_the_length_only():
+    """The prefill plan takes no workspace size: the 8B shape's projections
+    split K at lengths where the estimate asks for it (so an engine-size cap
+    would have changed them), never in batch-invariant mode; every
+    projection of the plan covers its K exactly."""
+    c = wl.config("8b")
+    split = set()
+    for n in (1, 7, 64, 100, 300, 600, 2048, 8192, 32768):
+        p = corun.describe_prefill_plan(c, n)
+        bi = corun.describe_prefill_plan(c, n, corun.options(bi_prefill=True))
+        for name in ("qkv", "o", "gate_up", "down"):
+            pr = p[name]
+            assert pr["split_k"] >= 1 and pr["split_k"] * pr["k_chunk"] >= pr["K"] > (pr["split_k"] - 1) * pr["k_chunk"]
+            if pr["split_k"] > 1:
+                split.add(n)
+            assert bi[name]["split_k"] == 1
+        assert p["router"]["N"] == 0
+    assert {300, 600} & split, split
+    moe = corun.describe_prefill_plan(wl.config("moe"), 300)
+    assert moe["router"]["N"] == 128 and moe["gate_up"]["N"] == 0

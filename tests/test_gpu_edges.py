@@ -126,24 +126,38 @@ def test_prefill_fills_the_workspace(model):
 
 
 @pytest.mark.parametrize("poison", [False, True])
-def test_attention_before_the_first_step(poison):
-    """The attention kernel's row order is valid from creation: timing it on
-    a fresh engine, before any step has uploaded inputs, runs (the cleared or
-    poisoned workspace makes every block exit at once), and a step afterwards
-    still matches a fresh engine's bit for bit."""
+def test_time_kernel_needs_a_step_and_keeps_results(poison):
+    """corun_time_kernel launches nothing before the engine's first decode
+    step (CORUN_E_STATE: no validated inputs exist yet).  After a step whose
+    rows sit at the last cache position (so the step's feedback moves them
+    to the capacity), timing the kernels that append to and read the cache
+    runs them at the step's own positions, and the next step still matches
+    a fresh engine's bit for bit, caches included."""
     cfg = wl.config("tiny")
     Wg = to_device(wl.make_weights(cfg, seed=71))
-    B = 4
-    K, V = wl.make_kv_contiguous(cfg, B, 160, seed=72, device=DEV)
+    B, cap = 4, 160
+    K, V = wl.make_kv_contiguous(cfg, B, cap, seed=72, device=DEV)
     b = wl.make_batch(B, cfg["vocab"], seed=73, len_lo=16, len_hi=128)
+    last = b.seq_lens.copy()
+    last[b.valid == 1] = cap - 1
     outs = []
-    for timed_first in (True, False):
-        eng = corun.Engine(cfg, Wg, B, [k.clone() for k in K], [v.clone() for v in V],
-                           opt=corun.options(poison_workspace=poison))
-        if timed_first:
-            assert eng.time_kernel(corun.K_ATTN_SPLIT, 0, 3) > 0
+    for timed in (True, False):
+        Kc, Vc = [k.clone() for k in K], [v.clone() for v in V]
+        eng = corun.Engine(cfg, Wg, B, Kc, Vc, opt=corun.options(poison_workspace=poison, qkv_epilogue=1))
+        if timed:
+            with pytest.raises(corun.CorunError) as ei:
+                eng.time_kernel(corun.K_ATTN_SPLIT, 0, 3)
+            assert ei.value.status == corun.E_STATE
         logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
-        eng.decode_step(b.tokens, b.valid, b.seq_lens, logits)
-        outs.append(logits.cpu().numpy().view(np.int32)[b.valid == 1])
+        eng.decode_step(b.tokens, b.valid, last, logits)
+        if timed:
+            for kern in (corun.K_QKV_POST, corun.K_ATTN_SPLIT, corun.K_ATTN_MERGE):
+                assert eng.time_kernel(kern, 0, 3) > 0
+        eng.decode_step(b.tokens, b.valid, last, logits)
+        torch.cuda.synchronize()
+        outs.append((logits.cpu().numpy().view(np.int32)[b.valid == 1],
+                     [wl.bits(k) for k in Kc], [wl.bits(v) for v in Vc]))
         eng.close()
-    assert np.array_equal(outs[0], outs[1])
+    assert np.array_equal(outs[0][0], outs[1][0])
+    for l in range(cfg["n_layers"]):
+        assert np.array_equal(outs[0][1][l], outs[1][1][l]) and np.array_equal(outs[0][2][l], outs[1][2][l])

@@ -64,9 +64,10 @@ def test_parity_with_oracle_8_greedy_steps(tiny, seed):
         # teacher forcing: both sides continue from the GPU's tokens
         tokens = np.where(valid == 1, nxt, tokens).astype(np.int32)
         lens = np.where(valid == 1, lens + 1, lens).astype(np.int32)
-    # near-ties are logged, not failed; a systematic token error would show
-    # up as many of them
-    assert len(near) <= max(1, int(valid.sum()) * 8 // 8), near
+    # near-ties (top-2 gap within four times the row's measured logit error)
+    # are logged; at most two per 8-step run, so a systematic token error
+    # cannot hide among them
+    assert len(near) <= 2, near
     print(f"max row-relative logit error {worst:.3e}, near-ties {near}")
 
 

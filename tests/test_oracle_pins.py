@@ -393,6 +393,96 @@ def test_moe_top1_equals_dense_expert_bitwise():
     assert np.array_equal(a, b)
 
 
+def test_routed_decode_records_and_forcing():
+    """The routing records and overrides of the MoE oracle, pinned three ways:
+    * its router logits and own top-k equal those of the torch composition
+      (matrix form, torch.topk on torch.softmax) at every layer;
+    * forcing each layer to the oracle's own choice changes no bit;
+    * forcing other expert sets (the 2nd..k+1-th ranked experts, a shuffled
+      order) gives the torch composition run with the same sets."""
+    cfg = wl.config("tiny_moe")
+    W = wl.make_weights(cfg, seed=30)
+    m = _host_model(W)
+    L, E, k = cfg["n_layers"], cfg["n_experts"], cfg["top_k"]
+    S, slot, pos, tok = 48, 0, 29, 211
+    kv = _contig_kv(cfg, 1, S, seed=31)
+    kpre = [torch.from_numpy(np.ascontiguousarray(x[slot, :, :pos]).view(np.int16)).view(torch.bfloat16) for x in kv.k]
+    vpre = [torch.from_numpy(np.ascontiguousarray(x[slot, :, :, :pos].transpose(0, 2, 1)).view(np.int16))
+            .view(torch.bfloat16) for x in kv.v]
+    plain = oracle.decode_row(m, kv, slot, tok, pos)
+    lg, rl, own = oracle.decode_row_routed(m, kv, slot, tok, pos)
+    assert np.array_equal(lg, plain)
+    routing = []
+    ref, _, _ = tref.forward_chunk(cfg, W, [tok], pos, kpre, vpre, routing=routing)
+    for l in range(L):
+        trl, tsel = routing[l]
+        np.testing.assert_allclose(rl[l], trl.numpy()[0], rtol=0, atol=1e-12 * np.abs(rl[l]).max())
+        assert list(own[l]) == tsel[0].tolist(), l
+    # the oracle's own choice, forced: bit-identical
+    lg2, _, own2 = oracle.decode_row_routed(m, kv, slot, tok, pos, force=own)
+    assert np.array_equal(lg2, plain) and np.array_equal(own2, own)
+    # other sets: drop the top expert for the (k+1)-th, and reverse the order
+    force = np.empty((L, k), np.int32)
+    for l in range(L):
+        order = np.argsort(-rl[l], kind="stable")
+        force[l] = order[1:k + 1][::-1]
+    lg3, rl3, own3 = oracle.decode_row_routed(m, kv, slot, tok, pos, force=force)
+    ref3, _, _ = tref.forward_chunk(cfg, W, [tok], pos, kpre, vpre, force=force[:, None, :])
+    scale = np.abs(ref3.numpy()).max()
+    assert np.abs(lg3 - ref3.numpy()[0]).max() <= 1e-10 * scale
+    assert np.abs(lg3 - plain).max() > 1e-6 * scale        # the forced sets do change the result
+    assert np.array_equal(rl3[0], rl[0])                   # layer 0's router input is unchanged
+    with pytest.raises(ValueError):                        # malformed sets are refused
+        bad = own.copy()
+        bad[0, 1] = bad[0, 0]
+        oracle.decode_row_routed(m, kv, slot, tok, pos, force=bad)
+
+
+def test_routed_prefill_matches_routed_decode_rows():
+    """Forced prefill routing [L][Lp][k] is the per-position forced decode:
+    the prefill of p with forced sets equals, at its last position, the
+    forced decode of p's last token after the forced prefill of the rest
+    (the routed form of decode == prefill), bit for bit; the records of both
+    agree."""
+    cfg = wl.config("tiny_moe")
+    W = wl.make_weights(cfg, seed=32)
+    m = _host_model(W)
+    L, k = cfg["n_layers"], cfg["top_k"]
+    Lp = 12
+    prompt = wl.make_prompt(cfg["vocab"], Lp, seed=33)
+    kva = _contig_kv(cfg, 1, 32, seed=34)
+    _, _, rl, own = oracle.prefill_routed(m, kva, 0, prompt)
+    force = np.empty_like(own)
+    for l in range(L):
+        for t in range(Lp):
+            force[l, t] = np.argsort(-rl[l, t], kind="stable")[1:k + 1]
+    kvb = _contig_kv(cfg, 1, 32, seed=34)
+    la, ta, rla, owna = oracle.prefill_routed(m, kvb, 0, prompt, force=force)
+    kvc = _contig_kv(cfg, 1, 32, seed=34)
+    oracle.prefill_routed(m, kvc, 0, prompt[:-1], force=force[:, :-1])
+    lb, rlb, ownb = oracle.decode_row_routed(m, kvc, 0, int(prompt[-1]), Lp - 1, force=force[:, -1])
+    assert np.array_equal(la, lb)
+    assert np.array_equal(rla[:, -1], rlb) and np.array_equal(owna[:, -1], ownb)
+    for l in range(L):
+        assert np.array_equal(kvb.k[l], kvc.k[l]) and np.array_equal(kvb.v[l], kvc.v[l])
+
+
+def test_route_forced_weights():
+    """Weights of a forced set: softmax over all experts, renormalised over
+    the set (torch), in the set's order."""
+    r = np.random.default_rng(35)
+    lg = r.standard_normal(128)
+    f = np.array([5, 77, 3, 120, 64, 9, 100, 31], np.int32)
+    p = torch.softmax(torch.from_numpy(lg), -1)[torch.from_numpy(f).long()]
+    np.testing.assert_allclose(oracle.route_forced(lg, f), (p / p.sum()).numpy(), rtol=1e-13)
+    sel, w = oracle.route(lg, 8)
+    assert np.array_equal(oracle.route_forced(lg, sel), w)   # the own choice: the same weights, bit for bit
+    with pytest.raises(ValueError):
+        oracle.route_forced(lg, np.array([1, 1], np.int32))
+    with pytest.raises(ValueError):
+        oracle.route_forced(lg, np.array([0, 128], np.int32))
+
+
 def test_thread_count_invariance():
     cfg = wl.config("tiny")
     m = _host_model(wl.make_weights(cfg, seed=20))

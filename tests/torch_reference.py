@@ -58,11 +58,15 @@ def _swiglu(h, wgu, wd, Fd):
     return a @ _w(wd).T
 
 
-def forward_chunk(cfg: dict, W, tokens, start: int, k_prefix, v_prefix):
+def forward_chunk(cfg: dict, W, tokens, start: int, k_prefix, v_prefix, force=None, routing=None):
     """Run tokens [T] at positions start..start+T-1 of one request.
 
     W: workload.Weights (bf16 tensors).  k_prefix, v_prefix: per layer bf16
     [nkv, start, d] cache of the positions before the chunk.
+    Mixture of experts: force ([L][T][k], optional) replaces each row's top-k
+    expert set (weights: the softmax renormalised over the given set);
+    routing (a list, optional) receives per layer (router logits [T, E],
+    torch.topk ids [T, k]).
     Returns (logits [T, V] float64, k_new, v_new: per layer bf16 [nkv, T, d]).
     """
     H, d = cfg["hidden"], cfg["head_dim"]
@@ -95,8 +99,14 @@ def forward_chunk(cfg: dict, W, tokens, start: int, k_prefix, v_prefix):
             y = _swiglu(h, W.w_gate_up[l], W.w_down[l], cfg["ffn"])
         else:
             E, K_, Fe = cfg["n_experts"], cfg["top_k"], cfg["expert_ffn"]
-            p = torch.softmax(h @ _w(W.w_router[l]).T, dim=-1)
+            rl = h @ _w(W.w_router[l]).T
+            p = torch.softmax(rl, dim=-1)
             top_p, top_e = torch.topk(p, K_, dim=-1)
+            if routing is not None:
+                routing.append((rl, top_e))
+            if force is not None:
+                top_e = torch.as_tensor(force[l], dtype=torch.long).reshape(T, K_)
+                top_p = torch.gather(p, 1, top_e)
             wts = top_p / top_p.sum(-1, keepdim=True)
             y = torch.zeros(T, H, dtype=f64)
             for t in range(T):
