@@ -22,7 +22,7 @@ import torch
 import oracle
 from paper_2608_14376_amd import corun
 from paper_2608_14376_amd import workload as wl
-from tests.gpu_helpers import DEV, host_model, row_rel_err
+from tests.gpu_helpers import DEV, check_tokens, host_model, row_rel_err
 
 pytestmark = pytest.mark.gpu
 TOL = 2e-2
@@ -83,6 +83,47 @@ def test_decode_B256_full_shapes(full):
     assert torch.equal(logits[c].view(torch.int32), ref_logits[a].view(torch.int32))
 
 
+# The small-B plans the decode benchmark times (8B shapes, capacity 4144):
+# packed 32- or 64-row weight tiles with split-K 5 (qkv) and 8 (o, down),
+# gate/up without split-K (its epilogue applies SwiGLU), and the attention
+# chunk that gives up to 33 splits at B <= 8 (where attention also applies
+# the QKV epilogue), 17 at B = 16, 5 at B = 64.
+SMALL_B = {1: (32, 128, 33), 8: (32, 128, 33), 16: (32, 256, 17), 64: (64, 1024, 5)}
+
+
+@pytest.mark.parametrize("Bs", sorted(SMALL_B))
+def test_decode_small_B_full_shapes(full, Bs):
+    cfg, Wg, m = full
+    K, V = wl.make_kv_contiguous(cfg, Bs, CAP, seed=60 + Bs, device=DEV)
+    eng = corun.Engine(cfg, Wg, Bs, K, V)
+    plan = eng.plan()
+    mt, chunk, splits = SMALL_B[Bs]
+    for name, S in (("qkv", 5), ("o", 8), ("gate_up", 1), ("down", 8), ("lm_head", 1)):
+        assert (plan[name]["split_k"], plan[name]["m_tile"], plan[name]["n_tile"]) == (S, mt, 128), (name, plan[name])
+    assert (plan["attn_chunk"], plan["attn_max_splits"]) == (chunk, splits)
+    b = wl.make_batch(Bs, cfg["vocab"], seed=70 + Bs, len_lo=512, len_hi=4096)
+    live = np.nonzero(b.valid)[0]
+    sample = [int(r) for r in (live if Bs <= 16 else live[:: max(1, len(live) // 6)][:6])]
+    okv = {r: row_cache(K, V, r, CAP) for r in sample}
+    tokens, lens = b.tokens.copy(), b.seq_lens.copy()
+    logits = torch.empty(Bs, cfg["vocab"], dtype=torch.float32, device=DEV)
+    worst, near = 0.0, []
+    for step in range(2):
+        nxt = eng.decode_step(tokens, b.valid, lens, logits)
+        gl = logits.cpu().numpy()
+        for r in sample:
+            ref = oracle.decode_row(m, okv[r], 0, int(tokens[r]), int(lens[r]))
+            err = row_rel_err(gl[r], ref)
+            worst = max(worst, err)
+            assert err <= TOL, (step, r, err)
+            check_tokens([nxt[r]], ref[None], gl[r][None], [1], near)
+        tokens = np.where(b.valid == 1, nxt, tokens).astype(np.int32)
+        lens = np.where(b.valid == 1, lens + 1, lens).astype(np.int32)
+    eng.close()
+    assert len(near) <= 1, near
+    print(f"B={Bs}: {len(sample)} rows x 2 steps, max row-relative logit error {worst:.2e}")
+
+
 def test_prefill_600_full_shapes_teacher_forced(full):
     cfg, Wg, m = full
     cap = 608
@@ -131,3 +172,30 @@ def test_prefill_32768_full_shapes_teacher_forced(full):
             err = row_rel_err(last.cpu().numpy(), ref)
             print(f"prefill of {lp}: last-position relative logit error {err:.2e}")
             assert err <= TOL
+
+
+def test_prefill_bits_do_not_depend_on_the_workspace(full):
+    """The same 300-token prompt on two engines whose prefill workspaces
+    differ (300 and 4096 tokens) gives identical k, v and logits bits: the
+    plan -- here with split-K on the narrow projections -- is a function of
+    the prompt length alone (Sec. IV, "Isolated Prefill")."""
+    cfg, Wg, m = full
+    lp, cap = 300, 320
+    plan = corun.describe_prefill_plan(cfg, lp)
+    assert max(plan[n]["split_k"] for n in ("qkv", "o", "gate_up", "down")) > 1, plan
+    prompt = wl.make_prompt(cfg["vocab"], lp, seed=48)
+    outs = []
+    for pf in (lp, 4096):
+        K, V = wl.make_kv_contiguous(cfg, 2, cap, seed=49, device=DEV)
+        eng = corun.Engine(cfg, Wg, 2, K, V, opt=corun.options(max_prefill_len=pf))
+        last = torch.empty(cfg["vocab"], dtype=torch.float32, device=DEV)
+        tok = eng.prefill(prompt, 1, last)
+        torch.cuda.synchronize()
+        outs.append((tok, last.view(torch.int32).cpu(), [k[1, :, :lp].clone() for k in K],
+                     [v[1, :, :, :lp].clone() for v in V]))
+        eng.close()
+    a, b = outs
+    assert a[0] == b[0] and torch.equal(a[1], b[1])
+    for l in range(cfg["n_layers"]):
+        assert torch.equal(a[2][l].view(torch.int16), b[2][l].view(torch.int16)), l
+        assert torch.equal(a[3][l].view(torch.int16), b[3][l].view(torch.int16)), l
