@@ -295,6 +295,33 @@ corun_status corun_sample(corun_engine *e, const float *logits_dev, int64_t ld, 
                           const uint8_t *valid, const int32_t *positions, const uint64_t *seeds,
                           const float *temperature, int32_t *tokens_out, float *logprobs_out);
 
+/* Most rows one corun_sample_noalloc call takes (the size of its static
+ * staging). */
+#define CORUN_SAMPLE_NOALLOC_MAX_ROWS 1024
+
+/* corun_sample without an engine and without allocating, for callers that
+ * cannot allocate device memory: code that must not call hipMalloc (a tight
+ * serving loop, a harness that forbids it).  The same sampler and result
+ * bits as corun_sample on the same logits and arguments; the per-row inputs
+ * and outputs are staged in a fixed static device array of 32 KiB that each
+ * GPU holds for the life of the process (rows at most
+ * CORUN_SAMPLE_NOALLOC_MAX_ROWS).  Runs on `stream` (a hipStream_t; NULL =
+ * the null stream) on the current device and waits for it before returning.
+ * Every call on a GPU shares that GPU's staging: calls that overlap on one
+ * device (from two threads, or on two streams at once) race; calls made one
+ * after another do not.
+ *  logits_dev   device fp32 [rows][ld], ld >= vocab (caller-owned)
+ *  vocab        columns sampled per row, >= 1
+ *  valid, positions, seeds, temperature, tokens_out, logprobs_out: as for
+ *               corun_sample (host arrays of `rows` entries; logprobs_out may
+ *               be NULL)
+ * Errors: CORUN_E_SHAPE for rows outside [1, CORUN_SAMPLE_NOALLOC_MAX_ROWS],
+ * vocab < 1 or ld < vocab; CORUN_E_INVAL as for corun_sample; CORUN_E_HIP. */
+corun_status corun_sample_noalloc(const float *logits_dev, int64_t ld, int32_t rows, int32_t vocab,
+                                  const uint8_t *valid, const int32_t *positions, const uint64_t *seeds,
+                                  const float *temperature, int32_t *tokens_out, float *logprobs_out,
+                                  void *stream);
+
 /* ---------------------------------------------------------------------------
  * Host scheduler (Sec. IV, "Isolated Prefill", Algorithms 1 and 2, around the
  * fixed-shape batched decode and the request-bound sampler): a

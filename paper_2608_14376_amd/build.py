@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libcorun.so")
-SOURCES = ["kernels.hip", "engine.cpp", "scheduler.cpp"]
+SOURCES = ["kernels.hip", "engine.cpp", "scheduler.cpp", "sample_noalloc.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -21,7 +21,8 @@ KV_CONTIGUOUS, KV_PAGED = 0, 1
 EXPORTS = ("corun_engine_create", "corun_engine_destroy", "corun_decode_step", "corun_decode_run",
            "corun_prefill", "corun_prefill_chunk", "corun_prefill_batch", "corun_check_config", "corun_check_batch",
            "corun_describe_plan", "corun_describe_prefill_plan",
-           "corun_last_error", "corun_time_kernel", "corun_sample", "corun_engine_info", "corun_routing_trace",
+           "corun_last_error", "corun_time_kernel", "corun_sample", "corun_sample_noalloc", "corun_engine_info",
+           "corun_routing_trace",
            "corun_sched_create", "corun_sched_destroy", "corun_sched_add_request", "corun_sched_step",
            "corun_sched_output", "corun_sched_state", "corun_sched_last_error")
 
@@ -110,6 +111,9 @@ def load():
     L.corun_sample.restype = st
     L.corun_sample.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
                                C.c_void_p, C.c_void_p, C.c_void_p]
+    L.corun_sample_noalloc.restype = st
+    L.corun_sample_noalloc.argtypes = [C.c_void_p, C.c_int64, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
+                                       C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
     L.corun_engine_info.restype = st
     L.corun_engine_info.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
     L.corun_routing_trace.restype = st
@@ -222,6 +226,32 @@ def describe_prefill_plan(cfg: dict, n: int, opt: Options | None = None) -> dict
         N, K, S, Kc, bm, bn = v[6 * i: 6 * i + 6]
         plan[name] = {"N": N, "K": K, "split_k": S, "k_chunk": Kc, "m_tile": bm, "n_tile": bn}
     return plan
+
+
+SAMPLE_NOALLOC_MAX_ROWS = 1024
+
+
+def sample_noalloc(logits, valid, positions, seeds, temperature, vocab=None, stream=None):
+    """corun_sample_noalloc: seeded sampling of the rows of a device fp32
+    logits tensor ([rows, ld] or [ld]) with no engine and no allocation;
+    returns (tokens int32[rows], logprobs float32[rows])."""
+    import torch
+    assert logits.is_cuda and logits.dtype == torch.float32 and logits.is_contiguous()
+    rows = 1 if logits.dim() == 1 else logits.shape[0]
+    ld = logits.shape[-1]
+    vocab = ld if vocab is None else vocab
+    vm = _np(valid, np.uint8).reshape(rows)
+    pos = _np(positions, np.int32).reshape(rows)
+    sd = np.ascontiguousarray(np.asarray(seeds, dtype=np.uint64).reshape(rows))
+    tp = np.ascontiguousarray(np.asarray(temperature, dtype=np.float32).reshape(rows))
+    tok = np.empty(rows, np.int32)
+    lp = np.empty(rows, np.float32)
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    _check(load().corun_sample_noalloc(logits.data_ptr(), ld, rows, vocab, vm.ctypes.data, pos.ctypes.data,
+                                       sd.ctypes.data, tp.ctypes.data, tok.ctypes.data, lp.ctypes.data,
+                                       C.c_void_p(stream.cuda_stream)))
+    return tok, lp
 
 
 class SchedCfg(C.Structure):

@@ -433,6 +433,15 @@ extern "C" int32_t corun_describe_plan(const corun_model_cfg *c, const corun_kv 
 
 extern "C" const char *corun_last_error(void) { return g_err.c_str(); }
 
+// The calling thread's error message, for the entry points of other files.
+namespace corun {
+corun_status set_error(corun_status s, const char *msg)
+{
+    g_err = msg;
+    return s;
+}
+}  // namespace corun
+
 // ---------------------------------------------------------------------------
 // Workspace carving
 // ---------------------------------------------------------------------------
