@@ -41,33 +41,51 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_bytes_flops(cfg, B, lens_live):
-    """Algorithmic HBM bytes and flops of one launch of each kernel class
-    (layer-0 launch; per-layer kernels repeat n_layers times per step).  A
-    projection moves its weights once, its bf16 input rows and its output
-    rows (bf16 where the next step rounds, fp32 where it is added to the
-    residual); padding rows are counted (padding is the method's cost).
-    Mixture-of-experts projections count every expert's weights: at B = 128
-    with top-8 of 128 experts nearly all experts are touched."""
+def kernel_bytes_flops(cfg, B, lens_live, plan, swiglu_fused=False):
+    """Algorithmic bytes (read + written) and flops of one launch of each
+    kernel class (per-layer kernels repeat n_layers times per step), for the
+    engine's plan (split-K factors, attention chunk).  A projection reads its
+    weights once and its bf16 input rows, and writes its outputs: fp32
+    split-K partials (split x rows x N), or bf16 activations where the
+    gate/up epilogue applies SwiGLU; the consumers read those partials back
+    (RMSNorm folds the O or down partials into the fp32 residual, the QKV
+    epilogue folds the QKV partials, SwiGLU the gate/up partials).  Decode
+    attention reads each live row's cached keys and values (seq_len + 1
+    tokens per kv head) and q, and writes one (max, sum, acc[G][d]) fp32
+    partial per (row, kv head, split); the merge reads them and writes o.
+    The argmax reads the lm_head epilogue's per-64-column (value, index)
+    partials.  Padding rows are counted in the projections (padding is the
+    method's cost).  Mixture-of-experts projections count every expert's
+    weights: at B = 128 with top-8 of 128 experts nearly all are touched."""
     from paper_2608_14376_amd import corun
     H, d, nq, nkv, F, V = (cfg[k] for k in ("hidden", "head_dim", "n_heads", "n_kv_heads", "ffn", "vocab"))
     E, k, Fe = cfg["n_experts"], cfg["top_k"], cfg["expert_ffn"]
+    G = nq // nkv
     nqkv = (nq + 2 * nkv) * d
+    S = {n: plan[n]["split_k"] for n in ("qkv", "o", "gate_up", "down", "lm_head")}
+    chunk = plan["attn_chunk"]
 
     def gemm(N, K, out_bytes, rows=B, mats=1):
         return 2 * N * K * mats + 2 * rows * K + out_bytes * rows * N, 2 * rows * N * K
 
-    kv_read = sum(int(L) + 1 for L in lens_live) * nkv * d * 2 * 2
     n_live = len(lens_live)
+    kv_read = sum(int(L) + 1 for L in lens_live) * nkv * d * 2 * 2
+    n_part = sum((int(L) + chunk) // chunk for L in lens_live) * nkv     # (row, kv head, split) partials
+    part_bytes = n_part * G * (d + 2) * 4
+    fold = lambda s_: B * H * 4 * (s_ + 1) + (B * H * 4 if s_ else 0) + B * H * 2 + H * 2   # x, partials in; x, h out
+    dense_S = 0 if E else S["down"]
     bf = {
-        corun.K_QKV_GEMM: gemm(nqkv, H, 2),
-        corun.K_O_GEMM: gemm(H, nq * d, 4),
-        corun.K_LM_HEAD: gemm(V, H, 4),
-        corun.K_ATTN_SPLIT: (kv_read + 2 * n_live * nq * d, 4 * n_live * nq * d * (sum(lens_live) / max(n_live, 1) + 1)),
-        corun.K_ATTN_MERGE: (2 * B * nq * d, 0),
-        corun.K_RMSNORM: (B * H * 4 * 2 + B * H * 2, 0),
-        corun.K_QKV_POST: (B * nqkv * 2 + n_live * 2 * nkv * d * 2, 0),
-        corun.K_ARGMAX: (B * V * 4, 0),
+        corun.K_QKV_GEMM: gemm(nqkv, H, 4 * S["qkv"]),
+        corun.K_O_GEMM: gemm(H, nq * d, 4 * S["o"]),
+        corun.K_LM_HEAD: (2 * V * H + 2 * B * H + 4 * B * V + 8 * B * ((V + 63) // 64), 2 * B * V * H),
+        corun.K_ATTN_SPLIT: (kv_read + 2 * n_live * nq * d + part_bytes,
+                             4 * n_live * nq * d * (sum(lens_live) / max(n_live, 1) + 1)),
+        corun.K_ATTN_MERGE: (part_bytes + 2 * B * nq * d, 0),
+        # the 2 L + 1 norms of a step: L fold the O partials, L + 1 the down partials (or the expert combine)
+        corun.K_RMSNORM: ((cfg["n_layers"] * fold(S["o"]) + (cfg["n_layers"] + 1) * fold(dense_S))
+                          // (2 * cfg["n_layers"] + 1), 0),
+        corun.K_QKV_POST: (4 * S["qkv"] * B * nqkv + 2 * B * nq * d + n_live * 2 * nkv * d * 2, 0),
+        corun.K_ARGMAX: (8 * B * ((V + 63) // 64) + 4 * B, 0),
     }
     if E:
         bf[corun.K_MOE_ROUTER] = gemm(E, H, 4)
@@ -75,12 +93,12 @@ def kernel_bytes_flops(cfg, B, lens_live):
         bf[corun.K_SWIGLU] = (n_live * k * (2 * Fe * 4 + Fe * 2), 0)
         bf[corun.K_DOWN_GEMM] = gemm(H, Fe, 4, rows=n_live * k, mats=E)
     else:
-        bf[corun.K_GATE_UP_GEMM] = gemm(2 * F, H, 2)
-        bf[corun.K_SWIGLU] = (B * 2 * F * 2 + B * F * 2, 0)
-        bf[corun.K_DOWN_GEMM] = gemm(H, F, 4)
-    per_step = {kk: (cfg["n_layers"] if kk not in (corun.K_LM_HEAD, corun.K_ARGMAX) else 1) for kk in bf}
-    per_step[corun.K_RMSNORM] = 2 * cfg["n_layers"] + 1
-    return bf, per_step
+        # with SwiGLU in its epilogue the gate/up projection writes the bf16 activations instead
+        bf[corun.K_GATE_UP_GEMM] = (gemm(2 * F, H, 0)[0] + 2 * B * F, gemm(2 * F, H, 0)[1]) if swiglu_fused else \
+            gemm(2 * F, H, 4 * S["gate_up"])
+        bf[corun.K_SWIGLU] = (4 * S["gate_up"] * B * 2 * F + B * F * 2, 0)
+        bf[corun.K_DOWN_GEMM] = gemm(H, F, 4 * S["down"])
+    return bf
 
 
 def make_paged(cfg, B, lens, extra, seed):
@@ -120,7 +138,9 @@ def run_B(cfg, W, B, args, seeds, measure_kernels, paged=False, len_lo=LEN_LO, l
         K, V, pt, ps = make_paged(cfg, B, np.where(batches[0].valid == 1, batches[0].seq_lens, 0), extra, 3000 + B)
         eng = corun.Engine(cfg, W, B, K, V, layout=corun.KV_PAGED, page_size=ps, page_table=pt)
     else:
-        K, V = wl.make_kv_contiguous(cfg, B, (len_hi + extra + 15) // 16 * 16, seed=1000 + B, device="cuda")
+        # capacity rounded to 64 tokens: every transposed value row (capacity x 2 bytes) then starts on a
+        # 128-byte line, so a value read of 128 tokens touches two lines, not three
+        K, V = wl.make_kv_contiguous(cfg, B, (len_hi + extra + 63) // 64 * 64, seed=1000 + B, device="cuda")
         eng = corun.Engine(cfg, W, B, K, V)
     torch.cuda.synchronize()
     log(f"[bench] {cfg['n_layers']}L H={cfg['hidden']} B={B} {'paged' if paged else 'contiguous'}: KV cache "
@@ -148,17 +168,26 @@ def run_B(cfg, W, B, args, seeds, measure_kernels, paged=False, len_lo=LEN_LO, l
                step_bytes_algorithmic=int(wl.streamed_weight_params(cfg) * 2 + kv_tok * (sum(med["lens"]) + 2 * len(med["lens"]))))
     res["step_hbm_frac"] = round(res["step_bytes_algorithmic"] / (med["step_ms"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
     if measure_kernels:
-        # re-run the median seed's batch so the workspace holds its state
+        # re-run the median seed's batch so the workspace holds its state;
+        # every kernel is timed inside eagerly launched steps of that batch
+        # (HIP events around each launch on the engine's stream)
         b = med["batch"]
         eng.decode_run(1, b.tokens, b.valid, b.seq_lens)
-        bf, per_step = kernel_bytes_flops(cfg, B, med["lens"])
+        prof = eng.profile_step(n_steps=args.profile_steps)
+        bf = kernel_bytes_flops(cfg, B, med["lens"], eng.plan(), swiglu_fused=not cfg["n_experts"] and "swiglu" not in prof)
         kern = {}
         for k in bf:
-            us = eng.time_kernel(k, layer=0, n_iters=args.kernel_iters)
+            name = corun.KERNEL_NAMES[k]
+            if name not in prof:
+                continue        # runs inside a neighbouring kernel at this B (QKV epilogue, SwiGLU)
+            us, per = prof[name]
             by, fl = bf[k]
-            kern[corun.KERNEL_NAMES[k]] = dict(us=round(us, 2), per_step=per_step[k], bytes=by, flops=fl,
-                                               gbs=round(by / us / 1e3, 1),
-                                               tflops=round(fl / us / 1e6, 2))
+            kern[name] = dict(us=round(us, 2), per_step=per, bytes=by, flops=fl, gbs=round(by / us / 1e3, 1),
+                              tflops=round(fl / us / 1e6, 2))
+            if by / us / 1e3 > HBM_PEAK_GBS:
+                raise AssertionError(f"{name}: {by} algorithmic bytes in {us} us exceed the HBM peak")
+        dom = max(kern, key=lambda n: kern[n]["us"] * kern[n]["per_step"])
+        res["dominant_isolated_us"] = round(eng.time_kernel(corun.KERNEL_NAMES.index(dom), 0, args.kernel_iters), 2)
         gem = [corun.KERNEL_NAMES[k] for k in (corun.K_QKV_GEMM, corun.K_O_GEMM, corun.K_GATE_UP_GEMM,
                                                corun.K_DOWN_GEMM, corun.K_LM_HEAD)]
         g_us = sum(kern[n]["us"] * kern[n]["per_step"] for n in gem)
@@ -170,11 +199,13 @@ def run_B(cfg, W, B, args, seeds, measure_kernels, paged=False, len_lo=LEN_LO, l
         res["kernel_sum_ms"] = round(tot_us / 1e3, 4)
         res["kernels"] = kern
     res["_eng"], res["_K"], res["_V"], res["_med"] = eng, K, V, med
+    if paged:
+        res["_pt"], res["_ps"] = pt, ps
     return res
 
 
 def _drop(res):
-    for k in ("_eng", "_K", "_V", "_med"):
+    for k in ("_eng", "_K", "_V", "_med", "_pt", "_ps"):
         res.pop(k, None)
     return res
 
@@ -309,12 +340,13 @@ def bench_bi_tradeoff(cfg, W, K, V, args):
         r = dict(step_ms=round(1e3 * (time.perf_counter() - t) / args.steps, 4))
         if breakdown or gemm_times:
             eng.decode_run(1, b.tokens, b.valid, b.seq_lens)
-            _, per_step = kernel_bytes_flops(cfg, B, b.seq_lens[b.valid == 1].tolist())
+            prof = eng.profile_step(n_steps=args.profile_steps)      # in-step launch durations
         if breakdown:
-            r["breakdown_ms"] = {g: round(sum(eng.time_kernel(k, 0, args.kernel_iters) * per_step[k] for k in ks) / 1e3, 3)
+            r["breakdown_ms"] = {g: round(sum(prof[corun.KERNEL_NAMES[k]][0] * prof[corun.KERNEL_NAMES[k]][1]
+                                              for k in ks if corun.KERNEL_NAMES[k] in prof) / 1e3, 3)
                                  for g, ks in groups.items()}
         if gemm_times:
-            r["gemm_us"] = {n: round(eng.time_kernel(k, 0, args.kernel_iters), 2) for n, k in gemms.items()}
+            r["gemm_us"] = {n: round(prof[corun.KERNEL_NAMES[k]][0], 2) for n, k in gemms.items()}
         eng.close()
         if rows is not None:
             r["_rows"] = rows_out
@@ -378,6 +410,16 @@ def bench_bi_tradeoff(cfg, W, K, V, args):
     out["split_kv_B256"] = sk
     log(f"[bench] split-KV off at B=256: ragged {100 * sk['ragged']['off_cost']:+.1f}%, "
         f"similar {100 * sk['similar']['off_cost']:+.1f}%")
+    # and at the small fixed sizes, where few rows leave most of the GPU idle without splits
+    small = {}
+    for Bs in (1, 8, 16):
+        b = wl.make_batch(Bs, cfg["vocab"], seed=40 + Bs, len_lo=LEN_LO, len_hi=LEN_HI)
+        on_ms, off_ms = timed(Bs, b)["step_ms"], timed(Bs, b, off)["step_ms"]
+        small[Bs] = dict(n_live=int(b.valid.sum()), split_on_ms=on_ms, split_off_ms=off_ms,
+                         off_cost=round(off_ms / on_ms - 1, 4))
+    out["split_kv_small_B"] = small
+    log("[bench] split-KV off, ragged contexts: " + ", ".join(f"B={k} {100 * v['off_cost']:+.1f}%"
+                                                            for k, v in small.items()))
     return out
 
 
@@ -432,47 +474,116 @@ def time_sampler(cfg, res, iters=20):
                 note="host arrays in, tokens + log-probabilities out; one synchronisation")
 
 
-def cpu_baseline(cfg, W, res, budget_s=12.0):
-    """The oracle (plain C, fp64 between bf16 storage points, row by row) on
-    a bounded sample: the first 2 of 36 layers plus lm_head for live rows of
-    the headline batch with their real caches, extrapolated to 36 layers."""
-    import torch
+def host_cpu():
+    """The host the CPU baseline runs on: lscpu's model name, logical CPUs,
+    physical cores (distinct (physical id, core id) pairs of /proc/cpuinfo),
+    sockets, and the CPUs this process may run on."""
+    import subprocess
+    info = {}
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=20).stdout
+        for ln in out.splitlines():
+            k, _, v = ln.partition(":")
+            info[k.strip()] = v.strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    cores, pid, cid = set(), None, None
+    try:
+        for ln in list(open("/proc/cpuinfo")) + [""]:
+            if ln.startswith("physical id"):
+                pid = ln.split(":", 1)[1].strip()
+            elif ln.startswith("core id"):
+                cid = ln.split(":", 1)[1].strip()
+            elif not ln.strip():
+                if pid is not None or cid is not None:
+                    cores.add((pid, cid))
+                pid = cid = None
+    except OSError:
+        pass
+    return dict(model=info.get("Model name") or _cpu_name(), logical_cpus=os.cpu_count(),
+                physical_cores=len(cores) or None, sockets=info.get("Socket(s)"),
+                affinity_cpus=len(os.sched_getaffinity(0)))
 
+
+def cpu_baseline(cfg, W, res, budget_s=12.0):
+    """The oracle (plain C, fp64 between bf16 storage points, row by row,
+    OpenMP across output features) on bounded samples of the workloads:
+
+    * decode, extrapolated: live rows of the headline batch with their real
+      caches through layers 0-1 plus lm_head (until budget_s), the per-layer
+      time scaled to all layers;
+    * decode, full depth: one live row through every layer and lm_head,
+      measured, which validates that extrapolation;
+    * prefill, extrapolated: a 64-token prompt through layer 0 plus the
+      last row's lm_head; per token and layer, scaled to a 512-token prompt
+      through all layers."""
     import oracle
     from paper_2608_14376_amd import workload as wl
     oracle.build()
     threads = oracle.get_threads()
-    c2 = dict(cfg, n_layers=2)
+    L = cfg["n_layers"]
     b = wl.bits
-    m = oracle.Model(c2, b(W.embed), b(W.final_norm), b(W.lm_head), [b(t) for t in W.attn_norm[:2]],
-                     [b(t) for t in W.w_qkv[:2]], [b(t) for t in W.w_o[:2]], [b(t) for t in W.mlp_norm[:2]],
-                     [b(t) for t in W.w_gate_up[:2]], [b(t) for t in W.w_down[:2]])
+
+    def model(n):
+        c = dict(cfg, n_layers=n)
+        return oracle.Model(c, b(W.embed), b(W.final_norm), b(W.lm_head), [b(t) for t in W.attn_norm[:n]],
+                            [b(t) for t in W.w_qkv[:n]], [b(t) for t in W.w_o[:n]], [b(t) for t in W.mlp_norm[:n]],
+                            [b(t) for t in W.w_gate_up[:n]], [b(t) for t in W.w_down[:n]])
+
+    m2 = model(2)
     K, V, med = res["_K"], res["_V"], res["_med"]
+    cap = K[0].shape[2]
     bb = wl.make_batch(res["B"], cfg["vocab"], seed=med["seed"], len_lo=LEN_LO, len_hi=LEN_HI)
     live = np.nonzero(bb.valid)[0]
     h = np.zeros(cfg["hidden"], np.uint16)
     t = time.perf_counter()
-    oracle.linear(h, m.lm_head)
+    oracle.linear(h, m2.lm_head)
     t_lm = time.perf_counter() - t
     t2, n = 0.0, 0
     t_start = time.perf_counter()
     for slot in live:
         kv = oracle.KVCache([b(K[l][slot:slot + 1]) for l in range(2)], [b(V[l][slot:slot + 1]) for l in range(2)],
-                            oracle.KV_CONTIGUOUS, 1, K[0].shape[2])
+                            oracle.KV_CONTIGUOUS, 1, cap)
         t = time.perf_counter()
-        oracle.decode_row(m, kv, 0, int(bb.tokens[slot]), int(bb.seq_lens[slot]))
+        oracle.decode_row(m2, kv, 0, int(bb.tokens[slot]), int(bb.seq_lens[slot]))
         t2 += time.perf_counter() - t
         n += 1
         if time.perf_counter() - t_start > budget_s:
             break
     per_row_2 = t2 / n
     per_layer = max(per_row_2 - t_lm, 1e-9) / 2
-    full = per_layer * cfg["n_layers"] + t_lm
-    return dict(value=round(1.0 / full, 4), unit="tokens/s", cores=threads, kind="oracle",
-                sample=f"{n} live rows of the B={res['B']} batch through layers 0-1 + lm_head "
-                       f"(measured {per_row_2:.3f} s/row, lm_head {t_lm:.3f} s), extrapolated to "
-                       f"{cfg['n_layers']} layers: {full:.2f} s per token",
-                host_cpu=_cpu_name())
+    full_extrap = per_layer * L + t_lm
+    # full depth, measured: the first sampled row again, through every layer
+    slot = int(live[0])
+    mL = model(L)
+    kv = oracle.KVCache([b(K[l][slot:slot + 1]) for l in range(L)], [b(V[l][slot:slot + 1]) for l in range(L)],
+                        oracle.KV_CONTIGUOUS, 1, cap)
+    t = time.perf_counter()
+    oracle.decode_row(mL, kv, 0, int(bb.tokens[slot]), int(bb.seq_lens[slot]))
+    full_meas = time.perf_counter() - t
+    del mL, kv
+    # prefill: 64 tokens through layer 0 and the last row's lm_head
+    m1 = model(1)
+    lp = 64
+    kv1 = oracle.KVCache([np.zeros((1, cfg["n_kv_heads"], lp, cfg["head_dim"]), np.uint16)],
+                         [np.zeros((1, cfg["n_kv_heads"], cfg["head_dim"], lp), np.uint16)], oracle.KV_CONTIGUOUS, 1, lp)
+    t = time.perf_counter()
+    oracle.prefill(m1, kv1, 0, wl.make_prompt(cfg["vocab"], lp, seed=3))
+    t_pf = time.perf_counter() - t
+    per_tok_layer = max(t_pf - t_lm, 1e-9) / lp
+    pf_lp = 512
+    pf_tok_s = pf_lp / (pf_lp * L * per_tok_layer + t_lm)
+    return dict(value=round(1.0 / full_meas, 4), unit="tokens/s", cores=threads, kind="oracle",
+                sample=f"one live row of the B={res['B']} headline batch (context {int(bb.seq_lens[slot])}) through "
+                       f"all {L} layers and lm_head, measured: {full_meas:.2f} s per token",
+                decode_extrapolated=dict(tok_s=round(1.0 / full_extrap, 4), s_per_token=round(full_extrap, 3),
+                                         sample=f"{n} live rows through layers 0-1 + lm_head ({per_row_2:.3f} s/row, "
+                                                f"lm_head {t_lm:.3f} s), scaled to {L} layers",
+                                         extrapolated_over_measured=round(full_extrap / full_meas, 4)),
+                prefill_extrapolated=dict(Lp=pf_lp, tok_s=round(pf_tok_s, 3),
+                                          sample=f"{lp}-token prompt through layer 0 + last-row lm_head "
+                                                 f"({t_pf:.2f} s), per token and layer scaled to {L} layers"),
+                threads=threads, host=host_cpu())
 
 
 def kernel_source_sha():
@@ -559,9 +670,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--B", type=int, default=256, help="headline fixed batch size")
     ap.add_argument("--sweep", default="1,8,16,64", help="further fixed batch sizes (comma list, '' for none)")
-    ap.add_argument("--seeds", type=int, default=3, help="batch seeds at the headline B (median reported)")
+    ap.add_argument("--seeds", type=int, default=5, help="batch seeds at the headline B (median reported)")
     ap.add_argument("--first-seed", type=int, default=1, help="first batch seed at the headline B")
-    ap.add_argument("--kernel-iters", type=int, default=10)
+    ap.add_argument("--kernel-iters", type=int, default=10,
+                    help="back-to-back launches of the dominant kernel for its isolated duration (context only)")
+    ap.add_argument("--profile-steps", type=int, default=3,
+                    help="eagerly launched steps with events around every launch, for the in-step kernel durations")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the 32B paged, MoE and prefill workloads")
@@ -603,7 +717,9 @@ def main():
     log(f"[bench] seeded sampler at B={sampler['B']}: {sampler['ms_per_call']} ms per call")
     cpu = None if args.no_cpu_baseline else cpu_baseline(cfg, W, head)
     if cpu:
-        log(f"[bench] cpu oracle: {cpu['value']} tok/s on {cpu['cores']} threads")
+        log(f"[bench] cpu oracle: {cpu['value']} tok/s measured at full depth on {cpu['cores']} threads "
+            f"({cpu['host']['model']}, {cpu['host']['physical_cores']} physical cores); extrapolated "
+            f"{cpu['decode_extrapolated']['tok_s']} tok/s, prefill {cpu['prefill_extrapolated']['tok_s']} tok/s")
     tradeoff = None if args.no_extra else bench_bi_tradeoff(cfg, W, head["_K"], head["_V"], args)
     _drop(head)
     torch.cuda.empty_cache()
@@ -635,8 +751,24 @@ def main():
         r32 = run_B(c32, W32, 32, args, seeds=[1], measure_kernels=True, paged=True, len_lo=1024, len_hi=32768,
                     log_uniform=True, live_frac=(1.0, 1.0))
         r32["kernels"] = {k: v for k, v in r32["kernels"].items() if k in ("attn_split", "attn_merge", "gate_up_gemm")}
+        # the same batch with split-KV off (one split covers a row's whole capacity): the analogue of
+        # the paper's ablation at long, ragged contexts
+        b32 = r32["_med"]["batch"]
+        cap32 = r32["_pt"].shape[1] * r32["_ps"]
+        e_off = corun.Engine(c32, W32, 32, r32["_K"], r32["_V"], layout=corun.KV_PAGED, page_size=r32["_ps"],
+                             page_table=r32["_pt"], opt=corun.options(attn_chunk=(cap32 + 63) // 64 * 64))
+        e_off.decode_run(args.warmup, b32.tokens, b32.valid, b32.seq_lens)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        e_off.decode_run(args.steps, b32.tokens, b32.valid, b32.seq_lens)
+        torch.cuda.synchronize()
+        off_ms = 1e3 * (time.perf_counter() - t) / args.steps
+        e_off.close()
+        del e_off                      # it holds the 32B weights and cache
+        r32["split_kv_off"] = dict(step_ms=round(off_ms, 4), off_cost=round(off_ms / r32["step_ms"] - 1, 4))
+        log(f"[bench] 32B B=32 split-KV off: {off_ms:.3f} ms per step ({100 * (off_ms / r32['step_ms'] - 1):+.1f}%)")
         extra["decode_32b_paged"] = _drop(r32)
-        del W32
+        del W32, b32
         torch.cuda.empty_cache()
         # MoE decode
         cm = wl.config("moe")
@@ -671,7 +803,10 @@ def main():
     traffic, traffic_src = measured_traffic(dom_name, args.B, head["seeds"][len(head["seeds"]) // 2])
     roof = dict(kernel=dom_name, bound="hbm", achieved=dom["gbs"], peak=HBM_PEAK_GBS, unit="GB/s",
                 frac=round(dom["gbs"] / HBM_PEAK_GBS, 4), traffic=traffic,
-                bytes_per_launch=dom["bytes"], us_per_launch=dom["us"], traffic_source=traffic_src,
+                bytes_per_launch=dom["bytes"], us_per_launch=dom["us"],
+                us_source=f"mean of the kernel's launches inside {args.profile_steps} steps of the median batch "
+                          f"(HIP events on the engine stream around each launch)",
+                us_per_launch_isolated=head.get("dominant_isolated_us"), traffic_source=traffic_src,
                 achievable_peak=peaks["hbm_read_gbs"], frac_of_achievable=round(dom["gbs"] / peaks["hbm_read_gbs"], 4))
     out = {
         "metric": METRIC,

@@ -409,6 +409,20 @@ enum {
  * embedding).  CORUN_E_STATE before the engine's first decode step. */
 corun_status corun_time_kernel(corun_engine *e, int32_t kernel, int32_t layer, int32_t n_iters, float *avg_us);
 
+/* Measurement aid: n_steps decode steps, each on the inputs of the last
+ * decode step (uploaded again first, as for corun_time_kernel), with the
+ * step's kernels launched eagerly in the step's order, each with a pair of
+ * HIP events recorded around its own execution (hipExtLaunchKernel).
+ * avg_us[k] receives the mean duration of kernel class k's launches inside
+ * those steps (a class that runs several kernels, such as the MoE router,
+ * counts their sum; each launch runs after the kernels that precede it in
+ * the step, as in the captured graph), launches[k] (or NULL) their count
+ * per step; classes
+ * that do not launch get 0.  Arrays of CORUN_K_COUNT entries.  The steps
+ * rewrite the cache positions the last step wrote, with the same values.
+ * CORUN_E_STATE before the engine's first decode step. */
+corun_status corun_profile_step(corun_engine *e, int32_t n_steps, float *avg_us, int32_t *launches);
+
 /* Host-only checks, usable without a GPU: the shape rules of
  * corun_model_cfg / corun_kv, and the per-row checks of corun_decode_step
  * for a batch of B rows (n_steps further tokens of capacity are required). */

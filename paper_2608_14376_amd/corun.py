@@ -21,7 +21,7 @@ KV_CONTIGUOUS, KV_PAGED = 0, 1
 EXPORTS = ("corun_engine_create", "corun_engine_destroy", "corun_decode_step", "corun_decode_run",
            "corun_prefill", "corun_prefill_chunk", "corun_prefill_batch", "corun_check_config", "corun_check_batch",
            "corun_describe_plan", "corun_describe_prefill_plan",
-           "corun_last_error", "corun_time_kernel", "corun_sample", "corun_sample_noalloc", "corun_engine_info",
+           "corun_last_error", "corun_time_kernel", "corun_profile_step", "corun_sample", "corun_sample_noalloc", "corun_engine_info",
            "corun_routing_trace",
            "corun_sched_create", "corun_sched_destroy", "corun_sched_add_request", "corun_sched_step",
            "corun_sched_output", "corun_sched_state", "corun_sched_last_error")
@@ -108,6 +108,8 @@ def load():
                                               C.c_int32]
     L.corun_time_kernel.restype = st
     L.corun_time_kernel.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.POINTER(C.c_float)]
+    L.corun_profile_step.restype = st
+    L.corun_profile_step.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
     L.corun_sample.restype = st
     L.corun_sample.argtypes = [C.c_void_p, C.c_void_p, C.c_int64, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
                                C.c_void_p, C.c_void_p, C.c_void_p]
@@ -424,6 +426,15 @@ class Engine:
         us = C.c_float()
         _check(self._L.corun_time_kernel(self._h, kernel, layer, n_iters, C.byref(us)))
         return float(us.value)
+
+    def profile_step(self, n_steps: int = 3):
+        """{kernel name: (mean in-step launch duration in us, launches per
+        step)} over n_steps eagerly launched steps with HIP events around
+        every launch (corun_profile_step)."""
+        us = np.zeros(len(KERNEL_NAMES), np.float32)
+        n = np.zeros(len(KERNEL_NAMES), np.int32)
+        _check(self._L.corun_profile_step(self._h, n_steps, us.ctypes.data, n.ctypes.data))
+        return {KERNEL_NAMES[k]: (float(us[k]), int(n[k])) for k in range(len(KERNEL_NAMES)) if n[k]}
 
     def sample(self, logits, valid, positions, seeds, temperature):
         """Seeded sampling of the rows of a device fp32 logits tensor

@@ -278,6 +278,16 @@ struct corun_engine {
     float *rt_logit = nullptr, *rt_pf_logit = nullptr;
     int pf_trace_rows = 0;
     bool decoded = false;   // a decode step has uploaded inputs
+    // corun_profile_step: every kernel of an eager step timed by events around
+    // its own execution; a launch of kernel class `kind` is the recorder's
+    // launches [first, end)
+    struct ProfRec {
+        int kind;
+        size_t first, end;
+    };
+    bool profiling = false;
+    std::vector<ProfRec> prof;
+    LaunchRecorder rec;
     std::vector<uint16_t *> kc, vc;
     KvView view{};
 
@@ -681,30 +691,67 @@ corun_status launch_one(corun_engine *e, int which, int l)
     return CORUN_OK;
 }
 
+// Whether launch_one(k) launches anything for this engine (the QKV epilogue
+// and SwiGLU may run inside the neighbouring kernels instead).
+bool launches(const corun_engine *e, int k)
+{
+    if (k == CORUN_K_QKV_POST) return !e->qkv_in_attn;
+    if (k == CORUN_K_SWIGLU) return e->moe ? !e->egu_fused : !gu_fuses(e, e->plan.gu);
+    return true;
+}
+
+// Run f (the launches of kernel class `kind`); while profiling, with a pair
+// of events around it on the engine's stream.
+template <class F>
+corun_status timed(corun_engine *e, int kind, F &&f)
+{
+    if (!e->profiling) return f();
+    const size_t first = e->rec.launches.size();
+    set_launch_recorder(&e->rec);
+    corun_status s = f();
+    set_launch_recorder(nullptr);
+    if (s == CORUN_OK) e->prof.push_back({kind, first, e->rec.launches.size()});
+    return s;
+}
+
 corun_status enqueue_step(corun_engine *e)
 {
     const corun_model_cfg &c = e->c;
     const Plan &p = e->plan;
     const int B = e->B, H = c.hidden;
     hipStream_t st = e->st;
-    HIP_TRY(launch_embed(e->embed, e->d_tokens, e->d_valid, B, H, e->x, st));
+    const int OTHER = CORUN_K_COUNT;   // embedding and feedback
+    ST_TRY(timed(e, OTHER, [&]() -> corun_status {
+        HIP_TRY(launch_embed(e->embed, e->d_tokens, e->d_valid, B, H, e->x, st));
+        return CORUN_OK;
+    }));
     const MoeBufs mb = decode_moe(e);
     const int dense_S = e->moe ? 0 : p.down.S;
     for (int l = 0; l < c.n_layers; ++l) {
-        HIP_TRY(launch_rmsnorm(e->x, l ? e->p_down : nullptr, l ? dense_S : 0, (long long)B * H, B, H,
-                               e->attn_norm[l], c.rms_eps, e->h, st, fold_of(e, mb, l)));
+        ST_TRY(timed(e, CORUN_K_RMSNORM, [&]() -> corun_status {
+            HIP_TRY(launch_rmsnorm(e->x, l ? e->p_down : nullptr, l ? dense_S : 0, (long long)B * H, B, H,
+                                   e->attn_norm[l], c.rms_eps, e->h, st, fold_of(e, mb, l)));
+            return CORUN_OK;
+        }));
         for (int k : {CORUN_K_QKV_GEMM, CORUN_K_QKV_POST, CORUN_K_ATTN_SPLIT, CORUN_K_ATTN_MERGE, CORUN_K_O_GEMM,
                       CORUN_K_RMSNORM})
-            ST_TRY(launch_one(e, k, l));
-        if (e->moe) ST_TRY(launch_one(e, CORUN_K_MOE_ROUTER, l));
-        for (int k : {CORUN_K_GATE_UP_GEMM, CORUN_K_SWIGLU, CORUN_K_DOWN_GEMM}) ST_TRY(launch_one(e, k, l));
+            if (launches(e, k)) ST_TRY(timed(e, k, [&] { return launch_one(e, k, l); }));
+        if (e->moe) ST_TRY(timed(e, CORUN_K_MOE_ROUTER, [&] { return launch_one(e, CORUN_K_MOE_ROUTER, l); }));
+        for (int k : {CORUN_K_GATE_UP_GEMM, CORUN_K_SWIGLU, CORUN_K_DOWN_GEMM})
+            if (launches(e, k)) ST_TRY(timed(e, k, [&] { return launch_one(e, k, l); }));
     }
-    HIP_TRY(launch_rmsnorm(e->x, e->p_down, dense_S, (long long)B * H, B, H, e->final_norm, c.rms_eps, e->h, st,
-                           fold_of(e, mb, c.n_layers)));
-    ST_TRY(launch_one(e, CORUN_K_LM_HEAD, 0));
-    ST_TRY(launch_one(e, CORUN_K_ARGMAX, 0));
-    HIP_TRY(launch_feedback(e->d_tokens, e->d_seq, e->d_valid, e->d_next, B, e->d_hist, e->d_counter, e->hist_cap,
-                            st));
+    ST_TRY(timed(e, CORUN_K_RMSNORM, [&]() -> corun_status {
+        HIP_TRY(launch_rmsnorm(e->x, e->p_down, dense_S, (long long)B * H, B, H, e->final_norm, c.rms_eps, e->h, st,
+                               fold_of(e, mb, c.n_layers)));
+        return CORUN_OK;
+    }));
+    ST_TRY(timed(e, CORUN_K_LM_HEAD, [&] { return launch_one(e, CORUN_K_LM_HEAD, 0); }));
+    ST_TRY(timed(e, CORUN_K_ARGMAX, [&] { return launch_one(e, CORUN_K_ARGMAX, 0); }));
+    ST_TRY(timed(e, OTHER, [&]() -> corun_status {
+        HIP_TRY(launch_feedback(e->d_tokens, e->d_seq, e->d_valid, e->d_next, B, e->d_hist, e->d_counter,
+                                e->hist_cap, st));
+        return CORUN_OK;
+    }));
     return CORUN_OK;
 }
 
@@ -1122,6 +1169,7 @@ extern "C" void corun_engine_destroy(corun_engine *e)
     if (e->h_valid) (void)hipHostFree(e->h_valid);
     if (e->h_hist) (void)hipHostFree(e->h_hist);
     if (e->h_samp) (void)hipHostFree(e->h_samp);
+    for (hipEvent_t ev : e->rec.pool) (void)hipEventDestroy(ev);
     if (e->ev) (void)hipEventDestroy(e->ev);
     if (e->st) (void)hipStreamDestroy(e->st);
     delete e;
@@ -1549,4 +1597,49 @@ extern "C" corun_status corun_time_kernel(corun_engine *e, int32_t kernel, int32
     (void)hipEventDestroy(t1);
     if (s == CORUN_OK) *avg_us = 1000.f * ms / n_iters;
     return s;
+}
+
+extern "C" corun_status corun_profile_step(corun_engine *e, int32_t n_steps, float *avg_us, int32_t *launches_out)
+{
+    if (!e || !avg_us) return fail(CORUN_E_INVAL, "null argument");
+    if (n_steps < 1) return fail(CORUN_E_INVAL, "n_steps must be >= 1");
+    if (!e->decoded) return fail(CORUN_E_STATE, "no decode step has run: the kernels have no validated inputs");
+    ST_TRY(enter(e));
+    double sum[CORUN_K_COUNT + 1] = {};
+    int cnt[CORUN_K_COUNT + 1] = {};
+    corun_status s = CORUN_OK;
+    for (int i = 0; i < n_steps && s == CORUN_OK; ++i) {
+        s = restore_inputs(e);   // every step at the last step's own validated inputs
+        if (s != CORUN_OK) break;
+        e->prof.clear();
+        e->rec.used = 0;
+        e->rec.launches.clear();
+        e->profiling = true;
+        s = enqueue_step(e);
+        e->profiling = false;
+        if (s != CORUN_OK) break;
+        if (hipStreamSynchronize(e->st) != hipSuccess) {
+            s = fail(CORUN_E_HIP, "profiled step failed");
+            break;
+        }
+        for (const auto &r : e->prof) {
+            double us = 0.0;   // the class's kernels, each from its own start to its own end
+            for (size_t j = r.first; j < r.end && s == CORUN_OK; ++j) {
+                float ms = 0.f;
+                if (hipEventElapsedTime(&ms, e->rec.launches[j].first, e->rec.launches[j].second) != hipSuccess)
+                    s = fail(CORUN_E_HIP, "event timing failed");
+                us += 1000.0 * ms;
+            }
+            if (s != CORUN_OK) break;
+            sum[r.kind] += us;
+            cnt[r.kind] += 1;
+        }
+    }
+    e->profiling = false;
+    if (s != CORUN_OK) return s;
+    for (int k = 0; k < CORUN_K_COUNT; ++k) {
+        avg_us[k] = cnt[k] ? (float)(sum[k] / cnt[k]) : 0.f;
+        if (launches_out) launches_out[k] = cnt[k] / n_steps;
+    }
+    return CORUN_OK;
 }

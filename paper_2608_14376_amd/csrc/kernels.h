@@ -6,7 +6,23 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <hip/hip_ext.h>
+
+#include <utility>
+#include <vector>
+
 namespace corun {
+
+// While set on the calling thread (nullptr: off), every kernel launch of the
+// launchers below records a pair of events around the kernel's own execution
+// and appends it to `launches`; events come from `pool` (grown as needed,
+// owned by the caller), `used` of them taken so far.
+struct LaunchRecorder {
+    std::vector<hipEvent_t> pool;
+    size_t used = 0;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> launches;
+};
+void set_launch_recorder(LaunchRecorder *r);
 
 // Per-row token selection and fp32 residual init: x[b] = float(E[tok_b]),
 // tok_b = valid[b] ? tokens[b] : 0.

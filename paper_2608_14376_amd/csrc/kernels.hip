@@ -25,6 +25,41 @@
 
 namespace corun {
 
+// Launch timing (corun_profile_step): while a recorder is set on the calling
+// thread, every launch below records a pair of events around the kernel's
+// own execution (hipExtLaunchKernel) and lists them in the recorder.
+namespace {
+thread_local LaunchRecorder *t_rec = nullptr;
+
+void launch_events(hipEvent_t *start, hipEvent_t *stop)
+{
+    *start = *stop = nullptr;
+    LaunchRecorder *r = t_rec;
+    if (r == nullptr) return;
+    while (r->used + 2 > r->pool.size()) {
+        hipEvent_t ev;
+        if (hipEventCreate(&ev) != hipSuccess) return;   // untimed launch; the recorder notes nothing
+        r->pool.push_back(ev);
+    }
+    *start = r->pool[r->used];
+    *stop = r->pool[r->used + 1];
+    r->used += 2;
+    r->launches.push_back({*start, *stop});
+}
+}  // namespace
+
+void set_launch_recorder(LaunchRecorder *r) { t_rec = r; }
+
+#define KLAUNCH(kernel, grid, block, shmem, stream, ...)                                                   \
+    do {                                                                                                    \
+        hipEvent_t ks_, ke_;                                                                                \
+        launch_events(&ks_, &ke_);                                                                          \
+        if (ks_ != nullptr)                                                                                 \
+            hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ks_, ke_, 0, __VA_ARGS__);            \
+        else                                                                                                \
+            hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);                            \
+    } while (0)
+
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -125,7 +160,7 @@ hipError_t launch_embed(const uint16_t *E, const int32_t *tokens, const uint8_t 
                         float *x, hipStream_t st)
 {
     const long long blocks = (long long)rows * ((H + 255) / 256);
-    hipLaunchKernelGGL(k_embed, dim3((unsigned)blocks), dim3(256), 0, st, E, tokens, valid, H, x);
+    KLAUNCH(k_embed, dim3((unsigned)blocks), dim3(256), 0, st, E, tokens, valid, H, x);
     return hipGetLastError();
 }
 
@@ -226,10 +261,10 @@ hipError_t launch_rmsnorm(float *x, const float *part, int S, long long part_str
     const int groups = H / 4;
     const int nth = groups >= 1024 ? 1024 : groups;        // multiple of 64
     if (groups <= nth)
-        hipLaunchKernelGGL((k_rmsnorm<1>), dim3(rows), dim3(nth), 0, st, x, part, S, part_stride, rows, H, g, eps, h,
+        KLAUNCH((k_rmsnorm<1>), dim3(rows), dim3(nth), 0, st, x, part, S, part_stride, rows, H, g, eps, h,
                            mf);
     else
-        hipLaunchKernelGGL((k_rmsnorm<2>), dim3(rows), dim3(nth), 0, st, x, part, S, part_stride, rows, H, g, eps, h,
+        KLAUNCH((k_rmsnorm<2>), dim3(rows), dim3(nth), 0, st, x, part, S, part_stride, rows, H, g, eps, h,
                            mf);
     return hipGetLastError();
 }
@@ -883,39 +918,39 @@ hipError_t launch_gemm_dma(const uint16_t *A, int lda, const uint16_t *W, const 
         if (act != nullptr) {   // gate/up-interleaved copy, SwiGLU epilogue, no split-K
             if (g.S != 1 || g.N % 128 != 0) return hipErrorInvalidValue;
             if (g.bm == 32 && g.bn == 128)
-                hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, true, true>), grid, dim3(128), 0, st, A, lda, W,
+                KLAUNCH((k_gemm_dma<32, 128, 64, 4, 1, 2, true, true>), grid, dim3(128), 0, st, A, lda, W,
                                    g.M, g.N, g.K, g.Kc, nullptr, 0, ldo, nullptr, act, ExpertTiles{});
             else if (g.bm == 64 && g.bn == 128)
-                hipLaunchKernelGGL((k_gemm_dma<64, 128, 64, 4, 1, 2, true, true>), grid, dim3(128), 0, st, A, lda, W,
+                KLAUNCH((k_gemm_dma<64, 128, 64, 4, 1, 2, true, true>), grid, dim3(128), 0, st, A, lda, W,
                                    g.M, g.N, g.K, g.Kc, nullptr, 0, ldo, nullptr, act, ExpertTiles{});
             else
                 return hipErrorInvalidValue;
             return hipGetLastError();
         }
         if (g.bm == 32 && g.bn == 128)
-            hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, true>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N,
+            KLAUNCH((k_gemm_dma<32, 128, 64, 4, 1, 2, true>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N,
                                g.K, g.Kc, out, split_stride, ldo, amax, nullptr, ExpertTiles{});
         else if (g.bm == 64 && g.bn == 128)
-            hipLaunchKernelGGL((k_gemm_dma<64, 128, 64, 4, 1, 2, true>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N,
+            KLAUNCH((k_gemm_dma<64, 128, 64, 4, 1, 2, true>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N,
                                g.K, g.Kc, out, split_stride, ldo, amax, nullptr, ExpertTiles{});
         else
             return hipErrorInvalidValue;
         return hipGetLastError();
     }
     if (g.bm == 32 && g.bn == 128)
-        hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
+        KLAUNCH((k_gemm_dma<32, 128, 64, 4, 1, 2>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
                            out, split_stride, ldo, amax, nullptr, ExpertTiles{});
     else if (g.bm == 64 && g.bn == 128)
-        hipLaunchKernelGGL((k_gemm_dma<64, 128, 64, 4, 1, 2>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
+        KLAUNCH((k_gemm_dma<64, 128, 64, 4, 1, 2>), grid, dim3(128), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
                            out, split_stride, ldo, amax, nullptr, ExpertTiles{});
     else if (g.bm == 128 && g.bn == 128)
-        hipLaunchKernelGGL((k_gemm_dma<128, 128, 64, 4, 2, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
+        KLAUNCH((k_gemm_dma<128, 128, 64, 4, 2, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
                            out, split_stride, ldo, amax, nullptr, ExpertTiles{});
     else if (g.bm == 256 && g.bn == 128)
-        hipLaunchKernelGGL((k_gemm_dma<256, 128, 64, 3, 2, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
+        KLAUNCH((k_gemm_dma<256, 128, 64, 3, 2, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
                            out, split_stride, ldo, amax, nullptr, ExpertTiles{});
     else if (g.bm == 256 && g.bn == 256)
-        hipLaunchKernelGGL((k_gemm_dma<256, 256, 32, 4, 2, 8>), grid, dim3(512), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
+        KLAUNCH((k_gemm_dma<256, 256, 32, 4, 2, 8>), grid, dim3(512), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc,
                            out, split_stride, ldo, amax, nullptr, ExpertTiles{});
     else
         return hipErrorInvalidValue;
@@ -931,15 +966,15 @@ hipError_t launch_gemm_tiled(const uint16_t *A, int lda, const uint16_t *W, cons
     dim3 grid(num_m * num_n, g.S);
     switch (bm) {
     case 64:
-        hipLaunchKernelGGL((k_gemm_tiled<64, 128, 1>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+        KLAUNCH((k_gemm_tiled<64, 128, 1>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
                            split_stride, ldo, amax);
         break;
     case 128:
-        hipLaunchKernelGGL((k_gemm_tiled<128, 128, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+        KLAUNCH((k_gemm_tiled<128, 128, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
                            split_stride, ldo, amax);
         break;
     case 256:
-        hipLaunchKernelGGL((k_gemm_tiled<256, 128, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+        KLAUNCH((k_gemm_tiled<256, 128, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
                            split_stride, ldo, amax);
         break;
     default:
@@ -957,15 +992,15 @@ hipError_t launch_gemm(const uint16_t *A, int lda, const uint16_t *W, const Gemm
     dim3 grid((ncb + 3) / 4, g.S, (g.M + rows_per_tile - 1) / rows_per_tile);
     switch (g.mt) {
     case 1:
-        hipLaunchKernelGGL((k_gemm<1, NT, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+        KLAUNCH((k_gemm<1, NT, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
                            split_stride, ldo, amax);
         break;
     case 2:
-        hipLaunchKernelGGL((k_gemm<2, NT, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+        KLAUNCH((k_gemm<2, NT, 4>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
                            split_stride, ldo, amax);
         break;
     case 4:
-        hipLaunchKernelGGL((k_gemm<4, NT, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
+        KLAUNCH((k_gemm<4, NT, 2>), grid, dim3(256), 0, st, A, lda, W, g.M, g.N, g.K, g.Kc, out,
                            split_stride, ldo, amax);
         break;
     default:
@@ -1060,7 +1095,7 @@ hipError_t launch_qkv_post(const float *part, int S, long long part_stride, int 
                            hipStream_t st)
 {
     const long long blocks = (long long)rows * (nq + 2 * nkv);
-    hipLaunchKernelGGL(k_qkv_post, dim3((unsigned)blocks), dim3(64), 0, st, part, S, part_stride, valid, pos,
+    KLAUNCH(k_qkv_post, dim3((unsigned)blocks), dim3(64), 0, st, part, S, part_stride, valid, pos,
                        slot_of_row, slot_const, nq, nkv, d, rope_tab, q, kc, vc, kv);
     return hipGetLastError();
 }
@@ -1597,7 +1632,7 @@ static void launch_attn_dg(const uint16_t *q, int rows, const uint8_t *valid, co
                            uint16_t *vc, KvView kv, int chunk, int max_splits, float *ws, hipStream_t st, QkvIn qi,
                            const int32_t *row_order)
 {
-    hipLaunchKernelGGL((k_attn_split<D, G>), dim3(nkv, max_splits, rows), dim3(256), 0, st, q, valid, pos,
+    KLAUNCH((k_attn_split<D, G>), dim3(nkv, max_splits, rows), dim3(256), 0, st, q, valid, pos,
                        slot_of_row, slot_const, nq, nkv, kc, vc, kv, chunk, max_splits, ws, qi, row_order);
 }
 
@@ -1607,13 +1642,13 @@ static void launch_merge_dg(const float *ws, int rows, const uint8_t *valid, con
 {
     if (max_splits <= 8) {   // one round trip either way: the per-kv-head layout launches fewer wavefronts
         const size_t shm = sizeof(float) * (2 * G * max_splits + 2 * G);
-        hipLaunchKernelGGL((k_attn_merge_kv<D, G>), dim3(nkv, rows), dim3(256), shm, st, ws, valid, pos, nq, nkv,
+        KLAUNCH((k_attn_merge_kv<D, G>), dim3(nkv, rows), dim3(256), shm, st, ws, valid, pos, nq, nkv,
                            chunk, max_splits, o);
         return;
     }
     constexpr int HB = merge_heads<D, G>();
     const size_t shm = sizeof(float) * 2 * HB * max_splits;
-    hipLaunchKernelGGL((k_attn_merge<D, G>), dim3(nq / HB, rows), dim3(D * HB), shm, st, ws, valid, pos, nq, nkv,
+    KLAUNCH((k_attn_merge<D, G>), dim3(nq / HB, rows), dim3(D * HB), shm, st, ws, valid, pos, nq, nkv,
                        chunk, max_splits, o);
 }
 
@@ -1682,7 +1717,7 @@ hipError_t launch_swiglu(const float *part, int S, long long part_stride, int ro
                          hipStream_t st)
 {
     const long long blocks = (long long)rows * ((F + 255) / 256);
-    hipLaunchKernelGGL(k_swiglu, dim3((unsigned)blocks), dim3(256), 0, st, part, S, part_stride, F, a, lda);
+    KLAUNCH(k_swiglu, dim3((unsigned)blocks), dim3(256), 0, st, part, S, part_stride, F, a, lda);
     return hipGetLastError();
 }
 
@@ -1699,7 +1734,7 @@ __global__ void k_reduce_splits(const float *__restrict__ part, int S, long long
 hipError_t launch_reduce_splits(const float *part, int S, long long stride, long long n, float *out, hipStream_t st)
 {
     long long blocks = std::min<long long>((n + 255) / 256, 65536);
-    hipLaunchKernelGGL(k_reduce_splits, dim3((unsigned)blocks), dim3(256), 0, st, part, S, stride, n, out);
+    KLAUNCH(k_reduce_splits, dim3((unsigned)blocks), dim3(256), 0, st, part, S, stride, n, out);
     return hipGetLastError();
 }
 
@@ -1773,13 +1808,13 @@ __global__ __launch_bounds__(256) void k_argmax_partials(const ArgBest *__restri
 hipError_t launch_argmax_partials(const ArgBest *part, int rows, int np, const uint8_t *valid, int32_t *next,
                                   hipStream_t st)
 {
-    hipLaunchKernelGGL(k_argmax_partials, dim3(rows), dim3(256), 0, st, part, np, valid, next);
+    KLAUNCH(k_argmax_partials, dim3(rows), dim3(256), 0, st, part, np, valid, next);
     return hipGetLastError();
 }
 
 hipError_t launch_argmax(const float *logits, int rows, int V, const uint8_t *valid, int32_t *next, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_argmax, dim3(rows), dim3(256), 0, st, logits, V, valid, next);
+    KLAUNCH(k_argmax, dim3(rows), dim3(256), 0, st, logits, V, valid, next);
     return hipGetLastError();
 }
 
@@ -1804,7 +1839,7 @@ __global__ void k_feedback(int32_t *tokens, int32_t *seq_lens, const uint8_t *va
 hipError_t launch_feedback(int32_t *tokens, int32_t *seq_lens, const uint8_t *valid, const int32_t *next, int B,
                            int32_t *history, int32_t *counter, int max_hist, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_feedback, dim3(1), dim3(256), 0, st, tokens, seq_lens, valid, next, B, history, counter,
+    KLAUNCH(k_feedback, dim3(1), dim3(256), 0, st, tokens, seq_lens, valid, next, B, history, counter,
                        max_hist);
     return hipGetLastError();
 }
@@ -1823,7 +1858,7 @@ __global__ void k_rope_table(float2 *tab, int d, double theta)
 
 hipError_t launch_rope_table(float2 *tab, int max_pos, int d, double theta, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_rope_table, dim3(max_pos), dim3(64), 0, st, tab, d, theta);
+    KLAUNCH(k_rope_table, dim3(max_pos), dim3(64), 0, st, tab, d, theta);
     return hipGetLastError();
 }
 
@@ -1838,7 +1873,7 @@ hipError_t launch_fill_u32(uint32_t *p, long long n_words, uint32_t v, hipStream
     if (n_words <= 0) return hipSuccess;
     long long blocks = (n_words + 255) / 256;
     if (blocks > 65536) blocks = 65536;
-    hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)blocks), dim3(256), 0, st, p, n_words, v);
+    KLAUNCH(k_fill_u32, dim3((unsigned)blocks), dim3(256), 0, st, p, n_words, v);
     return hipGetLastError();
 }
 
@@ -1871,7 +1906,7 @@ hipError_t launch_pack_weights(const uint16_t *W, int N, int K, uint16_t *P, hip
     const long long units = (long long)packed_weight_elems(N, K) / 8;
     long long blocks = (units + 255) / 256;
     if (blocks > 65536) blocks = 65536;
-    hipLaunchKernelGGL(k_pack_weights, dim3((unsigned)blocks), dim3(256), 0, st, W, N, K, P, units,
+    KLAUNCH(k_pack_weights, dim3((unsigned)blocks), dim3(256), 0, st, W, N, K, P, units,
                        interleave ? N / 2 : 0);
     return hipGetLastError();
 }
@@ -1884,7 +1919,7 @@ __global__ void k_iota(int32_t *p, int n)
 
 hipError_t launch_iota(int32_t *p, int n, hipStream_t st)
 {
-    hipLaunchKernelGGL(k_iota, dim3((n + 255) / 256), dim3(256), 0, st, p, n);
+    KLAUNCH(k_iota, dim3((n + 255) / 256), dim3(256), 0, st, p, n);
     return hipGetLastError();
 }
 
@@ -1979,7 +2014,7 @@ hipError_t launch_moe_route(const float *part, int S, long long part_stride, int
                             float *logit_trace)
 {
     if (E > 256 || top_k > 16 || top_k > E) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_moe_route, dim3(rows), dim3(64), 0, st, part, S, part_stride, E, top_k, valid, sel, wsel,
+    KLAUNCH(k_moe_route, dim3(rows), dim3(64), 0, st, part, S, part_stride, E, top_k, valid, sel, wsel,
                        sel_trace, logit_trace);
     return hipGetLastError();
 }
@@ -2065,7 +2100,7 @@ hipError_t launch_moe_dispatch(const int32_t *sel, int n_assign, int E, int n_sl
                                hipStream_t st)
 {
     if (E > 256) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_moe_dispatch, dim3(1), dim3(1024), 0, st, sel, n_assign, E, n_slots, list, tiles);
+    KLAUNCH(k_moe_dispatch, dim3(1), dim3(1024), 0, st, sel, n_assign, E, n_slots, list, tiles);
     return hipGetLastError();
 }
 
@@ -2156,7 +2191,7 @@ hipError_t launch_moe_gemm(const uint16_t *A, int lda, int row_div, const uint16
 {
     constexpr int NT = 4;
     const int ncb = (N + 16 * NT - 1) / (16 * NT);
-    hipLaunchKernelGGL((k_moe_gemm<NT, 4>), dim3((ncb + 3) / 4, n_slots), dim3(256), 0, st, A, lda, row_div, W,
+    KLAUNCH((k_moe_gemm<NT, 4>), dim3((ncb + 3) / 4, n_slots), dim3(256), 0, st, A, lda, row_div, W,
                        w_expert_stride, N, K, list, tiles, out, ldo);
     return hipGetLastError();
 }
@@ -2169,13 +2204,13 @@ hipError_t launch_moe_gemm_dma(const uint16_t *A, int lda, int row_div, const ui
     const ExpertTiles et{list, tiles, row_div, w_expert_stride};
     const dim3 grid((N + 127) / 128, n_slots);
     if (act != nullptr)
-        hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, true, true, true>), grid, dim3(128), 0, st, A, lda, W, 16,
+        KLAUNCH((k_gemm_dma<32, 128, 64, 4, 1, 2, true, true, true>), grid, dim3(128), 0, st, A, lda, W, 16,
                            N, K, K, nullptr, 0, ldo, nullptr, act, et);
     else if (packed)
-        hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, true, false, true>), grid, dim3(128), 0, st, A, lda, W,
+        KLAUNCH((k_gemm_dma<32, 128, 64, 4, 1, 2, true, false, true>), grid, dim3(128), 0, st, A, lda, W,
                            16, N, K, K, out, 0, ldo, nullptr, nullptr, et);
     else
-        hipLaunchKernelGGL((k_gemm_dma<32, 128, 64, 4, 1, 2, false, false, true>), grid, dim3(128), 0, st, A, lda, W,
+        KLAUNCH((k_gemm_dma<32, 128, 64, 4, 1, 2, false, false, true>), grid, dim3(128), 0, st, A, lda, W,
                            16, N, K, K, out, 0, ldo, nullptr, nullptr, et);
     return hipGetLastError();
 }
@@ -2461,9 +2496,9 @@ hipError_t launch_prefill_attn_multi(const uint16_t *q, const int32_t *seq, int 
     if (nseq <= 0 || total_groups <= 0) return hipErrorInvalidValue;
     dim3 grid(nkv, total_groups);
     if (d == 128)
-        hipLaunchKernelGGL((k_prefill_attn_multi<128>), grid, dim3(512), 0, st, q, seq, nseq, nq, nkv, kc, vc, kv, o);
+        KLAUNCH((k_prefill_attn_multi<128>), grid, dim3(512), 0, st, q, seq, nseq, nq, nkv, kc, vc, kv, o);
     else if (d == 64)
-        hipLaunchKernelGGL((k_prefill_attn_multi<64>), grid, dim3(512), 0, st, q, seq, nseq, nq, nkv, kc, vc, kv, o);
+        KLAUNCH((k_prefill_attn_multi<64>), grid, dim3(512), 0, st, q, seq, nseq, nq, nkv, kc, vc, kv, o);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
@@ -2483,7 +2518,7 @@ __global__ __launch_bounds__(256) void k_gather_last_rows(const uint16_t *__rest
 hipError_t launch_gather_last_rows(const uint16_t *src, const int32_t *seq, int n, int H, uint16_t *dst, hipStream_t st)
 {
     if (n <= 0 || H % 8) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_gather_last_rows, dim3(n), dim3(256), 0, st, src, seq, H, dst);
+    KLAUNCH(k_gather_last_rows, dim3(n), dim3(256), 0, st, src, seq, H, dst);
     return hipGetLastError();
 }
 
@@ -2495,9 +2530,9 @@ hipError_t launch_prefill_attn(const uint16_t *q, int n, int p0, int nq, int nkv
     const int units = ((n + 31) / 32) * G;
     dim3 grid(nkv, (units + 7) / 8);
     if (d == 128)
-        hipLaunchKernelGGL((k_prefill_attn<128>), grid, dim3(512), 0, st, q, n, p0, nq, nkv, slot, kc, vc, kv, o);
+        KLAUNCH((k_prefill_attn<128>), grid, dim3(512), 0, st, q, n, p0, nq, nkv, slot, kc, vc, kv, o);
     else if (d == 64)
-        hipLaunchKernelGGL((k_prefill_attn<64>), grid, dim3(512), 0, st, q, n, p0, nq, nkv, slot, kc, vc, kv, o);
+        KLAUNCH((k_prefill_attn<64>), grid, dim3(512), 0, st, q, n, p0, nq, nkv, slot, kc, vc, kv, o);
     else
         return hipErrorInvalidValue;
     return hipGetLastError();
@@ -2619,7 +2654,7 @@ hipError_t launch_sample(const float *logits, long long ld, int rows, int V, con
                          const uint64_t *seed, const float *temp, int32_t *token, float *logprob, hipStream_t st)
 {
     if (rows <= 0 || V <= 0) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_sample, dim3(rows), dim3(1024), 0, st, logits, ld, V, valid, pos, seed, temp, token,
+    KLAUNCH(k_sample, dim3(rows), dim3(1024), 0, st, logits, ld, V, valid, pos, seed, temp, token,
                        logprob);
     return hipGetLastError();
 }

@@ -161,3 +161,39 @@ def test_time_kernel_needs_a_step_and_keeps_results(poison):
     assert np.array_equal(outs[0][0], outs[1][0])
     for l in range(cfg["n_layers"]):
         assert np.array_equal(outs[0][1][l], outs[1][1][l]) and np.array_equal(outs[0][2][l], outs[1][2][l])
+
+
+def test_profile_step_times_every_launch_and_changes_nothing():
+    """corun_profile_step: every kernel class the step launches gets a
+    positive in-step duration and its launch count (norms 2 L + 1, the other
+    per-layer kernels L, lm_head and argmax once); it refuses before the first
+    step; and the next step's logits and cache match an engine that never
+    profiled, bit for bit."""
+    cfg = wl.config("tiny")
+    Wg = to_device(wl.make_weights(cfg, seed=74))
+    B, cap = 4, 160
+    K, V = wl.make_kv_contiguous(cfg, B, cap, seed=75, device=DEV)
+    b = wl.make_batch(B, cfg["vocab"], seed=76, len_lo=16, len_hi=128)
+    outs = []
+    for prof in (True, False):
+        Kc, Vc = [k.clone() for k in K], [v.clone() for v in V]
+        eng = corun.Engine(cfg, Wg, B, Kc, Vc, opt=corun.options(qkv_epilogue=1))
+        logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+        if prof:
+            with pytest.raises(corun.CorunError) as ei:
+                eng.profile_step(2)
+            assert ei.value.status == corun.E_STATE
+        eng.decode_step(b.tokens, b.valid, b.seq_lens, logits)
+        if prof:
+            p = eng.profile_step(2)
+            L = cfg["n_layers"]
+            want = {"rmsnorm": 2 * L + 1, "qkv_gemm": L, "qkv_post": L, "attn_split": L, "attn_merge": L,
+                    "o_gemm": L, "gate_up_gemm": L, "down_gemm": L, "lm_head": 1, "argmax": 1}
+            for name, n in want.items():
+                assert name in p and p[name][1] == n and 0.0 < p[name][0] < 1e5, (name, p.get(name))
+        eng.decode_step(b.tokens, b.valid, b.seq_lens, logits)
+        torch.cuda.synchronize()
+        outs.append((logits.cpu().numpy().view(np.int32)[b.valid == 1], [wl.bits(k) for k in Kc]))
+        eng.close()
+    assert np.array_equal(outs[0][0], outs[1][0])
+    assert all(np.array_equal(x, y) for x, y in zip(outs[0][1], outs[1][1]))
