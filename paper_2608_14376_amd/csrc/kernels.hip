@@ -1259,11 +1259,14 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
     fetch_pages(t0, 0);
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     lds_barrier();
+    // Step i's loads are issued as soon as every wavefront has taken step
+    // i - 1's fragments out of the tile into registers, so they are in flight
+    // while step i - 1 is computed; a paged cache's pages for step i + 1 are
+    // fetched right behind them.
+    issue(t0, 0);
+    if (nsteps > 1) fetch_pages(t0 + STEP, 1);
     for (int st_i = 0; st_i < nsteps; ++st_i) {
         const int tb0 = t0 + STEP * st_i;
-        if (st_i > 0) lds_barrier();                  // every wavefront is done with the previous step
-        issue(tb0, st_i & 1);
-        if (st_i + 1 < nsteps) fetch_pages(tb0 + STEP, (st_i + 1) & 1);
         if (fused && st_i == 0) {
             // The QKV epilogue while the first step's loads are in flight:
             // pair pi < G d/2 is q (head pi / (d/2)); the owner of the new
@@ -1336,10 +1339,12 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
             lds_barrier();
         }
         const int tb = tb0 + 32 * wave;
-        if (tb >= t1) continue;                       // wave-uniform: no token of this block is real
+        const bool active = tb < t1;                  // wave-uniform: some token of this 32-token block is real
         const int wt1 = t1;
         // fragments from LDS
         bf16x8 kf[2][D / 32];
+        uint4 vfr[ET];
+        if (active) {
 #pragma unroll
         for (int T = 0; T < 2; ++T) {
             const int tl = 32 * wave + attn_tok(T, hl);
@@ -1347,7 +1352,6 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
             for (int kk = 0; kk < D / 32; ++kk)
                 kf[T][kk] = __builtin_bit_cast(bf16x8, tile[tl * KCH + ((kg + 4 * kk) ^ attn_kswz<KCH>(tl))]);
         }
-        uint4 vfr[ET];
         {
             const int nv = min(8, wt1 - (tb + 8 * kg));   // how many of the lane's eight tokens are real
             const int c = 4 * wave + kg;
@@ -1369,6 +1373,16 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
                 vfr[et] = v;
             }
         }
+        }
+        // the tile is free once every wavefront holds its fragments: the next
+        // step's loads (and the pages of the one after) go out now
+        __builtin_amdgcn_s_waitcnt(0xC07F);           // lgkmcnt(0): this wavefront's LDS reads are done
+        lds_barrier();
+        if (st_i + 1 < nsteps) {
+            issue(tb0 + STEP, (st_i + 1) & 1);
+            if (st_i + 2 < nsteps) fetch_pages(tb0 + 2 * STEP, st_i & 1);
+        }
+        if (!active) continue;
         f32x4 st[2];
 #pragma unroll
         for (int T = 0; T < 2; ++T) {
