@@ -87,6 +87,24 @@ def kernel_bytes_flops(cfg, B, lens_live, plan, swiglu_fused=False):
         corun.K_QKV_POST: (4 * S["qkv"] * B * nqkv + 2 * B * nq * d + n_live * 2 * nkv * d * 2, 0),
         corun.K_ARGMAX: (8 * B * ((V + 63) // 64) + 4 * B, 0),
     }
+    gv = all((plan[n]["m_tile"], plan[n]["n_tile"]) == (16, 16) for n in ("qkv", "o", "gate_up", "down"))
+    if gv:
+        # the small-batch layer: projections from fragment-packed copies (K
+        # padded to 32), no split-K; qkv and gate/up read the fp32 residual,
+        # the gain and the 16-column sums of squares (their norm), qkv writes
+        # q and the appended k, v, gate/up the bf16 activations; o and down
+        # read and write the residual and write the sums of squares; the one
+        # RMSNorm of the step (the final one) reads x and writes h
+        Kp = lambda K: (K + 31) // 32 * 32
+        norm_in = 4 * B * H + 2 * H + 4 * B * (H // 16)
+        resid = 8 * B * H + 4 * B * (H // 16)
+        bf[corun.K_QKV_GEMM] = (2 * nqkv * Kp(H) + norm_in + 2 * B * nq * d + n_live * 2 * nkv * d * 2,
+                                2 * B * nqkv * H)
+        bf[corun.K_O_GEMM] = (2 * H * Kp(nq * d) + 2 * B * nq * d + resid, 2 * B * H * nq * d)
+        bf[corun.K_GATE_UP_GEMM] = (2 * 2 * F * Kp(H) + norm_in + 2 * B * F, 2 * B * 2 * F * H)
+        bf[corun.K_DOWN_GEMM] = (2 * H * Kp(F) + 2 * B * F + resid, 2 * B * H * F)
+        bf[corun.K_RMSNORM] = (4 * B * H + 2 * B * H + 2 * H, 0)
+        return bf
     if E:
         bf[corun.K_MOE_ROUTER] = gemm(E, H, 4)
         bf[corun.K_GATE_UP_GEMM] = gemm(2 * Fe, H, 4, rows=n_live * k, mats=E)

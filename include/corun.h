@@ -138,8 +138,10 @@ typedef struct {
                                   decode plan streams it with the small-M kernel (B_fixed <= 64) into a layout of
                                   contiguous 128 x 64 tiles, in memory it owns (one more copy of those weights),
                                   and reads that copy from then on, in decode and in prefill projections of up to
-                                  64 rows; results are bit-identical either way.  The weights must not change
-                                  after creation.  1 = no copies: read the caller's row-major weights. */
+                                  64 rows; results are bit-identical either way.  With the small-batch layer
+                                  (small_batch_layer) the four layer projections are copied into its fragment
+                                  layout instead.  The weights must not change after creation.  1 = no copies:
+                                  read the caller's row-major weights (and no small-batch layer). */
     int32_t qkv_epilogue;      /* where the decode step applies the QKV epilogue (RoPE, KV append): 0 = chosen
                                   from B (inside the attention kernel for B_fixed <= 8, where it saves a launch;
                                   its own kernel above, where recomputing q in every attention block costs
@@ -148,6 +150,17 @@ typedef struct {
                                   and the router logits they were chosen from, for the last decode step and the
                                   last prefill call (corun_routing_trace).  Extra workspace of
                                   n_layers x rows x (top_k + n_experts) x 4 bytes; results are unchanged. */
+    int32_t small_batch_layer; /* the decode layer for the smallest batches: every layer projection streams a
+                                  fragment-packed weight copy (16 output columns x 32 K elements per 1 KB MFMA
+                                  operand, made at creation in memory the engine owns) over the whole of K, with no
+                                  split-K; O and down add straight into the fp32 residual, QKV and gate/up
+                                  normalise their input on the fly, RoPE + KV append and SwiGLU run in their
+                                  epilogues, and a layer launches no RMSNorm.  Results differ in rounding from the
+                                  split-K plan (a different fixed K order), not in position invariance.
+                                  0 = automatic: dense models at B_fixed = 1 (unless no_weight_pack,
+                                  batch_invariant, qkv_epilogue, split_k_override or gemm_bm is set);
+                                  1 = on for a dense model with B_fixed <= 8 (CORUN_E_INVAL otherwise);
+                                  2 = off. */
 } corun_options;
 
 /* Create an engine for one fixed padded batch size B_fixed (Sec. IV,
@@ -434,9 +447,12 @@ corun_status corun_check_batch(const corun_model_cfg *cfg, const corun_kv *kv, c
 /* The launch plan an engine would use (host-only, no GPU): fills `out` with
  * up to `cap` int32 values -- B, padded M, then (N, K, split_k, k_chunk,
  * m_tile, n_tile) for the qkv, o, gate_up, down and lm_head projections
- * (m_tile 0 = the skinny kernel; n_tile 0 = the LDS-tiled kernel, else the
- * pipelined kernel's N tile), then the attention chunk and its maximum split
- * count (32 values).  Returns the count written or a negative corun_status. */
+ * (m_tile 0 = the skinny kernel; n_tile 0 = the LDS-tiled kernel; m_tile =
+ * n_tile = 16 the small-batch layer's fragment-packed kernel, k_chunk = K
+ * rounded up to 32; else the pipelined kernel's N tile), then the attention
+ * chunk and its maximum split count (32 values).  Returns the count written
+ * or a negative corun_status (CORUN_E_INVAL for small_batch_layer = 1 where
+ * the layer cannot run). */
 int32_t corun_describe_plan(const corun_model_cfg *cfg, const corun_kv *kv, int32_t B_fixed,
                             const corun_options *opt, int32_t *out, int32_t cap);
 

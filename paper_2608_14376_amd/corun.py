@@ -57,7 +57,8 @@ class KV(C.Structure):
 class Options(C.Structure):
     _fields_ = [(n, C.c_int32) for n in (
         "attn_chunk", "max_prefill_len", "no_graph", "poison_workspace", "split_k_override", "gemm_bm",
-        "batch_invariant", "bi_prefill", "no_weight_pack", "qkv_epilogue", "record_routing")]
+        "batch_invariant", "bi_prefill", "no_weight_pack", "qkv_epilogue", "record_routing",
+        "small_batch_layer")]
 
 
 class CorunError(RuntimeError):
@@ -175,10 +176,10 @@ def kv_struct(layout: int, n_slots: int, k, v, keep, max_seq_len=0, page_size=0,
 
 def options(attn_chunk=0, max_prefill_len=0, no_graph=False, poison_workspace=False, split_k_override=0,
             gemm_bm=0, batch_invariant=False, bi_prefill=False, no_weight_pack=False, qkv_epilogue=0,
-            record_routing=False):
+            record_routing=False, small_batch_layer=0):
     return Options(attn_chunk, max_prefill_len, int(no_graph), int(poison_workspace), split_k_override, gemm_bm,
                    int(batch_invariant), int(bi_prefill), int(no_weight_pack), int(qkv_epilogue),
-                   int(record_routing))
+                   int(record_routing), int(small_batch_layer))
 
 
 def _np(a, dt):

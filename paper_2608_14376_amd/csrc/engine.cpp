@@ -61,6 +61,12 @@ struct Proj {
 
 struct Plan {
     int B = 0, Mp = 0, mt = 1;
+    // gv: the small-batch layer -- qkv, o, gate/up and down on the
+    // fragment-packed projection kernel (launch_gemv), no split-K anywhere:
+    // o and down add into the residual, qkv and gate/up normalise their
+    // input on the fly, RoPE + KV append and SwiGLU run in their epilogues,
+    // so a layer launches no RMSNorm, QKV-epilogue or SwiGLU kernel
+    bool gv = false;
     Proj qkv, o, gu, down, lm, router;
     int moe_slots = 0;   // tile slots of the expert projections: E + ceil(B top_k / 16)
     int chunk = 0, max_splits = 0;
@@ -229,6 +235,31 @@ Plan make_plan(const corun_model_cfg *c, const corun_kv *kv, int B, const corun_
     // under the split override test aid; the 64-row tile has no argmax epilogue
     p.lm = choose_proj(c->vocab, H, B, so > 0 ? so : 1, 0, bo == 64 ? 0 : bo, bi);
     if (p.lm.bm == 64 && p.lm.bn == 0) p.lm = choose_proj(c->vocab, H, 64, so > 0 ? so : 1, 0, 0);
+    // lm_head at 128 < M <= 256: 256 x 128 tiles (two wavefronts per 128
+    // rows, 64-column wavefront tiles, as the argmax epilogue needs) stream
+    // the vocabulary faster than 256 x 256 tiles: 393 against 435 us at
+    // M = 256 over 151936 x 4096.  Same K order per element, same bits.
+    if (p.lm.bm == 256 && p.lm.bn == 256 && B <= 256 && p.lm.S == 1) p.lm.bn = 128;
+    // The small-batch layer (small_batch_layer): automatic for dense models
+    // at B = 1 (its kernels stream the fragment-packed copies the engine
+    // makes, so not with no_weight_pack, nor under the tuning overrides or
+    // batch-invariant mode).  At B = 1 it drops both RMSNorm launches of a
+    // layer and the QKV fold in attention: the 8B-shaped step measured 3.58
+    // against 3.77 ms.  At B = 8 the eight rows' norm, recomputed by every
+    // workgroup, and its projections' in-step rate (the pipelined kernel's
+    // 32-row tiles stream faster there) made it 5.3-5.5 against 4.2 ms; it
+    // can still be asked for up to B = 8.
+    const bool gv_ok = !bi && c->n_experts == 0 && !opt.no_weight_pack && opt.qkv_epilogue == 0 && so == 0 &&
+                       bo == 0 && c->hidden % 256 == 0 && c->head_dim % 16 == 0;
+    p.gv = opt.small_batch_layer == 1 ? gv_ok && B <= 8 : (opt.small_batch_layer == 0 && gv_ok && B == 1);
+    if (p.gv) {
+        for (Proj *pr : {&p.qkv, &p.o, &p.gu, &p.down}) {
+            pr->S = 1;
+            pr->Kc = (pr->K + 31) / 32 * 32;
+            pr->bm = 16;
+            pr->bn = 16;
+        }
+    }
     const int cap = kv_capacity(kv);
     // batch-invariant mode turns split-KV off: one split covers the capacity
     p.chunk = bi ? (cap + 63) / 64 * 64 : choose_chunk(B, c->n_kv_heads, cap, opt.attn_chunk);
@@ -258,6 +289,9 @@ struct corun_engine {
     // whose decode plan streams weights with the small-M pipelined kernel;
     // empty = that projection reads the row-major weight only
     std::vector<const uint16_t *> packed[W_COUNT];
+    // fragment-packed copies (per layer) for the small-batch layer (plan.gv):
+    // qkv in rotation pairs, o, gate/up in feature pairs, down
+    std::vector<const uint16_t *> gvw[4];
     char *pk_buf = nullptr;
     size_t pk_bytes = 0;
     bool gu_fused = false;   // the gate/up copy is interleaved for the fused SwiGLU epilogue
@@ -297,6 +331,7 @@ struct corun_engine {
     int32_t *d_tokens = nullptr, *d_seq = nullptr, *d_next = nullptr, *d_hist = nullptr, *d_counter = nullptr;
     int32_t *d_order = nullptr, *h_order = nullptr;   // attention's row dispatch order
     uint8_t *d_valid = nullptr;
+    float *gss = nullptr;   // plan.gv: sums of squares of 16-column groups of x, [B][hidden / 16]
     float *x = nullptr, *p_qkv = nullptr, *p_o = nullptr, *p_gu = nullptr, *p_down = nullptr, *attn_ws = nullptr,
           *logits = nullptr, *p_lm = nullptr;
     ArgBest *amax = nullptr;
@@ -410,6 +445,8 @@ static corun_status check_options(const corun_options &o)
     if (o.no_weight_pack != 0 && o.no_weight_pack != 1) return fail(CORUN_E_INVAL, "no_weight_pack must be 0 or 1");
     if (o.qkv_epilogue < 0 || o.qkv_epilogue > 2) return fail(CORUN_E_INVAL, "qkv_epilogue must be 0, 1 or 2");
     if (o.record_routing != 0 && o.record_routing != 1) return fail(CORUN_E_INVAL, "record_routing must be 0 or 1");
+    if (o.small_batch_layer < 0 || o.small_batch_layer > 2)
+        return fail(CORUN_E_INVAL, "small_batch_layer must be 0, 1 or 2");
     if (o.batch_invariant && (o.attn_chunk || o.split_k_override || o.gemm_bm))
         return fail(CORUN_E_INVAL, "batch_invariant fixes the plan: attn_chunk, split_k_override and gemm_bm must be 0");
     return CORUN_OK;
@@ -425,6 +462,8 @@ extern "C" int32_t corun_describe_plan(const corun_model_cfg *c, const corun_kv 
     s = check_options(o);
     if (s != CORUN_OK) return s;
     Plan p = make_plan(c, kv, B, o);
+    if (o.small_batch_layer == 1 && !p.gv) return fail(CORUN_E_INVAL, "small_batch_layer = 1 needs a dense model, "
+                                                       "B_fixed <= 8, weight packing and no plan overrides");
     std::vector<int32_t> v = {p.B, p.Mp};
     for (const Proj *pr : {&p.qkv, &p.o, &p.gu, &p.down, &p.lm}) {
         v.push_back(pr->N);
@@ -607,6 +646,55 @@ MoeFold fold_of(corun_engine *e, const MoeBufs &m, int l)
     return f;
 }
 
+// The small-batch layer's projections (plan.gv): which = 0 qkv (norm of x
+// with attn_norm, RoPE + KV append), 1 o (into the residual), 2 gate/up
+// (norm of x with mlp_norm, SwiGLU into a), 3 down (into the residual).
+hipError_t gemv_proj(corun_engine *e, int which, int l)
+{
+    const corun_model_cfg &c = e->c;
+    const Plan &p = e->plan;
+    const int B = e->B, H = c.hidden;
+    GemvIn in;
+    GemvOut out;
+    switch (which) {
+    case 0:
+        in.x = e->x;
+        in.ss = e->gss;
+        in.g = e->attn_norm[l];
+        in.eps = c.rms_eps;
+        out.q = e->q;
+        out.kc = e->kc[l];
+        out.vc = e->vc[l];
+        out.kv = e->view;
+        out.rope = e->rope;
+        out.valid = e->d_valid;
+        out.pos = e->d_seq;
+        out.nq = c.n_heads;
+        out.nkv = c.n_kv_heads;
+        out.d = c.head_dim;
+        return launch_gemv(e->gvw[0][l], B, p.qkv.N, H, GV_QKV, in, out, e->st);
+    case 1:
+        in.a = e->o;
+        in.lda = c.n_heads * c.head_dim;
+        out.x = e->x;
+        out.ss = e->gss;
+        return launch_gemv(e->gvw[1][l], B, H, p.o.K, GV_RESID, in, out, e->st);
+    case 2:
+        in.x = e->x;
+        in.ss = e->gss;
+        in.g = e->mlp_norm[l];
+        in.eps = c.rms_eps;
+        out.act = e->a;
+        return launch_gemv(e->gvw[2][l], B, p.gu.N, H, GV_SWIGLU, in, out, e->st);
+    default:
+        in.a = e->a;
+        in.lda = c.ffn;
+        out.x = e->x;
+        out.ss = e->gss;
+        return launch_gemv(e->gvw[3][l], B, H, p.down.K, GV_RESID, in, out, e->st);
+    }
+}
+
 // One kernel of layer l of the decode step; the step is these in order.
 corun_status launch_one(corun_engine *e, int which, int l)
 {
@@ -615,6 +703,20 @@ corun_status launch_one(corun_engine *e, int which, int l)
     const int B = e->B, H = c.hidden, d = c.head_dim, nq = c.n_heads, nkv = c.n_kv_heads, F = c.ffn;
     const int nqkv = (nq + 2 * nkv) * d;
     hipStream_t st = e->st;
+    if (p.gv) {   // the small-batch layer: four projections, attention and its merge
+        switch (which) {
+        case CORUN_K_QKV_GEMM: HIP_TRY(gemv_proj(e, 0, l)); return CORUN_OK;
+        case CORUN_K_O_GEMM: HIP_TRY(gemv_proj(e, 1, l)); return CORUN_OK;
+        case CORUN_K_GATE_UP_GEMM: HIP_TRY(gemv_proj(e, 2, l)); return CORUN_OK;
+        case CORUN_K_DOWN_GEMM: HIP_TRY(gemv_proj(e, 3, l)); return CORUN_OK;
+        case CORUN_K_QKV_POST:
+        case CORUN_K_SWIGLU: return CORUN_OK;
+        case CORUN_K_RMSNORM:   // the step's only norm, the final one
+            HIP_TRY(launch_rmsnorm(e->x, nullptr, 0, 0, B, H, e->final_norm, c.rms_eps, e->h, st));
+            return CORUN_OK;
+        default: break;
+        }
+    }
     switch (which) {
     case CORUN_K_QKV_GEMM: {
         HIP_TRY(proj(e, e->h, H, W_QKV, l, p.qkv, B, e->p_qkv, (long long)B * nqkv, nqkv));
@@ -695,6 +797,7 @@ corun_status launch_one(corun_engine *e, int which, int l)
 // and SwiGLU may run inside the neighbouring kernels instead).
 bool launches(const corun_engine *e, int k)
 {
+    if (e->plan.gv) return k != CORUN_K_QKV_POST && k != CORUN_K_SWIGLU && k != CORUN_K_RMSNORM;
     if (k == CORUN_K_QKV_POST) return !e->qkv_in_attn;
     if (k == CORUN_K_SWIGLU) return e->moe ? !e->egu_fused : !gu_fuses(e, e->plan.gu);
     return true;
@@ -722,17 +825,18 @@ corun_status enqueue_step(corun_engine *e)
     hipStream_t st = e->st;
     const int OTHER = CORUN_K_COUNT;   // embedding and feedback
     ST_TRY(timed(e, OTHER, [&]() -> corun_status {
-        HIP_TRY(launch_embed(e->embed, e->d_tokens, e->d_valid, B, H, e->x, st));
+        HIP_TRY(launch_embed(e->embed, e->d_tokens, e->d_valid, B, H, e->x, st, p.gv ? e->gss : nullptr));
         return CORUN_OK;
     }));
     const MoeBufs mb = decode_moe(e);
-    const int dense_S = e->moe ? 0 : p.down.S;
+    const int dense_S = e->moe || p.gv ? 0 : p.down.S;
     for (int l = 0; l < c.n_layers; ++l) {
-        ST_TRY(timed(e, CORUN_K_RMSNORM, [&]() -> corun_status {
-            HIP_TRY(launch_rmsnorm(e->x, l ? e->p_down : nullptr, l ? dense_S : 0, (long long)B * H, B, H,
-                                   e->attn_norm[l], c.rms_eps, e->h, st, fold_of(e, mb, l)));
-            return CORUN_OK;
-        }));
+        if (!p.gv)
+            ST_TRY(timed(e, CORUN_K_RMSNORM, [&]() -> corun_status {
+                HIP_TRY(launch_rmsnorm(e->x, l ? e->p_down : nullptr, l ? dense_S : 0, (long long)B * H, B, H,
+                                       e->attn_norm[l], c.rms_eps, e->h, st, fold_of(e, mb, l)));
+                return CORUN_OK;
+            }));
         for (int k : {CORUN_K_QKV_GEMM, CORUN_K_QKV_POST, CORUN_K_ATTN_SPLIT, CORUN_K_ATTN_MERGE, CORUN_K_O_GEMM,
                       CORUN_K_RMSNORM})
             if (launches(e, k)) ST_TRY(timed(e, k, [&] { return launch_one(e, k, l); }));
@@ -948,6 +1052,12 @@ static corun_status pack_weights(corun_engine *e)
     size_t total = (size_t)L * (egu_elems + edown_elems) * 2;   // each copy is a whole number of 16 KB tiles
     for (const Item &it : items)
         if (it.count && takes_packed(*it.pr)) total += (size_t)it.count * packed_weight_elems(it.pr->N, it.pr->K) * 2;
+    // the small-batch layer's fragment-packed copies (1 KB fragments)
+    const Proj *gvp[4] = {&p.qkv, &p.o, &p.gu, &p.down};
+    const int gv_mode[4] = {1, 0, 2, 0};
+    const int gv_w[4] = {W_QKV, W_O, W_GATE_UP, W_DOWN};
+    if (p.gv)
+        for (const Proj *pr : gvp) total += (size_t)L * frag_packed_elems(pr->N, pr->K) * 2;
     if (total == 0) return CORUN_OK;
     if (hipMalloc(&e->pk_buf, total) != hipSuccess)
         return fail(CORUN_E_HIP, "packed weight copies (%zu bytes) do not fit; no_weight_pack = 1 reads the row-major "
@@ -970,6 +1080,15 @@ static corun_status pack_weights(corun_engine *e)
         }
     }
     e->gu_fused = interleave;
+    for (int i = 0; p.gv && i < 4; ++i) {
+        const size_t bytes = frag_packed_elems(gvp[i]->N, gvp[i]->K) * 2;
+        for (int l = 0; l < L; ++l) {
+            HIP_TRY(launch_pack_frag(row_major_weight(e, gv_w[i], l), gvp[i]->N, gvp[i]->K, gv_mode[i],
+                                     e->c.head_dim, (uint16_t *)q, e->st));
+            e->gvw[i].push_back((const uint16_t *)q);
+            q += bytes;
+        }
+    }
     // expert stacks, expert by expert; gate/up interleaved when its halves
     // split into 64-row tiles
     const bool e_interleave = Fe % 64 == 0;
@@ -1043,11 +1162,16 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     e->view.page_table = kv->page_table;
     e->plan = make_plan(cfg, kv, B, o);
     const Plan &p = e->plan;
+    if (o.small_batch_layer == 1 && !p.gv) {
+        delete e;
+        return fail(CORUN_E_INVAL, "small_batch_layer = 1 needs a dense model, B_fixed <= 8, weight packing and no "
+                    "plan overrides");
+    }
     // Inside attention every block rebuilds its group's q from the split
     // partials: one launch fewer, which pays where launches dominate (B = 1:
     // about 3%) and costs where many blocks repeat the work (B = 256: the
     // attention kernel 187 -> 206 us against 7 us for the epilogue kernel).
-    e->qkv_in_attn = o.qkv_epilogue == 2 || (o.qkv_epilogue == 0 && B <= 8);
+    e->qkv_in_attn = !p.gv && (o.qkv_epilogue == 2 || (o.qkv_epilogue == 0 && B <= 8));
 
     auto bail = [&](corun_status s) {
         corun_engine_destroy(e);
@@ -1070,6 +1194,7 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     cv.take(&e->d_valid, B);
     cv.take(&e->d_order, B);
     cv.take(&e->x, (size_t)B * H);
+    cv.take(&e->gss, p.gv ? (size_t)B * (H / 16) : 1);
     cv.take(&e->p_qkv, proj_part_elems(p.qkv, B));
     cv.take(&e->p_o, proj_part_elems(p.o, B));
     cv.take(&e->p_gu, proj_part_elems(p.gu, B));
@@ -1108,6 +1233,7 @@ extern "C" corun_status corun_engine_create(const corun_model_cfg *cfg, const co
     if (hipMalloc(&e->ws, total) != hipSuccess) return bail(fail(CORUN_E_HIP, "workspace allocation of %zu bytes", total));
     rebase(e->d_tokens, e->ws); rebase(e->d_seq, e->ws); rebase(e->d_next, e->ws); rebase(e->d_counter, e->ws);
     rebase(e->d_hist, e->ws); rebase(e->d_valid, e->ws); rebase(e->d_order, e->ws); rebase(e->x, e->ws);
+    rebase(e->gss, e->ws);
     rebase(e->p_qkv, e->ws);
     rebase(e->p_o, e->ws); rebase(e->p_gu, e->ws); rebase(e->p_down, e->ws); rebase(e->attn_ws, e->ws);
     rebase(e->logits, e->ws); rebase(e->p_lm, e->ws); rebase(e->amax, e->ws); rebase(e->h, e->ws); rebase(e->q, e->ws); rebase(e->o, e->ws); rebase(e->a, e->ws);

@@ -25,9 +25,10 @@ struct LaunchRecorder {
 void set_launch_recorder(LaunchRecorder *r);
 
 // Per-row token selection and fp32 residual init: x[b] = float(E[tok_b]),
-// tok_b = valid[b] ? tokens[b] : 0.
+// tok_b = valid[b] ? tokens[b] : 0; with ss, also the sums of squares of x[b]
+// over 16-column groups, ss[b][H / 16] (launch_gemv's norm input).
 hipError_t launch_embed(const uint16_t *E, const int32_t *tokens, const uint8_t *valid, int rows,
-                        int H, float *x, hipStream_t st);
+                        int H, float *x, hipStream_t st, float *ss = nullptr);
 
 // Mixture-of-experts combine folded into the next RMSNorm:
 // x[b] += sum_{r < top_k} w[b][r] y[b top_k + r] (rank order) for valid rows.
@@ -223,6 +224,45 @@ size_t packed_weight_elems(int N, int K);
 hipError_t launch_pack_weights(const uint16_t *W, int N, int K, uint16_t *P, hipStream_t st, bool interleave = false);
 
 // prefill helpers: pos[t] = t for t < n
+// Fragment-packed copy of a row-major [N, K] weight for launch_gemv (layout
+// and row orders at k_pack_frag): mode 0 rows in order, 1 rotation pairs of
+// head_dim d (qkv), 2 gate/up feature pairs ([2F, K], gate rows first).
+// N % 16 == 0, K % 8 == 0; P holds frag_packed_elems(N, K) bf16.
+size_t frag_packed_elems(int N, int K);
+hipError_t launch_pack_frag(const uint16_t *W, int N, int K, int mode, int d, uint16_t *P, hipStream_t st);
+
+enum { GV_RESID = 0, GV_QKV = 1, GV_SWIGLU = 2 };
+// A operand of launch_gemv: bf16 activations a [M][lda], or (a == nullptr)
+// the RMSNorm of the fp32 residual x [M][K] with gain g and eps, its 1 / rms
+// from ss [M][K / 16], the sums of squares of 16-column groups of x.
+struct GemvIn {
+    const uint16_t *a = nullptr;
+    int lda = 0;
+    const float *x = nullptr;
+    const float *ss = nullptr;
+    const uint16_t *g = nullptr;
+    float eps = 0.f;
+};
+// Outputs per epilogue: GV_RESID x [M][N] (added into) and ss [M][N / 16];
+// GV_SWIGLU act [M][N / 2]; GV_QKV q [M][nq d] and the cache (row = slot,
+// position pos[row], rows with valid[row] == 0 skipped), rotation table rope.
+struct GemvOut {
+    float *x = nullptr;
+    float *ss = nullptr;
+    uint16_t *act = nullptr;
+    uint16_t *q = nullptr, *kc = nullptr, *vc = nullptr;
+    KvView kv{};
+    const float2 *rope = nullptr;
+    const uint8_t *valid = nullptr;
+    const int32_t *pos = nullptr;
+    int nq = 0, nkv = 0, d = 0;
+};
+// y = A W^T over M <= 16 rows from the fragment-packed W, one workgroup per
+// 16 output columns; supported: (GV_RESID, activations), (GV_QKV, norm),
+// (GV_SWIGLU, norm).
+hipError_t launch_gemv(const uint16_t *Wp, int M, int N, int K, int epi, const GemvIn &in, const GemvOut &out,
+                       hipStream_t st);
+
 hipError_t launch_iota(int32_t *p, int n, hipStream_t st);
 
 }  // namespace corun

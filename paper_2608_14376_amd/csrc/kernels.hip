@@ -89,14 +89,6 @@ __device__ __forceinline__ uint16_t swiglu_bf16(float gs, float us)
     return f2bf(silu * u);
 }
 
-// Fixed butterfly over the 64 lanes, then lane 0's value to every lane.
-__device__ __forceinline__ float wave_sum(float v)
-{
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-    return __shfl(v, 0, 64);
-}
-
 __device__ __forceinline__ float wave_max(float v)
 {
 #pragma unroll
@@ -141,26 +133,69 @@ __device__ __forceinline__ void better(float &v, int &i, float v2, int i2)
 }
 
 // ---------------------------------------------------------------------------
+// Fixed reduction trees on the cross-lane hardware.
+//
+// dpp_f<CTRL>: lane i takes the value of the lane CTRL selects (a DPP move).
+// row16_sum: the sum over the 16 lanes of a DPP row -- pairs i ^ 1, then
+// i ^ 2 (quad permutes), then i and 7 - i within eight lanes (half-row
+// mirror), then i and 15 - i (row mirror).  wave_sum_dpp: row16_sum, then
+// the two rows of each 32-lane half (ds_swizzle, i ^ 16), then lane 0 plus
+// lane 32.  At every stage a lane and its partner add the same two values
+// (addition commutes), so every lane ends with the same bits.
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float row16_sum(float v)
+{
+    v += dpp_f<0xB1>(v);    // quad_perm [1, 0, 3, 2]: lane i ^ 1
+    v += dpp_f<0x4E>(v);    // quad_perm [2, 3, 0, 1]: lane i ^ 2
+    v += dpp_f<0x141>(v);   // row_half_mirror: lane 7 - i of its eight
+    v += dpp_f<0x140>(v);   // row_mirror: lane 15 - i of its sixteen
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum_dpp(float v)
+{
+    v = row16_sum(v);
+    // bit-mask swizzle within 32 lanes: and 0x1f, or 0, xor 0x10
+    v += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
+    const float lo = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+    const float hi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+    return lo + hi;
+}
+
+// ---------------------------------------------------------------------------
 // Embedding gather
 // ---------------------------------------------------------------------------
 // Grid: rows x ceil(H / 256) blocks, flattened into x (rows may exceed the
-// 65535 limit of the other grid dimensions in a long prefill).
+// 65535 limit of the other grid dimensions in a long prefill).  With ss
+// (H a multiple of 256) it also writes each row's sums of squares over
+// 16-column groups, ss[b][i / 16], for the small-batch projections' norm.
 __global__ void k_embed(const uint16_t *__restrict__ E, const int32_t *__restrict__ tokens,
-                        const uint8_t *__restrict__ valid, int H, float *__restrict__ x)
+                        const uint8_t *__restrict__ valid, int H, float *__restrict__ x, float *__restrict__ ss)
 {
     const int nb = (H + 255) / 256;
     const int b = blockIdx.x / nb;
     const int i = (blockIdx.x % nb) * 256 + threadIdx.x;
-    if (i >= H) return;
     const int tok = (valid == nullptr || valid[b]) ? tokens[b] : 0;
-    x[(size_t)b * H + i] = bf2f(E[(size_t)tok * H + i]);
+    const float v = i < H ? bf2f(E[(size_t)tok * H + i]) : 0.f;
+    if (i < H) x[(size_t)b * H + i] = v;
+    if (ss != nullptr) {
+        const float sq = row16_sum(v * v);            // lanes 16 k .. 16 k + 15: one 16-column group
+        if ((threadIdx.x & 15) == 0 && i < H) ss[(size_t)b * (H / 16) + i / 16] = sq;
+    }
 }
 
 hipError_t launch_embed(const uint16_t *E, const int32_t *tokens, const uint8_t *valid, int rows, int H,
-                        float *x, hipStream_t st)
+                        float *x, hipStream_t st, float *ss)
 {
+    if (ss != nullptr && H % 256 != 0) return hipErrorInvalidValue;
     const long long blocks = (long long)rows * ((H + 255) / 256);
-    KLAUNCH(k_embed, dim3((unsigned)blocks), dim3(256), 0, st, E, tokens, valid, H, x);
+    KLAUNCH(k_embed, dim3((unsigned)blocks), dim3(256), 0, st, E, tokens, valid, H, x, ss);
     return hipGetLastError();
 }
 
@@ -169,14 +204,18 @@ hipError_t launch_embed(const uint16_t *E, const int32_t *tokens, const uint8_t 
 // folded in.  One workgroup of min(H/4, 1024) threads per row; thread j owns
 // the float4 groups 4 (j + nth i), kept in registers (H <= 8192).  Each
 // element adds its partials in split order; the sum of squares runs
-// sequentially per thread, then through a fixed tree: the 64-lane butterfly,
-// then the wavefront sums in wavefront order.
+// sequentially per thread, then through a fixed tree: each wavefront's DPP /
+// ds_swizzle tree (wave_sum_dpp), then the wavefront sums in wavefront order.
+// A row spans up to 16 wavefronts because the fold reads the split-K
+// partials too ((S + 2) x 16 KB per row of 4096): one wavefront per row,
+// built and measured, took 16.3 against 6.2 us at B = 256 (64 workgroups of
+// four single-row wavefronts), too few loads in flight per row.
 // ---------------------------------------------------------------------------
-// Fixed-order sum over a block of nw wavefronts: the 64-lane butterfly,
+// Fixed-order sum over a block of nw wavefronts: each wavefront's DPP tree,
 // then the wavefront sums added in wavefront order.
 __device__ __forceinline__ float block_sum(float v, float *red, int nw)
 {
-    v = wave_sum(v);
+    v = wave_sum_dpp(v);
     const int w = threadIdx.x >> 6;
     if ((threadIdx.x & 63) == 0) red[w] = v;
     __syncthreads();
@@ -1922,6 +1961,292 @@ hipError_t launch_pack_weights(const uint16_t *W, int N, int K, uint16_t *P, hip
     if (blocks > 65536) blocks = 65536;
     KLAUNCH(k_pack_weights, dim3((unsigned)blocks), dim3(256), 0, st, W, N, K, P, units,
                        interleave ? N / 2 : 0);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Small-batch projections (M <= 16 rows) from a fragment-packed weight copy.
+//
+// Fragment-packed layout (launch_pack_frag): [N / 16][ceil(K / 32)][64][8]
+// bf16, where lane l of (column tile t, K block b) holds the eight weights
+// W[row(t, l % 16)][32 b + 8 (l / 16) .. +7] -- exactly the B operand of
+// v_mfma_f32_16x16x32_bf16 for 16 output columns and 32 K elements, K past
+// the weight's width zero.  One wavefront load then reads 1 KB of contiguous
+// memory (eight whole 128-byte lines) straight into the fragment registers:
+// no LDS staging and no 16-rows-of-64-bytes access, which caps a stream
+// near 4.7 TB/s.  row(t, r) is the identity (16 t + r), or pairs columns so
+// that an epilogue finds both halves of an operation in lanes r and r ^ 8:
+//  * rotation pairs (qkv): tile t = (head t / (d / 16), a = t % (d / 16))
+//    holds head elements 8 a .. 8 a + 7 in rows 0..7 and d / 2 + 8 a .. +7
+//    in rows 8..15;
+//  * gate/up ([2F, K], gate rows first): rows 0..7 of tile t are gate
+//    features 8 t .. 8 t + 7, rows 8..15 the up rows of the same features.
+// ---------------------------------------------------------------------------
+__global__ void k_pack_frag(const uint16_t *__restrict__ W, int N, int K, int mode, int d,
+                            uint4 *__restrict__ P, long long units)
+{
+    const int nkb = (K + 31) / 32;
+    for (long long u = (long long)blockIdx.x * blockDim.x + threadIdx.x; u < units;
+         u += (long long)gridDim.x * blockDim.x) {
+        const int l = (int)(u & 63), r = l & 15, c = l >> 4;
+        const long long tb = u >> 6, t = tb / nkb;
+        const int kb = (int)(tb % nkb);
+        long long row;
+        if (mode == 1) {
+            const int per = d / 16;
+            const long long hd = t / per;
+            const int a = (int)(t % per);
+            row = hd * d + (r < 8 ? 8 * a + r : d / 2 + 8 * a + (r - 8));
+        } else if (mode == 2) {
+            row = r < 8 ? 8 * t + r : N / 2 + 8 * t + (r - 8);
+        } else {
+            row = 16 * t + r;
+        }
+        const int k0 = 32 * kb + 8 * c;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (k0 < K) v = *reinterpret_cast<const uint4 *>(W + row * K + k0);
+        P[u] = v;
+    }
+}
+
+size_t frag_packed_elems(int N, int K) { return (size_t)N * ((K + 31) / 32 * 32); }
+
+hipError_t launch_pack_frag(const uint16_t *W, int N, int K, int mode, int d, uint16_t *P, hipStream_t st)
+{
+    if (N <= 0 || K <= 0 || N % 16 != 0 || K % 8 != 0) return hipErrorInvalidValue;
+    if (mode == 1 && (d % 16 != 0 || N % d != 0)) return hipErrorInvalidValue;
+    const long long units = (long long)frag_packed_elems(N, K) / 8;
+    long long blocks = (units + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    KLAUNCH(k_pack_frag, dim3((unsigned)blocks), dim3(256), 0, st, W, N, K, mode, d,
+            reinterpret_cast<uint4 *>(P), units);
+    return hipGetLastError();
+}
+
+// The projection.  Workgroup = one 16-column tile over the whole of K: four
+// wavefronts take four contiguous quarters of the K blocks and their 16 x 16
+// fp32 tiles are added in wavefront order (0 + 1 + 2 + 3); every output
+// element is that one fixed chain whatever its row.  Each wavefront streams
+// its weights U blocks at a time, double-buffered: batch i + 1's loads are
+// issued before batch i's products (and after batch i's activation loads,
+// so that waiting on those never drains the weight stream).  A rows >= M
+// are zero fragments and are never stored.
+//
+// The A operand is bf16 activations from memory, or (NORM) the RMSNorm of
+// the fp32 residual: the rows' 1 / rms from the per-16-column sums of
+// squares their producer wrote (each wavefront adds a row's sums lane by
+// lane, then the DPP tree), then bf16(x * rstd * g) per element, the norm
+// kernel's rounding, written once into LDS in fragment order while the first
+// weights are in flight (2 K M bytes: unit (4 kb + c) M + m holds row m's
+// elements 32 kb + 8 c .. +7).
+// Epilogues (wavefront 0; lane l holds column l % 16, rows 4 (l / 16) + i):
+//  GV_RESID:  x[row][col] += y (each element owned by one thread, no
+//             partials), and the sum of squares of the tile's 16 new
+//             values of each row (row16_sum) to ss[row][tile] for the next
+//             norm;
+//  GV_QKV:    bf16 rounding, rotation at the row's position, bf16 rounding
+//             (the split-partials epilogue's arithmetic on one sum), q to
+//             the q buffer, k and v appended to the row's cache slot;
+//             padding rows write nothing;
+//  GV_SWIGLU: act[row][feature] = SwiGLU of the gate and up sums.
+// ---------------------------------------------------------------------------
+template <int U, int EPI, bool NORM>
+__global__ __launch_bounds__(256) void k_gemv(const uint4 *__restrict__ Wp, int M, int N, int K, GemvIn in,
+                                              GemvOut out)
+{
+    extern __shared__ __attribute__((aligned(16))) uint4 hs[];
+    __shared__ f32x4 red[3][64];
+    __shared__ float rs[16];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int t = blockIdx.x;
+    const int nkb = (K + 31) / 32;
+    const int kb0 = wave * nkb / 4, kb1 = (wave + 1) * nkb / 4;
+    const int r = lane & 15, c = lane >> 4;
+    const bool arow = r < M;
+    const uint4 *wp = Wp + (size_t)t * nkb * 64 + lane;
+    const uint4 z = {0u, 0u, 0u, 0u};
+    // Every load of the main loop is unconditional (clamped addresses,
+    // selects instead of branches), so the wait before a batch's products
+    // counts exactly the loads issued after it and leaves them in flight.
+    // Blocks past the wavefront's last are clamped re-reads of it, never
+    // multiplied.
+    auto wload = [&](uint4 (&w)[U], int kb) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) w[u] = wp[(size_t)min(kb + u, kb1 - 1) * 64];
+    };
+    const int rr = min(r, M - 1);
+    auto aload = [&](uint4 (&a)[U], int kb) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int k = min(kb + u, kb1 - 1);
+            uint4 v;
+            if constexpr (NORM) {
+                v = hs[(4 * k + c) * M + rr];
+                a[u] = arow ? v : z;
+            } else {
+                const int k0 = 32 * k + 8 * c;
+                v = *reinterpret_cast<const uint4 *>(in.a + (size_t)rr * in.lda + min(k0, K - 8));
+                a[u] = (arow && k0 < K) ? v : z;
+            }
+        }
+    };
+    uint4 wa[U], wb[U], aa[U], ab[U];
+    wload(wa, kb0);                                  // two batches of weights go out before anything else
+    if constexpr (!NORM) aload(aa, kb0);
+    wload(wb, kb0 + U);
+    if constexpr (!NORM) aload(ab, kb0 + U);
+    if constexpr (NORM) {
+        for (int m = wave; m < M; m += 4) {
+            const float *sr = in.ss + (size_t)m * (K / 16);
+            float a = 0.f;
+            for (int j = lane; 4 * j < K / 16; j += 64) {
+                const float4 v = *reinterpret_cast<const float4 *>(sr + 4 * j);
+                a += v.x;
+                a += v.y;
+                a += v.z;
+                a += v.w;
+            }
+            a = wave_sum_dpp(a);
+            if (lane == 0) rs[m] = 1.0f / sqrtf(a / (float)K + in.eps);
+        }
+        __syncthreads();
+        const int units = (K / 8) * M;
+        for (int u = threadIdx.x; u < units; u += 256) {
+            const int m = u % M, k0 = 8 * (u / M);
+            const float rstd = rs[m];
+            const float *xr = in.x + (size_t)m * K + k0;
+            const float4 x0 = *reinterpret_cast<const float4 *>(xr);
+            const float4 x1 = *reinterpret_cast<const float4 *>(xr + 4);
+            const uint4 gg = *reinterpret_cast<const uint4 *>(in.g + k0);
+            uint4 h;
+            h.x = (uint32_t)f2bf(x0.x * rstd * bf2f((uint16_t)gg.x)) |
+                  ((uint32_t)f2bf(x0.y * rstd * bf2f((uint16_t)(gg.x >> 16))) << 16);
+            h.y = (uint32_t)f2bf(x0.z * rstd * bf2f((uint16_t)gg.y)) |
+                  ((uint32_t)f2bf(x0.w * rstd * bf2f((uint16_t)(gg.y >> 16))) << 16);
+            h.z = (uint32_t)f2bf(x1.x * rstd * bf2f((uint16_t)gg.z)) |
+                  ((uint32_t)f2bf(x1.y * rstd * bf2f((uint16_t)(gg.z >> 16))) << 16);
+            h.w = (uint32_t)f2bf(x1.z * rstd * bf2f((uint16_t)gg.w)) |
+                  ((uint32_t)f2bf(x1.w * rstd * bf2f((uint16_t)(gg.w >> 16))) << 16);
+            hs[u] = h;
+        }
+        __syncthreads();
+        aload(aa, kb0);
+        aload(ab, kb0 + U);
+    }
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    auto mma = [&](const uint4 (&a)[U], const uint4 (&w)[U], int kb) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (kb + u < kb1)
+                acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[u]),
+                                                              __builtin_bit_cast(bf16x8, w[u]), acc, 0, 0, 0);
+    };
+    for (int kb = kb0; kb < kb1; kb += 2 * U) {
+        mma(aa, wa, kb);
+        wload(wa, kb + 2 * U);
+        aload(aa, kb + 2 * U);
+        mma(ab, wb, kb + U);
+        wload(wb, kb + 3 * U);
+        aload(ab, kb + 3 * U);
+    }
+    if (wave > 0) red[wave - 1][lane] = acc;
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int w2 = 0; w2 < 3; ++w2) {
+        const f32x4 o = red[w2][lane];
+        acc[0] += o[0];
+        acc[1] += o[1];
+        acc[2] += o[2];
+        acc[3] += o[3];
+    }
+    if constexpr (EPI == GV_RESID) {
+        const int col = 16 * t + r;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = 4 * c + i;
+            float xn = 0.f;
+            if (row < M) {
+                float *xp = out.x + (size_t)row * N + col;
+                xn = *xp + acc[i];
+                *xp = xn;
+            }
+            const float sq = row16_sum(xn * xn);      // the tile's 16 columns of this row
+            if (row < M && r == 0) out.ss[(size_t)row * (N / 16) + t] = sq;
+        }
+    } else if constexpr (EPI == GV_SWIGLU) {
+        const int F = N / 2;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float up = __shfl_xor(acc[i], 8, 64);
+            const int row = 4 * c + i;
+            if (r < 8 && row < M) out.act[(size_t)row * F + 8 * t + r] = swiglu_bf16(acc[i], up);
+        }
+    } else {   // GV_QKV
+        const int d = out.d, half = d / 2, per = d / 16;
+        const int hd = t / per, e0 = 8 * (t % per) + r;
+        const int nq = out.nq, nkv = out.nkv;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float other = __shfl_xor(acc[i], 8, 64);
+            const int row = 4 * c + i;
+            if (r >= 8 || row >= M || (out.valid != nullptr && !out.valid[row])) continue;
+            const int p = out.pos[row];
+            float x0 = bf2f(f2bf(acc[i]));
+            float x1 = bf2f(f2bf(other));
+            if (hd < nq + nkv) {
+                const float2 cs = out.rope[(size_t)p * half + e0];
+                const float y0 = __builtin_fmaf(x0, cs.x, -(x1 * cs.y));
+                const float y1 = __builtin_fmaf(x1, cs.x, x0 * cs.y);
+                x0 = y0;
+                x1 = y1;
+            }
+            const uint16_t b0 = f2bf(x0), b1 = f2bf(x1);
+            if (hd < nq) {
+                uint16_t *qr = out.q + (size_t)row * nq * d + (size_t)hd * d;
+                qr[e0] = b0;
+                qr[e0 + half] = b1;
+            } else if (hd < nq + nkv) {
+                uint16_t *dst = out.kc + kv_offset(out.kv, nkv, d, row, hd - nq, p);
+                dst[e0] = b0;
+                dst[e0 + half] = b1;
+            } else {
+                const int kvh = hd - nq - nkv;
+                out.vc[v_offset(out.kv, nkv, d, row, kvh, p, e0)] = b0;
+                out.vc[v_offset(out.kv, nkv, d, row, kvh, p, e0 + half)] = b1;
+            }
+        }
+    }
+}
+
+hipError_t launch_gemv(const uint16_t *Wp, int M, int N, int K, int epi, const GemvIn &in, const GemvOut &out,
+                       hipStream_t st)
+{
+    // every wavefront gets at least one of the ceil(K / 32) K blocks
+    if (M <= 0 || M > 16 || N % 16 != 0 || K % 16 != 0 || K < 128) return hipErrorInvalidValue;
+    const bool norm = in.a == nullptr;
+    // the normed rows live in LDS (2 K M bytes); the sums of squares come in groups of 16 x 4
+    if (norm && (K % 64 != 0 || (size_t)2 * K * M > 128 * 1024)) return hipErrorInvalidValue;
+    if (epi == GV_QKV && (out.d % 16 != 0 || N % out.d != 0)) return hipErrorInvalidValue;
+    const dim3 grid(N / 16), block(256);
+    const uint4 *W = reinterpret_cast<const uint4 *>(Wp);
+    const unsigned lds = norm ? (unsigned)(2 * K * M) : 0u;
+    if (norm) {   // the normed rows may exceed the default 64 KB of dynamic LDS (a host-side attribute, per device)
+        hipError_t e = hipFuncSetAttribute((const void *)k_gemv<8, GV_QKV, true>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 128 * 1024);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void *)k_gemv<8, GV_SWIGLU, true>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, 128 * 1024);
+        if (e != hipSuccess) return e;
+    }
+    if (epi == GV_RESID && !norm)
+        KLAUNCH((k_gemv<8, GV_RESID, false>), grid, block, 0, st, W, M, N, K, in, out);
+    else if (epi == GV_QKV && norm)
+        KLAUNCH((k_gemv<8, GV_QKV, true>), grid, block, lds, st, W, M, N, K, in, out);
+    else if (epi == GV_SWIGLU && norm)
+        KLAUNCH((k_gemv<8, GV_SWIGLU, true>), grid, block, lds, st, W, M, N, K, in, out);
+    else
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 

@@ -107,9 +107,48 @@ def test_plan_is_a_function_of_shape_only():
         assert p["lm_head"]["split_k"] == 1
         assert p["attn_chunk"] % 64 == 0 and p["attn_max_splits"] * p["attn_chunk"] >= 4224
     assert plans[1] == corun.describe_plan(c, _kv(n_slots=256, max_seq_len=4224), 1)
-    assert plans[1]["qkv"]["split_k"] >= plans[256]["qkv"]["split_k"]
+    assert plans[16]["qkv"]["split_k"] >= plans[256]["qkv"]["split_k"]
     forced = corun.describe_plan(c, _kv(n_slots=256, max_seq_len=4224), 16, corun.options(split_k_override=3))
     assert forced["qkv"]["split_k"] == 3 and forced["down"]["split_k"] == 3
+
+
+def _small_batch_layer(p):
+    return all((p[n]["m_tile"], p[n]["n_tile"], p[n]["split_k"]) == (16, 16, 1)
+               for n in ("qkv", "o", "gate_up", "down"))
+
+
+def test_small_batch_layer_plan():
+    """Dense models at B = 1 run the small-batch layer by default, up to B =
+    8 when asked (small_batch_layer = 1): every projection on 16-column
+    fragment-packed tiles over the whole of K (no split-K), K padded to 32 in
+    the description; the lm_head keeps the pipelined kernel.  It needs the
+    packed copies and the default epilogue placement; batch-invariant mode
+    and mixture-of-experts models never take it, and small_batch_layer = 2
+    turns it off."""
+    kv = _kv(n_slots=256, max_seq_len=4224)
+    for name in ("8b", "tiny", "small128", "32b"):
+        c = wl.config(name)
+        p = corun.describe_plan(c, kv, 1)
+        assert _small_batch_layer(p), name
+        for n in ("qkv", "o", "gate_up", "down"):
+            assert p[n]["k_chunk"] == (p[n]["K"] + 31) // 32 * 32
+        assert p["lm_head"]["n_tile"] != 16
+        assert not _small_batch_layer(corun.describe_plan(c, kv, 1, corun.options(small_batch_layer=2)))
+        for B in (2, 8, 16, 64):
+            assert not _small_batch_layer(corun.describe_plan(c, kv, B)), (name, B)
+        for B in (2, 5, 8):
+            assert _small_batch_layer(corun.describe_plan(c, kv, B, corun.options(small_batch_layer=1))), (name, B)
+        for opt in (corun.options(no_weight_pack=True), corun.options(qkv_epilogue=1),
+                    corun.options(qkv_epilogue=2), corun.options(batch_invariant=True),
+                    corun.options(split_k_override=2)):
+            assert not _small_batch_layer(corun.describe_plan(c, kv, 1, opt)), name
+        for B, kw in ((9, {}), (1, dict(no_weight_pack=True)), (1, dict(batch_invariant=True))):
+            with pytest.raises(corun.CorunError):
+                corun.describe_plan(c, kv, B, corun.options(small_batch_layer=1, **kw))
+    for name in ("tiny_moe", "moe"):
+        assert not _small_batch_layer(corun.describe_plan(wl.config(name), kv, 1)), name
+    with pytest.raises(corun.CorunError):
+        corun.describe_plan(wl.config("tiny"), kv, 1, corun.options(small_batch_layer=3))
 
 
 def test_batch_invariant_plan_ignores_the_batch_size():

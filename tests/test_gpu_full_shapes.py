@@ -48,10 +48,10 @@ def test_decode_B256_full_shapes(full):
     K, V = wl.make_kv_contiguous(cfg, B, CAP, seed=42, device=DEV)
     eng = corun.Engine(cfg, Wg, B, K, V)
     plan = eng.plan()
-    # the benchmark's configurations: 256 x 256 tiles for gate/up and the
-    # lm_head (with its argmax epilogue), 128 x 128 (two M tiles) elsewhere
+    # the benchmark's configurations: 256 x 256 tiles for gate/up, 256 x 128
+    # for the lm_head (with its argmax epilogue), 128 x 128 (two M tiles) elsewhere
     assert (plan["gate_up"]["m_tile"], plan["gate_up"]["n_tile"]) == (256, 256)
-    assert (plan["lm_head"]["m_tile"], plan["lm_head"]["n_tile"], plan["lm_head"]["split_k"]) == (256, 256, 1)
+    assert (plan["lm_head"]["m_tile"], plan["lm_head"]["n_tile"], plan["lm_head"]["split_k"]) == (256, 128, 1)
     for name in ("qkv", "o", "down"):
         assert (plan[name]["m_tile"], plan[name]["n_tile"]) == (128, 128), name
     b = wl.make_batch(B, cfg["vocab"], seed=43, len_lo=512, len_hi=4096)
@@ -84,10 +84,13 @@ def test_decode_B256_full_shapes(full):
 
 
 # The small-B plans the decode benchmark times (8B shapes, capacity 4144):
-# packed 32- or 64-row weight tiles with split-K 5 (qkv) and 8 (o, down),
-# gate/up without split-K (its epilogue applies SwiGLU), and the attention
-# chunk that gives up to 33 splits at B <= 8 (where attention also applies
-# the QKV epilogue), 17 at B = 16, 5 at B = 64.
+# at B = 1 the small-batch layer (every layer projection on 16-column
+# fragment-packed tiles over the whole of K, norm / RoPE + KV append /
+# SwiGLU / residual in the projections); at B = 8, 16 and 64 packed 32- or
+# 64-row weight tiles with split-K 5 (qkv) and 8 (o, down), gate/up without
+# split-K (its epilogue applies SwiGLU; at B = 8 attention applies the QKV
+# epilogue); the lm_head on the packed 32- or 64-row tiles; the attention
+# chunk that gives up to 33 splits at B <= 8, 17 at B = 16, 5 at B = 64.
 SMALL_B = {1: (32, 128, 33), 8: (32, 128, 33), 16: (32, 256, 17), 64: (64, 1024, 5)}
 
 
@@ -98,8 +101,13 @@ def test_decode_small_B_full_shapes(full, Bs):
     eng = corun.Engine(cfg, Wg, Bs, K, V)
     plan = eng.plan()
     mt, chunk, splits = SMALL_B[Bs]
-    for name, S in (("qkv", 5), ("o", 8), ("gate_up", 1), ("down", 8), ("lm_head", 1)):
-        assert (plan[name]["split_k"], plan[name]["m_tile"], plan[name]["n_tile"]) == (S, mt, 128), (name, plan[name])
+    if Bs == 1:
+        for name in ("qkv", "o", "gate_up", "down"):
+            assert (plan[name]["split_k"], plan[name]["m_tile"], plan[name]["n_tile"]) == (1, 16, 16), name
+    else:
+        for name, S in (("qkv", 5), ("o", 8), ("gate_up", 1), ("down", 8)):
+            assert (plan[name]["split_k"], plan[name]["m_tile"], plan[name]["n_tile"]) == (S, mt, 128), name
+    assert (plan["lm_head"]["split_k"], plan["lm_head"]["m_tile"], plan["lm_head"]["n_tile"]) == (1, mt, 128)
     assert (plan["attn_chunk"], plan["attn_max_splits"]) == (chunk, splits)
     b = wl.make_batch(Bs, cfg["vocab"], seed=70 + Bs, len_lo=512, len_hi=4096)
     live = np.nonzero(b.valid)[0]

@@ -5,7 +5,9 @@ elements in the same order, so everything must be bit-identical to an engine
 that reads the caller's row-major weights:
 
 * decode logits, greedy tokens and appended k/v over two steps at B = 1, 24
-  and 48 (32- and 64-row tiles; split-K on the narrow projections);
+  and 48 (32- and 64-row tiles; split-K on the narrow projections; at B = 1
+  with the small-batch layer off, which would otherwise stream copies of
+  its own: tests/test_gpu_small_batch_layer.py);
 * prefill of a 40-token prompt (its projections take the packed copies) and
   a 100-token prompt (they do not; the last-row lm_head does);
 * the packed copies exist: creating the engine takes the memory they need
@@ -37,7 +39,8 @@ def engine(cfg, Wg, B, pack):
     K, V = wl.make_kv_contiguous(cfg, B, CAP, seed=610)
     K = [k.to(DEV) for k in K]
     V = [v.to(DEV) for v in V]
-    eng = corun.Engine(cfg, Wg, B, K, V, opt=corun.options(max_prefill_len=128, no_weight_pack=not pack))
+    eng = corun.Engine(cfg, Wg, B, K, V, opt=corun.options(max_prefill_len=128, no_weight_pack=not pack,
+                                                           small_batch_layer=2))
     return eng, K, V
 
 
@@ -88,7 +91,7 @@ def test_packed_prefill_is_bit_identical(model, Lp):
 
 
 def packed_bytes(cfg):
-    """What the B = 1 plan packs: every projection with K % 64 == 0."""
+    """What the B = 1 split-K plan packs: every projection with K % 64 == 0."""
     H, d = cfg["hidden"], cfg["head_dim"]
     nqkv = (cfg["n_heads"] + 2 * cfg["n_kv_heads"]) * d
     shapes = [(nqkv, H), (H, cfg["n_heads"] * d)]
@@ -112,7 +115,7 @@ def test_packed_copies_are_made():
     for pack in (False, True):
         torch.cuda.synchronize()
         free0 = torch.cuda.mem_get_info()[0]
-        eng = corun.Engine(cfg, Wg, 1, K, V, opt=corun.options(no_weight_pack=not pack))
+        eng = corun.Engine(cfg, Wg, 1, K, V, opt=corun.options(no_weight_pack=not pack, small_batch_layer=2))
         torch.cuda.synchronize()
         used.append(free0 - torch.cuda.mem_get_info()[0])
         eng.close()

@@ -1,0 +1,221 @@
+"""The small-batch layer (corun_options.small_batch_layer; automatic for
+dense models at B = 1): every layer projection streams a fragment-packed
+weight copy over the whole of K with no split-K; the O and down projections
+add into the fp32 residual and write per-16-column sums of squares, the QKV
+and gate/up projections normalise their input from those on the fly, RoPE +
+KV append and SwiGLU run in their epilogues, and a layer launches no
+RMSNorm.
+
+* against the oracle over three teacher-forced steps at B = 1 (automatic)
+  and B = 3, 8 (asked for) on small128 (head_dim 128) and tiny (head_dim 64,
+  down K = 688: a K tail past the last 32-wide block), with the appended k
+  and v of every live row;
+* against the split-K plan of the same engine shape (small_batch_layer = 2):
+  within the oracle tolerance, not bitwise -- the K reduction is split
+  across four wavefronts instead of across workgroups;
+* position invariance at B = 8: three requests moved to other slots beside
+  other co-runners give bit-identical logits, tokens and cache rows;
+* paged and contiguous caches give bit-identical results (the epilogue's
+  paged append), at B = 1 and 8;
+* what the option refuses."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_14376_amd import corun
+from paper_2608_14376_amd import workload as wl
+from tests.gpu_helpers import DEV, check_tokens, host_model, oracle_kv, row_rel_err, to_device
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-2
+CAP = 192
+
+
+@pytest.fixture(scope="module", params=["small128", "tiny"])
+def model(request):
+    cfg = wl.config(request.param)
+    Wc = wl.make_weights(cfg, seed=71)
+    return cfg, to_device(Wc), host_model(Wc)
+
+
+def cache(cfg, B, seed):
+    K, V = wl.make_kv_contiguous(cfg, B, CAP, seed=seed)
+    return [k.to(DEV) for k in K], [v.to(DEV) for v in V]
+
+
+def layer_opt(B, **kw):
+    """The small-batch layer: automatic at B = 1, asked for above."""
+    return corun.options(small_batch_layer=0 if B == 1 else 1, **kw)
+
+
+def is_small_batch_layer(plan):
+    return all((plan[n]["m_tile"], plan[n]["n_tile"], plan[n]["split_k"]) == (16, 16, 1)
+               for n in ("qkv", "o", "gate_up", "down"))
+
+
+@pytest.mark.parametrize("B", [1, 3, 8])
+def test_parity_with_oracle(model, B):
+    cfg, Wg, m = model
+    K, V = cache(cfg, B, seed=700 + B)
+    okv = oracle_kv(K, V)
+    eng = corun.Engine(cfg, Wg, B, K, V, opt=layer_opt(B))
+    assert is_small_batch_layer(eng.plan())
+    b = wl.make_batch(B, cfg["vocab"], seed=710 + B, len_lo=16, len_hi=CAP - 8)
+    tokens, valid, lens = b.tokens.copy(), b.valid.copy(), b.seq_lens.copy()
+    logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+    near, worst = [], 0.0
+    for step in range(3):
+        nxt = eng.decode_step(tokens, valid, lens, logits)
+        ref, _ = oracle.decode_batch(m, okv, tokens, valid, lens)
+        gl = logits.cpu().numpy()
+        for r in range(B):
+            if valid[r]:
+                e = row_rel_err(gl[r], ref[r])
+                worst = max(worst, e)
+                assert e <= TOL, (step, r, e)
+        check_tokens(nxt, ref, gl, valid, near)
+        # the appended k and v of every live row, every layer
+        for l in range(cfg["n_layers"]):
+            gk, gv = wl.bits(K[l]), wl.bits(V[l])
+            for r in np.nonzero(valid)[0]:
+                p = lens[r]
+                for got, want in ((gk[r, :, p], okv.k[l][r, :, p]), (gv[r, :, :, p], okv.v[l][r, :, :, p])):
+                    g = (got.astype(np.uint32) << 16).view(np.float32)
+                    o = (want.astype(np.uint32) << 16).view(np.float32)
+                    assert np.abs(g - o).max() <= TOL * np.abs(o).max() + 1e-6, (step, l, r)
+        tokens = np.where(valid == 1, nxt, tokens).astype(np.int32)
+        lens = np.where(valid == 1, lens + 1, lens).astype(np.int32)
+    eng.close()
+    assert len(near) <= 1, near
+    print(f"B={B}: max row-relative logit error {worst:.2e}")
+
+
+def test_padding_row_at_B1(model):
+    """B = 1 with its one row padding: next token -1 and no cache write."""
+    cfg, Wg, m = model
+    K, V = cache(cfg, 1, seed=760)
+    K0 = [k.clone() for k in K]
+    V0 = [v.clone() for v in V]
+    eng = corun.Engine(cfg, Wg, 1, K, V)
+    assert is_small_batch_layer(eng.plan())
+    nxt = eng.decode_step(np.array([5], np.int32), np.array([0], np.uint8), np.array([3], np.int32))
+    assert nxt[0] == -1
+    for l in range(cfg["n_layers"]):
+        assert torch.equal(K[l].view(torch.int16), K0[l].view(torch.int16))
+        assert torch.equal(V[l].view(torch.int16), V0[l].view(torch.int16))
+    eng.close()
+
+
+@pytest.mark.parametrize("B", [1, 8])
+def test_against_the_split_k_plan(model, B):
+    cfg, Wg, m = model
+    b = wl.make_batch(B, cfg["vocab"], seed=720 + B, len_lo=16, len_hi=CAP - 8)
+    out = []
+    for layer in (True, False):
+        K, V = cache(cfg, B, seed=730 + B)
+        opt = layer_opt(B) if layer else corun.options(small_batch_layer=2)
+        eng = corun.Engine(cfg, Wg, B, K, V, opt=opt)
+        assert is_small_batch_layer(eng.plan()) == layer
+        logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+        eng.decode_step(b.tokens, b.valid, b.seq_lens, logits)
+        out.append(logits.cpu().numpy())
+        eng.close()
+    for r in np.nonzero(b.valid)[0]:
+        assert row_rel_err(out[0][r], out[1][r].astype(np.float64)) <= TOL, r
+
+
+def test_slot_moves_are_bit_identical(model):
+    """Three requests (own token, length, cache) at slots 0, 1, 2 beside five
+    other requests, then at slots 6, 3, 7 beside five different ones."""
+    cfg, Wg, m = model
+    B = 8
+    rng = np.random.default_rng(740)
+    Kr, Vr = cache(cfg, 3, seed=741)
+    req_tok = rng.integers(0, cfg["vocab"], 3).astype(np.int32)
+    req_len = rng.integers(16, CAP - 8, 3).astype(np.int32)
+    runs = []
+    for slots, seed in (([0, 1, 2], 742), ([6, 3, 7], 743)):
+        K, V = cache(cfg, B, seed=seed)                  # the co-runners' caches
+        for i, s in enumerate(slots):
+            for l in range(cfg["n_layers"]):
+                K[l][s] = Kr[l][i]
+                V[l][s] = Vr[l][i]
+        other = np.random.default_rng(seed)
+        tokens = other.integers(0, cfg["vocab"], B).astype(np.int32)
+        lens = other.integers(16, CAP - 8, B).astype(np.int32)
+        valid = other.integers(0, 2, B).astype(np.uint8)
+        tokens[slots], lens[slots], valid[slots] = req_tok, req_len, 1
+        eng = corun.Engine(cfg, Wg, B, K, V, opt=layer_opt(B))
+        logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+        res = []
+        for _ in range(2):
+            nxt = eng.decode_step(tokens, valid, lens, logits)
+            res.append((nxt[slots].copy(), logits[slots].clone()))
+            tokens = np.where(valid == 1, nxt, tokens).astype(np.int32)
+            lens = np.where(valid == 1, lens + 1, lens).astype(np.int32)
+        runs.append((res, [[K[l][s].clone() for s in slots] for l in range(cfg["n_layers"])],
+                     [[V[l][s].clone() for s in slots] for l in range(cfg["n_layers"])]))
+        eng.close()
+    (ra, Ka, Va), (rb, Kb, Vb) = runs
+    for (na, la), (nb, lb) in zip(ra, rb):
+        assert np.array_equal(na, nb)
+        assert torch.equal(la.view(torch.int32), lb.view(torch.int32))
+    for l in range(cfg["n_layers"]):
+        for i in range(3):
+            assert torch.equal(Ka[l][i].view(torch.int16), Kb[l][i].view(torch.int16)), (l, i)
+            assert torch.equal(Va[l][i].view(torch.int16), Vb[l][i].view(torch.int16)), (l, i)
+
+
+@pytest.mark.parametrize("B", [1, 8])
+def test_paged_equals_contiguous(model, B):
+    cfg, Wg, m = model
+    ps = 16
+    mpp = CAP // ps
+    num_pages = B * mpp
+    pt = wl.make_page_table(B, mpp, num_pages, seed=750 + B)
+    Kc, Vc = cache(cfg, B, seed=751 + B)
+    Kp = [torch.empty((num_pages, cfg["n_kv_heads"], ps, cfg["head_dim"]), dtype=torch.bfloat16, device=DEV)
+          for _ in range(cfg["n_layers"])]
+    Vp = [torch.empty((num_pages, cfg["n_kv_heads"], cfg["head_dim"], ps), dtype=torch.bfloat16, device=DEV)
+          for _ in range(cfg["n_layers"])]
+    for l in range(cfg["n_layers"]):
+        for s in range(B):
+            for j in range(mpp):
+                Kp[l][pt[s, j]] = Kc[l][s, :, j * ps:(j + 1) * ps]
+                Vp[l][pt[s, j]] = Vc[l][s, :, :, j * ps:(j + 1) * ps]
+    ec = corun.Engine(cfg, Wg, B, Kc, Vc, opt=layer_opt(B))
+    ep = corun.Engine(cfg, Wg, B, Kp, Vp, layout=corun.KV_PAGED, page_size=ps,
+                      page_table=torch.from_numpy(pt).to(DEV), opt=layer_opt(B))
+    assert is_small_batch_layer(ec.plan()) and ec.plan() == ep.plan()
+    b = wl.make_batch(B, cfg["vocab"], seed=752 + B, len_lo=16, len_hi=CAP - 8)
+    la = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+    lb = torch.empty_like(la)
+    live = torch.from_numpy(b.valid.astype(bool)).to(DEV)
+    for _ in range(3):
+        na = ec.decode_step(b.tokens, b.valid, b.seq_lens, la)
+        nb = ep.decode_step(b.tokens, b.valid, b.seq_lens, lb)
+        assert np.array_equal(na, nb)
+        assert torch.equal(la[live].view(torch.int32), lb[live].view(torch.int32))
+        b.tokens = np.where(b.valid == 1, na, b.tokens).astype(np.int32)
+        b.seq_lens = np.where(b.valid == 1, b.seq_lens + 1, b.seq_lens).astype(np.int32)
+    for l in range(cfg["n_layers"]):
+        for s in np.nonzero(b.valid)[0]:
+            for j in range(mpp):
+                assert torch.equal(Kp[l][pt[s, j]].view(torch.int16),
+                                   Kc[l][s, :, j * ps:(j + 1) * ps].view(torch.int16)), (l, s, j)
+                assert torch.equal(Vp[l][pt[s, j]].view(torch.int16),
+                                   Vc[l][s, :, :, j * ps:(j + 1) * ps].view(torch.int16)), (l, s, j)
+    ec.close()
+    ep.close()
+
+
+def test_option_refusals(model):
+    cfg, Wg, m = model
+    K, V = cache(cfg, 16, seed=770)
+    for B, kw in ((16, {}), (1, dict(no_weight_pack=True)), (1, dict(batch_invariant=True)),
+                  (1, dict(qkv_epilogue=1))):
+        with pytest.raises(corun.CorunError):
+            corun.Engine(cfg, Wg, B, K, V, opt=corun.options(small_batch_layer=1, **kw))
+    with pytest.raises(corun.CorunError):
+        corun.Engine(cfg, Wg, 1, K, V, opt=corun.options(small_batch_layer=3))
