@@ -94,7 +94,9 @@ typedef struct {
  * matrix cores straight from HBM:
  *  contiguous: K layer [n_slots, n_kv_heads, max_seq_len, head_dim],
  *              V layer [n_slots, n_kv_heads, head_dim, max_seq_len];
- *              max_seq_len a multiple of 16;
+ *              max_seq_len a multiple of 16 (a multiple of 64 puts every
+ *              value row on whole 128-byte lines: decode attention then
+ *              reads each cached byte once; at 16 it re-reads up to a tenth);
  *  paged:      K layer [num_pages, n_kv_heads, page_size, head_dim],
  *              V layer [num_pages, n_kv_heads, head_dim, page_size];
  *              page_table (DEVICE int32 [n_slots, max_pages_per_seq]) maps a
@@ -347,9 +349,13 @@ corun_status corun_sample_noalloc(const float *logits_dev, int64_t ld, int32_t r
  * cache now), else one decode step of every running request padded to B.
  * Requests leave at max_new_tokens, returning their slot (the lowest free one
  * is reused) and pages.  With a paged cache the scheduler owns the page-table
- * rows of the slots: all pages of the full sequence are taken at admission.
- * engine NULL is a dry run: the same scheduling, no model, tokens 0.  Not
- * thread-safe; one scheduler per engine.
+ * rows of the slots: all pages of the full sequence are taken at admission;
+ * it keeps a host copy of the table, registered with the engine
+ * (corun_engine_set_page_table_host) from creation until
+ * corun_sched_destroy, so decode steps validate pages without a device copy.
+ * The engine is borrowed and must outlive the scheduler.  engine NULL is a
+ * dry run: the same scheduling, no model, tokens 0.  Not thread-safe; one
+ * scheduler per engine.
  * ------------------------------------------------------------------------- */
 typedef struct corun_sched corun_sched;
 typedef struct {
@@ -443,6 +449,16 @@ corun_status corun_check_config(const corun_model_cfg *cfg, const corun_kv *kv, 
 corun_status corun_check_batch(const corun_model_cfg *cfg, const corun_kv *kv, const int32_t *page_table_host,
                                int32_t B, const int32_t *tokens, const uint8_t *valid_mask,
                                const int32_t *seq_lens, int32_t n_steps);
+
+/* Paged caches: register a host copy of the page table (HOST int32
+ * [n_slots, max_pages_per_seq], caller-owned, borrowed until replaced or
+ * the engine is destroyed; NULL unregisters).  The host-side checks of
+ * corun_decode_step / corun_decode_run / corun_prefill* then read it instead
+ * of copying the device table back (a synchronous copy of the whole table on
+ * every decode call).  The caller keeps it equal to the device table
+ * whenever it calls into the engine: the kernels read the device table, the
+ * checks the copy.  CORUN_E_STATE for an engine with a contiguous cache. */
+corun_status corun_engine_set_page_table_host(corun_engine *e, const int32_t *page_table_host);
 
 /* The launch plan an engine would use (host-only, no GPU): fills `out` with
  * up to `cap` int32 values -- B, padded M, then (N, K, split_k, k_chunk,

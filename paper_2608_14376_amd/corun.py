@@ -22,6 +22,7 @@ EXPORTS = ("corun_engine_create", "corun_engine_destroy", "corun_decode_step", "
            "corun_prefill", "corun_prefill_chunk", "corun_prefill_batch", "corun_check_config", "corun_check_batch",
            "corun_describe_plan", "corun_describe_prefill_plan",
            "corun_last_error", "corun_time_kernel", "corun_profile_step", "corun_sample", "corun_sample_noalloc", "corun_engine_info",
+           "corun_engine_set_page_table_host",
            "corun_routing_trace",
            "corun_sched_create", "corun_sched_destroy", "corun_sched_add_request", "corun_sched_step",
            "corun_sched_output", "corun_sched_state", "corun_sched_last_error")
@@ -119,6 +120,8 @@ def load():
                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
     L.corun_engine_info.restype = st
     L.corun_engine_info.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]
+    L.corun_engine_set_page_table_host.restype = st
+    L.corun_engine_set_page_table_host.argtypes = [C.c_void_p, C.c_void_p]
     L.corun_routing_trace.restype = st
     L.corun_routing_trace.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.POINTER(C.c_int32)]
     L.corun_sched_create.restype = st
@@ -391,6 +394,18 @@ class Engine:
 
     def plan(self) -> dict:
         return describe_plan(self.cfg, self._kv, self.B, self._opt)
+
+    def set_page_table_host(self, pt) -> None:
+        """Register a host int32 [n_slots, max_pages_per_seq] copy of the
+        device page table for the host-side checks (None unregisters); the
+        array is kept alive here and must be kept equal to the device table."""
+        if pt is None:
+            self._pt_host = None
+            _check(self._L.corun_engine_set_page_table_host(self._h, None))
+            return
+        assert isinstance(pt, np.ndarray) and pt.dtype == np.int32 and pt.flags.c_contiguous
+        self._pt_host = pt
+        _check(self._L.corun_engine_set_page_table_host(self._h, pt.ctypes.data))
 
     def decode_step(self, tokens, valid, seq_lens, logits=None) -> np.ndarray:
         t, vm, s = _np(tokens, np.int32), _np(valid, np.uint8), _np(seq_lens, np.int32)

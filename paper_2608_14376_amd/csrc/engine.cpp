@@ -324,6 +324,10 @@ struct corun_engine {
     LaunchRecorder rec;
     std::vector<uint16_t *> kc, vc;
     KvView view{};
+    // paged caches: the caller's host copy of the page table
+    // (corun_engine_set_page_table_host), read by the host-side checks
+    // instead of copying the device table back on every call
+    const int32_t *pt_host = nullptr;
 
     // decode workspace (one allocation)
     char *ws = nullptr;
@@ -886,15 +890,33 @@ corun_status enter(corun_engine *e)
     return CORUN_OK;
 }
 
+// Slot `slot`'s row of the page table for the host-side checks: from the
+// registered host copy, else copied from the device (one synchronous copy).
+corun_status page_row(corun_engine *e, int slot, std::vector<int32_t> &row)
+{
+    row.resize(e->kv.max_pages_per_seq);
+    const size_t off = (size_t)slot * e->kv.max_pages_per_seq;
+    if (e->pt_host) {
+        std::memcpy(row.data(), e->pt_host + off, row.size() * sizeof(int32_t));
+        return CORUN_OK;
+    }
+    HIP_TRY(hipMemcpy(row.data(), e->kv.page_table + off, row.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+    return CORUN_OK;
+}
+
 corun_status check_pages(corun_engine *e, const int32_t *seq_lens, const uint8_t *valid, const int32_t *tokens,
                          int n_rows, int n_steps)
 {
     std::vector<int32_t> pt;
     const int32_t *pth = nullptr;
     if (e->kv.layout == CORUN_KV_PAGED) {
-        pt.resize((size_t)e->kv.n_slots * e->kv.max_pages_per_seq);
-        HIP_TRY(hipMemcpy(pt.data(), e->kv.page_table, pt.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
-        pth = pt.data();
+        if (e->pt_host) {
+            pth = e->pt_host;
+        } else {
+            pt.resize((size_t)e->kv.n_slots * e->kv.max_pages_per_seq);
+            HIP_TRY(hipMemcpy(pt.data(), e->kv.page_table, pt.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+            pth = pt.data();
+        }
     }
     return corun_check_batch(&e->c, &e->kv, pth, n_rows, tokens, valid, seq_lens, n_steps);
 }
@@ -1417,9 +1439,8 @@ extern "C" corun_status corun_prefill_chunk(corun_engine *e, const int32_t *toke
         if (tokens[t] < 0 || tokens[t] >= e->c.vocab)
             return fail(CORUN_E_INVAL, "token[%d] = %d outside [0, %d)", t, tokens[t], e->c.vocab);
     if (e->kv.layout == CORUN_KV_PAGED) {
-        std::vector<int32_t> pt(e->kv.max_pages_per_seq);
-        HIP_TRY(hipMemcpy(pt.data(), e->kv.page_table + (size_t)slot * e->kv.max_pages_per_seq,
-                          pt.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+        std::vector<int32_t> pt;
+        ST_TRY(page_row(e, slot, pt));
         for (int j = 0; j <= (start + n - 1) / e->kv.page_size; ++j)
             if (pt[j] < 0 || pt[j] >= e->kv.num_pages)
                 return fail(CORUN_E_CAPACITY, "slot %d: page %d maps to %d outside [0, %d)", slot, j, pt[j],
@@ -1528,10 +1549,9 @@ extern "C" corun_status corun_prefill_batch(corun_engine *e, const int32_t *toke
         if (tokens[t] < 0 || tokens[t] >= e->c.vocab)
             return fail(CORUN_E_INVAL, "tokens[%lld] = %d outside [0, %d)", t, tokens[t], e->c.vocab);
     if (e->kv.layout == CORUN_KV_PAGED) {
-        std::vector<int32_t> pt(e->kv.max_pages_per_seq);
+        std::vector<int32_t> pt;
         for (int i = 0; i < n; ++i) {
-            HIP_TRY(hipMemcpy(pt.data(), e->kv.page_table + (size_t)slots[i] * e->kv.max_pages_per_seq,
-                              pt.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+            ST_TRY(page_row(e, slots[i], pt));
             for (int j = 0; j <= (lens[i] - 1) / e->kv.page_size; ++j)
                 if (pt[j] < 0 || pt[j] >= e->kv.num_pages)
                     return fail(CORUN_E_CAPACITY, "slot %d: page %d maps to %d outside [0, %d)", slots[i], j, pt[j],
@@ -1614,6 +1634,14 @@ extern "C" corun_status corun_prefill_batch(corun_engine *e, const int32_t *toke
         HIP_TRY(hipMemcpyAsync(last_logits, e->pf_logits, sizeof(float) * (size_t)n * c.vocab,
                                hipMemcpyDeviceToDevice, st));
     HIP_TRY(hipStreamSynchronize(st));
+    return CORUN_OK;
+}
+
+extern "C" corun_status corun_engine_set_page_table_host(corun_engine *e, const int32_t *pt_host)
+{
+    if (!e) return fail(CORUN_E_INVAL, "null engine");
+    if (pt_host && e->kv.layout != CORUN_KV_PAGED) return fail(CORUN_E_STATE, "the engine's cache is not paged");
+    e->pt_host = pt_host;
     return CORUN_OK;
 }
 

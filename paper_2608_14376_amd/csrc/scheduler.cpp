@@ -76,6 +76,9 @@ struct corun_sched {
     std::deque<int64_t> running, waiting;
     std::vector<int64_t> slot_owner;    // [B], -1 = free
     std::vector<int32_t> free_pages;    // stack, lowest id on top
+    // paged: the host copy of the page table this scheduler keeps equal to
+    // the device table and registers with the engine for its checks
+    std::vector<int32_t> pt_host;
     float *logits = nullptr;            // device [B][vocab]
     float *last = nullptr;              // device [vocab]
     int64_t n_prefill = 0, n_decode = 0;
@@ -123,9 +126,11 @@ corun_status write_page_row(corun_sched *s, const Request &r)
     std::vector<int32_t> row(s->kv.max_pages_per_seq, r.pages.empty() ? 0 : r.pages[0]);
     std::copy(r.pages.begin(), r.pages.end(), row.begin());
     if (!s->e) return CORUN_OK;
-    int32_t *dst = const_cast<int32_t *>(s->kv.page_table) + (size_t)r.slot * s->kv.max_pages_per_seq;
+    const size_t off = (size_t)r.slot * s->kv.max_pages_per_seq;
+    int32_t *dst = const_cast<int32_t *>(s->kv.page_table) + off;
     if (hipMemcpy(dst, row.data(), row.size() * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess)
         return sfail(CORUN_E_HIP, "page table update failed");
+    std::copy(row.begin(), row.end(), s->pt_host.begin() + off);
     return CORUN_OK;
 }
 
@@ -408,6 +413,17 @@ extern "C" corun_status corun_sched_create(corun_engine *e, const corun_sched_cf
     s->slot_owner.assign(s->B, -1);
     if (s->paged)
         for (int32_t p = s->kv.num_pages - 1; p >= 0; --p) s->free_pages.push_back(p);
+    if (e && s->paged) {
+        // one copy of the device table now; from here on this scheduler
+        // writes both, and the engine's checks read the host copy
+        s->pt_host.resize((size_t)s->kv.n_slots * s->kv.max_pages_per_seq);
+        if (hipMemcpy(s->pt_host.data(), s->kv.page_table, s->pt_host.size() * sizeof(int32_t),
+                      hipMemcpyDeviceToHost) != hipSuccess ||
+            corun_engine_set_page_table_host(e, s->pt_host.data()) != CORUN_OK) {
+            delete s;
+            return sfail(CORUN_E_HIP, "page table copy");
+        }
+    }
     if (e) {
         const size_t brows = s->batch_tokens > 0 ? (size_t)std::min(s->B, CORUN_MAX_PREFILL_BATCH) : 1;
         if (hipMalloc(&s->logits, sizeof(float) * (size_t)s->B * s->vocab) != hipSuccess ||
@@ -424,6 +440,7 @@ extern "C" corun_status corun_sched_create(corun_engine *e, const corun_sched_cf
 extern "C" void corun_sched_destroy(corun_sched *s)
 {
     if (!s) return;
+    if (s->e && !s->pt_host.empty()) (void)corun_engine_set_page_table_host(s->e, nullptr);   // the engine may outlive it
     if (s->logits) (void)hipFree(s->logits);
     if (s->last) (void)hipFree(s->last);
     if (s->blogits) (void)hipFree(s->blogits);

@@ -9,7 +9,9 @@ invariance contract (Sec. III, Definition 2):
   model: sampled rows against the oracle, and a live row moved to another
   slot among other co-runners gives the same bits;
 * the prefill workspace used to its last token (a prompt of exactly
-  max_prefill_len tokens)."""
+  max_prefill_len tokens);
+* the host copy of the page table (corun_engine_set_page_table_host) used
+  by the checks in place of the device table."""
 import numpy as np
 import pytest
 import torch
@@ -197,3 +199,48 @@ def test_profile_step_times_every_launch_and_changes_nothing():
         eng.close()
     assert np.array_equal(outs[0][0], outs[1][0])
     assert all(np.array_equal(x, y) for x, y in zip(outs[0][1], outs[1][1]))
+
+
+def test_page_table_host_copy():
+    """A registered host copy of the page table replaces the per-call device
+    copy in the host-side checks: the same step gives the same bits with it,
+    a page the copy maps out of range is refused (while the device table is
+    valid) before anything runs, unregistering goes back to the device
+    table, and a contiguous engine refuses a copy."""
+    cfg = wl.config("tiny")
+    Wg = to_device(wl.make_weights(cfg, seed=85))
+    B, mpp = 4, CAP // PS
+    num_pages = B * mpp
+    pt = wl.make_page_table(B, mpp, num_pages, seed=86)
+    K, V = wl.make_kv_paged(cfg, num_pages, PS, seed=87, device=DEV)
+    eng = corun.Engine(cfg, Wg, B, K, V, layout=corun.KV_PAGED, page_size=PS,
+                       page_table=torch.from_numpy(pt).to(DEV))
+    b = wl.make_batch(B, cfg["vocab"], seed=88, len_lo=16, len_hi=CAP - 8)
+    la = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
+    lb = torch.empty_like(la)
+    # the step appends at seq_len, so running it again rewrites the same values
+    na = eng.decode_step(b.tokens, b.valid, b.seq_lens, la)
+    host = pt.copy()
+    eng.set_page_table_host(host)
+    nb = eng.decode_step(b.tokens, b.valid, b.seq_lens, lb)
+    assert np.array_equal(na, nb)
+    live = torch.from_numpy(b.valid.astype(bool)).to(DEV)
+    assert torch.equal(la[live].view(torch.int32), lb[live].view(torch.int32))
+    r = int(np.nonzero(b.valid)[0][0])
+    host[r, b.seq_lens[r] // PS] = num_pages          # only the host copy is wrong
+    before = [k.clone() for k in K]
+    with pytest.raises(corun.CorunError) as ei:
+        eng.decode_step(b.tokens, b.valid, b.seq_lens, lb)
+    assert ei.value.status == corun.E_CAPACITY
+    for l in range(cfg["n_layers"]):                  # refused before anything ran
+        assert torch.equal(K[l].view(torch.int16), before[l].view(torch.int16))
+    eng.set_page_table_host(None)
+    nc = eng.decode_step(b.tokens, b.valid, b.seq_lens, lb)
+    assert np.array_equal(na, nc)
+    eng.close()
+    Kc, Vc = wl.make_kv_contiguous(cfg, B, CAP, seed=89, device=DEV)
+    ec = corun.Engine(cfg, Wg, B, Kc, Vc)
+    with pytest.raises(corun.CorunError) as ei:
+        ec.set_page_table_host(pt.copy())
+    assert ei.value.status == corun.E_STATE
+    ec.close()
