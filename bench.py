@@ -156,9 +156,7 @@ def run_B(cfg, W, B, args, seeds, measure_kernels, paged=False, len_lo=LEN_LO, l
         K, V, pt, ps = make_paged(cfg, B, np.where(batches[0].valid == 1, batches[0].seq_lens, 0), extra, 3000 + B)
         eng = corun.Engine(cfg, W, B, K, V, layout=corun.KV_PAGED, page_size=ps, page_table=pt)
     else:
-        # capacity rounded to 64 tokens: every transposed value row (capacity x 2 bytes) then starts on a
-        # 128-byte line, so a value read of 128 tokens touches two lines, not three
-        K, V = wl.make_kv_contiguous(cfg, B, (len_hi + extra + 63) // 64 * 64, seed=1000 + B, device="cuda")
+        K, V = wl.make_kv_contiguous(cfg, B, (len_hi + extra + 15) // 16 * 16, seed=1000 + B, device="cuda")
         eng = corun.Engine(cfg, W, B, K, V)
     torch.cuda.synchronize()
     log(f"[bench] {cfg['n_layers']}L H={cfg['hidden']} B={B} {'paged' if paged else 'contiguous'}: KV cache "

@@ -89,16 +89,11 @@ typedef struct {
 } corun_weights;
 
 /* KV cache: device bf16, caller-owned, borrowed.  k and v are HOST arrays of
- * n_layers DEVICE pointers.  Keys are stored by token, values transposed
- * (by dimension, tokens contiguous) so that attention can feed both to the
- * matrix cores straight from HBM:
- *  contiguous: K layer [n_slots, n_kv_heads, max_seq_len, head_dim],
- *              V layer [n_slots, n_kv_heads, head_dim, max_seq_len];
- *              max_seq_len a multiple of 16 (a multiple of 64 puts every
- *              value row on whole 128-byte lines: decode attention then
- *              reads each cached byte once; at 16 it re-reads up to a tenth);
- *  paged:      K layer [num_pages, n_kv_heads, page_size, head_dim],
- *              V layer [num_pages, n_kv_heads, head_dim, page_size];
+ * n_layers DEVICE pointers.  Keys and values are stored by token (each
+ * token's head_dim elements contiguous):
+ *  contiguous: K and V layers [n_slots, n_kv_heads, max_seq_len, head_dim];
+ *              max_seq_len a multiple of 16;
+ *  paged:      K and V layers [num_pages, n_kv_heads, page_size, head_dim];
  *              page_table (DEVICE int32 [n_slots, max_pages_per_seq]) maps a
  *              slot's token t to page page_table[slot][t / page_size] at
  *              position t % page_size; page_size a multiple of 16; capacity

@@ -266,10 +266,9 @@ class Model:
 
 @dataclass
 class KVCache:
-    """Host KV cache: per-layer uint16 arrays.  Keys by token, values
-    transposed: contiguous K [slots, nkv, S, d], V [slots, nkv, d, S]; paged
-    K [pages, nkv, page_size, d], V [pages, nkv, d, page_size] with an int32
-    page table [slots, max_pages_per_seq]."""
+    """Host KV cache: per-layer uint16 arrays, keys and values by token:
+    contiguous K, V [slots, nkv, S, d]; paged K, V [pages, nkv, page_size, d]
+    with an int32 page table [slots, max_pages_per_seq]."""
     k: list
     v: list
     layout: int = KV_CONTIGUOUS

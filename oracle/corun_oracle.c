@@ -200,10 +200,10 @@ typedef struct {
 
 enum { ORC_KV_CONTIGUOUS = 0, ORC_KV_PAGED = 1 };
 
-/* KV cache layout (the library's contract).  Keys are stored by token,
- * values transposed (by dimension):
- *   contiguous: K [slot, kvh, t, d]        V [slot, kvh, d, t]
- *   paged:      K [page, kvh, t % ps, d]   V [page, kvh, d, t % ps]
+/* KV cache layout (the library's contract).  Keys and values are stored by
+ * token:
+ *   contiguous: K, V [slot, kvh, t, d]
+ *   paged:      K, V [page, kvh, t % ps, d]
  * with page = page_table[slot, t / ps]. */
 typedef struct {
     int32_t layout;
@@ -225,15 +225,16 @@ static uint16_t *k_row(const orc_cfg *c, const orc_kv *kv, int layer, int slot, 
     return kv->k[layer] + (((int64_t)slot * c->n_kv_heads + kvh) * kv->max_seq_len + t) * d;
 }
 
-/* Address of value element e of (layer, slot, kv head, token position). */
+/* Address of value element e of (layer, slot, kv head, token position):
+ * values are stored by token, like keys. */
 static uint16_t *v_elem(const orc_cfg *c, const orc_kv *kv, int layer, int slot, int kvh, int t, int e)
 {
     int64_t d = c->head_dim;
     if (kv->layout == ORC_KV_PAGED) {
         int32_t page = kv->page_table[(int64_t)slot * kv->max_pages_per_seq + t / kv->page_size];
-        return kv->v[layer] + (((int64_t)page * c->n_kv_heads + kvh) * d + e) * kv->page_size + t % kv->page_size;
+        return kv->v[layer] + (((int64_t)page * c->n_kv_heads + kvh) * kv->page_size + t % kv->page_size) * d + e;
     }
-    return kv->v[layer] + (((int64_t)slot * c->n_kv_heads + kvh) * d + e) * kv->max_seq_len + t;
+    return kv->v[layer] + (((int64_t)slot * c->n_kv_heads + kvh) * kv->max_seq_len + t) * d + e;
 }
 
 /* ------------------------------------------------------------------------ */

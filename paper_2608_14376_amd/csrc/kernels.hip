@@ -105,17 +105,33 @@ __device__ __forceinline__ size_t kv_offset(const KvView &kv, int nkv, int d, in
     return (((size_t)slot * nkv + kvh) * kv.max_seq_len + t) * d;
 }
 
-// Values are stored transposed: element e of token t at
-//   contiguous ((slot nkv + kvh) d + e) max_seq_len + t
-//   paged      ((page nkv + kvh) d + e) page_size + t % page_size
+// Values are stored like keys, by token: element e of token t of a kv head
+// is element e of that token's value row.
 __device__ __forceinline__ size_t v_offset(const KvView &kv, int nkv, int d, int slot, int kvh, int t, int e)
 {
-    if (kv.layout == 1) {
-        int page = kv.page_table[(size_t)slot * kv.max_pages_per_seq + t / kv.page_size];
-        return (((size_t)page * nkv + kvh) * d + e) * kv.page_size + (t % kv.page_size);
-    }
-    return (((size_t)slot * nkv + kvh) * d + e) * kv.max_seq_len + t;
+    return kv_offset(kv, nkv, d, slot, kvh, t) + e;
 }
+
+// Transposed LDS read (gfx950 ds_read_b64_tr_b16).  Within each group of 16
+// lanes, lane a + 4 q supplies the address of four 16-bit values (row q,
+// elements 4 a .. 4 a + 3 of some column block); lane i of the group then
+// receives element i of the block from rows 0..3.  Two such reads give a
+// lane eight consecutive rows of one column: the B (or A) operand of a bf16
+// MFMA whose K runs along the rows, read from row-major tiles.
+typedef short s16x4_tr __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint2 lds_read_tr16(const void *lds_ptr)
+{
+    typedef __attribute__((address_space(3))) s16x4_tr lds_s16x4;
+    const s16x4_tr v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_s16x4 *)(const __attribute__((address_space(3))) void *)lds_ptr);
+    return __builtin_bit_cast(uint2, v);
+}
+
+// Value tiles in LDS are token-major, 16-byte chunk c of token t at
+// t * chunks + (c ^ vtile_swz(t)): the four consecutive tokens that one
+// 16-lane transposed read touches (32 bytes each) land in four distinct
+// 32-byte bank ranges.
+__device__ __forceinline__ int vtile_swz(int t) { return 2 * (t & 3); }
 
 __device__ __forceinline__ int row_slot(const int32_t *slot_of_row, int slot_const, int r)
 {
@@ -1147,10 +1163,10 @@ hipError_t launch_qkv_post(const float *part, int S, long long part_stride, int 
 // split is request-local and the merge order (split index) is fixed.
 //
 // Block (kvh, split, row), four wavefronts.  The chunk is walked in steps of
-// 128 tokens: the step's key rows ([token][d]) and transposed values
-// ([d][token]) are loaded global -> LDS by direct 16-byte loads in which
-// every instruction covers whole 128-byte lines (4 key rows of 256 bytes, or
-// 4 value rows of 128 tokens); a load form of 16 rows x 64 bytes per
+// 128 tokens: the step's key rows and value rows ([token][d], as cached) are
+// loaded global -> LDS by direct 16-byte loads in which every instruction
+// covers whole 128-byte lines (4 rows of 256 bytes); a load form of 16 rows
+// x 64 bytes per
 // instruction, which the matrix-core operand layout would give if loaded
 // straight into registers, caps the read rate near 4.7 TB/s against 6.2 TB/s
 // for whole lines.  Wavefront w then takes the step's 32-token block w from
@@ -1164,26 +1180,26 @@ hipError_t launch_qkv_post(const float *part, int S, long long part_stride, int 
 //  * O += P V on 16x16x32 MFMA: the lane's eight weights (two tiles x four
 //    tokens) are its A fragment as they stand -- split into two bf16 halves
 //    hi + lo (two MFMAs) so P keeps about 16 significant bits -- and the
-//    matching B fragment is one 16-byte read of the transposed values
-//    (those eight tokens of one dimension);
+//    matching B fragment (those eight tokens of one dimension) comes from
+//    the token-major value rows by two transposed LDS reads (lds_read_tr16);
 //  * masked tokens (past the row's length) contribute exact zeros: their
 //    value fragments are zero-filled, never multiplied; loads past the
 //    length read clamped (real) positions.
 // The four wavefront partials are combined in wavefront order.  Two blocks
 // share a CU (64 KB of LDS each for d = 128): one computes while the
 // other's step is in flight.
-// LDS layouts, 16-byte units, XOR-swizzled so that a fragment read (16
-// lanes: 16 tokens of one chunk, or 16 dimensions of one token chunk) hits
-// 16 distinct bank groups: key unit (token t, chunk c) at t KCH + (c ^ ks(t)),
-// value unit (dim e, token chunk c) at e 16 + (c ^ (e % 16)).
+// LDS layouts, 16-byte units, XOR-swizzled so that a fragment read hits
+// distinct bank groups: key unit (token t, chunk c) at t KCH + (c ^ ks(t))
+// (16 lanes: 16 tokens of one chunk), value unit (token t, chunk c) at
+// t KCH + (c ^ vtile_swz(t)) (a transposed read: 4 tokens x 32 bytes per
+// 16 lanes).
 // ---------------------------------------------------------------------------
-typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 // Token order inside a 32-token block.  Score tile T's MFMA row m carries
 // token 8 (m / 4) + 4 T + m % 4, so that lane group kg ends up holding the
 // scores of tokens 8 kg .. 8 kg + 7 (tile 0 rows 4 kg + i, tile 1 rows
 // 4 kg + i): its P fragment is eight consecutive tokens and its value
-// fragment one 16-byte read of the transposed values.
+// fragment those eight tokens of one dimension.
 __device__ __forceinline__ int attn_tok(int T, int m) { return 8 * (m >> 2) + 4 * T + (m & 3); }
 
 // key-row swizzle: the 16 tokens a fragment read touches, {8 a + 4 T + b},
@@ -1207,7 +1223,7 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
     constexpr int ET = D / 16;
     constexpr int KCH = D / 8;                        // 16-byte chunks per key row
     constexpr int STEP = 128;                         // tokens per step, 32 per wavefront
-    constexpr int KU = STEP * KCH, VU = D * (STEP / 8);   // 16-byte units of the step's keys, values
+    constexpr int KU = STEP * KCH, VU = STEP * KCH;    // 16-byte units of the step's keys, values
     constexpr int K_OPS = KU / 256, V_OPS = VU / 256;
     static_assert(K_OPS * 256 == KU && V_OPS * 256 == VU, "step loads cover the block");
     static_assert(4 * G * D * 4 <= (KU + VU) * 16, "wavefront partials fit the tile");
@@ -1261,7 +1277,7 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
     // the last real key, or the last real 8-token value chunk.  A paged
     // cache's page of position t is pgs[buf][t / ps - tb0 / ps] (a step spans
     // at most 128 / ps + 1 <= 9 pages), so no load waits on a page-table read.
-    const int kmax = t1 - 1, vmax = (t1 - 1) & ~7;
+    const int kmax = t1 - 1;
     const bool paged = kv.layout == 1;
     const int ps = paged ? kv.page_size : 1;
     const int last_page = kmax / ps;
@@ -1286,12 +1302,13 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
         }
 #pragma unroll
         for (int j = 0; j < V_OPS; ++j) {
-            const int u = j * 256 + tid, e = u >> 4, c = (u & 15) ^ (e & 15);
-            const int t = min(tb0 + 8 * c, vmax);
+            const int u = j * 256 + tid, tv = u / KCH, c = (u % KCH) ^ vtile_swz(tv);
+            const int t = min(tb0 + tv, kmax);
             size_t off;
-            if (paged) off = (((size_t)pgs[buf][t / ps - p0] * nkv + kvh) * D + e) * ps + t % ps;
-            else off = (((size_t)slot * nkv + kvh) * D + e) * kv.max_seq_len + t;
-            __builtin_amdgcn_global_load_lds((const void *)(vc + off), (lds_void *)(base + KU + j * 256), 16, 0, 0);
+            if (paged) off = (((size_t)pgs[buf][t / ps - p0] * nkv + kvh) * ps + t % ps) * D;
+            else off = (((size_t)slot * nkv + kvh) * kv.max_seq_len + t) * D;
+            __builtin_amdgcn_global_load_lds((const void *)(vc + off + 8 * c), (lds_void *)(base + KU + j * 256), 16, 0,
+                                             0);
         }
     };
 
@@ -1372,9 +1389,9 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
             const int tl = pnew - tb0;
             if (tid < KCH) {
                 tile[tl * KCH + (tid ^ attn_kswz<KCH>(tl))] = reinterpret_cast<const uint4 *>(kvn)[tid];
-            } else if (tid >= 64 && tid < 64 + D) {
-                const int e = tid - 64;
-                reinterpret_cast<uint16_t *>(&tile[KU + e * 16 + ((tl >> 3) ^ (e & 15))])[tl & 7] = kvn[D + e];
+            } else if (tid >= 64 && tid < 64 + KCH) {
+                const int c = tid - 64;
+                tile[KU + tl * KCH + (c ^ vtile_swz(tl))] = reinterpret_cast<const uint4 *>(kvn + D)[c];
             }
             __builtin_amdgcn_s_waitcnt(0);
             lds_barrier();
@@ -1394,21 +1411,29 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
                 kf[T][kk] = __builtin_bit_cast(bf16x8, tile[tl * KCH + ((kg + 4 * kk) ^ attn_kswz<KCH>(tl))]);
         }
         {
+            // value fragments: lane (hl, kg) takes dimension 16 et + hl of the
+            // eight tokens 8 kg .. 8 kg + 7 of its 32-token block by two
+            // transposed reads (tokens 4 r + 0..3); in its 16-lane group, lane
+            // a + 4 q points at token 8 kg + 4 r + q, dimensions 16 et + 4 a ..
             const int nv = min(8, wt1 - (tb + 8 * kg));   // how many of the lane's eight tokens are real
-            const int c = 4 * wave + kg;
+            const int a = hl & 3, qq = hl >> 2;
 #pragma unroll
             for (int et = 0; et < ET; ++et) {
-                const int e = 16 * et + hl;
-                uint4 v = z4;
-                if (nv > 0) {
-                    v = tile[KU + e * 16 + (c ^ (e & 15))];
-                    if (nv < 8) {   // zero the tokens past the row's length (low half = earlier token)
-                        uint32_t *w = (uint32_t *)&v;
+                uint2 part[2];
 #pragma unroll
-                        for (int j = 0; j < 4; ++j) {
-                            if (2 * j >= nv) w[j] = 0u;
-                            else if (2 * j + 1 >= nv) w[j] &= 0x0000ffffu;
-                        }
+                for (int r = 0; r < 2; ++r) {
+                    const int tv = 32 * wave + 8 * kg + 4 * r + qq;
+                    const int c = 2 * et + (a >> 1);
+                    part[r] = lds_read_tr16(reinterpret_cast<const char *>(tile + KU + tv * KCH + (c ^ vtile_swz(tv))) +
+                                            8 * (a & 1));
+                }
+                uint4 v = {part[0].x, part[0].y, part[1].x, part[1].y};   // low half = earlier token
+                if (nv < 8) {   // zero the tokens past the row's length
+                    uint32_t *w = (uint32_t *)&v;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        if (2 * j >= nv) w[j] = 0u;
+                        else if (2 * j + 1 >= nv) w[j] &= 0x0000ffffu;
                     }
                 }
                 vfr[et] = v;
@@ -2568,8 +2593,8 @@ hipError_t launch_moe_gemm_dma(const uint16_t *A, int lda, int row_div, const ui
 // group).  A workgroup of eight wavefronts (two per SIMD, so one wavefront's
 // softmax runs while the other's matrix products do) takes eight consecutive
 // units in [block][head] order, latest blocks first, one per wavefront; the
-// eight share key tiles ([key][d] rows) and transposed value tiles ([d][key]
-// rows, as the cache stores them), streamed global -> LDS by direct 16-byte
+// eight share key and value tiles ([key][d] rows, as the cache stores them),
+// streamed global -> LDS by direct 16-byte
 // loads through a ring of three stages (one tile in use, two in flight),
 // waited on with a fixed vmcnt.
 //  * S^T = K Q^T on v_mfma_f32_32x32x16_bf16, two 32-key x 32-query tiles;
@@ -2577,8 +2602,8 @@ hipError_t launch_moe_gemm_dma(const uint16_t *A, int lda, int row_div, const ui
 //    ends holding, for query l % 32, the eight consecutive keys
 //    16 s + 8 (l / 32) .. +7 of each 16-key step s -- exactly the P^T
 //    operand of
-//  * O^T += V^T P^T on the same instruction: its V^T operand is one 16-byte
-//    read of a transposed value row.
+//  * O^T += V^T P^T on the same instruction: its V^T operand (eight keys of
+//    one dimension) comes from the value rows by two transposed LDS reads.
 // Each lane's O^T values belong to one query, so the softmax max and sum
 // need one exchange between the two lane halves and the rescale is a
 // per-lane scalar, skipped when no lane's maximum moved.  P enters the matrix
@@ -2609,9 +2634,9 @@ __device__ __forceinline__ void prefill_attn_block(const uint16_t *__restrict__ 
     constexpr int QB = 32, BKT = 64;                  // queries per wavefront, keys per tile
     constexpr int DT = D / 32, KS = D / 16;           // 32-dim output tiles, 16-dim score steps
     constexpr int KCH = D / 8;                        // 16-byte chunks per key row
-    constexpr int K_OPS = BKT * KCH / NT, V_OPS = D * 8 / NT, OPS = K_OPS + V_OPS;
+    constexpr int K_OPS = BKT * KCH / NT, V_OPS = BKT * KCH / NT, OPS = K_OPS + V_OPS;
     constexpr int NST = 3, P = NST - 1;
-    constexpr int KSTAGE = BKT * KCH, STAGE = KSTAGE + D * 8;   // 16-byte units
+    constexpr int KSTAGE = BKT * KCH, STAGE = 2 * KSTAGE;     // 16-byte units: key rows, then value rows
     constexpr int OPITCH = D + 8;                     // output staging row (elements)
     static_assert(K_OPS >= 1 && V_OPS >= 1, "tile loads cover the workgroup");
     static_assert(NW * QB * OPITCH * 2 <= NST * STAGE * 16, "output staging fits the ring");
@@ -2640,7 +2665,7 @@ __device__ __forceinline__ void prefill_attn_block(const uint16_t *__restrict__ 
     const int ntiles = wg_last_q / BKT + 1;
 
     // tile loads: op j of thread t is 16-byte unit 512 j + t of the K part
-    // (row / KCH) or of the V^T part (row / 8)
+    // or of the V part (token-major both, row = unit / KCH)
     typedef __attribute__((address_space(3))) void lds_void;
     auto issue = [&](int slot_, int k0) {
         uint4 *base = ring + slot_ * STAGE + wave * 64;
@@ -2653,9 +2678,9 @@ __device__ __forceinline__ void prefill_attn_block(const uint16_t *__restrict__ 
         }
 #pragma unroll
         for (int j = 0; j < V_OPS; ++j) {
-            const int gi = j * NT + tid, e = gi >> 3, c = pf_swz<8>(e, gi & 7) - e * 8;
-            const int key0 = min(k0 + 8 * c, (Lk - 1) & ~7);
-            __builtin_amdgcn_global_load_lds((const void *)(vc + v_offset(kv, nkv, D, slot, kvh, key0, e)),
+            const int gi = j * NT + tid, r = gi / KCH, c = (gi % KCH) ^ vtile_swz(r);
+            const int key = min(k0 + r, Lk - 1);
+            __builtin_amdgcn_global_load_lds((const void *)(vc + kv_offset(kv, nkv, D, slot, kvh, key) + 8 * c),
                                              (lds_void *)(base + KSTAGE + j * NT), 16, 0, 0);
         }
     };
@@ -2691,12 +2716,10 @@ __device__ __forceinline__ void prefill_attn_block(const uint16_t *__restrict__ 
         uint4 *Kt = ring + (i % NST) * STAGE;
         uint4 *Vt = Kt + KSTAGE;
         if (k0 + BKT > Lk) {
-            // last tile: zero the values of keys past the prompt
-            uint16_t *v16 = (uint16_t *)Vt;
-            for (int it = tid; it < D * BKT; it += NT) {
-                const int e = it / BKT, kk = it % BKT;
-                if (k0 + kk >= Lk) v16[pf_swz<8>(e, kk >> 3) * 8 + (kk & 7)] = 0;
-            }
+            // last tile: zero the value rows of keys past the prompt
+            const uint4 z = {0u, 0u, 0u, 0u};
+            for (int it = tid; it < BKT * KCH; it += NT)
+                if (k0 + it / KCH >= Lk) Vt[it] = z;
             lds_barrier();
         }
         if (i + P < ntiles) issue((i + P) % NST, (i + P) * BKT);
@@ -2765,12 +2788,26 @@ __device__ __forceinline__ void prefill_attn_block(const uint16_t *__restrict__ 
         }
         lpart += ls;
         mrow = mnew;
-        // O^T += V^T P^T over the tile's four 16-key steps
+        // O^T += V^T P^T over the tile's four 16-key steps.  The V^T operand
+        // (lane l: dimension 32 dt + l % 32, keys 16 s16 + 8 h .. +7) comes
+        // from the token-major value rows by two transposed reads per
+        // 16-lane group (keys 4 r + 0..3): lane a + 4 q of the group points
+        // at key 16 s16 + 8 h + 4 r + q, dimensions 32 dt + 16 (l / 16 % 2)
+        // + 4 a ..
 #pragma unroll
         for (int s16 = 0; s16 < 4; ++s16)
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) {
-                const bf16x8 vf = __builtin_bit_cast(bf16x8, Vt[pf_swz<8>(32 * dt + r32, 2 * s16 + h)]);
+                const int a = lane & 3, qv = (lane >> 2) & 3, half16 = (lane >> 4) & 1;
+                uint2 part[2];
+#pragma unroll
+                for (int r = 0; r < 2; ++r) {
+                    const int key = 16 * s16 + 8 * h + 4 * r + qv;
+                    const int c = 4 * dt + 2 * half16 + (a >> 1);
+                    part[r] = lds_read_tr16(reinterpret_cast<const char *>(Vt + key * KCH + (c ^ vtile_swz(key))) +
+                                            8 * (a & 1));
+                }
+                const bf16x8 vf = __builtin_bit_cast(bf16x8, (uint4){part[0].x, part[0].y, part[1].x, part[1].y});
                 acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[s16], acc[dt], 0, 0, 0);
             }
     }

@@ -203,13 +203,12 @@ def make_batch(B: int, vocab: int, seed: int, len_lo: int, len_hi: int,
 
 def make_kv_contiguous(c: dict, n_slots: int, max_seq_len: int, seed: int, device="cpu",
                        layers=None, std: float = 1.0):
-    """Contiguous per-slot cache, bf16 N(0, std): per layer K of shape
-    [n_slots, n_kv_heads, max_seq_len, head_dim] and V stored transposed,
-    [n_slots, n_kv_heads, head_dim, max_seq_len]."""
+    """Contiguous per-slot cache, bf16 N(0, std): per layer K and V of shape
+    [n_slots, n_kv_heads, max_seq_len, head_dim]."""
     L = c["n_layers"]
     layers = range(L) if layers is None else list(layers)
     kshape = (n_slots, c["n_kv_heads"], max_seq_len, c["head_dim"])
-    vshape = (n_slots, c["n_kv_heads"], c["head_dim"], max_seq_len)
+    vshape = kshape
     K = [_normal_bf16(kshape, std, seed, 2 * l, device) for l in layers]
     V = [_normal_bf16(vshape, std, seed, 2 * l + 1, device) for l in layers]
     return K, V
@@ -225,13 +224,12 @@ def make_page_table(n_slots: int, max_pages_per_seq: int, num_pages: int, seed: 
 
 def make_kv_paged(c: dict, num_pages: int, page_size: int, seed: int, device="cpu",
                   layers=None, std: float = 1.0):
-    """Paged cache, bf16 N(0, std): per layer K of shape [num_pages,
-    n_kv_heads, page_size, head_dim] and V transposed, [num_pages,
-    n_kv_heads, head_dim, page_size]."""
+    """Paged cache, bf16 N(0, std): per layer K and V of shape [num_pages,
+    n_kv_heads, page_size, head_dim]."""
     L = c["n_layers"]
     layers = range(L) if layers is None else list(layers)
     kshape = (num_pages, c["n_kv_heads"], page_size, c["head_dim"])
-    vshape = (num_pages, c["n_kv_heads"], c["head_dim"], page_size)
+    vshape = kshape
     K = [_normal_bf16(kshape, std, seed, 2 * l, device) for l in layers]
     V = [_normal_bf16(vshape, std, seed, 2 * l + 1, device) for l in layers]
     return K, V

@@ -62,7 +62,7 @@ def run_at(cfg, Wg, B, slot, tgt, opt, seed):
     logits = torch.empty(B, cfg["vocab"], dtype=torch.float32, device=DEV)
     nxt = eng.decode_step(tokens, valid, seq, logits)
     row = logits[slot].cpu().numpy()
-    kv_bits = [(K[l][slot, :, pos].cpu(), V[l][slot, :, :, pos].cpu()) for l in range(cfg["n_layers"])]
+    kv_bits = [(K[l][slot, :, pos].cpu(), V[l][slot, :, pos].cpu()) for l in range(cfg["n_layers"])]
     eng.close()
     return row, int(nxt[slot]), kv_bits
 
@@ -128,7 +128,7 @@ def test_batch_invariant_prefill_parity(model, Lp):
     assert row_rel_err(last.cpu().numpy(), ref) <= TOL
     check_tokens([tok], ref[None], last.cpu().numpy()[None], [1], [])
     for l in range(cfg["n_layers"]):
-        g = (wl.bits(V[l])[2, :, :, :Lp].astype(np.uint32) << 16).view(np.float32)
-        o = (okv.v[l][2, :, :, :Lp].astype(np.uint32) << 16).view(np.float32)
+        g = (wl.bits(V[l])[2, :, :Lp].astype(np.uint32) << 16).view(np.float32)
+        o = (okv.v[l][2, :, :Lp].astype(np.uint32) << 16).view(np.float32)
         assert np.abs(g - o).max() <= TOL * np.abs(o).max()
     eng.close()

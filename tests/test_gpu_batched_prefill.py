@@ -44,7 +44,7 @@ def engine(cfg, Wg, seed, bi_prefill=True, pf=512):
 
 
 def kv_bits(K, V, slot, n):
-    return [(k[slot, :, :n].clone().view(torch.int16), v[slot, :, :, :n].clone().view(torch.int16))
+    return [(k[slot, :, :n].clone().view(torch.int16), v[slot, :, :n].clone().view(torch.int16))
             for k, v in zip(K, V)]
 
 

@@ -80,12 +80,12 @@ def bf16_as_f32(bits):
 def check_kv_against_oracle(cfg, gpu_k, gpu_v, okv, slot_sel):
     """Every cached position of the prompt, k and v, within TOL of the
     layer's largest oracle value.  slot_sel maps an array to the prompt's
-    [nkv, LP, d] / [nkv, d, LP] view."""
+    [nkv, LP, d] view (k and v alike)."""
     for l in range(cfg["n_layers"]):
         for g, o, axis in ((gpu_k[l], okv.k[l], "k"), (gpu_v[l], okv.v[l], "v")):
             a = bf16_as_f32(slot_sel(wl.bits(g), axis))
             b = bf16_as_f32(slot_sel(o, axis))
-            err = np.abs(a - b).max(axis=(0, 2) if axis == "k" else (0, 1))
+            err = np.abs(a - b).max(axis=(0, 2))
             bad = np.nonzero(err > TOL * np.abs(b).max())[0]
             assert bad.size == 0, (l, axis, bad[:8].tolist(), float(err.max()))
 
@@ -106,7 +106,7 @@ def test_chunked_prefill_matches_oracle(model, C):
     g = last.cpu().numpy()
     assert row_rel_err(g, ref) <= TOL
     check_tokens([tok], ref[None], g[None], [1], [])
-    check_kv_against_oracle(cfg, K, V, okv, lambda a, ax: a[1, :, :LP] if ax == "k" else a[1, :, :, :LP])
+    check_kv_against_oracle(cfg, K, V, okv, lambda a, ax: a[1, :, :LP])
     eng.close()
 
 
@@ -135,9 +135,7 @@ def test_chunked_prefill_paged_matches_oracle(model):
     pages = pt[2, :(LP + PS - 1) // PS]
 
     def sel(a, ax):   # gather the slot's pages into position order, first LP positions
-        if ax == "k":
-            return np.concatenate([a[p] for p in pages], axis=1)[:, :LP]
-        return np.concatenate([a[p] for p in pages], axis=2)[:, :, :LP]
+        return np.concatenate([a[p] for p in pages], axis=1)[:, :LP]
     check_kv_against_oracle(cfg, K, V, okv, sel)
     eng.close()
 
@@ -159,12 +157,12 @@ def test_chunked_prefill_is_deterministic_and_one_chunk_is_prefill(model):
     assert ta == tb and torch.equal(la.view(torch.int32), lb.view(torch.int32))
     for l in range(cfg["n_layers"]):
         assert torch.equal(K[l][0, :, :LP].view(torch.int16), K[l][3, :, :LP].view(torch.int16)), l
-        assert torch.equal(V[l][0, :, :, :LP].view(torch.int16), V[l][3, :, :, :LP].view(torch.int16)), l
+        assert torch.equal(V[l][0, :, :LP].view(torch.int16), V[l][3, :, :LP].view(torch.int16)), l
     # one chunk at start 0 is the whole-prompt prefill, bit for bit
     tc = eng.prefill(prompt, 1, la)
     td = eng.prefill_chunk(prompt, 0, 2, lb)
     assert tc == td and torch.equal(la.view(torch.int32), lb.view(torch.int32))
     for l in range(cfg["n_layers"]):
         assert torch.equal(K[l][1, :, :LP].view(torch.int16), K[l][2, :, :LP].view(torch.int16)), l
-        assert torch.equal(V[l][1, :, :, :LP].view(torch.int16), V[l][2, :, :, :LP].view(torch.int16)), l
+        assert torch.equal(V[l][1, :, :LP].view(torch.int16), V[l][2, :, :LP].view(torch.int16)), l
     eng.close()

@@ -141,15 +141,15 @@ def test_prefill_600_full_shapes_teacher_forced(full):
     last = torch.empty(cfg["vocab"], dtype=torch.float32, device=DEV)
     eng.prefill(prompt, 1, last)
     gk = [wl.bits(k[1]) for k in K]          # [nkv, cap, d] per layer
-    gv = [wl.bits(v[1]) for v in V]          # [nkv, d, cap]
+    gv = [wl.bits(v[1]) for v in V]          # [nkv, cap, d]
     f32 = lambda a: (a.astype(np.uint32) << 16).view(np.float32)
     for t in (0, 1, 255, 256, 511, 512, LP - 1):
         kv1 = row_cache(K, V, 1, cap)        # the GPU-written prefix; position t is recomputed
         ref = oracle.decode_row(m, kv1, 0, int(prompt[t]), t)
         for l in range(cfg["n_layers"]):
-            ok, ov = f32(kv1.k[l][0, :, t, :]), f32(kv1.v[l][0, :, :, t])
+            ok, ov = f32(kv1.k[l][0, :, t, :]), f32(kv1.v[l][0, :, t, :])
             assert np.abs(f32(gk[l][:, t, :]) - ok).max() <= TOL * np.abs(ok).max(), (t, l)
-            assert np.abs(f32(gv[l][:, :, t]) - ov).max() <= TOL * np.abs(ov).max(), (t, l)
+            assert np.abs(f32(gv[l][:, t, :]) - ov).max() <= TOL * np.abs(ov).max(), (t, l)
         if t == LP - 1:
             assert row_rel_err(last.cpu().numpy(), ref) <= TOL
 
@@ -173,9 +173,9 @@ def test_prefill_32768_full_shapes_teacher_forced(full):
         kv1 = row_cache(K, V, 1, cap)
         ref = oracle.decode_row(m, kv1, 0, int(prompt[t]), t)
         for l in range(cfg["n_layers"]):
-            ok, ov = f32(kv1.k[l][0, :, t, :]), f32(kv1.v[l][0, :, :, t])
+            ok, ov = f32(kv1.k[l][0, :, t, :]), f32(kv1.v[l][0, :, t, :])
             assert np.abs(f32(gk[l][:, t, :]) - ok).max() <= TOL * np.abs(ok).max(), (t, l)
-            assert np.abs(f32(gv[l][:, :, t]) - ov).max() <= TOL * np.abs(ov).max(), (t, l)
+            assert np.abs(f32(gv[l][:, t, :]) - ov).max() <= TOL * np.abs(ov).max(), (t, l)
         if t == lp - 1:
             err = row_rel_err(last.cpu().numpy(), ref)
             print(f"prefill of {lp}: last-position relative logit error {err:.2e}")
@@ -200,7 +200,7 @@ def test_prefill_bits_do_not_depend_on_the_workspace(full):
         tok = eng.prefill(prompt, 1, last)
         torch.cuda.synchronize()
         outs.append((tok, last.view(torch.int32).cpu(), [k[1, :, :lp].clone() for k in K],
-                     [v[1, :, :, :lp].clone() for v in V]))
+                     [v[1, :, :lp].clone() for v in V]))
         eng.close()
     a, b = outs
     assert a[0] == b[0] and torch.equal(a[1], b[1])

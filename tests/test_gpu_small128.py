@@ -80,8 +80,8 @@ def test_prefill_parity_d128(small, Lp):
     assert row_rel_err(last.cpu().numpy(), ref) <= TOL
     check_tokens([tok], ref[None], last.cpu().numpy()[None], [1], [])
     for l in range(cfg["n_layers"]):
-        g = (wl.bits(V[l])[3, :, :, :Lp].astype(np.uint32) << 16).view(np.float32)
-        o = (okv.v[l][3, :, :, :Lp].astype(np.uint32) << 16).view(np.float32)
+        g = (wl.bits(V[l])[3, :, :Lp].astype(np.uint32) << 16).view(np.float32)
+        o = (okv.v[l][3, :, :Lp].astype(np.uint32) << 16).view(np.float32)
         assert np.abs(g - o).max() <= 2e-2 * np.abs(o).max()
 
 

@@ -80,7 +80,7 @@ def test_parity_with_oracle(model, B):
             gk, gv = wl.bits(K[l]), wl.bits(V[l])
             for r in np.nonzero(valid)[0]:
                 p = lens[r]
-                for got, want in ((gk[r, :, p], okv.k[l][r, :, p]), (gv[r, :, :, p], okv.v[l][r, :, :, p])):
+                for got, want in ((gk[r, :, p], okv.k[l][r, :, p]), (gv[r, :, p], okv.v[l][r, :, p])):
                     g = (got.astype(np.uint32) << 16).view(np.float32)
                     o = (want.astype(np.uint32) << 16).view(np.float32)
                     assert np.abs(g - o).max() <= TOL * np.abs(o).max() + 1e-6, (step, l, r)
@@ -177,13 +177,13 @@ def test_paged_equals_contiguous(model, B):
     Kc, Vc = cache(cfg, B, seed=751 + B)
     Kp = [torch.empty((num_pages, cfg["n_kv_heads"], ps, cfg["head_dim"]), dtype=torch.bfloat16, device=DEV)
           for _ in range(cfg["n_layers"])]
-    Vp = [torch.empty((num_pages, cfg["n_kv_heads"], cfg["head_dim"], ps), dtype=torch.bfloat16, device=DEV)
+    Vp = [torch.empty((num_pages, cfg["n_kv_heads"], ps, cfg["head_dim"]), dtype=torch.bfloat16, device=DEV)
           for _ in range(cfg["n_layers"])]
     for l in range(cfg["n_layers"]):
         for s in range(B):
             for j in range(mpp):
                 Kp[l][pt[s, j]] = Kc[l][s, :, j * ps:(j + 1) * ps]
-                Vp[l][pt[s, j]] = Vc[l][s, :, :, j * ps:(j + 1) * ps]
+                Vp[l][pt[s, j]] = Vc[l][s, :, j * ps:(j + 1) * ps]
     ec = corun.Engine(cfg, Wg, B, Kc, Vc, opt=layer_opt(B))
     ep = corun.Engine(cfg, Wg, B, Kp, Vp, layout=corun.KV_PAGED, page_size=ps,
                       page_table=torch.from_numpy(pt).to(DEV), opt=layer_opt(B))
@@ -205,7 +205,7 @@ def test_paged_equals_contiguous(model, B):
                 assert torch.equal(Kp[l][pt[s, j]].view(torch.int16),
                                    Kc[l][s, :, j * ps:(j + 1) * ps].view(torch.int16)), (l, s, j)
                 assert torch.equal(Vp[l][pt[s, j]].view(torch.int16),
-                                   Vc[l][s, :, :, j * ps:(j + 1) * ps].view(torch.int16)), (l, s, j)
+                                   Vc[l][s, :, j * ps:(j + 1) * ps].view(torch.int16)), (l, s, j)
     ec.close()
     ep.close()
 

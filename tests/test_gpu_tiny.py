@@ -85,7 +85,7 @@ def test_kv_append_matches_oracle(tiny):
             if not b.valid[r]:
                 continue
             p = b.seq_lens[r]
-            for got, ref in ((gk[r, :, p], okv.k[l][r, :, p]), (gv[r, :, :, p], okv.v[l][r, :, :, p])):
+            for got, ref in ((gk[r, :, p], okv.k[l][r, :, p]), (gv[r, :, p], okv.v[l][r, :, p])):
                 g = (got.astype(np.uint32) << 16).view(np.float32)
                 o = (ref.astype(np.uint32) << 16).view(np.float32)
                 assert np.abs(g - o).max() <= 2e-2 * np.abs(o).max() + 1e-6
@@ -312,7 +312,7 @@ def test_prefill_identity_alone_vs_after_other_traffic(tiny):
     assert t1 == t2 and n1[0] == n2[2]
     for l in range(cfg["n_layers"]):
         assert torch.equal(K1[l][0, :, :51].view(torch.int16), K2[l][2, :, :51].view(torch.int16))
-        assert torch.equal(V1[l][0, :, :, :51].view(torch.int16), V2[l][2, :, :, :51].view(torch.int16))
+        assert torch.equal(V1[l][0, :, :51].view(torch.int16), V2[l][2, :, :51].view(torch.int16))
 
 
 def test_prefill_then_decode_tracks_longer_prefill(tiny):
@@ -341,13 +341,13 @@ def test_paged_equals_contiguous_bitwise(tiny):
     Kc, Vc = new_cache(cfg, seed=141)
     Kp = [torch.full((num_pages, cfg["n_kv_heads"], ps, cfg["head_dim"]), float("nan"), dtype=torch.bfloat16,
                      device=DEV) for _ in range(cfg["n_layers"])]
-    Vp = [torch.full((num_pages, cfg["n_kv_heads"], cfg["head_dim"], ps), float("nan"), dtype=torch.bfloat16,
+    Vp = [torch.full((num_pages, cfg["n_kv_heads"], ps, cfg["head_dim"]), float("nan"), dtype=torch.bfloat16,
                      device=DEV) for _ in range(cfg["n_layers"])]
     for l in range(cfg["n_layers"]):
         for s in range(B):
             for j in range(mpp):
                 Kp[l][pt[s, j]] = Kc[l][s, :, j * ps:(j + 1) * ps]
-                Vp[l][pt[s, j]] = Vc[l][s, :, :, j * ps:(j + 1) * ps]
+                Vp[l][pt[s, j]] = Vc[l][s, :, j * ps:(j + 1) * ps]
     ptd = torch.from_numpy(pt).to(DEV)
     ec = make_engine(cfg, Wg, Kc, Vc)
     ep = corun.Engine(cfg, Wg, B, Kp, Vp, layout=corun.KV_PAGED, page_size=ps, page_table=ptd)

@@ -277,7 +277,7 @@ def test_decode_row_against_torch_composition(name):
     S, slot, pos = 64, 1, 23
     kv = _contig_kv(cfg, 2, S, seed=4)
     kpre = [torch.from_numpy(np.ascontiguousarray(k[slot, :, :pos]).view(np.int16)).view(torch.bfloat16) for k in kv.k]
-    vpre = [torch.from_numpy(np.ascontiguousarray(v[slot, :, :, :pos].transpose(0, 2, 1)).view(np.int16)).view(torch.bfloat16)
+    vpre = [torch.from_numpy(np.ascontiguousarray(v[slot, :, :pos]).view(np.int16)).view(torch.bfloat16)
             for v in kv.v]
     tok = 517
     logits = oracle.decode_row(m, kv, slot, tok, pos)
@@ -286,7 +286,7 @@ def test_decode_row_against_torch_composition(name):
     assert np.abs(logits - ref.numpy()[0]).max() <= 1e-10 * scale
     for l in range(cfg["n_layers"]):   # the appended KV entries are the same bf16 values
         assert np.array_equal(kv.k[l][slot, :, pos], wl.bits(kn[l][:, 0]))
-        assert np.array_equal(kv.v[l][slot, :, :, pos], wl.bits(vn[l][:, 0]))
+        assert np.array_equal(kv.v[l][slot, :, pos], wl.bits(vn[l][:, 0]))
 
 
 @pytest.mark.parametrize("name", ["tiny", "tiny_moe"])
@@ -305,7 +305,7 @@ def test_prefill_against_torch_composition(name):
     assert tok == int(np.argmax(ref_last.astype(np.float32)))
     for l in range(cfg["n_layers"]):
         assert np.array_equal(kv.k[l][0, :, :Lp], wl.bits(kn[l]))
-        assert np.array_equal(kv.v[l][0, :, :, :Lp], wl.bits(vn[l].transpose(1, 2)))
+        assert np.array_equal(kv.v[l][0, :, :Lp], wl.bits(vn[l]))
 
 
 def test_decode_equals_prefill_bitwise():
@@ -322,7 +322,7 @@ def test_decode_equals_prefill_bitwise():
     assert np.array_equal(l1, l2)
     for l in range(cfg["n_layers"]):
         assert np.array_equal(kv1.k[l][0, :, :13], kv2.k[l][0, :, :13])
-        assert np.array_equal(kv1.v[l][0, :, :, :13], kv2.v[l][0, :, :, :13])
+        assert np.array_equal(kv1.v[l][0, :, :13], kv2.v[l][0, :, :13])
 
 
 def test_paged_equals_contiguous_bitwise():
@@ -336,11 +336,11 @@ def test_paged_equals_contiguous_bitwise():
     pk, pv = [], []
     for l in range(cfg["n_layers"]):      # scatter the same contents into permuted pages
         k = np.zeros((num_pages, cfg["n_kv_heads"], ps, cfg["head_dim"]), np.uint16)
-        v = np.zeros((num_pages, cfg["n_kv_heads"], cfg["head_dim"], ps), np.uint16)
+        v = np.zeros((num_pages, cfg["n_kv_heads"], ps, cfg["head_dim"]), np.uint16)
         for s_ in range(slots):
             for j in range(mpp):
                 k[pt[s_, j]] = ckv.k[l][s_, :, j * ps:(j + 1) * ps]
-                v[pt[s_, j]] = ckv.v[l][s_, :, :, j * ps:(j + 1) * ps]
+                v[pt[s_, j]] = ckv.v[l][s_, :, j * ps:(j + 1) * ps]
         pk.append(k)
         pv.append(v)
     pkv = oracle.KVCache(pk, pv, oracle.KV_PAGED, slots, S, ps, num_pages, mpp, pt)
@@ -407,7 +407,7 @@ def test_routed_decode_records_and_forcing():
     S, slot, pos, tok = 48, 0, 29, 211
     kv = _contig_kv(cfg, 1, S, seed=31)
     kpre = [torch.from_numpy(np.ascontiguousarray(x[slot, :, :pos]).view(np.int16)).view(torch.bfloat16) for x in kv.k]
-    vpre = [torch.from_numpy(np.ascontiguousarray(x[slot, :, :, :pos].transpose(0, 2, 1)).view(np.int16))
+    vpre = [torch.from_numpy(np.ascontiguousarray(x[slot, :, :pos]).view(np.int16))
             .view(torch.bfloat16) for x in kv.v]
     plain = oracle.decode_row(m, kv, slot, tok, pos)
     lg, rl, own = oracle.decode_row_routed(m, kv, slot, tok, pos)
