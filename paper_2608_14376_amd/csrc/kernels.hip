@@ -127,11 +127,23 @@ __device__ __forceinline__ uint2 lds_read_tr16(const void *lds_ptr)
     return __builtin_bit_cast(uint2, v);
 }
 
-// Value tiles in LDS are token-major, 16-byte chunk c of token t at
-// t * chunks + (c ^ vtile_swz(t)): the four consecutive tokens that one
-// 16-lane transposed read touches (32 bytes each) land in four distinct
-// 32-byte bank ranges.
-__device__ __forceinline__ int vtile_swz(int t) { return 2 * (t & 3); }
+// Value tiles in LDS are token-major, 16-byte chunk c of token t (KCH
+// chunks per token) at t KCH + (c ^ vtile_swz<KCH>(t)).  A transposed read
+// of the attention kernels takes, per 16-lane group, 32 bytes (two chunks)
+// of four consecutive tokens 4 r + 0..3, and the two groups of a half
+// wavefront read either the next two chunks of the same tokens or the same
+// chunks of the tokens 8 further on.  The swizzle moves the four tokens to
+// four distinct 16-bank ranges (bits 2-3 of the chunk, with the token's
+// parity for 128-byte rows) and those 8 tokens further to the other half of
+// each range (bit 1), so the 64 lanes of a half wavefront pair touch each
+// of the 64 banks once.
+template <int KCH>
+__device__ __forceinline__ int vtile_swz(int t)
+{
+    static_assert(KCH == 8 || KCH == 16, "128- or 256-byte value rows");
+    if constexpr (KCH == 16) return (4 * (t & 3)) ^ (2 * ((t >> 3) & 1));
+    else return (4 * ((t >> 1) & 1)) ^ (2 * ((t >> 3) & 1));
+}
 
 __device__ __forceinline__ int row_slot(const int32_t *slot_of_row, int slot_const, int r)
 {
@@ -1191,8 +1203,8 @@ hipError_t launch_qkv_post(const float *part, int S, long long part_stride, int 
 // LDS layouts, 16-byte units, XOR-swizzled so that a fragment read hits
 // distinct bank groups: key unit (token t, chunk c) at t KCH + (c ^ ks(t))
 // (16 lanes: 16 tokens of one chunk), value unit (token t, chunk c) at
-// t KCH + (c ^ vtile_swz(t)) (a transposed read: 4 tokens x 32 bytes per
-// 16 lanes).
+// t KCH + (c ^ vtile_swz<KCH>(t)) (a transposed read: 4 tokens x 32 bytes
+// per 16 lanes).
 // ---------------------------------------------------------------------------
 
 // Token order inside a 32-token block.  Score tile T's MFMA row m carries
@@ -1302,7 +1314,7 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
         }
 #pragma unroll
         for (int j = 0; j < V_OPS; ++j) {
-            const int u = j * 256 + tid, tv = u / KCH, c = (u % KCH) ^ vtile_swz(tv);
+            const int u = j * 256 + tid, tv = u / KCH, c = (u % KCH) ^ vtile_swz<KCH>(tv);
             const int t = min(tb0 + tv, kmax);
             size_t off;
             if (paged) off = (((size_t)pgs[buf][t / ps - p0] * nkv + kvh) * ps + t % ps) * D;
@@ -1391,7 +1403,7 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
                 tile[tl * KCH + (tid ^ attn_kswz<KCH>(tl))] = reinterpret_cast<const uint4 *>(kvn)[tid];
             } else if (tid >= 64 && tid < 64 + KCH) {
                 const int c = tid - 64;
-                tile[KU + tl * KCH + (c ^ vtile_swz(tl))] = reinterpret_cast<const uint4 *>(kvn + D)[c];
+                tile[KU + tl * KCH + (c ^ vtile_swz<KCH>(tl))] = reinterpret_cast<const uint4 *>(kvn + D)[c];
             }
             __builtin_amdgcn_s_waitcnt(0);
             lds_barrier();
@@ -1424,7 +1436,7 @@ __global__ __launch_bounds__(256) void k_attn_split(const uint16_t *__restrict__
                 for (int r = 0; r < 2; ++r) {
                     const int tv = 32 * wave + 8 * kg + 4 * r + qq;
                     const int c = 2 * et + (a >> 1);
-                    part[r] = lds_read_tr16(reinterpret_cast<const char *>(tile + KU + tv * KCH + (c ^ vtile_swz(tv))) +
+                    part[r] = lds_read_tr16(reinterpret_cast<const char *>(tile + KU + tv * KCH + (c ^ vtile_swz<KCH>(tv))) +
                                             8 * (a & 1));
                 }
                 uint4 v = {part[0].x, part[0].y, part[1].x, part[1].y};   // low half = earlier token
@@ -2678,7 +2690,7 @@ __device__ __forceinline__ void prefill_attn_block(const uint16_t *__restrict__ 
         }
 #pragma unroll
         for (int j = 0; j < V_OPS; ++j) {
-            const int gi = j * NT + tid, r = gi / KCH, c = (gi % KCH) ^ vtile_swz(r);
+            const int gi = j * NT + tid, r = gi / KCH, c = (gi % KCH) ^ vtile_swz<KCH>(r);
             const int key = min(k0 + r, Lk - 1);
             __builtin_amdgcn_global_load_lds((const void *)(vc + kv_offset(kv, nkv, D, slot, kvh, key) + 8 * c),
                                              (lds_void *)(base + KSTAGE + j * NT), 16, 0, 0);
@@ -2804,7 +2816,7 @@ __device__ __forceinline__ void prefill_attn_block(const uint16_t *__restrict__ 
                 for (int r = 0; r < 2; ++r) {
                     const int key = 16 * s16 + 8 * h + 4 * r + qv;
                     const int c = 4 * dt + 2 * half16 + (a >> 1);
-                    part[r] = lds_read_tr16(reinterpret_cast<const char *>(Vt + key * KCH + (c ^ vtile_swz(key))) +
+                    part[r] = lds_read_tr16(reinterpret_cast<const char *>(Vt + key * KCH + (c ^ vtile_swz<KCH>(key))) +
                                             8 * (a & 1));
                 }
                 const bf16x8 vf = __builtin_bit_cast(bf16x8, (uint4){part[0].x, part[0].y, part[1].x, part[1].y});

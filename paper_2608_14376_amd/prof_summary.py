@@ -8,6 +8,7 @@ line in the summaries it writes):
                                                        --kernel k_attn_split --first N --algorithmic BYTES ...
   python -m paper_2608_14376_amd.prof_summary mfma     --pmc P.csv --trace T.csv ...
   python -m paper_2608_14376_amd.prof_summary fetch    --pmc P.csv --trace T.csv ...
+  python -m paper_2608_14376_amd.prof_summary prefill  --pmc P.csv --trace T.csv --call 1 --op qkv=FLOPS ...
 
 Dispatch windows follow bench.py's order for the headline batch: `warmup`
 graph steps, `steps` graph steps, one more step, `profile_steps` eagerly
@@ -248,10 +249,80 @@ def cmd_fetch(a):
     print("\n".join(lines))
 
 
+def prefill_window(disp, call):
+    """The dispatches of the call-th prefill of the run (0-based): from its
+    k_embed to the next one (each prefill call starts with the embedding)."""
+    starts = [i for i, d in enumerate(disp) if d[0] == "k_embed"]
+    if call >= len(starts):
+        raise SystemExit(f"the run has {len(starts)} prefill calls, not {call + 1}")
+    end = starts[call + 1] if call + 1 < len(starts) else len(disp)
+    return disp[starts[call]:end]
+
+
+def label_prefill(window, ops, layers):
+    """Name each dispatch of one prefill: the projections cycle through `ops`
+    per layer (the last is lm_head), k_prefill_attn is attention."""
+    out, j = [], 0
+    for d in window:
+        n = d[0]
+        if n.startswith("k_gemm"):
+            out.append(ops[j % len(ops)] if j < len(ops) * layers else "lm_head")
+            j += 1
+        elif n.startswith("k_prefill_attn"):
+            out.append("attention")
+        else:
+            out.append(n)
+    return out
+
+
+def cmd_prefill(a):
+    ops = [x.split("=")[0] for x in a.op]
+    flops = {x.split("=")[0]: float(x.split("=")[1]) for x in a.op}
+    flops["attention"] = a.attn_flops
+    tw = prefill_window(trace_dispatches(a.trace), a.call)
+    pw = prefill_window(pmc_dispatches(a.pmc, []), a.call)
+    if [d[0] for d in tw] != [d[0] for d in pw]:
+        raise SystemExit("the trace and counter runs launched different kernels in this prefill")
+    names = label_prefill(tw, ops, a.layers)
+    dur, cnt, kern = collections.defaultdict(list), collections.defaultdict(list), {}
+    for nm, t, c in zip(names, tw, pw):
+        dur[nm].append((t[3] - t[2]) / 1e3)
+        cnt[nm].append(c[2])
+        kern[nm] = t[0]
+    lines = header(a)
+    lines += [f"# busy = SQ_VALU_MFMA_BUSY_CYCLES / (duration x {CLOCK_GHZ} GHz x {SIMDS} SIMDs) (32 cycles per "
+              "32x32x16 bf16 MFMA);",
+              "# VALU / MFMA and LDS / MFMA are instruction-count ratios (SQ_INSTS_VALU counts the MFMAs too);",
+              "# durations from the kernel-trace run, counters from the counter run, matched dispatch by dispatch",
+              "", f"{'op':12s} {'kernel':16s} {'dispatches':>10s} {'us':>9s} {'busy':>6s} {'TFLOP/s':>8s} "
+                  f"{'VALU/MFMA':>9s} {'LDS/MFMA':>8s} {'conflicts/LDS':>13s}"]
+    total_us = sum(sum(v) for v in dur.values())
+    for nm in ops + ["attention", "lm_head"]:
+        if nm not in dur:
+            continue
+        us = sum(dur[nm]) / len(dur[nm])
+        mean = lambda k: sum(c.get(k, 0.0) for c in cnt[nm]) / len(cnt[nm])
+        mf = mean("SQ_INSTS_MFMA")
+        busy = mean("SQ_VALU_MFMA_BUSY_CYCLES") / (us * 1e-6 * CLOCK_GHZ * 1e9 * SIMDS)
+        tf = flops.get(nm, 0.0) / us / 1e6
+        lds = mean("SQ_INSTS_LDS")
+        lines.append(f"{nm:12s} {kern[nm]:16s} {len(dur[nm]):10d} {us:9.2f} {100 * busy:5.1f}% {tf:8.1f} "
+                     f"{mean('SQ_INSTS_VALU') / mf if mf else 0:9.2f} {lds / mf if mf else 0:8.2f} "
+                     f"{mean('SQ_LDS_BANK_CONFLICT') / lds if lds else 0:13.3f}")
+    rest = sorted(((nm, sum(v)) for nm, v in dur.items() if nm not in ops + ["attention", "lm_head"]),
+                  key=lambda kv: -kv[1])
+    lines += ["", f"# the prefill's {len(tw)} dispatches take {total_us / 1e3:.2f} ms of kernel time; "
+                  "the other kernels: " + ", ".join(f"{nm} {v / 1e3:.2f} ms" for nm, v in rest)]
+    for ln in a.note or []:
+        lines.append(f"# {ln}")
+    open(a.out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
-    for name in ("kernels", "traffic", "mfma", "fetch"):
+    for name in ("kernels", "traffic", "mfma", "fetch", "prefill"):
         s = sub.add_parser(name)
         s.add_argument("--out", required=True)
         s.add_argument("--title", required=True)
@@ -273,6 +344,14 @@ def main():
             s.add_argument("--kernel", required=True)
             s.add_argument("--first", type=int, required=True)
             s.add_argument("--algorithmic", type=int, required=True)
+        elif name == "prefill":
+            s.add_argument("--pmc", required=True)
+            s.add_argument("--trace", required=True)
+            s.add_argument("--call", type=int, default=1, help="which prefill call of the run (0-based)")
+            s.add_argument("--layers", type=int, default=36)
+            s.add_argument("--op", action="append", default=[],
+                           help="name=flops of each projection, in launch order within a layer")
+            s.add_argument("--attn-flops", type=float, default=0.0)
         else:
             s.add_argument("--pmc", required=True)
             s.add_argument("--trace", required=True)
@@ -285,7 +364,8 @@ def main():
         for item in a.label:
             parts = item.split("=")
             a.labels[parts[0]] = parts[1] if a.cmd == "mfma" else (parts[1], int(parts[2]))
-    {"kernels": cmd_kernels, "traffic": cmd_traffic, "mfma": cmd_mfma, "fetch": cmd_fetch}[a.cmd](a)
+    {"kernels": cmd_kernels, "traffic": cmd_traffic, "mfma": cmd_mfma, "fetch": cmd_fetch,
+     "prefill": cmd_prefill}[a.cmd](a)
 
 
 if __name__ == "__main__":
