@@ -610,6 +610,24 @@ def kernel_source_sha():
     return h.hexdigest()[:16]
 
 
+def read_summary(path):
+    """The `key: value` lines of a profiles/ summary, with the kernel-source
+    hash from its `# kernel_source_sha256_16:` header line; other comment
+    lines are skipped."""
+    kv = {}
+    for ln in open(path):
+        ln = ln.strip()
+        if ln.startswith("#"):
+            body = ln.lstrip("#").strip()
+            if body.startswith("kernel_source_sha256_16:"):
+                kv["kernel_source_sha256_16"] = body.split(":", 1)[1].strip()
+            continue
+        if ":" in ln:
+            k, v = ln.split(":", 1)
+            kv[k.strip()] = v.strip()
+    return kv
+
+
 def measured_traffic(kernel, B, seed):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
     summary of this workload (FETCH_SIZE and WRITE_SIZE, each scaled by what
@@ -618,11 +636,7 @@ def measured_traffic(kernel, B, seed):
     path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_8b_B{B}_seed{seed}.txt")
     if not os.path.exists(path):
         return None, None
-    kv = {}
-    for ln in open(path):
-        if ":" in ln and not ln.startswith("#"):
-            k, v = ln.split(":", 1)
-            kv[k.strip()] = v.strip()
+    kv = read_summary(path)
     if kv.get("kernel_source_sha256_16") != kernel_source_sha():
         return None, os.path.relpath(path, ROOT) + " (stale: kernels changed since the counters were taken)"
     return int(float(kv["traffic_bytes_per_launch"])), os.path.relpath(path, ROOT)
