@@ -862,6 +862,35 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
         }
         mma(cur);
     };
+    // The same step where stage i + 1 exists and stage i + P is still to be
+    // issued: no branch, a constant wait.  With the conditional form alone
+    // the loop body joins a path on which the previous step's fragment reads
+    // were never waited for, so the compiler waited for every LDS read
+    // (including the ones just issued for the next stage) before each
+    // second step's products.
+    auto step_full = [&](int i, const Frags &cur, Frags &nxt) {
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm((P - 2) * OPS));
+        __builtin_amdgcn_s_waitcnt(0xC07F);
+        lds_barrier();
+        issue((i + P) % NST, (i + P) * BK);
+        read(nxt, (i + 1) % NST);
+        mma(cur);
+        // Issue order for one wavefront per SIMD (four wavefronts): the stage
+        // loads, then one fragment read between consecutive products, so the
+        // reads drain while the matrix cores run (lm_head at M = 256: 451 ->
+        // 423 us).  With two wavefronts per SIMD the compiler's own order was
+        // faster (the 256 x 256 tile: 70 against 73 us at M = 256).
+        if constexpr (NW == 4) {
+            constexpr int NRD = (BK / 16) * (FM + FN), NMM = (BK / 16) * FM * FN;
+            __builtin_amdgcn_sched_group_barrier(0x020, OPS, 0);
+#pragma unroll
+            for (int k = 0; k < NRD && k < NMM; ++k) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+            if constexpr (NMM > NRD) __builtin_amdgcn_sched_group_barrier(0x008, NMM - NRD, 0);
+        }
+    };
 #pragma unroll
     for (int i = 0; i < P; ++i)
         if (i < nk) issue(i, i * BK);
@@ -872,6 +901,10 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_dma(const uint16_t *__restrict
         read(f0, 0);
     }
     int i = 0;
+    for (; i + 1 + P < nk; i += 2) {
+        step_full(i, f0, f1);
+        step_full(i + 1, f1, f0);
+    }
     for (; i + 1 < nk; i += 2) {
         step(i, f0, f1);
         step(i + 1, f1, f0);
