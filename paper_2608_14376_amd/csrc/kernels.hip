@@ -2707,7 +2707,7 @@ __device__ __forceinline__ void prefill_attn_block(const uint16_t *__restrict__ 
     const int u_first = units - 1 - grp * NW;
     const int wg_last_q = p0 + min(n, (u_first / G + 1) * QB) - 1;
     const int my_last_q = active ? p0 + min(n, q0 + QB) - 1 : -1;
-    const int ntiles = wg_last_q / BKT + 1;
+    const int ntiles = __builtin_amdgcn_readfirstlane(wg_last_q / BKT + 1);   // uniform: scalar branches
 
     // tile loads: op j of thread t is 16-byte unit 512 j + t of the K part
     // or of the V part (token-major both, row = unit / KCH)
@@ -2751,9 +2751,16 @@ __device__ __forceinline__ void prefill_attn_block(const uint16_t *__restrict__ 
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
     const int qq = p0 + q0 + r32;                     // this lane's query position
 
+    // P stages go out whatever the tile count: a stage past the last tile
+    // loads clamped (real) rows into a slot that no tile reads, and the wait
+    // after the loop drains it.  So one constant wait here completes the q
+    // fragments (loaded before the stages; vmcnt retires in order).  Without
+    // it the compiler, unable to tell on entry to the loop whether they had
+    // landed, waited for every load in flight (the whole ring) before each
+    // tile's score products.
 #pragma unroll
-    for (int i = 0; i < P; ++i)
-        if (i < ntiles) issue(i, i * BKT);
+    for (int i = 0; i < P; ++i) issue(i, i * BKT);
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(P * OPS));
     for (int i = 0; i < ntiles; ++i) {
         wait_stages<OPS, P - 1>(min(P - 1, ntiles - 1 - i));
         lds_barrier();
