@@ -313,7 +313,7 @@ corun_status corun_sample(corun_engine *e, const float *logits_dev, int64_t ld, 
  * cannot allocate device memory: code that must not call hipMalloc (a tight
  * serving loop, a harness that forbids it).  The same sampler and result
  * bits as corun_sample on the same logits and arguments; the per-row inputs
- * and outputs are staged in a fixed static device array of 32 KiB that each
+ * and outputs are staged in a fixed static device array of 25 KiB that each
  * GPU holds for the life of the process (rows at most
  * CORUN_SAMPLE_NOALLOC_MAX_ROWS).  Runs on `stream` (a hipStream_t; NULL =
  * the null stream) on the current device and waits for it before returning.
