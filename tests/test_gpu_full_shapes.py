@@ -91,7 +91,7 @@ def test_decode_B256_full_shapes(full):
 # split-K (its epilogue applies SwiGLU; at B = 8 attention applies the QKV
 # epilogue); the lm_head on the packed 32- or 64-row tiles; the attention
 # chunk that gives up to 33 splits at B <= 8, 17 at B = 16, 5 at B = 64.
-SMALL_B = {1: (32, 128, 33), 8: (32, 128, 33), 16: (32, 256, 17), 64: (64, 1024, 5)}
+SMALL_B = {1: (32, 128, 33), 8: (32, 256, 17), 16: (32, 512, 9), 64: (64, 1024, 5)}
 
 
 @pytest.mark.parametrize("Bs", sorted(SMALL_B))
