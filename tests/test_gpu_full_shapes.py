@@ -90,7 +90,7 @@ def test_decode_B256_full_shapes(full):
 # 64-row weight tiles with split-K 5 (qkv) and 8 (o, down), gate/up without
 # split-K (its epilogue applies SwiGLU; at B = 8 attention applies the QKV
 # epilogue); the lm_head on the packed 32- or 64-row tiles; the attention
-# chunk that gives up to 33 splits at B <= 8, 17 at B = 16, 5 at B = 64.
+# chunk that gives up to 33 splits at B = 1, 17 at B = 8, 9 at B = 16, 5 at B = 64.
 SMALL_B = {1: (32, 128, 33), 8: (32, 256, 17), 16: (32, 512, 9), 64: (64, 1024, 5)}
 
 
