@@ -112,6 +112,22 @@ def test_plan_is_a_function_of_shape_only():
     assert forced["qkv"]["split_k"] == 3 and forced["down"]["split_k"] == 3
 
 
+def test_attention_chunk_rule():
+    """The split-KV chunk: the smallest power of two from 128 up to 1024 with
+    B * kv_heads * ceil(capacity / chunk) <= 2048, fixed per engine (the
+    decode benchmark's capacity 4144: 128 / 256 / 512 / 1024 tokens at
+    B = 1 / 8 / 16 / 32 and up); an explicit chunk wins."""
+    c = wl.config("8b")
+    got = {B: corun.describe_plan(c, _kv(n_slots=256, max_seq_len=4144), B)["attn_chunk"]
+           for B in (1, 2, 4, 8, 16, 32, 64, 256)}
+    assert got == {1: 128, 2: 128, 4: 128, 8: 256, 16: 512, 32: 1024, 64: 1024, 256: 1024}, got
+    for B, ch in got.items():
+        assert B * c["n_kv_heads"] * -(-4144 // ch) <= 2048 or ch == 1024
+        assert ch == 128 or B * c["n_kv_heads"] * -(-4144 // (ch // 2)) > 2048
+    assert corun.describe_plan(c, _kv(n_slots=256, max_seq_len=4144), 8,
+                               corun.options(attn_chunk=192))["attn_chunk"] == 192
+
+
 def _small_batch_layer(p):
     return all((p[n]["m_tile"], p[n]["n_tile"], p[n]["split_k"]) == (16, 16, 1)
                for n in ("qkv", "o", "gate_up", "down"))
